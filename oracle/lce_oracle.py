@@ -1,0 +1,183 @@
+"""Plain CPU oracle of the linear-cross-entropy (LCE) objective.
+
+TEST INFRASTRUCTURE ONLY. Only the tests, the package's ``smoke()`` check and
+the benchmark's CPU-baseline leg may import this module. The product path (the
+HIP library and its Python binding) never calls it and shares no code with it.
+
+What it computes (paper Sec. 4.2 and Sec. 3.3): LCE fuses the model's final
+output projection with the cross-entropy over the whole vocabulary, drops the
+ignored target positions before the projection, and is a drop-in for the
+standard cross-entropy objective -- it reaches the same value, only without
+holding the [tokens, vocab] logit matrix at once. The oracle therefore is the
+textbook cross-entropy written out in float64 from the bf16 inputs (exactly
+representable in float64), materialising each row's full-vocabulary logits:
+
+  valid set        M = {n : t_n != ignore_index and 0 <= t_n < V},  Nv = |M|
+  logits           s[n, v] = sum_d H[n, d] * W[v, d]
+  log-sum-exp      lse_n = m_n + ln sum_v exp(s[n, v] - m_n),  m_n = max_v s[n, v]
+  per-row loss     l_n = lse_n - s[n, t_n]                        (n in M)
+  reduction        L = (1 / Nv) sum_{n in M} l_n   ("mean")  or  sum_{n in M} l_n  ("sum")
+  softmax grad     G[n, v] = c * (exp(s[n, v] - lse_n) - [v == t_n])  (n in M; 0 otherwise)
+                   c = g / Nv for "mean", c = g for "sum"; g = upstream gradient of L
+  gradients        dH = G W,  dW = G^T H
+
+Readings where the paper is silent (each is also listed in the design notes):
+* "mean" divides by the valid-token count of this call; Nv = 0 gives L = 0 and
+  zero gradients (not NaN);
+* a target outside [0, V) that is not ignore_index is treated as ignored and
+  raises status bit 0;
+* lse is reported for valid rows only and is 0.0 on every other row;
+* targets are already aligned with H (no next-token shift inside the loss).
+
+Pins: the oracle is checked (``tests/test_oracle.py``) against closed forms
+(zero weights give L = ln V; a geometric-series vocabulary; V = 1 and V = 2),
+central finite differences, an independent library routine (torch CPU float64
+cross-entropy with autograd), and invariants (softmax-grad rows sum to zero,
+masked rows contribute nothing, shift and permutation invariance).
+"""
+from __future__ import annotations
+
+import numpy as np
+
+STATUS_TARGET_OUT_OF_RANGE = 1
+
+
+def bf16_to_f64(bits: np.ndarray) -> np.ndarray:
+    """Decode bf16 bit patterns (uint16) to float64; every bf16 value is exact in float64."""
+    b = np.asarray(bits, dtype=np.uint16)
+    return (b.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+def valid_rows(targets: np.ndarray, v: int, ignore_index: int = -100):
+    """Valid-row mask and status word (bit 0: some target outside [0, V) that is not ignored)."""
+    t = np.asarray(targets, dtype=np.int64)
+    ignored = t == ignore_index
+    bad = (~ignored) & ((t < 0) | (t >= v))
+    status = STATUS_TARGET_OUT_OF_RANGE if bad.any() else 0
+    return (~ignored) & (~bad), status
+
+
+def row_lse(h_rows: np.ndarray, w: np.ndarray) -> np.ndarray:
+    """lse_n = m_n + ln sum_v exp(s[n, v] - m_n) for the given float64 rows of H."""
+    s = h_rows @ w.T
+    m = s.max(axis=1)
+    return m + np.log(np.exp(s - m[:, None]).sum(axis=1))
+
+
+def scale_c(n_valid: int, reduction: str, grad: float) -> float:
+    """Scale of the softmax gradient: g / Nv for "mean", g for "sum" (0 when Nv = 0)."""
+    if reduction not in ("mean", "sum"):
+        raise ValueError(f"unknown reduction {reduction!r}")
+    if n_valid == 0:
+        return 0.0
+    return grad / n_valid if reduction == "mean" else grad
+
+
+def forward(h, w, targets, ignore_index=-100, reduction="mean", block=512):
+    """Loss, per-row lse (0 on non-valid rows), Nv and status, from float64 H [N, D] and W [V, D]."""
+    n, v = h.shape[0], w.shape[0]
+    ok, status = valid_rows(targets, v, ignore_index)
+    rows = np.nonzero(ok)[0]
+    t = np.asarray(targets, dtype=np.int64)
+    lse = np.zeros(n, dtype=np.float64)
+    per_row = np.zeros(n, dtype=np.float64)
+    for s0 in range(0, rows.size, block):
+        r = rows[s0:s0 + block]
+        s = h[r] @ w.T                                  # full-vocabulary logits of these rows
+        m = s.max(axis=1)
+        lse_r = m + np.log(np.exp(s - m[:, None]).sum(axis=1))
+        lse[r] = lse_r
+        per_row[r] = lse_r - s[np.arange(r.size), t[r]]
+    nv = int(rows.size)
+    if nv == 0:
+        loss = 0.0
+    elif reduction == "mean":
+        loss = per_row[rows].sum() / nv
+    elif reduction == "sum":
+        loss = per_row[rows].sum()
+    else:
+        raise ValueError(f"unknown reduction {reduction!r}")
+    return {"loss": float(loss), "lse": lse, "per_row": per_row, "n_valid": nv, "status": status}
+
+
+def softmax_grad_rows(h_rows, w, t_rows, c):
+    """G rows c * (softmax(s) - onehot(t)) for valid float64 rows of H."""
+    s = h_rows @ w.T
+    m = s.max(axis=1)
+    lse = m + np.log(np.exp(s - m[:, None]).sum(axis=1))
+    g = np.exp(s - lse[:, None])
+    g[np.arange(len(t_rows)), t_rows] -= 1.0
+    return c * g
+
+
+def backward(h, w, targets, ignore_index=-100, reduction="mean", grad=1.0, block=512):
+    """dH = G W and dW = G^T H with G the scaled softmax-minus-onehot of the valid rows."""
+    n, v = h.shape[0], w.shape[0]
+    ok, _ = valid_rows(targets, v, ignore_index)
+    rows = np.nonzero(ok)[0]
+    t = np.asarray(targets, dtype=np.int64)
+    c = scale_c(int(rows.size), reduction, grad)
+    dh = np.zeros_like(h)
+    dw = np.zeros_like(w)
+    for s0 in range(0, rows.size, block):
+        r = rows[s0:s0 + block]
+        g = softmax_grad_rows(h[r], w, t[r], c)
+        dh[r] = g @ w
+        dw += g.T @ h[r]
+    return {"dH": dh, "dW": dw}
+
+
+def lce(h_bits, w_bits, targets, ignore_index=-100, reduction="mean", grad=1.0):
+    """Whole objective from bf16 bit patterns: loss, lse, Nv, status, dH, dW (all float64)."""
+    h = bf16_to_f64(h_bits)
+    w = bf16_to_f64(w_bits)
+    out = forward(h, w, targets, ignore_index, reduction)
+    out.update(backward(h, w, targets, ignore_index, reduction, grad))
+    return out
+
+
+# ---- sampled outputs for full-size workloads -------------------------------------------------
+
+def lse_of_rows(h_bits, w_bits, rows, block=64):
+    """lse_n of the given rows (no masking logic: rows are taken as they are)."""
+    w = bf16_to_f64(w_bits)
+    out = np.empty(len(rows), dtype=np.float64)
+    for s0 in range(0, len(rows), block):
+        r = np.asarray(rows[s0:s0 + block])
+        out[s0:s0 + block] = row_lse(bf16_to_f64(h_bits[r]), w)
+    return out
+
+
+def dh_of_rows(h_bits, w_bits, targets, rows, n_valid, ignore_index=-100,
+               reduction="mean", grad=1.0):
+    """Rows of dH = G W; rows whose target is ignored or out of range are zero."""
+    w = bf16_to_f64(w_bits)
+    v = w.shape[0]
+    ok, _ = valid_rows(targets, v, ignore_index)
+    c = scale_c(n_valid, reduction, grad)
+    t = np.asarray(targets, dtype=np.int64)
+    out = np.zeros((len(rows), w.shape[1]), dtype=np.float64)
+    for i, r in enumerate(rows):
+        if ok[r]:
+            g = softmax_grad_rows(bf16_to_f64(h_bits[r:r + 1]), w, t[r:r + 1], c)
+            out[i] = (g @ w)[0]
+    return out
+
+
+def dw_of_rows(h_bits, w_bits, targets, vrows, lse_valid, ignore_index=-100,
+               reduction="mean", grad=1.0, block=4096):
+    """Rows of dW = G^T H for vocabulary ids ``vrows``; ``lse_valid`` is the oracle's lse vector."""
+    v = w_bits.shape[0]
+    ok, _ = valid_rows(targets, v, ignore_index)
+    rows = np.nonzero(ok)[0]
+    c = scale_c(int(rows.size), reduction, grad)
+    t = np.asarray(targets, dtype=np.int64)
+    wv = bf16_to_f64(w_bits[np.asarray(vrows)])                 # [k, D]
+    out = np.zeros((len(vrows), w_bits.shape[1]), dtype=np.float64)
+    for s0 in range(0, rows.size, block):
+        r = rows[s0:s0 + block]
+        hr = bf16_to_f64(h_bits[r])                            # [b, D]
+        p = np.exp(hr @ wv.T - lse_valid[r][:, None])          # softmax columns of these ids
+        p -= (t[r][:, None] == np.asarray(vrows)[None, :])
+        out += (c * p).T @ hr
+    return out

@@ -1,0 +1,193 @@
+"""Seeded synthetic inputs for the linear-cross-entropy (LCE) hot path.
+
+This module only *draws* inputs: hidden states H, the output-projection weight
+W and the target ids. It holds none of the objective's arithmetic, so both the
+HIP path and the CPU oracle can be fed from it without sharing any of the
+method's code.
+
+The five named workloads are vocabulary-head shapes of the models the paper
+fine-tunes (Sec. 3.2 model zoo, Tab. 1-2 and App. D): a tiny case that the
+oracle finishes in seconds, and Llama-3.2-1B, Llama-3.1-8B, Qwen2.5-7B
+(long sequence) and Llama-3.1-70B heads. The paper measures on Alpaca-style
+SFT data with real checkpoints (Sec. 4.3); neither is available here, and the
+LCE kernels only see shapes and value statistics, so seeded synthetic tensors
+with the same shapes stand in for them:
+
+* H ~ N(0, 1) rounded to bf16 (round-to-nearest-even), shape [N, D], row
+  n = b * seq + s;
+* W ~ N(0, sigma_w) rounded to bf16, shape [V, D] (``nn.Linear(D, V).weight``);
+* targets: uniform ids (tiny case) or a truncated Zipf law
+  P(id = k) ~ (k + 1)^-1.1 over the vocabulary (frequent ids low, as in BPE
+  vocabularies), drawn by inverse CDF;
+* a masked share of positions set to ``ignore_index`` (-100), standing in for
+  the prompt tokens that SFT masks: an exact count drawn uniformly without
+  replacement, or a contiguous prompt span at the start of every sequence.
+
+Every stream uses ``numpy.random.Generator(PCG64(SeedSequence([seed, case,
+stream])))`` so a (workload, seed) pair always gives the same bytes.
+"""
+from __future__ import annotations
+
+import dataclasses
+from typing import Optional
+
+import numpy as np
+
+IGNORE_INDEX = -100
+
+# RNG stream ids
+_S_H, _S_W, _S_T, _S_MASK = 0, 1, 2, 3
+
+
+@dataclasses.dataclass(frozen=True)
+class Workload:
+    """Shape and value recipe of one LCE input set."""
+
+    name: str
+    n: int                      # tokens = batch * seq
+    d: int                      # hidden size
+    v: int                      # vocabulary size
+    batch: int = 1
+    seq: int = 0                # 0 means n
+    sigma_w: float = 0.02
+    targets: str = "zipf"       # "zipf" | "uniform"
+    zipf_s: float = 1.1
+    mask_frac: float = 0.0      # share of positions set to ignore_index
+    mask_kind: str = "random"   # "random" | "prefix" (contiguous prompt span per sequence)
+    case_id: int = 0            # RNG domain separator
+
+    @property
+    def seq_len(self) -> int:
+        return self.seq if self.seq else self.n
+
+    def masked_count(self) -> int:
+        if self.mask_kind == "prefix":
+            return self.batch * int(round(self.mask_frac * self.seq_len))
+        return int(round(self.mask_frac * self.n))
+
+    def n_valid(self) -> int:
+        return self.n - self.masked_count()
+
+    def flops(self) -> float:
+        """Algorithmic multiply-add work of one fwd+bwd: 8 * Nv * D * V."""
+        return 8.0 * self.n_valid() * self.d * self.v
+
+
+# The five workloads, in order: tiny, Llama-3.2-1B, Llama-3.1-8B, Qwen2.5-7B, Llama-3.1-70B.
+WORKLOADS = {
+    "tiny": Workload("tiny", n=256, d=512, v=4096, targets="uniform",
+                     mask_frac=0.10, case_id=1),
+    "llama1b": Workload("llama1b", n=8192, d=2048, v=128256, batch=4, seq=2048,
+                        mask_frac=0.25, case_id=2),
+    "llama8b": Workload("llama8b", n=16384, d=4096, v=128256, batch=8, seq=2048,
+                        mask_frac=0.25, case_id=3),
+    "qwen7b": Workload("qwen7b", n=32768, d=3584, v=152064, batch=4, seq=8192,
+                       mask_frac=0.30, mask_kind="prefix", case_id=4),
+    "llama70b": Workload("llama70b", n=16384, d=8192, v=128256, batch=2, seq=8192,
+                         sigma_w=0.015, mask_frac=0.20, case_id=5),
+}
+
+
+def _rng(seed: int, case: int, stream: int) -> np.random.Generator:
+    return np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, case, stream])))
+
+
+def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
+    """Round float32 values to bfloat16 (nearest, ties to even); returns uint16 bit patterns."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    u = x.view(np.uint32)
+    out = np.empty(u.shape, dtype=np.uint16)
+    # process in slabs to bound the temporaries for billion-element weights
+    flat_u, flat_o = u.reshape(-1), out.reshape(-1)
+    step = 1 << 24
+    for s in range(0, flat_u.size, step):
+        b = flat_u[s:s + step].astype(np.uint64)
+        r = (b + 0x7FFF + ((b >> 16) & 1)) >> 16
+        nan = (b & 0x7FFFFFFF) > 0x7F800000
+        r = np.where(nan, (b >> 16) | 0x40, r)
+        flat_o[s:s + step] = r.astype(np.uint16)
+    return out
+
+
+def bf16_bits_to_f32(bits: np.ndarray) -> np.ndarray:
+    """Widen bf16 bit patterns to float32 (exact)."""
+    return (np.asarray(bits, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32)
+
+
+def draw_normal_bf16(rng: np.random.Generator, shape, sigma: float) -> np.ndarray:
+    x = rng.standard_normal(shape, dtype=np.float32)
+    if sigma != 1.0:
+        x *= np.float32(sigma)
+    return f32_to_bf16_bits(x)
+
+
+def draw_targets(rng: np.random.Generator, n: int, v: int, kind: str, zipf_s: float) -> np.ndarray:
+    if kind == "uniform":
+        return rng.integers(0, v, size=n, dtype=np.int64).astype(np.int32)
+    if kind == "zipf":
+        p = np.arange(1, v + 1, dtype=np.float64) ** (-zipf_s)
+        cdf = np.cumsum(p)
+        cdf /= cdf[-1]
+        u = rng.random(n)
+        t = np.searchsorted(cdf, u, side="right")
+        return np.minimum(t, v - 1).astype(np.int32)
+    raise ValueError(f"unknown target distribution {kind!r}")
+
+
+def apply_mask(rng: np.random.Generator, t: np.ndarray, w: Workload,
+               ignore_index: int = IGNORE_INDEX) -> np.ndarray:
+    t = t.copy()
+    if w.mask_frac <= 0:
+        return t
+    if w.mask_kind == "prefix":
+        span = int(round(w.mask_frac * w.seq_len))
+        for b in range(w.batch):
+            t[b * w.seq_len: b * w.seq_len + span] = ignore_index
+    elif w.mask_kind == "random":
+        k = w.masked_count()
+        pos = rng.choice(w.n, size=k, replace=False)
+        t[pos] = ignore_index
+    else:
+        raise ValueError(f"unknown mask kind {w.mask_kind!r}")
+    return t
+
+
+@dataclasses.dataclass
+class Inputs:
+    """One drawn input set: bf16 bit patterns for H and W, int32 targets."""
+
+    workload: Workload
+    seed: int
+    h_bits: np.ndarray          # uint16 [N, D]
+    w_bits: np.ndarray          # uint16 [V, D]
+    targets: np.ndarray         # int32 [N]
+    ignore_index: int = IGNORE_INDEX
+
+
+def generate(w: Workload, seed: int = 0, *, draw_w: bool = True,
+             ignore_index: int = IGNORE_INDEX) -> Inputs:
+    """Draw the inputs of workload ``w``; ``draw_w=False`` leaves W empty (for callers that only need H and targets)."""
+    h = draw_normal_bf16(_rng(seed, w.case_id, _S_H), (w.n, w.d), 1.0)
+    wb = (draw_normal_bf16(_rng(seed, w.case_id, _S_W), (w.v, w.d), w.sigma_w)
+          if draw_w else np.empty((0, w.d), np.uint16))
+    t = draw_targets(_rng(seed, w.case_id, _S_T), w.n, w.v, w.targets, w.zipf_s)
+    t = apply_mask(_rng(seed, w.case_id, _S_MASK), t, w, ignore_index)
+    return Inputs(w, seed, h, wb, t, ignore_index)
+
+
+def custom(n: int, d: int, v: int, *, seed: int = 0, sigma_w: float = 0.02,
+           sigma_h: float = 1.0, targets: str = "uniform", mask_frac: float = 0.1,
+           mask_kind: str = "random", batch: int = 1, case_id: int = 99,
+           ignore_index: int = IGNORE_INDEX, target_override: Optional[np.ndarray] = None) -> Inputs:
+    """Small ad-hoc input sets for edge cases (ragged tiles, tiny V, all-masked ...)."""
+    w = Workload(f"custom_{n}x{d}x{v}", n=n, d=d, v=v, batch=batch,
+                 seq=(n // batch if batch > 1 else 0), sigma_w=sigma_w,
+                 targets=targets, mask_frac=mask_frac, mask_kind=mask_kind, case_id=case_id)
+    h = draw_normal_bf16(_rng(seed, case_id, _S_H), (n, d), sigma_h)
+    wb = draw_normal_bf16(_rng(seed, case_id, _S_W), (v, d), sigma_w)
+    if target_override is not None:
+        t = np.asarray(target_override, dtype=np.int32).copy()
+    else:
+        t = draw_targets(_rng(seed, case_id, _S_T), n, v, targets, 1.1)
+        t = apply_mask(_rng(seed, case_id, _S_MASK), t, w, ignore_index)
+    return Inputs(w, seed, h, wb, t, ignore_index)
