@@ -1,0 +1,140 @@
+/*
+ * lce.h -- C ABI of the MI355X (gfx950) linear-cross-entropy library, liblce.so.
+ *
+ * The objective (paper Sec. 4.2, "Linear Cross-Entropy loss"): fuse the model's
+ * final output projection with the cross-entropy over the whole vocabulary,
+ * drop ignored target positions before the projection, and never hold the
+ * [tokens, vocab] logit matrix. It is a drop-in for the standard cross-entropy
+ * objective (Sec. 3.3), so for hidden states H [N, D], projection weight
+ * W [V, D] (the nn.Linear(D, V) weight) and targets t [N]:
+ *
+ *   M   = { n : t_n != ignore_index and 0 <= t_n < V },  Nv = |M|
+ *   s   = H W^T (per row; never stored whole)
+ *   lse_n = log sum_v exp(s[n, v]),   l_n = lse_n - s[n, t_n]            (n in M)
+ *   L   = (1/Nv) sum_{n in M} l_n  (mean)   or   sum_{n in M} l_n  (sum)
+ *   G   = c (softmax(s) - onehot(t)) on rows in M, 0 elsewhere;  c = g/Nv (mean) or g (sum)
+ *   dH  = G W,   dW = G^T H
+ *
+ * Conventions shared by every entry point
+ *  - All tensors are caller-owned device memory; the library never allocates
+ *    device memory and keeps no state between calls except the optional
+ *    kernel-timing records below.
+ *  - H, W, dH and dW are bf16 (stored as 16-bit words), row-major. H and W may
+ *    have a row stride (ld_h, ld_w, in elements, >= d, multiple of 8); dH and dW
+ *    are dense [N, D] and [V, D]. Every pointer must be 16-byte aligned; the
+ *    workspace must be 256-byte aligned. d must be a multiple of 8.
+ *  - targets are int32 (target_bytes = 4) or int64 (target_bytes = 8).
+ *  - Outputs must not alias inputs.
+ *  - Calls only enqueue work on `stream` (a hipStream_t; NULL = the default
+ *    stream): no host synchronisation and no allocation, so a forward/backward
+ *    pair can be captured in a HIP graph. The workspace may be reused as soon
+ *    as the stream has finished the call.
+ *  - Host-detectable errors (null pointers, bad sizes, misalignment, small
+ *    workspace) are returned before anything is launched. A failed launch
+ *    returns LCE_ERR_HIP. Bad target values are data, seen only on the device:
+ *    such rows are treated as ignored and bit 0 of *dev_status is set.
+ *  - Results are deterministic: the same inputs give the same bits on every run
+ *    (no atomics in any reduction; fixed summation orders).
+ */
+#ifndef LCE_H_
+#define LCE_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum lce_status {
+  LCE_OK = 0,
+  LCE_ERR_NULL = 1,         /* a required pointer is NULL */
+  LCE_ERR_SHAPE = 2,        /* n < 0, d < 1, v < 1, ld < d, or sizes beyond 32-bit offsets */
+  LCE_ERR_ALIGN = 3,        /* pointer, stride or workspace misaligned */
+  LCE_ERR_UNSUPPORTED = 4,  /* d % 8 != 0, unknown reduction or target width */
+  LCE_ERR_WORKSPACE = 5,    /* workspace smaller than lce_workspace_size() */
+  LCE_ERR_HIP = 6,          /* a HIP runtime call or kernel launch failed */
+  LCE_ERR_ARG = 7           /* other invalid argument */
+} lce_status_t;
+
+typedef enum lce_reduction {
+  LCE_REDUCE_MEAN = 0,      /* divide by the valid-token count Nv of this call */
+  LCE_REDUCE_SUM = 1
+} lce_reduction_t;
+
+/* Bit set in *dev_status by lce_forward when some target is neither ignore_index nor in [0, V). */
+#define LCE_STATUS_TARGET_OUT_OF_RANGE 1
+
+typedef struct lce_problem {
+  int64_t n;                /* tokens (rows of H, entries of targets) */
+  int64_t d;                /* hidden size (multiple of 8) */
+  int64_t v;                /* vocabulary size (rows of W), >= 1 */
+  int64_t ld_h;             /* row stride of H in elements; 0 means d */
+  int64_t ld_w;             /* row stride of W in elements; 0 means d */
+  int32_t ignore_index;     /* targets equal to this are ignored (e.g. -100) */
+  int32_t reduction;        /* lce_reduction_t */
+  int32_t target_bytes;     /* 4 (int32 targets) or 8 (int64 targets) */
+  int32_t reserved;         /* must be 0 */
+} lce_problem_t;
+
+/*
+ * Workspace sizes, in bytes, for lce_forward (*fwd_bytes) and lce_backward
+ * (*bwd_bytes). They grow as O(N*D + D*V_slab) with V_slab <= max(4096, 2*D)
+ * rounded to 256: never O(N*V). Either output pointer may be NULL.
+ */
+lce_status_t lce_workspace_size(const lce_problem_t* p, size_t* fwd_bytes, size_t* bwd_bytes);
+
+/*
+ * Forward pass (paper Sec. 4.2): computes the loss without materialising the
+ * logits. Outputs, all device memory:
+ *   loss        [1] fp32: L (mean or sum; 0 when Nv = 0)
+ *   lse         [N] fp32: lse_n for valid rows, 0.0 for ignored / bad rows;
+ *               keep it for lce_backward
+ *   n_valid     [1] int32: Nv
+ *   dev_status  [1] int32 or NULL: overwritten with status bits
+ *               (LCE_STATUS_TARGET_OUT_OF_RANGE)
+ */
+lce_status_t lce_forward(const lce_problem_t* p,
+                         const void* H, const void* W, const void* targets,
+                         float* loss, float* lse, int32_t* n_valid, int32_t* dev_status,
+                         void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Backward pass: recomputes the logits tile by tile, forms
+ * G = c (softmax - onehot) and writes both gradients.
+ *   lse         [N] fp32 from lce_forward on the same inputs
+ *   n_valid     [1] int32: the count that "mean" divides by (lce_forward's
+ *               n_valid on one device; a global count when the tokens of one
+ *               batch are spread over several calls)
+ *   grad_loss   [1] fp32: upstream gradient g of L (read on the device)
+ *   dH          [N, D] bf16, overwritten; rows of ignored tokens are +0.0
+ *   dW          [V, D] bf16, overwritten
+ */
+lce_status_t lce_backward(const lce_problem_t* p,
+                          const void* H, const void* W, const void* targets,
+                          const float* lse, const int32_t* n_valid, const float* grad_loss,
+                          void* dH, void* dW,
+                          void* workspace, size_t workspace_bytes, void* stream);
+
+/* Static, human-readable name of a status code. */
+const char* lce_status_string(lce_status_t s);
+
+/*
+ * Optional per-kernel timing, for profiling only. When enabled, every kernel
+ * launch of the calls above is bracketed by a pair of HIP events recorded on
+ * the caller's stream (up to a fixed pool of pairs per enable; later launches
+ * are not recorded). lce_timing_read waits for the recorded events and
+ * returns the summed milliseconds and the number of launches of kernel `k`
+ * (0 <= k < lce_timing_kernel_count()). Enabling resets the records. These
+ * calls create and destroy HIP events, so they are not for graph capture.
+ */
+lce_status_t lce_timing_enable(int on);
+int lce_timing_kernel_count(void);
+const char* lce_timing_kernel_name(int k);
+lce_status_t lce_timing_read(int k, double* total_ms, int64_t* launches);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LCE_H_ */

@@ -1,0 +1,132 @@
+"""ctypes binding of liblce.so: the C ABI of include/lce.h, same names, argument marshalling only.
+
+Every function here forwards plain integers (device pointers, sizes, a stream
+handle) to the library and turns a non-zero status into ``LceError``. Nothing
+is computed in Python. The library is loaded on first use from this package's
+directory; if it was not built, loading raises instead of falling back to
+anything else.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import threading
+
+LIB_NAME = "liblce.so"
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), LIB_NAME)
+
+LCE_OK = 0
+LCE_ERR_NULL = 1
+LCE_ERR_SHAPE = 2
+LCE_ERR_ALIGN = 3
+LCE_ERR_UNSUPPORTED = 4
+LCE_ERR_WORKSPACE = 5
+LCE_ERR_HIP = 6
+LCE_ERR_ARG = 7
+
+LCE_REDUCE_MEAN = 0
+LCE_REDUCE_SUM = 1
+LCE_STATUS_TARGET_OUT_OF_RANGE = 1
+
+REDUCTIONS = {"mean": LCE_REDUCE_MEAN, "sum": LCE_REDUCE_SUM}
+
+# every symbol include/lce.h declares
+EXPORTED = ("lce_workspace_size", "lce_forward", "lce_backward", "lce_status_string",
+            "lce_timing_enable", "lce_timing_kernel_count", "lce_timing_kernel_name",
+            "lce_timing_read")
+
+
+class LceError(RuntimeError):
+    def __init__(self, code: int, where: str):
+        self.code = code
+        super().__init__(f"{where}: {lce_status_string(code)} (status {code})")
+
+
+class LceProblem(ctypes.Structure):
+    _fields_ = [("n", ctypes.c_int64), ("d", ctypes.c_int64), ("v", ctypes.c_int64),
+                ("ld_h", ctypes.c_int64), ("ld_w", ctypes.c_int64),
+                ("ignore_index", ctypes.c_int32), ("reduction", ctypes.c_int32),
+                ("target_bytes", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+
+def problem(n: int, d: int, v: int, *, ld_h: int = 0, ld_w: int = 0, ignore_index: int = -100,
+            reduction: str | int = "mean", target_bytes: int = 4) -> LceProblem:
+    red = REDUCTIONS[reduction] if isinstance(reduction, str) else int(reduction)
+    return LceProblem(n, d, v, ld_h, ld_w, ignore_index, red, target_bytes, 0)
+
+
+_lib = None
+_lock = threading.Lock()
+
+
+def load() -> ctypes.CDLL:
+    """Load liblce.so once; raise if it is missing (there is no other implementation)."""
+    global _lib
+    with _lock:
+        if _lib is not None:
+            return _lib
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built; run `python -c 'import __graft_entry__ as g; "
+                               f"g.build()'` from the repository root")
+        lib = ctypes.CDLL(LIB_PATH)
+        P = ctypes.POINTER(LceProblem)
+        vp, sz = ctypes.c_void_p, ctypes.c_size_t
+        lib.lce_workspace_size.argtypes = [P, ctypes.POINTER(sz), ctypes.POINTER(sz)]
+        lib.lce_forward.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+        lib.lce_backward.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+        lib.lce_status_string.argtypes = [ctypes.c_int]
+        lib.lce_status_string.restype = ctypes.c_char_p
+        lib.lce_timing_enable.argtypes = [ctypes.c_int]
+        lib.lce_timing_kernel_count.argtypes = []
+        lib.lce_timing_kernel_name.argtypes = [ctypes.c_int]
+        lib.lce_timing_kernel_name.restype = ctypes.c_char_p
+        lib.lce_timing_read.argtypes = [ctypes.c_int, ctypes.POINTER(ctypes.c_double),
+                                        ctypes.POINTER(ctypes.c_int64)]
+        for name in ("lce_workspace_size", "lce_forward", "lce_backward", "lce_timing_enable",
+                     "lce_timing_read", "lce_timing_kernel_count"):
+            getattr(lib, name).restype = ctypes.c_int
+        _lib = lib
+        return lib
+
+
+def _check(code: int, where: str) -> None:
+    if code != LCE_OK:
+        raise LceError(code, where)
+
+
+def lce_status_string(code: int) -> str:
+    return load().lce_status_string(int(code)).decode()
+
+
+def lce_workspace_size(p: LceProblem) -> tuple[int, int]:
+    f, b = ctypes.c_size_t(0), ctypes.c_size_t(0)
+    _check(load().lce_workspace_size(ctypes.byref(p), ctypes.byref(f), ctypes.byref(b)),
+           "lce_workspace_size")
+    return f.value, b.value
+
+
+def lce_forward(p: LceProblem, H: int, W: int, targets: int, loss: int, lse: int, n_valid: int,
+                dev_status: int, workspace: int, workspace_bytes: int, stream: int) -> None:
+    _check(load().lce_forward(ctypes.byref(p), H, W, targets, loss, lse, n_valid, dev_status or None,
+                              workspace, workspace_bytes, stream or None), "lce_forward")
+
+
+def lce_backward(p: LceProblem, H: int, W: int, targets: int, lse: int, n_valid: int, grad_loss: int,
+                 dH: int, dW: int, workspace: int, workspace_bytes: int, stream: int) -> None:
+    _check(load().lce_backward(ctypes.byref(p), H, W, targets, lse, n_valid, grad_loss, dH, dW,
+                               workspace, workspace_bytes, stream or None), "lce_backward")
+
+
+def lce_timing_enable(on: bool) -> None:
+    _check(load().lce_timing_enable(1 if on else 0), "lce_timing_enable")
+
+
+def lce_timing_kernel_names() -> list[str]:
+    lib = load()
+    return [lib.lce_timing_kernel_name(k).decode() for k in range(lib.lce_timing_kernel_count())]
+
+
+def lce_timing_read(k: int) -> tuple[float, int]:
+    ms, cnt = ctypes.c_double(0.0), ctypes.c_int64(0)
+    _check(load().lce_timing_read(k, ctypes.byref(ms), ctypes.byref(cnt)), "lce_timing_read")
+    return ms.value, cnt.value

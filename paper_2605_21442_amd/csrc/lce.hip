@@ -1,0 +1,898 @@
+// liblce: linear-cross-entropy (LCE) forward and backward for MI355X (gfx950).
+//
+// The objective is the paper's Linear Cross-Entropy loss (Sec. 4.2): the final
+// output projection H W^T is fused with the cross-entropy over the whole
+// vocabulary, ignored targets are dropped before the projection, and the dense
+// [tokens, vocab] logits never exist. The result equals the standard
+// cross-entropy (Sec. 3.3). The ABI, its conventions and its error codes are
+// documented in include/lce.h.
+//
+// Path (all kernels enqueue on the caller's stream, no host synchronisation):
+//   forward : compact -> fwd_stats (bf16 MFMA tiles of S^T = W H_valid^T with an
+//             online max / sum-exp epilogue) -> combine (merge partials, target
+//             logit, per-row loss) -> loss (fixed-order reduction)
+//   backward: compact -> gather/transpose H_valid -> per vocabulary slab:
+//             transpose W slab, G tile (recompute S^T, G = c (softmax - onehot)),
+//             dW slab = G^T H_valid, dH32 (+)= G W_slab -> finalise dH
+//
+// Every contraction is a "both operands K-contiguous" product C = A B^T run by
+// one MFMA main loop: 256x256 output tiles, 4 waves of 128x128, bf16
+// v_mfma_f32_32x32x16 with fp32 accumulation, K staged through LDS in 64-wide
+// slices (double-buffered, XOR-swizzled 16-byte chunks).
+
+#include <hip/hip_runtime.h>
+
+#include <math.h>
+#include <stdint.h>
+#include <string.h>
+
+#include <mutex>
+#include <vector>
+
+#include "lce.h"
+
+namespace {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef int i32x4_t __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
+
+constexpr int TILE = 256;         // output tile edge (rows of A and of B per workgroup)
+constexpr int BK = 64;            // K slice staged in LDS per step
+constexpr int NTHREADS = 256;     // 4 waves
+constexpr int LDS_STAGE = 65536;  // A slice (32 KB) + B slice (32 KB)
+constexpr int MAX_PARTS = 32;     // vocabulary partitions of the forward (x2 wave rows <= 64 lanes)
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+constexpr uint32_t kRsrcWord3 = 0x00020000u;  // gfx9 raw buffer: 32-bit data format
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint64_t bytes) {
+  uint32_t n = bytes > 0xFFFFFFFFull ? 0xFFFFFFFFu : (uint32_t)bytes;
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)n, (int)kRsrcWord3);
+}
+
+__device__ __forceinline__ float bf16_to_f32(uint32_t bits16) { return __uint_as_float(bits16 << 16); }
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  __bf16 a = (__bf16)lo, b = (__bf16)hi;
+  return (uint32_t)__builtin_bit_cast(uint16_t, a) | ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
+}
+
+__device__ __forceinline__ uint16_t to_bf16(float x) { return __builtin_bit_cast(uint16_t, (__bf16)x); }
+
+__device__ __forceinline__ int64_t load_target(const void* t, int tbytes, int64_t i) {
+  return tbytes == 8 ? ((const int64_t*)t)[i] : (int64_t)((const int32_t*)t)[i];
+}
+
+__device__ __forceinline__ float wave_sum(float x) {
+  for (int m = 32; m >= 1; m >>= 1) x += __shfl_xor(x, m);
+  return x;
+}
+__device__ __forceinline__ float wave_max(float x) {
+  for (int m = 32; m >= 1; m >>= 1) x = fmaxf(x, __shfl_xor(x, m));
+  return x;
+}
+
+// ---------------------------------------------------------------------------------------------
+// MFMA main loop: acc[bi][bj] (+)= A[256 x K] * B[256 x K]^T for this workgroup's tile.
+//
+// Thread t stages rows (t >> 3) + 32 i (i = 0..7) of both operands, 16-byte chunk (t & 7) of the
+// current 64-wide K slice. In LDS a row is 128 bytes; chunk c of row r sits at position
+// c ^ (r & 7) so that the 32 rows one MFMA operand read touches spread over all banks.
+// Wave w = 2 wr + wc owns output rows wr*128.. and columns wc*128.. of the tile:
+// acc[bi][bj] holds the 32x32 block (bi, bj); lane l, register r of a block is
+// row 8 (r / 4) + 4 (l / 32) + r % 4, column l % 32.
+// aoff/boff are byte offsets (row start + chunk) into the buffer resources; K is a multiple of 8.
+// ---------------------------------------------------------------------------------------------
+__device__ __forceinline__ void mma_mainloop(f32x16_t (&acc)[4][4],
+                                             __amdgpu_buffer_rsrc_t ra, const uint32_t (&aoff)[8],
+                                             __amdgpu_buffer_rsrc_t rb, const uint32_t (&boff)[8],
+                                             int K, char* smem) {
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int wr = wave >> 1, wc = wave & 1;
+  const int chunk = tid & 7;
+  const uint32_t wofs = (uint32_t)((tid >> 3) * 128 + ((chunk ^ ((tid >> 3) & 7)) * 16));
+  const uint32_t abase = (uint32_t)((wr * 128 + (lane & 31)) * 128);
+  const uint32_t bbase = (uint32_t)((wc * 128 + (lane & 31)) * 128) + 32768u;
+  uint32_t kso[4];
+#pragma unroll
+  for (int ks = 0; ks < 4; ++ks) kso[ks] = (uint32_t)((((ks * 2) + (lane >> 5)) ^ (lane & 7)) * 16);
+
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = (f32x16_t){};
+
+  const int nk = (K + BK - 1) / BK;
+  if (nk <= 0) return;
+
+  i32x4_t sa[8], sb[8];
+  auto gload = [&](int kt) {
+    const int k0 = kt * BK;
+    const bool ok = (k0 + chunk * 8) < K;
+    const int kb = k0 * 2;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      sa[i] = ok ? __builtin_amdgcn_raw_buffer_load_b128(ra, (int)aoff[i], kb, 0) : (i32x4_t){};
+      sb[i] = ok ? __builtin_amdgcn_raw_buffer_load_b128(rb, (int)boff[i], kb, 0) : (i32x4_t){};
+    }
+  };
+  auto lstore = [&](int buf) {
+    char* base = smem + buf * LDS_STAGE;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      *reinterpret_cast<i32x4_t*>(base + wofs + i * 4096) = sa[i];
+      *reinterpret_cast<i32x4_t*>(base + 32768 + wofs + i * 4096) = sb[i];
+    }
+  };
+
+  gload(0);
+  lstore(0);
+  __syncthreads();
+  for (int kt = 0; kt < nk; ++kt) {
+    const int cur = kt & 1;
+    const char* buf = smem + cur * LDS_STAGE;
+    if (kt + 1 < nk) gload(kt + 1);
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      bf16x8_t a[4], b[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) a[i] = *reinterpret_cast<const bf16x8_t*>(buf + abase + i * 4096 + kso[ks]);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) b[j] = *reinterpret_cast<const bf16x8_t*>(buf + bbase + j * 4096 + kso[ks]);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+    }
+    if (kt + 1 < nk) lstore(cur ^ 1);
+    __syncthreads();
+  }
+}
+
+// Byte offsets of this thread's 8 staged rows for a dense operand whose rows
+// [row0, row0 + 256) are wanted; rows at or beyond `rows` are clamped to the last one.
+__device__ __forceinline__ void dense_offsets(uint32_t (&off)[8], int rows_left, int64_t ld) {
+  const int tid = threadIdx.x;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    int r = (tid >> 3) + 32 * i;
+    r = r < rows_left ? r : rows_left - 1;
+    off[i] = (uint32_t)((int64_t)r * ld * 2 + (tid & 7) * 16);
+  }
+}
+
+// Same for rows gathered through the compacted valid-row list idx[0..nv).
+__device__ __forceinline__ void gather_offsets(uint32_t (&off)[8], const int* idx, int n0, int nv, int64_t ld) {
+  const int tid = threadIdx.x;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    int r = n0 + (tid >> 3) + 32 * i;
+    r = r < nv ? r : nv - 1;
+    off[i] = (uint32_t)((int64_t)idx[r] * ld * 2 + (tid & 7) * 16);
+  }
+}
+
+// ---------------------------------------------------------------------------------------------
+// K1: valid-row compaction ("masks ignored tokens before projection", Sec. 4.2).
+// idx[0..Nv) = ascending rows whose target is in [0, V); pos[n] = its index there or -1.
+// One workgroup; thread t owns a contiguous run of rows, so idx comes out sorted.
+// ---------------------------------------------------------------------------------------------
+__global__ __launch_bounds__(1024) void k_compact(const void* targets, int tbytes, int64_t n, int64_t v,
+                                                  int ignore, int* idx, int* pos, int* nv_ws,
+                                                  int* nv_user, int* status, float* lse_zero) {
+  __shared__ int scan[1024];
+  __shared__ int bad_any;
+  const int t = threadIdx.x;
+  const int64_t per = (n + 1023) / 1024;
+  const int64_t beg = t * per < n ? t * per : n;
+  const int64_t end = beg + per < n ? beg + per : n;
+  if (t == 0) bad_any = 0;
+  int cnt = 0, bad = 0;
+  for (int64_t i = beg; i < end; ++i) {
+    const int64_t tg = load_target(targets, tbytes, i);
+    const bool ign = tg == (int64_t)ignore;
+    const bool ok = !ign && tg >= 0 && tg < v;
+    cnt += ok;
+    bad |= (!ign && !ok);
+  }
+  scan[t] = cnt;
+  __syncthreads();
+  if (bad) bad_any = 1;  // benign same-value race
+  for (int off = 1; off < 1024; off <<= 1) {
+    const int x = t >= off ? scan[t - off] : 0;
+    __syncthreads();
+    scan[t] += x;
+    __syncthreads();
+  }
+  int o = scan[t] - cnt;
+  for (int64_t i = beg; i < end; ++i) {
+    const int64_t tg = load_target(targets, tbytes, i);
+    const bool ok = tg != (int64_t)ignore && tg >= 0 && tg < v;
+    if (ok) {
+      idx[o] = (int)i;
+      pos[i] = o;
+      ++o;
+    } else {
+      pos[i] = -1;
+      if (lse_zero) lse_zero[i] = 0.0f;
+    }
+  }
+  if (t == 1023) {
+    *nv_ws = scan[1023];
+    if (nv_user) *nv_user = scan[1023];
+  }
+  __syncthreads();
+  if (t == 0 && status) *status = bad_any ? LCE_STATUS_TARGET_OUT_OF_RANGE : 0;
+}
+
+// ---------------------------------------------------------------------------------------------
+// K2: forward statistics. Workgroup (token tile nt, vocabulary partition p) walks the partition's
+// 256-wide vocabulary tiles; per tile it computes S^T = W_tile H_valid^T (so a token's logits run
+// down a lane's registers) and folds them into a running (max, sum of exp) per token and lane.
+// At the end the two lane halves are merged and each wave row writes one partial pair per token
+// (in log2 units): part[(2 p + wave_row) * npad + token].
+// ---------------------------------------------------------------------------------------------
+__global__ __launch_bounds__(NTHREADS, 1) void k_fwd_stats(const uint16_t* __restrict__ W, int64_t ldw, int v,
+                                                           const uint16_t* __restrict__ H, int64_t ldh, int64_t n,
+                                                           const int* __restrict__ idx, const int* __restrict__ nv_ptr,
+                                                           int d, int nparts, int nt_max, int vt_count,
+                                                           float* __restrict__ part_m, float* __restrict__ part_s,
+                                                           int npad) {
+  __shared__ __attribute__((aligned(16))) char smem[2 * LDS_STAGE];
+  const int nt = blockIdx.x % nt_max, p = blockIdx.x / nt_max;
+  const int nv = *nv_ptr;
+  const int n0 = nt * TILE;
+  if (n0 >= nv) return;
+  const int vt0 = (int)((int64_t)p * vt_count / nparts), vt1 = (int)((int64_t)(p + 1) * vt_count / nparts);
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, wr = wave >> 1, wc = wave & 1;
+  __amdgpu_buffer_rsrc_t rb = make_rsrc(H, (uint64_t)n * ldh * 2);
+  uint32_t boff[8];
+  gather_offsets(boff, idx, n0, nv, ldh);
+
+  float m2[4], ss[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) { m2[j] = -INFINITY; ss[j] = 0.f; }
+
+  f32x16_t acc[4][4];
+  for (int vt = vt0; vt < vt1; ++vt) {
+    const int v0 = vt * TILE;
+    const int vleft = v - v0;
+    __amdgpu_buffer_rsrc_t ra = make_rsrc(W + (int64_t)v0 * ldw, (uint64_t)vleft * ldw * 2);
+    uint32_t aoff[8];
+    dense_offsets(aoff, vleft, ldw);
+    mma_mainloop(acc, ra, aoff, rb, boff, d, smem);
+
+    // rows (vocabulary ids) of this lane: v0 + wr*128 + 32 bi + 8 (r/4) + 4 (lane/32) + r%4
+    const int vb = wr * 128 + (lane >> 5) * 4;
+    const bool ragged = vleft < TILE;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      float mx = -INFINITY;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          if (ragged && (vb + i * 32 + (r >> 2) * 8 + (r & 3)) >= vleft) acc[i][j][r] = -INFINITY;
+          mx = fmaxf(mx, acc[i][j][r]);
+        }
+      const float nm = fmaxf(m2[j], mx * kLog2e);
+      if (nm == -INFINITY) continue;
+      float s = 0.f;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) s += __builtin_amdgcn_exp2f(fmaf(acc[i][j][r], kLog2e, -nm));
+      ss[j] = (m2[j] == -INFINITY ? 0.f : ss[j] * __builtin_amdgcn_exp2f(m2[j] - nm)) + s;
+      m2[j] = nm;
+    }
+  }
+  // merge the two lane halves (disjoint vocabulary rows), then write this wave row's partial
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const float om = __shfl_xor(m2[j], 32), os = __shfl_xor(ss[j], 32);
+    const float nm = fmaxf(m2[j], om);
+    float s = 0.f;
+    if (nm != -INFINITY) {
+      s = (m2[j] == -INFINITY ? 0.f : ss[j] * __builtin_amdgcn_exp2f(m2[j] - nm)) +
+          (om == -INFINITY ? 0.f : os * __builtin_amdgcn_exp2f(om - nm));
+    }
+    const int tok = n0 + wc * 128 + j * 32 + (lane & 31);
+    if (lane < 32 && tok < nv) {
+      const int64_t o = (int64_t)(2 * p + wr) * npad + tok;
+      part_m[o] = nm;
+      part_s[o] = s;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------------------------
+// K3: per valid token: merge the vocabulary partials into lse, take the target logit
+// s[n, t_n] = H[n] . W[t_n] in fp32, and the per-row loss l_n = lse_n - s[n, t_n].
+// One wave per token; all reductions use a fixed butterfly order.
+// ---------------------------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_combine(const uint16_t* __restrict__ H, int64_t ldh,
+                                                 const uint16_t* __restrict__ W, int64_t ldw,
+                                                 const void* targets, int tbytes,
+                                                 const int* __restrict__ idx, const int* __restrict__ nv_ptr,
+                                                 int d, int nparts2, const float* __restrict__ part_m,
+                                                 const float* __restrict__ part_s, int npad,
+                                                 float* __restrict__ lse_out, float* __restrict__ terms) {
+  const int lane = threadIdx.x & 63;
+  const int i = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int nv = *nv_ptr;
+  if (i >= nv) return;
+  const int row = idx[i];
+  const int64_t tg = load_target(targets, tbytes, row);
+  const uint4* hr = reinterpret_cast<const uint4*>(H + (int64_t)row * ldh);
+  const uint4* wt = reinterpret_cast<const uint4*>(W + tg * ldw);
+  float dot = 0.f;
+  for (int c = lane; c < d / 8; c += 64) {
+    const uint4 a = hr[c], b = wt[c];
+    const uint32_t av[4] = {a.x, a.y, a.z, a.w}, bv[4] = {b.x, b.y, b.z, b.w};
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      dot = fmaf(bf16_to_f32(av[q] & 0xFFFF), bf16_to_f32(bv[q] & 0xFFFF), dot);
+      dot = fmaf(bf16_to_f32(av[q] >> 16), bf16_to_f32(bv[q] >> 16), dot);
+    }
+  }
+  dot = wave_sum(dot);
+  const float m = lane < nparts2 ? part_m[(int64_t)lane * npad + i] : -INFINITY;
+  const float s = lane < nparts2 ? part_s[(int64_t)lane * npad + i] : 0.f;
+  const float mm = wave_max(m);
+  const float e = (m == -INFINITY) ? 0.f : s * exp2f(m - mm);
+  const float se = wave_sum(e);
+  const float lse = (mm + log2f(se)) * kLn2;
+  if (lane == 0) {
+    lse_out[row] = lse;
+    terms[i] = lse - dot;
+  }
+}
+
+// K3b: loss = sum or mean of the per-row terms, fixed-order fp64 tree.
+__global__ __launch_bounds__(1024) void k_loss(const float* __restrict__ terms, const int* __restrict__ nv_ptr,
+                                               int reduction, float* __restrict__ loss) {
+  __shared__ double red[1024];
+  const int t = threadIdx.x;
+  const int nv = *nv_ptr;
+  double s = 0.0;
+  for (int i = t; i < nv; i += 1024) s += (double)terms[i];
+  red[t] = s;
+  __syncthreads();
+  for (int w = 512; w > 0; w >>= 1) {
+    if (t < w) red[t] += red[t + w];
+    __syncthreads();
+  }
+  if (t == 0) {
+    double r = red[0];
+    if (nv == 0) r = 0.0;
+    else if (reduction == LCE_REDUCE_MEAN) r /= (double)nv;
+    *loss = (float)r;
+  }
+}
+
+__global__ void k_fwd_empty(float* loss, int* nv_user, int* status) {
+  if (threadIdx.x == 0) {
+    *loss = 0.f;
+    *nv_user = 0;
+    if (status) *status = 0;
+  }
+}
+
+// ---------------------------------------------------------------------------------------------
+// Backward helpers
+// ---------------------------------------------------------------------------------------------
+
+// out[c][r] = src row (idx ? idx[r] : r0 + r) column c, for r < rows_ok; 0 for rows_ok <= r < rows_out.
+// 64x64 tiles through LDS. rows_ok comes from *cnt_ptr when given (device count), else cnt.
+__global__ __launch_bounds__(256) void k_transpose(const uint16_t* __restrict__ src, int64_t lds_, const int* __restrict__ idx,
+                                                   int64_t r0, const int* __restrict__ cnt_ptr, int cnt, int cols,
+                                                   uint16_t* __restrict__ out, int64_t ldo, int rows_out_pad64) {
+  __shared__ uint16_t tile[64][64 + 2];
+  const int rows_ok = cnt_ptr ? *cnt_ptr : cnt;
+  const int rt = blockIdx.x, ct = blockIdx.y;
+  const int rbeg = rt * 64, cbeg = ct * 64;
+  const int rlim = cnt_ptr ? ((rows_ok + 63) / 64) * 64 : rows_out_pad64;
+  if (rbeg >= rlim) return;
+  const int t = threadIdx.x;
+  {  // load: thread t -> row t/4, 16 columns starting at (t%4)*16
+    const int r = rbeg + t / 4;
+    const int c0 = cbeg + (t % 4) * 16;
+    uint16_t vals[16];
+#pragma unroll
+    for (int q = 0; q < 16; ++q) vals[q] = 0;
+    if (r < rows_ok) {
+      const int64_t srow = idx ? (int64_t)idx[r] : r0 + r;
+      const uint16_t* p = src + srow * lds_;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        if (c0 + h * 8 < cols) {
+          const uint4 u = *reinterpret_cast<const uint4*>(p + c0 + h * 8);
+          const uint32_t w4[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            vals[h * 8 + 2 * q] = (uint16_t)(w4[q] & 0xFFFF);
+            vals[h * 8 + 2 * q + 1] = (uint16_t)(w4[q] >> 16);
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < 16; ++q) tile[t / 4][(t % 4) * 16 + q] = vals[q];
+  }
+  __syncthreads();
+  {  // store: thread t -> output row (column of src) t/4, 16 consecutive source rows
+    const int c = cbeg + t / 4;
+    const int rr = (t % 4) * 16;
+    if (c < cols) {
+      uint32_t w8[8];
+#pragma unroll
+      for (int q = 0; q < 8; ++q)
+        w8[q] = (uint32_t)tile[rr + 2 * q][t / 4] | ((uint32_t)tile[rr + 2 * q + 1][t / 4] << 16);
+      uint4* o = reinterpret_cast<uint4*>(out + (int64_t)c * ldo + rbeg + rr);
+      o[0] = make_uint4(w8[0], w8[1], w8[2], w8[3]);
+      o[1] = make_uint4(w8[4], w8[5], w8[6], w8[7]);
+    }
+  }
+}
+
+// scale c = g / n_norm (mean) or g (sum); 0 when the count is 0
+__device__ __forceinline__ float grad_scale(const float* grad, const int* n_norm, int reduction) {
+  const float g = *grad;
+  if (reduction == LCE_REDUCE_SUM) return g;
+  const int nn = *n_norm;
+  return nn > 0 ? g / (float)nn : 0.f;
+}
+
+// ---------------------------------------------------------------------------------------------
+// K4: softmax-gradient tile for one vocabulary slab. Tile (vocabulary tile tm, token tile tn) of
+// S^T = W_slab H_valid^T is recomputed and turned into G = c (exp(s - lse) - onehot), rounded to
+// bf16 and written twice: G[token][v] (row stride vc) and Gt[v][token] (row stride ldt).
+// Entries outside the valid tokens / slab columns are written as zeros where the later
+// contractions read them (K padding), so those loops need no masking.
+// ---------------------------------------------------------------------------------------------
+__global__ __launch_bounds__(NTHREADS, 1) void k_bwd_g(const uint16_t* __restrict__ W, int64_t ldw, int64_t v0, int vs,
+                                                       const uint16_t* __restrict__ H, int64_t ldh, int64_t n,
+                                                       const void* targets, int tbytes,
+                                                       const int* __restrict__ idx, const int* __restrict__ nv_ptr,
+                                                       const float* __restrict__ lse, const float* __restrict__ grad,
+                                                       const int* __restrict__ n_norm, int reduction, int d, int tm_count,
+                                                       uint16_t* __restrict__ G, int vc, uint16_t* __restrict__ Gt, int ldt) {
+  __shared__ __attribute__((aligned(16))) char smem[2 * LDS_STAGE];
+  const int tm = blockIdx.x % tm_count, tn = blockIdx.x / tm_count;
+  const int nv = *nv_ptr;
+  const int n0 = tn * TILE;
+  if (n0 >= nv) return;
+  const int vt0 = tm * TILE;                 // slab-relative
+  const int vleft = vs - vt0;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, wr = wave >> 1, wc = wave & 1;
+
+  __amdgpu_buffer_rsrc_t ra = make_rsrc(W + (v0 + vt0) * ldw, (uint64_t)vleft * ldw * 2);
+  __amdgpu_buffer_rsrc_t rb = make_rsrc(H, (uint64_t)n * ldh * 2);
+  uint32_t aoff[8], boff[8];
+  dense_offsets(aoff, vleft, ldw);
+  gather_offsets(boff, idx, n0, nv, ldh);
+  f32x16_t acc[4][4];
+  mma_mainloop(acc, ra, aoff, rb, boff, d, smem);
+
+  const float c = grad_scale(grad, n_norm, reduction);
+  int tok[4], tgt[4];
+  float l2[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    tok[j] = n0 + wc * 128 + j * 32 + (lane & 31);
+    if (tok[j] < nv) {
+      const int row = idx[tok[j]];
+      l2[j] = lse[row] * kLog2e;
+      tgt[j] = (int)(load_target(targets, tbytes, row) - v0) - vt0;   // tile-relative target row
+    } else {
+      l2[j] = 0.f;
+      tgt[j] = -1;
+    }
+  }
+  const int vb = wr * 128 + (lane >> 5) * 4;  // tile-relative vocabulary row base of this lane
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const bool tok_ok = tok[j] < nv;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int vr = vb + i * 32 + (r >> 2) * 8 + (r & 3);
+        float g = 0.f;
+        if (tok_ok && vr < vleft) {
+          g = c * __builtin_amdgcn_exp2f(fmaf(acc[i][j][r], kLog2e, -l2[j]));
+          if (vr == tgt[j]) g -= c;
+        }
+        acc[i][j][r] = g;
+      }
+    // G[token][v]: 4 consecutive v per register group -> 8-byte stores
+    if (tok_ok) {
+      uint16_t* grow = G + (int64_t)tok[j] * vc + vt0;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int vr = vb + i * 32 + q * 8;
+          u32x2_t pk;
+          pk.x = pack_bf16x2(acc[i][j][q * 4 + 0], acc[i][j][q * 4 + 1]);
+          pk.y = pack_bf16x2(acc[i][j][q * 4 + 2], acc[i][j][q * 4 + 3]);
+          *reinterpret_cast<u32x2_t*>(grow + vr) = pk;
+        }
+    }
+    // Gt[v][token]: lanes hold consecutive tokens -> 2-byte stores, 64 contiguous bytes per row
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int vr = vb + i * 32 + (r >> 2) * 8 + (r & 3);
+        if (vr < vleft) Gt[(int64_t)(vt0 + vr) * ldt + tok[j]] = to_bf16(acc[i][j][r]);
+      }
+  }
+}
+
+// K5: dW[v0 + m][dd] = sum_k Gt[m][k] Hvt[dd][k] over k < round_up(Nv, 64), written once in bf16.
+__global__ __launch_bounds__(NTHREADS, 1) void k_bwd_dw(const uint16_t* __restrict__ Gt, int ldt, int vs,
+                                                        const uint16_t* __restrict__ Hvt, int d,
+                                                        const int* __restrict__ nv_ptr, int tm_count,
+                                                        uint16_t* __restrict__ dW, int64_t v0) {
+  __shared__ __attribute__((aligned(16))) char smem[2 * LDS_STAGE];
+  const int tm = blockIdx.x % tm_count, tn = blockIdx.x / tm_count;
+  const int m0 = tm * TILE, d0 = tn * TILE;
+  const int nv = *nv_ptr;
+  const int kpad = ((nv + BK - 1) / BK) * BK;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, wr = wave >> 1, wc = wave & 1;
+  __amdgpu_buffer_rsrc_t ra = make_rsrc(Gt + (int64_t)m0 * ldt, (uint64_t)(vs - m0) * ldt * 2);
+  __amdgpu_buffer_rsrc_t rb = make_rsrc(Hvt + (int64_t)d0 * ldt, (uint64_t)(d - d0) * ldt * 2);
+  uint32_t aoff[8], boff[8];
+  dense_offsets(aoff, vs - m0, ldt);
+  dense_offsets(boff, d - d0, ldt);
+  f32x16_t acc[4][4];
+  mma_mainloop(acc, ra, aoff, rb, boff, kpad, smem);
+  const int mb = m0 + wr * 128 + (lane >> 5) * 4;
+  const int dc = d0 + wc * 128 + (lane & 31);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int col = dc + j * 32;
+    if (col >= d) continue;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int m = mb + i * 32 + (r >> 2) * 8 + (r & 3);
+        if (m < vs) dW[(v0 + m) * d + col] = to_bf16(acc[i][j][r]);
+      }
+  }
+}
+
+// K6: dH32[m][dd] (+)= sum_k G[m][k] WsT[dd][k] over k < round_up(vs, 64); rows m < Nv.
+__global__ __launch_bounds__(NTHREADS, 1) void k_bwd_dh(const uint16_t* __restrict__ G, int vc, int kpad,
+                                                        const uint16_t* __restrict__ WsT, int d,
+                                                        const int* __restrict__ nv_ptr, int tm_count,
+                                                        float* __restrict__ dH32, int accumulate) {
+  __shared__ __attribute__((aligned(16))) char smem[2 * LDS_STAGE];
+  const int tm = blockIdx.x % tm_count, tn = blockIdx.x / tm_count;
+  const int m0 = tm * TILE, d0 = tn * TILE;
+  const int nv = *nv_ptr;
+  if (m0 >= nv) return;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, wr = wave >> 1, wc = wave & 1;
+  __amdgpu_buffer_rsrc_t ra = make_rsrc(G + (int64_t)m0 * vc, (uint64_t)(nv - m0) * vc * 2);
+  __amdgpu_buffer_rsrc_t rb = make_rsrc(WsT + (int64_t)d0 * vc, (uint64_t)(d - d0) * vc * 2);
+  uint32_t aoff[8], boff[8];
+  dense_offsets(aoff, nv - m0, vc);
+  dense_offsets(boff, d - d0, vc);
+  f32x16_t acc[4][4];
+  mma_mainloop(acc, ra, aoff, rb, boff, kpad, smem);
+  const int mb = m0 + wr * 128 + (lane >> 5) * 4;
+  const int dc = d0 + wc * 128 + (lane & 31);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int col = dc + j * 32;
+    if (col >= d) continue;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int m = mb + i * 32 + (r >> 2) * 8 + (r & 3);
+        if (m < nv) {
+          float* p = dH32 + (int64_t)m * d + col;
+          *p = accumulate ? *p + acc[i][j][r] : acc[i][j][r];
+        }
+      }
+  }
+}
+
+// K7: dH[row] = bf16(dH32[pos[row]]) for valid rows, +0.0 for the others. 8 elements per thread.
+__global__ __launch_bounds__(256) void k_dh_finalize(const float* __restrict__ dH32, const int* __restrict__ pos,
+                                                     int64_t n, int d, uint16_t* __restrict__ dH, int has_slabs) {
+  const int64_t e = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 8;
+  if (e >= n * d) return;
+  const int64_t row = e / d;
+  const int col = (int)(e - row * d);
+  const int p = pos[row];
+  uint4 out = make_uint4(0, 0, 0, 0);
+  if (p >= 0 && has_slabs) {
+    const float4 a = *reinterpret_cast<const float4*>(dH32 + (int64_t)p * d + col);
+    const float4 b = *reinterpret_cast<const float4*>(dH32 + (int64_t)p * d + col + 4);
+    out = make_uint4(pack_bf16x2(a.x, a.y), pack_bf16x2(a.z, a.w), pack_bf16x2(b.x, b.y), pack_bf16x2(b.z, b.w));
+  }
+  *reinterpret_cast<uint4*>(dH + e) = out;
+}
+
+__global__ __launch_bounds__(256) void k_zero16(uint4* __restrict__ p, int64_t n16) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < n16) p[i] = make_uint4(0, 0, 0, 0);
+}
+
+// ---------------------------------------------------------------------------------------------
+// Host side: validation, plan, workspace carve-up, launches, optional timing.
+// ---------------------------------------------------------------------------------------------
+enum KernelId { K_COMPACT = 0, K_FWD_STATS, K_COMBINE, K_LOSS, K_TRANSPOSE_H, K_TRANSPOSE_W, K_BWD_G,
+                K_BWD_DW, K_BWD_DH, K_DH_FINAL, K_MISC, K_COUNT };
+const char* const kKernelNames[K_COUNT] = {"compact", "fwd_stats", "combine", "loss", "transpose_h",
+                                           "transpose_w", "bwd_g", "bwd_dw", "bwd_dh", "dh_finalize", "misc"};
+
+struct Timing {
+  std::mutex mu;
+  bool on = false;
+  static constexpr int kPool = 8192;
+  std::vector<hipEvent_t> ev;   // 2 per record
+  std::vector<int> kind;
+  int used = 0;
+};
+Timing g_timing;
+
+struct Plan {
+  int64_t n, d, v, ldh, ldw, npad;
+  int nt_max, vt_count, nparts;
+  int64_t vc, nslab;
+  // workspace offsets
+  size_t o_idx, o_pos, o_nv, o_pm, o_ps, o_terms, fwd_bytes;
+  size_t o_hvt, o_g, o_gt, o_wst, o_dh32, bwd_bytes;
+};
+
+inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+
+lce_status_t make_plan(const lce_problem_t* p, Plan* pl) {
+  if (!p) return LCE_ERR_NULL;
+  if (p->reserved != 0) return LCE_ERR_ARG;
+  if (p->n < 0 || p->d < 1 || p->v < 1) return LCE_ERR_SHAPE;
+  if (p->d % 8 != 0) return LCE_ERR_UNSUPPORTED;
+  if (p->reduction != LCE_REDUCE_MEAN && p->reduction != LCE_REDUCE_SUM) return LCE_ERR_UNSUPPORTED;
+  if (p->target_bytes != 4 && p->target_bytes != 8) return LCE_ERR_UNSUPPORTED;
+  const int64_t ldh = p->ld_h ? p->ld_h : p->d, ldw = p->ld_w ? p->ld_w : p->d;
+  if (ldh < p->d || ldw < p->d) return LCE_ERR_SHAPE;
+  if (ldh % 8 != 0 || ldw % 8 != 0) return LCE_ERR_ALIGN;
+  // 32-bit limits: token / vocabulary indices, and byte offsets inside one buffer resource
+  if (p->n >= (int64_t)1 << 30 || p->v >= (int64_t)1 << 30 || p->d >= (int64_t)1 << 20) return LCE_ERR_SHAPE;
+  if ((uint64_t)p->n * ldh * 2 > 0xFFFFFFFFull) return LCE_ERR_SHAPE;
+  if ((uint64_t)TILE * ldw * 2 > 0xFFFFFFFFull) return LCE_ERR_SHAPE;
+  pl->n = p->n; pl->d = p->d; pl->v = p->v; pl->ldh = ldh; pl->ldw = ldw;
+  pl->npad = round_up(p->n > 0 ? p->n : 1, TILE);
+  pl->nt_max = (int)(pl->npad / TILE);
+  pl->vt_count = (int)((p->v + TILE - 1) / TILE);
+  pl->nparts = pl->vt_count < MAX_PARTS ? pl->vt_count : MAX_PARTS;
+  int64_t vc = 2 * p->d;
+  if (vc < 4096) vc = 4096;
+  vc = round_up(vc, TILE);
+  const int64_t vround = round_up(p->v, TILE);
+  if (vc > vround) vc = vround;
+  pl->vc = vc;
+  pl->nslab = (p->v + vc - 1) / vc;
+  if ((uint64_t)pl->npad * vc * 2 > 0xFFFFFFFFull || (uint64_t)vc * pl->npad * 2 > 0xFFFFFFFFull ||
+      (uint64_t)p->d * pl->npad * 2 > 0xFFFFFFFFull)
+    return LCE_ERR_SHAPE;
+
+  auto take = [](size_t& cur, size_t bytes) { size_t o = cur; cur += (bytes + 255) / 256 * 256; return o; };
+  size_t cur = 0;
+  pl->o_idx = take(cur, 4 * (size_t)pl->npad);
+  pl->o_pos = take(cur, 4 * (size_t)pl->npad);
+  pl->o_nv = take(cur, 256);
+  const size_t common = cur;
+  pl->o_pm = take(cur, 4 * (size_t)(2 * pl->nparts) * pl->npad);
+  pl->o_ps = take(cur, 4 * (size_t)(2 * pl->nparts) * pl->npad);
+  pl->o_terms = take(cur, 4 * (size_t)pl->npad);
+  pl->fwd_bytes = cur;
+  cur = common;
+  pl->o_hvt = take(cur, 2 * (size_t)p->d * pl->npad);
+  pl->o_g = take(cur, 2 * (size_t)pl->npad * vc);
+  pl->o_gt = take(cur, 2 * (size_t)vc * pl->npad);
+  pl->o_wst = take(cur, 2 * (size_t)p->d * vc);
+  pl->o_dh32 = take(cur, 4 * (size_t)pl->npad * p->d);
+  pl->bwd_bytes = cur;
+  return LCE_OK;
+}
+
+inline bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
+
+struct Launcher {
+  hipStream_t s;
+  lce_status_t st = LCE_OK;
+  template <typename... KArgs, typename... Args>
+  void operator()(int kind, void (*kern)(KArgs...), dim3 grid, dim3 block, Args... args) {
+    if (st != LCE_OK) return;
+    if (grid.x == 0 || grid.y == 0 || grid.z == 0) return;
+    int slot = -1;
+    if (g_timing.on) {
+      std::lock_guard<std::mutex> lk(g_timing.mu);
+      if (g_timing.on && g_timing.used < Timing::kPool) {
+        slot = g_timing.used++;
+        g_timing.kind[slot] = kind;
+      }
+    }
+    if (slot >= 0 && hipEventRecord(g_timing.ev[2 * slot], s) != hipSuccess) { st = LCE_ERR_HIP; return; }
+    hipLaunchKernelGGL(kern, grid, block, 0, s, static_cast<KArgs>(args)...);
+    if (hipGetLastError() != hipSuccess) { st = LCE_ERR_HIP; return; }
+    if (slot >= 0 && hipEventRecord(g_timing.ev[2 * slot + 1], s) != hipSuccess) st = LCE_ERR_HIP;
+  }
+};
+
+}  // namespace
+
+extern "C" {
+
+const char* lce_status_string(lce_status_t s) {
+  switch (s) {
+    case LCE_OK: return "ok";
+    case LCE_ERR_NULL: return "required pointer is NULL";
+    case LCE_ERR_SHAPE: return "invalid or too large shape / stride";
+    case LCE_ERR_ALIGN: return "pointer, stride or workspace misaligned";
+    case LCE_ERR_UNSUPPORTED: return "unsupported configuration (d % 8, reduction or target width)";
+    case LCE_ERR_WORKSPACE: return "workspace too small";
+    case LCE_ERR_HIP: return "HIP runtime or kernel launch failure";
+    case LCE_ERR_ARG: return "invalid argument";
+  }
+  return "unknown status";
+}
+
+lce_status_t lce_workspace_size(const lce_problem_t* p, size_t* fwd_bytes, size_t* bwd_bytes) {
+  Plan pl;
+  lce_status_t st = make_plan(p, &pl);
+  if (st != LCE_OK) return st;
+  if (fwd_bytes) *fwd_bytes = pl.fwd_bytes;
+  if (bwd_bytes) *bwd_bytes = pl.bwd_bytes;
+  return LCE_OK;
+}
+
+lce_status_t lce_forward(const lce_problem_t* p, const void* H, const void* W, const void* targets,
+                         float* loss, float* lse, int32_t* n_valid, int32_t* dev_status,
+                         void* workspace, size_t workspace_bytes, void* stream) {
+  Plan pl;
+  lce_status_t st = make_plan(p, &pl);
+  if (st != LCE_OK) return st;
+  if (!loss || !n_valid) return LCE_ERR_NULL;
+  if (pl.n > 0 && (!H || !W || !targets || !lse || !workspace)) return LCE_ERR_NULL;
+  if (pl.n > 0 && (!aligned16(H) || !aligned16(W) || ((uintptr_t)workspace & 255) != 0)) return LCE_ERR_ALIGN;
+  if (pl.n > 0 && workspace_bytes < pl.fwd_bytes) return LCE_ERR_WORKSPACE;
+  Launcher L{(hipStream_t)stream};
+  if (pl.n == 0) {
+    L(K_MISC, k_fwd_empty, dim3(1), dim3(64), loss, n_valid, dev_status);
+    return L.st;
+  }
+  char* ws = (char*)workspace;
+  int* idx = (int*)(ws + pl.o_idx);
+  int* pos = (int*)(ws + pl.o_pos);
+  int* nv = (int*)(ws + pl.o_nv);
+  float* pm = (float*)(ws + pl.o_pm);
+  float* ps = (float*)(ws + pl.o_ps);
+  float* terms = (float*)(ws + pl.o_terms);
+  const uint16_t* h = (const uint16_t*)H;
+  const uint16_t* w = (const uint16_t*)W;
+
+  L(K_COMPACT, k_compact, dim3(1), dim3(1024), targets, p->target_bytes, pl.n, pl.v, p->ignore_index,
+    idx, pos, nv, n_valid, dev_status, lse);
+  L(K_FWD_STATS, k_fwd_stats, dim3(pl.nt_max * pl.nparts), dim3(NTHREADS), w, pl.ldw, (int)pl.v, h, pl.ldh,
+    pl.n, (const int*)idx, (const int*)nv, (int)pl.d, pl.nparts, pl.nt_max, pl.vt_count, pm, ps, (int)pl.npad);
+  L(K_COMBINE, k_combine, dim3((unsigned)((pl.n + 3) / 4)), dim3(256), h, pl.ldh, w, pl.ldw, targets,
+    p->target_bytes, (const int*)idx, (const int*)nv, (int)pl.d, 2 * pl.nparts, (const float*)pm,
+    (const float*)ps, (int)pl.npad, lse, terms);
+  L(K_LOSS, k_loss, dim3(1), dim3(1024), (const float*)terms, (const int*)nv, p->reduction, loss);
+  return L.st;
+}
+
+lce_status_t lce_backward(const lce_problem_t* p, const void* H, const void* W, const void* targets,
+                          const float* lse, const int32_t* n_valid, const float* grad_loss,
+                          void* dH, void* dW, void* workspace, size_t workspace_bytes, void* stream) {
+  Plan pl;
+  lce_status_t st = make_plan(p, &pl);
+  if (st != LCE_OK) return st;
+  if (!W || !dW || !n_valid || !grad_loss) return LCE_ERR_NULL;
+  if (pl.n > 0 && (!H || !targets || !lse || !dH || !workspace)) return LCE_ERR_NULL;
+  if (!aligned16(W) || !aligned16(dW)) return LCE_ERR_ALIGN;
+  if (pl.n > 0 && (!aligned16(H) || !aligned16(dH) || ((uintptr_t)workspace & 255) != 0)) return LCE_ERR_ALIGN;
+  if (pl.n > 0 && workspace_bytes < pl.bwd_bytes) return LCE_ERR_WORKSPACE;
+  Launcher L{(hipStream_t)stream};
+  if (pl.n == 0) {
+    const int64_t n16 = pl.v * pl.d / 8;
+    L(K_MISC, k_zero16, dim3((unsigned)((n16 + 255) / 256)), dim3(256), (uint4*)dW, n16);
+    return L.st;
+  }
+  char* ws = (char*)workspace;
+  int* idx = (int*)(ws + pl.o_idx);
+  int* pos = (int*)(ws + pl.o_pos);
+  int* nv = (int*)(ws + pl.o_nv);
+  uint16_t* hvt = (uint16_t*)(ws + pl.o_hvt);
+  uint16_t* g = (uint16_t*)(ws + pl.o_g);
+  uint16_t* gt = (uint16_t*)(ws + pl.o_gt);
+  uint16_t* wst = (uint16_t*)(ws + pl.o_wst);
+  float* dh32 = (float*)(ws + pl.o_dh32);
+  const uint16_t* h = (const uint16_t*)H;
+  const uint16_t* w = (const uint16_t*)W;
+  const int d = (int)pl.d, npad = (int)pl.npad, vc = (int)pl.vc;
+
+  L(K_COMPACT, k_compact, dim3(1), dim3(1024), targets, p->target_bytes, pl.n, pl.v, p->ignore_index,
+    idx, pos, nv, (int*)nullptr, (int*)nullptr, (float*)nullptr);
+  // Hvt[d][i] = H[idx[i]][d] for i < Nv, zero up to round_up(Nv, 64)
+  L(K_TRANSPOSE_H, k_transpose, dim3((unsigned)(npad / 64), (unsigned)((d + 63) / 64)), dim3(256), h, pl.ldh,
+    (const int*)idx, (int64_t)0, (const int*)nv, 0, d, hvt, (int64_t)npad, npad);
+  const int dt = (d + TILE - 1) / TILE;
+  for (int64_t s = 0; s < pl.nslab; ++s) {
+    const int64_t v0 = s * pl.vc;
+    const int vs = (int)(pl.v - v0 < pl.vc ? pl.v - v0 : pl.vc);
+    const int vs64 = (int)round_up(vs, 64);
+    const int tm = (vs + TILE - 1) / TILE;
+    L(K_TRANSPOSE_W, k_transpose, dim3((unsigned)(vs64 / 64), (unsigned)((d + 63) / 64)), dim3(256), w, pl.ldw,
+      (const int*)nullptr, v0, (const int*)nullptr, vs, d, wst, (int64_t)vc, vs64);
+    L(K_BWD_G, k_bwd_g, dim3((unsigned)(tm * pl.nt_max)), dim3(NTHREADS), w, pl.ldw, v0, vs, h, pl.ldh, pl.n,
+      targets, p->target_bytes, (const int*)idx, (const int*)nv, lse, grad_loss, (const int*)n_valid,
+      p->reduction, d, tm, g, vc, gt, npad);
+    L(K_BWD_DW, k_bwd_dw, dim3((unsigned)(tm * dt)), dim3(NTHREADS), (const uint16_t*)gt, npad, vs,
+      (const uint16_t*)hvt, d, (const int*)nv, tm, (uint16_t*)dW, v0);
+    L(K_BWD_DH, k_bwd_dh, dim3((unsigned)(pl.nt_max * dt)), dim3(NTHREADS), (const uint16_t*)g, vc, vs64,
+      (const uint16_t*)wst, d, (const int*)nv, pl.nt_max, dh32, (int)(s > 0));
+  }
+  const int64_t nthr = pl.n * pl.d / 8;
+  L(K_DH_FINAL, k_dh_finalize, dim3((unsigned)((nthr + 255) / 256)), dim3(256), (const float*)dh32,
+    (const int*)pos, pl.n, d, (uint16_t*)dH, 1);
+  return L.st;
+}
+
+lce_status_t lce_timing_enable(int on) {
+  std::lock_guard<std::mutex> lk(g_timing.mu);
+  if (on) {
+    if (g_timing.ev.empty()) {
+      g_timing.ev.resize(2 * Timing::kPool);
+      g_timing.kind.assign(Timing::kPool, 0);
+      for (auto& e : g_timing.ev)
+        if (hipEventCreate(&e) != hipSuccess) {
+          g_timing.ev.clear();
+          return LCE_ERR_HIP;
+        }
+    }
+    g_timing.used = 0;
+    g_timing.on = true;
+  } else {
+    g_timing.on = false;
+  }
+  return LCE_OK;
+}
+
+int lce_timing_kernel_count(void) { return K_COUNT; }
+
+const char* lce_timing_kernel_name(int k) { return (k >= 0 && k < K_COUNT) ? kKernelNames[k] : nullptr; }
+
+lce_status_t lce_timing_read(int k, double* total_ms, int64_t* launches) {
+  if (k < 0 || k >= K_COUNT) return LCE_ERR_ARG;
+  if (!total_ms || !launches) return LCE_ERR_NULL;
+  std::lock_guard<std::mutex> lk(g_timing.mu);
+  double tot = 0.0;
+  int64_t cnt = 0;
+  for (int i = 0; i < g_timing.used; ++i) {
+    if (g_timing.kind[i] != k) continue;
+    if (hipEventSynchronize(g_timing.ev[2 * i + 1]) != hipSuccess) return LCE_ERR_HIP;
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, g_timing.ev[2 * i], g_timing.ev[2 * i + 1]) != hipSuccess) return LCE_ERR_HIP;
+    tot += ms;
+    ++cnt;
+  }
+  *total_ms = tot;
+  *launches = cnt;
+  return LCE_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,118 @@
+"""The C ABI without a GPU: the library loads, exports what include/lce.h declares, sizes its
+workspace as documented and rejects bad arguments before launching anything."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2605_21442_amd import binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+pytestmark = pytest.mark.skipif(not os.path.exists(B.LIB_PATH), reason="liblce.so not built")
+
+
+def _declared_functions():
+    src = open(os.path.join(ROOT, "include", "lce.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(lce_[a-z_]+)\s*\(", src)))
+
+
+def test_every_declared_symbol_is_exported():
+    lib = B.load()
+    declared = _declared_functions()
+    assert set(declared) == set(B.EXPORTED)
+    for name in declared:
+        assert hasattr(lib, name), name
+
+
+def test_status_strings():
+    for code in range(8):
+        assert B.lce_status_string(code) and B.lce_status_string(code) != "unknown status"
+    assert B.lce_status_string(99) == "unknown status"
+
+
+def test_workspace_is_linear_in_tokens_and_never_tokens_times_vocab():
+    f1, b1 = B.lce_workspace_size(B.problem(16384, 4096, 128256))
+    f2, b2 = B.lce_workspace_size(B.problem(32768, 4096, 128256))
+    assert f2 < 2.1 * f1 and b2 < 2.1 * b1
+    n, d, v = 16384, 4096, 128256
+    assert b1 < n * v * 2 // 4                              # far below one bf16 copy of the logits
+    slab = max(4096, 2 * d)
+    bound = 4 * n * 4 + 2 * d * n + 2 * 2 * n * slab + 2 * d * slab + 4 * n * d + 4096
+    assert b1 <= bound
+    # doubling the vocabulary leaves the workspace (almost) unchanged
+    f3, b3 = B.lce_workspace_size(B.problem(16384, 4096, 256512))
+    assert b3 == b1 and f3 <= f1 * 1.01
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(n=-1, d=64, v=10), B.LCE_ERR_SHAPE),
+    (dict(n=4, d=0, v=10), B.LCE_ERR_SHAPE),
+    (dict(n=4, d=64, v=0), B.LCE_ERR_SHAPE),
+    (dict(n=4, d=60, v=10), B.LCE_ERR_UNSUPPORTED),
+    (dict(n=4, d=64, v=10, ld_h=32), B.LCE_ERR_SHAPE),
+    (dict(n=4, d=64, v=10, ld_w=68), B.LCE_ERR_ALIGN),
+    (dict(n=4, d=64, v=10, reduction=7), B.LCE_ERR_UNSUPPORTED),
+    (dict(n=4, d=64, v=10, target_bytes=2), B.LCE_ERR_UNSUPPORTED),
+    (dict(n=1 << 22, d=1024, v=10), B.LCE_ERR_SHAPE),       # H beyond 32-bit byte offsets
+])
+def test_bad_problems_are_rejected(kw, code):
+    with pytest.raises(B.LceError) as e:
+        B.lce_workspace_size(B.problem(**kw))
+    assert e.value.code == code
+
+
+def test_reserved_field_must_be_zero():
+    p = B.problem(4, 64, 10)
+    p.reserved = 1
+    with pytest.raises(B.LceError) as e:
+        B.lce_workspace_size(p)
+    assert e.value.code == B.LCE_ERR_ARG
+
+
+def _fake(addr=0x100000):
+    return addr
+
+
+def test_forward_argument_checks_run_before_any_launch():
+    p = B.problem(8, 64, 10)
+    fwd, _ = B.lce_workspace_size(p)
+    ok = dict(H=_fake(), W=_fake(0x200000), targets=_fake(0x300000), loss=_fake(0x400000),
+              lse=_fake(0x500000), n_valid=_fake(0x600000), dev_status=0,
+              workspace=_fake(0x700000), workspace_bytes=fwd, stream=0)
+    cases = [
+        (dict(H=0), B.LCE_ERR_NULL), (dict(loss=0), B.LCE_ERR_NULL), (dict(lse=0), B.LCE_ERR_NULL),
+        (dict(W=0x200008), B.LCE_ERR_ALIGN), (dict(workspace=0x700010), B.LCE_ERR_ALIGN),
+        (dict(workspace_bytes=fwd - 1), B.LCE_ERR_WORKSPACE),
+    ]
+    for change, code in cases:
+        args = dict(ok, **change)
+        with pytest.raises(B.LceError) as e:
+            B.lce_forward(p, **args)
+        assert e.value.code == code, change
+
+
+def test_backward_argument_checks_run_before_any_launch():
+    p = B.problem(8, 64, 10)
+    _, bwd = B.lce_workspace_size(p)
+    ok = dict(H=_fake(), W=_fake(0x200000), targets=_fake(0x300000), lse=_fake(0x400000),
+              n_valid=_fake(0x500000), grad_loss=_fake(0x600000), dH=_fake(0x700000),
+              dW=_fake(0x800000), workspace=_fake(0x900000), workspace_bytes=bwd, stream=0)
+    cases = [
+        (dict(dW=0), B.LCE_ERR_NULL), (dict(grad_loss=0), B.LCE_ERR_NULL),
+        (dict(dH=0x700004), B.LCE_ERR_ALIGN), (dict(workspace_bytes=16), B.LCE_ERR_WORKSPACE),
+    ]
+    for change, code in cases:
+        args = dict(ok, **change)
+        with pytest.raises(B.LceError) as e:
+            B.lce_backward(p, **args)
+        assert e.value.code == code, change
+
+
+def test_missing_library_fails_loudly(monkeypatch, tmp_path):
+    monkeypatch.setattr(B, "_lib", None)
+    monkeypatch.setattr(B, "LIB_PATH", str(tmp_path / "liblce.so"))
+    with pytest.raises(RuntimeError, match="not built"):
+        B.load()
