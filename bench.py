@@ -1,0 +1,181 @@
+"""Benchmark of the LCE hot path (forward + backward) on one MI355X.
+
+python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload llama8b] [--no-cpu-baseline]
+
+One step is one lce_forward + lce_backward over the whole batch of the named
+workload (default: the Llama-3.1-8B vocabulary head, N = 8 x 2048 tokens,
+D = 4096, V = 128256, 25% of targets masked). Inputs are seeded synthetic
+tensors already resident in HBM; outputs and workspace are allocated once
+before the timed region. The script prints one JSON line on stdout.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0        # MI355X dense bf16 MFMA peak
+PEAK_HBM_GBS = 8000.0
+METRIC = "LCE fwd+bwd tokens/sec, % bf16 MFMA peak, peak HBM bytes (1 GPU)"
+GEMM_KERNELS = ("fwd_stats", "bwd_g", "bwd_dw", "bwd_dh")
+
+
+def _cpu_baseline(inp, seconds_target=10.0):
+    """The CPU oracle, as it stands, on a bounded sample of the workload's tokens."""
+    from oracle import lce_oracle as O
+    try:
+        import threadpoolctl
+        threads = max(i.get("num_threads", 1) for i in threadpoolctl.threadpool_info()) or 1
+    except Exception:  # pragma: no cover
+        threads = os.cpu_count() or 1
+    valid = np.nonzero(inp.targets != inp.ignore_index)[0]
+    sample = 16
+    t0 = time.perf_counter()
+    O.lce(inp.h_bits[valid[:sample]], inp.w_bits, inp.targets[valid[:sample]])
+    dt = time.perf_counter() - t0
+    # grow the sample to roughly the target duration (one more run, not timed twice)
+    per_tok = dt / sample
+    sample2 = int(min(len(valid), max(sample, seconds_target / max(per_tok, 1e-9))))
+    if sample2 > sample:
+        t0 = time.perf_counter()
+        O.lce(inp.h_bits[valid[:sample2]], inp.w_bits, inp.targets[valid[:sample2]])
+        dt = time.perf_counter() - t0
+        sample = sample2
+    return {"value": sample / dt, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{sample} valid tokens of the {inp.workload.name} batch, full D and V, "
+                      f"fp64 forward+backward ({dt:.1f} s)"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="llama8b")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (asked for {args.gpus}); the LCE path here has no "
+              f"multi-GPU mode", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2605_21442_amd import binding as B
+    from paper_2605_21442_amd import workloads as WL
+
+    wl = WL.WORKLOADS[args.workload]
+    t_gen = time.perf_counter()
+    inp = WL.generate(wl, args.seed)
+    print(f"[bench] {wl.name}: N={wl.n} D={wl.d} V={wl.v} Nv={wl.n_valid()} "
+          f"(inputs drawn in {time.perf_counter() - t_gen:.1f} s)", file=sys.stderr, flush=True)
+    dev = torch.device("cuda:0")
+    h = torch.from_numpy(inp.h_bits.view(np.int16)).view(torch.bfloat16).to(dev)
+    w = torch.from_numpy(inp.w_bits.view(np.int16)).view(torch.bfloat16).to(dev)
+    t = torch.from_numpy(inp.targets).to(dev)
+    n, d, v = wl.n, wl.d, wl.v
+    p = B.problem(n, d, v, ignore_index=inp.ignore_index, reduction="mean", target_bytes=4)
+    fwd_bytes, bwd_bytes = B.lce_workspace_size(p)
+    torch.cuda.synchronize()
+    base_alloc = torch.cuda.memory_allocated()
+    torch.cuda.reset_peak_memory_stats()
+
+    loss = torch.empty((), dtype=torch.float32, device=dev)
+    lse = torch.empty(n, dtype=torch.float32, device=dev)
+    nv = torch.empty(1, dtype=torch.int32, device=dev)
+    status = torch.empty(1, dtype=torch.int32, device=dev)
+    grad = torch.ones(1, dtype=torch.float32, device=dev)
+    dh = torch.empty((n, d), dtype=torch.bfloat16, device=dev)
+    dw = torch.empty((v, d), dtype=torch.bfloat16, device=dev)
+    ws = torch.empty(max(fwd_bytes, bwd_bytes), dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream(dev).cuda_stream
+
+    def step():
+        B.lce_forward(p, h.data_ptr(), w.data_ptr(), t.data_ptr(), loss.data_ptr(), lse.data_ptr(),
+                      nv.data_ptr(), status.data_ptr(), ws.data_ptr(), fwd_bytes, stream)
+        B.lce_backward(p, h.data_ptr(), w.data_ptr(), t.data_ptr(), lse.data_ptr(), nv.data_ptr(),
+                       grad.data_ptr(), dh.data_ptr(), dw.data_ptr(), ws.data_ptr(), bwd_bytes, stream)
+
+    for i in range(args.warmup):
+        step()
+        torch.cuda.synchronize()
+        print(f"[bench] warmup {i + 1}/{args.warmup} done", file=sys.stderr, flush=True)
+    peak = torch.cuda.max_memory_allocated()
+    resident = (h.numel() + w.numel() + dh.numel() + dw.numel()) * 2 + t.numel() * 4 + n * 4
+
+    B.lce_timing_enable(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    names = B.lce_timing_kernel_names()
+    kernels = {}
+    for k, name in enumerate(names):
+        ms, cnt = B.lce_timing_read(k)
+        if cnt:
+            kernels[name] = {"total_ms": ms, "launches": cnt, "avg_ms": ms / cnt}
+    B.lce_timing_enable(False)
+    print(f"[bench] timed {args.steps} steps in {elapsed:.3f} s; loss={loss.item():.6f} "
+          f"Nv={int(nv.item())}", file=sys.stderr, flush=True)
+
+    nvalid = int(nv.item())
+    ms_step = elapsed * 1e3 / args.steps
+    flops_step = 8.0 * nvalid * d * v
+    dom = max((k for k in kernels if k in GEMM_KERNELS), key=lambda k: kernels[k]["total_ms"])
+    launches_per_step = kernels[dom]["launches"] / args.steps
+    flops_launch = 2.0 * nvalid * d * v / launches_per_step
+    achieved = flops_launch / (kernels[dom]["avg_ms"] * 1e-3) / 1e12
+    for k, r in sorted(kernels.items(), key=lambda kv: -kv[1]["total_ms"]):
+        extra = ""
+        if k in GEMM_KERNELS:
+            tf = 2.0 * nvalid * d * v / (r["launches"] / args.steps) / (r["avg_ms"] * 1e-3) / 1e12
+            extra = f" {tf:7.1f} TFLOP/s ({100 * tf / PEAK_BF16_TFLOPS:4.1f}% of peak)"
+        print(f"[bench]   {k:12s} {r['total_ms'] / args.steps:8.3f} ms/step  {r['launches']:5d} launches"
+              f"  avg {r['avg_ms']:.4f} ms{extra}", file=sys.stderr)
+
+    out = {
+        "metric": METRIC,
+        "value": n * args.steps / elapsed,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "n_tokens": n, "hidden": d, "vocab": v, "n_valid": nvalid,
+                   "global_batch": wl.batch, "seq_len": wl.seq_len, "parallelism": "none",
+                   "reduction": "mean", "ignore_index": inp.ignore_index},
+        "valid_tokens_per_s": nvalid * args.steps / elapsed,
+        "mfma_frac_step": flops_step / (ms_step * 1e-3) / (PEAK_BF16_TFLOPS * 1e12),
+        "peak_hbm_bytes": int(peak),
+        "peak_hbm_bytes_transient": int(peak - resident),
+        "workspace_bytes": int(max(fwd_bytes, bwd_bytes)),
+        "logits_bytes_avoided_fp32": int(n) * int(v) * 4,
+        "roofline": {"bound": "mfma", "kernel": dom, "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
+                     "flops_per_launch": flops_launch, "avg_launch_ms": kernels[dom]["avg_ms"]},
+        "kernels_ms_per_step": {k: r["total_ms"] / args.steps for k, r in kernels.items()},
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle on a token sample ...", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = _cpu_baseline(inp)
+    else:
+        out["cpu_baseline"] = None
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -16,9 +16,9 @@
 //             dW slab = G^T H_valid, dH32 (+)= G W_slab -> finalise dH
 //
 // Every contraction is a "both operands K-contiguous" product C = A B^T run by
-// one MFMA main loop: 256x256 output tiles, 4 waves of 128x128, bf16
-// v_mfma_f32_32x32x16 with fp32 accumulation, K staged through LDS in 64-wide
-// slices (double-buffered, XOR-swizzled 16-byte chunks).
+// one MFMA main loop: 256x256 output tiles, 8 waves of 128x64, bf16
+// v_mfma_f32_32x32x16 with fp32 accumulation, K streamed through two 64-wide LDS
+// slices filled by direct-to-LDS buffer loads (XOR-swizzled 16-byte chunks).
 
 #include <hip/hip_runtime.h>
 
@@ -39,16 +39,17 @@ typedef int i32x4_t __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
 
 constexpr int TILE = 256;         // output tile edge (rows of A and of B per workgroup)
-constexpr int BK = 64;            // K slice staged in LDS per step
-constexpr int NTHREADS = 256;     // 4 waves
-constexpr int LDS_STAGE = 65536;  // A slice (32 KB) + B slice (32 KB)
+constexpr int KPAD = 64;          // K padding granularity of the backward's staged operands
+constexpr int NTHREADS = 512;     // 8 waves, two per SIMD
 constexpr int MAX_PARTS = 32;     // vocabulary partitions of the forward (x2 wave rows <= 64 lanes)
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 constexpr uint32_t kRsrcWord3 = 0x00020000u;  // gfx9 raw buffer: 32-bit data format
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint64_t bytes) {
-  uint32_t n = bytes > 0xFFFFFFFFull ? 0xFFFFFFFFu : (uint32_t)bytes;
+  // capped below 2^31 so that offset 2^31 is always out of range (the zero-fill trick for ragged
+  // K slices); every access of a tile lies within its first 2^31 bytes (checked on the host)
+  uint32_t n = bytes > 0x7FFFFFFFull ? 0x7FFFFFFFu : (uint32_t)bytes;
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)n, (int)kRsrcWord3);
 }
 
@@ -75,105 +76,174 @@ __device__ __forceinline__ float wave_max(float x) {
 }
 
 // ---------------------------------------------------------------------------------------------
-// MFMA main loop: acc[bi][bj] (+)= A[256 x K] * B[256 x K]^T for this workgroup's tile.
+// MFMA main loop: acc[bi][bj] = A[256 x K] * B[256 x K]^T for this workgroup's 256x256 tile.
 //
-// Thread t stages rows (t >> 3) + 32 i (i = 0..7) of both operands, 16-byte chunk (t & 7) of the
-// current 64-wide K slice. In LDS a row is 128 bytes; chunk c of row r sits at position
-// c ^ (r & 7) so that the 32 rows one MFMA operand read touches spread over all banks.
-// Wave w = 2 wr + wc owns output rows wr*128.. and columns wc*128.. of the tile:
-// acc[bi][bj] holds the 32x32 block (bi, bj); lane l, register r of a block is
-// row 8 (r / 4) + 4 (l / 32) + r % 4, column l % 32.
-// aoff/boff are byte offsets (row start + chunk) into the buffer resources; K is a multiple of 8.
+// Eight waves (two per SIMD, so one wave's memory stalls are covered by the other's MFMAs) in a
+// 2 x 4 grid; wave w = 4 wr + wc owns output rows wr*128.. (A rows) and columns wc*64.. (B rows).
+// acc[bi][bj] (bi < 4, bj < 2) is the 32x32 block (bi, bj) of that 128x64 wave tile; lane l,
+// register r of a block holds row 8 (r / 4) + 4 (l / 32) + r % 4, column l % 32. A fragment
+// for v_mfma_f32_32x32x16_bf16 is 8 consecutive K values of one row (lane l: row l % 32, K
+// chunk l / 32 of the 16-wide substep).
+//
+// K streams through two LDS buffers of 64-wide slices (A 256x64 and B 256x64 bf16: 64 KB per
+// buffer). A slice is copied global -> LDS by buffer loads that write LDS directly; each moves 8
+// rows x 128 bytes (one full cache line per row, which the memory pipeline turns into whole-line
+// requests), one 16-byte chunk per lane. In LDS a row is 128 bytes and chunk c of row r sits at
+// position c ^ swz(r), swz(r) = (r & 7) ^ ((r >> 3) & 1): the 128-bit fragment reads of any 8 or
+// 16 consecutive rows then hit distinct banks. Each load picks its source chunk so that it lands
+// in that order.
+//
+// Schedule of slice j (four 16-wide substeps, fragments read one substep ahead): after the
+// third substep's MFMAs are issued, one barrier both publishes slice j+1 (its loads were issued a
+// whole slice earlier) and frees slice j's buffer, into which slice j+2 is then loaded while the
+// fourth substep runs and the first fragments of slice j+1 are read.
+//
+// aoff/boff: byte offset (row start + this lane's chunk) of the 4 rows this lane loads per slice
+// and operand. K must be a multiple of 8; a ragged last slice is zero-filled by pointing the
+// lanes past K outside the buffer resource (buffer loads return 0 there).
 // ---------------------------------------------------------------------------------------------
-__device__ __forceinline__ void mma_mainloop(f32x16_t (&acc)[4][4],
-                                             __amdgpu_buffer_rsrc_t ra, const uint32_t (&aoff)[8],
-                                             __amdgpu_buffer_rsrc_t rb, const uint32_t (&boff)[8],
-                                             int K, char* smem) {
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = tid >> 6;
-  const int wr = wave >> 1, wc = wave & 1;
-  const int chunk = tid & 7;
-  const uint32_t wofs = (uint32_t)((tid >> 3) * 128 + ((chunk ^ ((tid >> 3) & 7)) * 16));
-  const uint32_t abase = (uint32_t)((wr * 128 + (lane & 31)) * 128);
-  const uint32_t bbase = (uint32_t)((wc * 128 + (lane & 31)) * 128) + 32768u;
-  uint32_t kso[4];
+constexpr int KSLICE = 64;
+constexpr int SLICE_BYTES = 65536;      // A (32 KB) + B (32 KB)
+constexpr int LDS_BYTES = 2 * SLICE_BYTES;
+constexpr uint32_t kOobOffset = 0x80000000u;
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+struct FragSet {
+  bf16x8_t a[4], b[2];
+};
+
+// chunk this lane loads for its even-numbered rows (odd rows: ^ 1)
+__device__ __forceinline__ int lane_chunk_even() {
+  const int j = threadIdx.x & 63;
+  return (j & 7) ^ ((j >> 3) & 7);
+}
+
+__device__ __forceinline__ void read_frags(FragSet& f, const char* buf, uint32_t a_rd, uint32_t b_rd, uint32_t kofs) {
 #pragma unroll
-  for (int ks = 0; ks < 4; ++ks) kso[ks] = (uint32_t)((((ks * 2) + (lane >> 5)) ^ (lane & 7)) * 16);
+  for (int i = 0; i < 4; ++i) f.a[i] = *reinterpret_cast<const bf16x8_t*>(buf + a_rd + i * 4096 + kofs);
+#pragma unroll
+  for (int j = 0; j < 2; ++j) f.b[j] = *reinterpret_cast<const bf16x8_t*>(buf + 32768 + b_rd + j * 4096 + kofs);
+}
+
+__device__ __forceinline__ void mma_substep(f32x16_t (&acc)[4][2], const FragSet& f) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[i], f.b[j], acc[i][j], 0, 0, 0);
+}
+
+template <bool kMasked>
+__device__ __forceinline__ void load_slice(__amdgpu_buffer_rsrc_t ra, const uint32_t (&aoff)[4],
+                                           __amdgpu_buffer_rsrc_t rb, const uint32_t (&boff)[4],
+                                           char* buf, int k0, int K) {
+  char* dst = buf + (threadIdx.x >> 6) * 4096;
+  if (!kMasked) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_void_t*)(dst + q * 1024), 16, (int)aoff[q], k0 * 2, 0, 0);
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_void_t*)(dst + 32768 + q * 1024), 16, (int)boff[q], k0 * 2, 0, 0);
+  } else {
+    const int ce = lane_chunk_even();
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const bool ok = k0 + (ce ^ (q & 1)) * 8 < K;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_void_t*)(dst + q * 1024), 16,
+                                               (int)(ok ? aoff[q] + (uint32_t)k0 * 2 : kOobOffset), 0, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_void_t*)(dst + 32768 + q * 1024), 16,
+                                               (int)(ok ? boff[q] + (uint32_t)k0 * 2 : kOobOffset), 0, 0, 0);
+    }
+  }
+}
+
+// s_waitcnt with only the vector-memory counter constrained (expcnt / lgkmcnt left at max)
+#define LCE_WAIT_VM(n) __builtin_amdgcn_s_waitcnt((((n) & 15) | (7 << 4) | (15 << 8) | (((n) >> 4) << 14)))
+
+__device__ __forceinline__ void mma_mainloop(f32x16_t (&acc)[4][2],
+                                             __amdgpu_buffer_rsrc_t ra, const uint32_t (&aoff)[4],
+                                             __amdgpu_buffer_rsrc_t rb, const uint32_t (&boff)[4],
+                                             int K, char* smem) {
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int wr = wave >> 2, wc = wave & 3;
+  const uint32_t a_rd = (uint32_t)((wr * 128 + (lane & 31)) * 128);
+  const uint32_t b_rd = (uint32_t)((wc * 64 + (lane & 31)) * 128);
+  const int swz = (lane & 7) ^ ((lane >> 3) & 1);
+  uint32_t kofs[4];
+#pragma unroll
+  for (int ks = 0; ks < 4; ++ks) kofs[ks] = (uint32_t)((((ks * 2) + (lane >> 5)) ^ swz) * 16);
 
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = (f32x16_t){};
+    for (int j = 0; j < 2; ++j) acc[i][j] = (f32x16_t){};
 
-  const int nk = (K + BK - 1) / BK;
-  if (nk <= 0) return;
-
-  i32x4_t sa[8], sb[8];
-  auto gload = [&](int kt) {
-    const int k0 = kt * BK;
-    const bool ok = (k0 + chunk * 8) < K;
-    const int kb = k0 * 2;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      sa[i] = ok ? __builtin_amdgcn_raw_buffer_load_b128(ra, (int)aoff[i], kb, 0) : (i32x4_t){};
-      sb[i] = ok ? __builtin_amdgcn_raw_buffer_load_b128(rb, (int)boff[i], kb, 0) : (i32x4_t){};
-    }
-  };
-  auto lstore = [&](int buf) {
-    char* base = smem + buf * LDS_STAGE;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      *reinterpret_cast<i32x4_t*>(base + wofs + i * 4096) = sa[i];
-      *reinterpret_cast<i32x4_t*>(base + 32768 + wofs + i * 4096) = sb[i];
-    }
+  const int S = (K + KSLICE - 1) / KSLICE;
+  if (S <= 0) return;
+  const bool ragged = (K % KSLICE) != 0;
+  auto load = [&](int s) {
+    char* buf = smem + (s & 1) * SLICE_BYTES;
+    if (ragged && s == S - 1) load_slice<true>(ra, aoff, rb, boff, buf, s * KSLICE, K);
+    else load_slice<false>(ra, aoff, rb, boff, buf, s * KSLICE, K);
   };
 
-  gload(0);
-  lstore(0);
-  __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    const char* buf = smem + cur * LDS_STAGE;
-    if (kt + 1 < nk) gload(kt + 1);
-#pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-      bf16x8_t a[4], b[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) a[i] = *reinterpret_cast<const bf16x8_t*>(buf + abase + i * 4096 + kso[ks]);
-#pragma unroll
-      for (int j = 0; j < 4; ++j) b[j] = *reinterpret_cast<const bf16x8_t*>(buf + bbase + j * 4096 + kso[ks]);
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
-    }
-    if (kt + 1 < nk) lstore(cur ^ 1);
-    __syncthreads();
+  load(0);
+  if (S > 1) {
+    load(1);
+    LCE_WAIT_VM(8);
+  } else {
+    LCE_WAIT_VM(0);
   }
+  __builtin_amdgcn_s_barrier();
+
+  FragSet f0, f1;
+  read_frags(f0, smem, a_rd, b_rd, kofs[0]);
+  for (int j = 0; j < S; ++j) {
+    const char* cur = smem + (j & 1) * SLICE_BYTES;
+    const char* nxt = smem + ((j + 1) & 1) * SLICE_BYTES;
+    read_frags(f1, cur, a_rd, b_rd, kofs[1]);
+    mma_substep(acc, f0);
+    read_frags(f0, cur, a_rd, b_rd, kofs[2]);
+    mma_substep(acc, f1);
+    read_frags(f1, cur, a_rd, b_rd, kofs[3]);
+    mma_substep(acc, f0);
+    if (j + 1 < S) {
+      // slice j+1 landed (own loads) and every wave is done with slice j's buffer
+      __builtin_amdgcn_s_waitcnt(0);
+      __builtin_amdgcn_s_barrier();
+      if (j + 2 < S) load(j + 2);
+      read_frags(f0, nxt, a_rd, b_rd, kofs[0]);
+    }
+    mma_substep(acc, f1);
+  }
+  // every wave is done reading LDS before the caller reuses it
+  __syncthreads();
 }
 
-// Byte offsets of this thread's 8 staged rows for a dense operand whose rows
-// [row0, row0 + 256) are wanted; rows at or beyond `rows` are clamped to the last one.
-__device__ __forceinline__ void dense_offsets(uint32_t (&off)[8], int rows_left, int64_t ld) {
-  const int tid = threadIdx.x;
+// Byte offsets (row start + this lane's chunk) of the 4 rows this lane loads per slice of a dense
+// operand whose rows [row0, row0 + 256) are wanted; rows at or beyond `rows_left` are clamped.
+__device__ __forceinline__ void dense_offsets(uint32_t (&off)[4], int rows_left, int64_t ld) {
+  const int j = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int ce = lane_chunk_even();
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    int r = (tid >> 3) + 32 * i;
+  for (int q = 0; q < 4; ++q) {
+    int r = w * 32 + q * 8 + (j >> 3);
     r = r < rows_left ? r : rows_left - 1;
-    off[i] = (uint32_t)((int64_t)r * ld * 2 + (tid & 7) * 16);
+    off[q] = (uint32_t)((int64_t)r * ld * 2 + (ce ^ (q & 1)) * 16);
   }
 }
 
 // Same for rows gathered through the compacted valid-row list idx[0..nv).
-__device__ __forceinline__ void gather_offsets(uint32_t (&off)[8], const int* idx, int n0, int nv, int64_t ld) {
-  const int tid = threadIdx.x;
+__device__ __forceinline__ void gather_offsets(uint32_t (&off)[4], const int* idx, int n0, int nv, int64_t ld) {
+  const int j = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int ce = lane_chunk_even();
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    int r = n0 + (tid >> 3) + 32 * i;
+  for (int q = 0; q < 4; ++q) {
+    int r = n0 + w * 32 + q * 8 + (j >> 3);
     r = r < nv ? r : nv - 1;
-    off[i] = (uint32_t)((int64_t)idx[r] * ld * 2 + (tid & 7) * 16);
+    off[q] = (uint32_t)((int64_t)idx[r] * ld * 2 + (ce ^ (q & 1)) * 16);
   }
 }
 
@@ -237,34 +307,34 @@ __global__ __launch_bounds__(1024) void k_compact(const void* targets, int tbyte
 // At the end the two lane halves are merged and each wave row writes one partial pair per token
 // (in log2 units): part[(2 p + wave_row) * npad + token].
 // ---------------------------------------------------------------------------------------------
-__global__ __launch_bounds__(NTHREADS, 1) void k_fwd_stats(const uint16_t* __restrict__ W, int64_t ldw, int v,
+__global__ __launch_bounds__(NTHREADS, 2) void k_fwd_stats(const uint16_t* __restrict__ W, int64_t ldw, int v,
                                                            const uint16_t* __restrict__ H, int64_t ldh, int64_t n,
                                                            const int* __restrict__ idx, const int* __restrict__ nv_ptr,
                                                            int d, int nparts, int nt_max, int vt_count,
                                                            float* __restrict__ part_m, float* __restrict__ part_s,
                                                            int npad) {
-  __shared__ __attribute__((aligned(16))) char smem[2 * LDS_STAGE];
+  __shared__ __attribute__((aligned(16))) char smem[LDS_BYTES];
   const int nt = blockIdx.x % nt_max, p = blockIdx.x / nt_max;
   const int nv = *nv_ptr;
   const int n0 = nt * TILE;
   if (n0 >= nv) return;
   const int vt0 = (int)((int64_t)p * vt_count / nparts), vt1 = (int)((int64_t)(p + 1) * vt_count / nparts);
 
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, wr = wave >> 1, wc = wave & 1;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, wr = wave >> 2, wc = wave & 3;
   __amdgpu_buffer_rsrc_t rb = make_rsrc(H, (uint64_t)n * ldh * 2);
-  uint32_t boff[8];
+  uint32_t boff[4];
   gather_offsets(boff, idx, n0, nv, ldh);
 
-  float m2[4], ss[4];
+  float m2[2], ss[2];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) { m2[j] = -INFINITY; ss[j] = 0.f; }
+  for (int j = 0; j < 2; ++j) { m2[j] = -INFINITY; ss[j] = 0.f; }
 
-  f32x16_t acc[4][4];
+  f32x16_t acc[4][2];
   for (int vt = vt0; vt < vt1; ++vt) {
     const int v0 = vt * TILE;
     const int vleft = v - v0;
     __amdgpu_buffer_rsrc_t ra = make_rsrc(W + (int64_t)v0 * ldw, (uint64_t)vleft * ldw * 2);
-    uint32_t aoff[8];
+    uint32_t aoff[4];
     dense_offsets(aoff, vleft, ldw);
     mma_mainloop(acc, ra, aoff, rb, boff, d, smem);
 
@@ -272,7 +342,7 @@ __global__ __launch_bounds__(NTHREADS, 1) void k_fwd_stats(const uint16_t* __res
     const int vb = wr * 128 + (lane >> 5) * 4;
     const bool ragged = vleft < TILE;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < 2; ++j) {
       float mx = -INFINITY;
 #pragma unroll
       for (int i = 0; i < 4; ++i)
@@ -294,7 +364,7 @@ __global__ __launch_bounds__(NTHREADS, 1) void k_fwd_stats(const uint16_t* __res
   }
   // merge the two lane halves (disjoint vocabulary rows), then write this wave row's partial
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
+  for (int j = 0; j < 2; ++j) {
     const float om = __shfl_xor(m2[j], 32), os = __shfl_xor(ss[j], 32);
     const float nm = fmaxf(m2[j], om);
     float s = 0.f;
@@ -302,7 +372,7 @@ __global__ __launch_bounds__(NTHREADS, 1) void k_fwd_stats(const uint16_t* __res
       s = (m2[j] == -INFINITY ? 0.f : ss[j] * __builtin_amdgcn_exp2f(m2[j] - nm)) +
           (om == -INFINITY ? 0.f : os * __builtin_amdgcn_exp2f(om - nm));
     }
-    const int tok = n0 + wc * 128 + j * 32 + (lane & 31);
+    const int tok = n0 + wc * 64 + j * 32 + (lane & 31);
     if (lane < 32 && tok < nv) {
       const int64_t o = (int64_t)(2 * p + wr) * npad + tok;
       part_m[o] = nm;
@@ -456,36 +526,36 @@ __device__ __forceinline__ float grad_scale(const float* grad, const int* n_norm
 // Entries outside the valid tokens / slab columns are written as zeros where the later
 // contractions read them (K padding), so those loops need no masking.
 // ---------------------------------------------------------------------------------------------
-__global__ __launch_bounds__(NTHREADS, 1) void k_bwd_g(const uint16_t* __restrict__ W, int64_t ldw, int64_t v0, int vs,
+__global__ __launch_bounds__(NTHREADS, 2) void k_bwd_g(const uint16_t* __restrict__ W, int64_t ldw, int64_t v0, int vs,
                                                        const uint16_t* __restrict__ H, int64_t ldh, int64_t n,
                                                        const void* targets, int tbytes,
                                                        const int* __restrict__ idx, const int* __restrict__ nv_ptr,
                                                        const float* __restrict__ lse, const float* __restrict__ grad,
                                                        const int* __restrict__ n_norm, int reduction, int d, int tm_count,
                                                        uint16_t* __restrict__ G, int vc, uint16_t* __restrict__ Gt, int ldt) {
-  __shared__ __attribute__((aligned(16))) char smem[2 * LDS_STAGE];
+  __shared__ __attribute__((aligned(16))) char smem[LDS_BYTES];
   const int tm = blockIdx.x % tm_count, tn = blockIdx.x / tm_count;
   const int nv = *nv_ptr;
   const int n0 = tn * TILE;
   if (n0 >= nv) return;
   const int vt0 = tm * TILE;                 // slab-relative
   const int vleft = vs - vt0;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, wr = wave >> 1, wc = wave & 1;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, wr = wave >> 2, wc = wave & 3;
 
   __amdgpu_buffer_rsrc_t ra = make_rsrc(W + (v0 + vt0) * ldw, (uint64_t)vleft * ldw * 2);
   __amdgpu_buffer_rsrc_t rb = make_rsrc(H, (uint64_t)n * ldh * 2);
-  uint32_t aoff[8], boff[8];
+  uint32_t aoff[4], boff[4];
   dense_offsets(aoff, vleft, ldw);
   gather_offsets(boff, idx, n0, nv, ldh);
-  f32x16_t acc[4][4];
+  f32x16_t acc[4][2];
   mma_mainloop(acc, ra, aoff, rb, boff, d, smem);
 
   const float c = grad_scale(grad, n_norm, reduction);
-  int tok[4], tgt[4];
-  float l2[4];
+  int tok[2], tgt[2];
+  float l2[2];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    tok[j] = n0 + wc * 128 + j * 32 + (lane & 31);
+  for (int j = 0; j < 2; ++j) {
+    tok[j] = n0 + wc * 64 + j * 32 + (lane & 31);
     if (tok[j] < nv) {
       const int row = idx[tok[j]];
       l2[j] = lse[row] * kLog2e;
@@ -497,7 +567,7 @@ __global__ __launch_bounds__(NTHREADS, 1) void k_bwd_g(const uint16_t* __restric
   }
   const int vb = wr * 128 + (lane >> 5) * 4;  // tile-relative vocabulary row base of this lane
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
+  for (int j = 0; j < 2; ++j) {
     const bool tok_ok = tok[j] < nv;
 #pragma unroll
     for (int i = 0; i < 4; ++i)
@@ -537,27 +607,27 @@ __global__ __launch_bounds__(NTHREADS, 1) void k_bwd_g(const uint16_t* __restric
 }
 
 // K5: dW[v0 + m][dd] = sum_k Gt[m][k] Hvt[dd][k] over k < round_up(Nv, 64), written once in bf16.
-__global__ __launch_bounds__(NTHREADS, 1) void k_bwd_dw(const uint16_t* __restrict__ Gt, int ldt, int vs,
+__global__ __launch_bounds__(NTHREADS, 2) void k_bwd_dw(const uint16_t* __restrict__ Gt, int ldt, int vs,
                                                         const uint16_t* __restrict__ Hvt, int d,
                                                         const int* __restrict__ nv_ptr, int tm_count,
                                                         uint16_t* __restrict__ dW, int64_t v0) {
-  __shared__ __attribute__((aligned(16))) char smem[2 * LDS_STAGE];
+  __shared__ __attribute__((aligned(16))) char smem[LDS_BYTES];
   const int tm = blockIdx.x % tm_count, tn = blockIdx.x / tm_count;
   const int m0 = tm * TILE, d0 = tn * TILE;
   const int nv = *nv_ptr;
-  const int kpad = ((nv + BK - 1) / BK) * BK;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, wr = wave >> 1, wc = wave & 1;
+  const int kpad = ((nv + KPAD - 1) / KPAD) * KPAD;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, wr = wave >> 2, wc = wave & 3;
   __amdgpu_buffer_rsrc_t ra = make_rsrc(Gt + (int64_t)m0 * ldt, (uint64_t)(vs - m0) * ldt * 2);
   __amdgpu_buffer_rsrc_t rb = make_rsrc(Hvt + (int64_t)d0 * ldt, (uint64_t)(d - d0) * ldt * 2);
-  uint32_t aoff[8], boff[8];
+  uint32_t aoff[4], boff[4];
   dense_offsets(aoff, vs - m0, ldt);
   dense_offsets(boff, d - d0, ldt);
-  f32x16_t acc[4][4];
+  f32x16_t acc[4][2];
   mma_mainloop(acc, ra, aoff, rb, boff, kpad, smem);
   const int mb = m0 + wr * 128 + (lane >> 5) * 4;
-  const int dc = d0 + wc * 128 + (lane & 31);
+  const int dc = d0 + wc * 64 + (lane & 31);
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
+  for (int j = 0; j < 2; ++j) {
     const int col = dc + j * 32;
     if (col >= d) continue;
 #pragma unroll
@@ -571,27 +641,27 @@ __global__ __launch_bounds__(NTHREADS, 1) void k_bwd_dw(const uint16_t* __restri
 }
 
 // K6: dH32[m][dd] (+)= sum_k G[m][k] WsT[dd][k] over k < round_up(vs, 64); rows m < Nv.
-__global__ __launch_bounds__(NTHREADS, 1) void k_bwd_dh(const uint16_t* __restrict__ G, int vc, int kpad,
+__global__ __launch_bounds__(NTHREADS, 2) void k_bwd_dh(const uint16_t* __restrict__ G, int vc, int kpad,
                                                         const uint16_t* __restrict__ WsT, int d,
                                                         const int* __restrict__ nv_ptr, int tm_count,
                                                         float* __restrict__ dH32, int accumulate) {
-  __shared__ __attribute__((aligned(16))) char smem[2 * LDS_STAGE];
+  __shared__ __attribute__((aligned(16))) char smem[LDS_BYTES];
   const int tm = blockIdx.x % tm_count, tn = blockIdx.x / tm_count;
   const int m0 = tm * TILE, d0 = tn * TILE;
   const int nv = *nv_ptr;
   if (m0 >= nv) return;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, wr = wave >> 1, wc = wave & 1;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, wr = wave >> 2, wc = wave & 3;
   __amdgpu_buffer_rsrc_t ra = make_rsrc(G + (int64_t)m0 * vc, (uint64_t)(nv - m0) * vc * 2);
   __amdgpu_buffer_rsrc_t rb = make_rsrc(WsT + (int64_t)d0 * vc, (uint64_t)(d - d0) * vc * 2);
-  uint32_t aoff[8], boff[8];
+  uint32_t aoff[4], boff[4];
   dense_offsets(aoff, nv - m0, vc);
   dense_offsets(boff, d - d0, vc);
-  f32x16_t acc[4][4];
+  f32x16_t acc[4][2];
   mma_mainloop(acc, ra, aoff, rb, boff, kpad, smem);
   const int mb = m0 + wr * 128 + (lane >> 5) * 4;
-  const int dc = d0 + wc * 128 + (lane & 31);
+  const int dc = d0 + wc * 64 + (lane & 31);
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
+  for (int j = 0; j < 2; ++j) {
     const int col = dc + j * 32;
     if (col >= d) continue;
 #pragma unroll
@@ -670,8 +740,7 @@ lce_status_t make_plan(const lce_problem_t* p, Plan* pl) {
   if (ldh % 8 != 0 || ldw % 8 != 0) return LCE_ERR_ALIGN;
   // 32-bit limits: token / vocabulary indices, and byte offsets inside one buffer resource
   if (p->n >= (int64_t)1 << 30 || p->v >= (int64_t)1 << 30 || p->d >= (int64_t)1 << 20) return LCE_ERR_SHAPE;
-  if ((uint64_t)p->n * ldh * 2 > 0xFFFFFFFFull) return LCE_ERR_SHAPE;
-  if ((uint64_t)TILE * ldw * 2 > 0xFFFFFFFFull) return LCE_ERR_SHAPE;
+  if ((uint64_t)p->n * ldh * 2 > 0x7FFFFFFFull) return LCE_ERR_SHAPE;
   pl->n = p->n; pl->d = p->d; pl->v = p->v; pl->ldh = ldh; pl->ldw = ldw;
   pl->npad = round_up(p->n > 0 ? p->n : 1, TILE);
   pl->nt_max = (int)(pl->npad / TILE);
@@ -684,9 +753,7 @@ lce_status_t make_plan(const lce_problem_t* p, Plan* pl) {
   if (vc > vround) vc = vround;
   pl->vc = vc;
   pl->nslab = (p->v + vc - 1) / vc;
-  if ((uint64_t)pl->npad * vc * 2 > 0xFFFFFFFFull || (uint64_t)vc * pl->npad * 2 > 0xFFFFFFFFull ||
-      (uint64_t)p->d * pl->npad * 2 > 0xFFFFFFFFull)
-    return LCE_ERR_SHAPE;
+  if ((uint64_t)TILE * pl->npad * 2 > 0x7FFFFFFFull) return LCE_ERR_SHAPE;
 
   auto take = [](size_t& cur, size_t bytes) { size_t o = cur; cur += (bytes + 255) / 256 * 256; return o; };
   size_t cur = 0;
