@@ -1,0 +1,83 @@
+"""HIP path vs the CPU oracle at the full workload sizes, in the launch configuration the
+benchmark times (same library calls, same shapes).
+
+The oracle's forward (loss and every row's lse) for seed 0 is stored under tests/golden/ by
+``tests/golden/make_golden.py`` (oracle only); sampled rows of dH and dW are computed here by the
+oracle one by one: dH rows need only their own logits, dW rows need the stored lse of every valid
+row. Whole-output properties (ignored dH rows are exactly zero, dW columns sum to ~0, everything
+finite) are checked on the full GPU outputs.
+"""
+import os
+
+import numpy as np
+import pytest
+
+from oracle import lce_oracle as O
+from paper_2605_21442_amd import workloads as WL
+from tests import lce_testutil as U
+from tests.golden import make_golden as MG
+
+pytestmark = pytest.mark.gpu
+
+NAMES = ["llama1b", "llama8b", "qwen7b", "llama70b"]
+
+
+def _say(msg):
+    print(msg, flush=True)
+
+
+@pytest.mark.parametrize("name", NAMES)
+def test_full_size_against_oracle(name):
+    import torch
+    path = MG.path_for(name, 0)
+    if not os.path.exists(path):
+        pytest.skip(f"{path} missing: run tests/golden/make_golden.py")
+    gold = np.load(path, allow_pickle=False)
+    wl = WL.WORKLOADS[name]
+    _say(f"[{name}] drawing inputs")
+    inp = WL.generate(wl, 0)
+    assert str(gold["fingerprint"]) == MG.fingerprint(inp), "golden file is stale"
+    h, w, t = U.to_device(inp)
+    _say(f"[{name}] running lce_forward + lce_backward")
+    gpu = U.run_gpu(h, w, t, backward=True)
+    dh_t, dw_t = gpu.pop("dH_t"), gpu.pop("dW_t")
+
+    # forward: exact count, loss, every lse
+    assert gpu["n_valid"] == int(gold["n_valid"]) == wl.n_valid()
+    assert gpu["status"] == 0
+    assert abs(gpu["loss"] - float(gold["loss"])) <= U.LOSS_ABS_TOL, (gpu["loss"], float(gold["loss"]))
+    valid = inp.targets != inp.ignore_index
+    lse_err = np.max(np.abs(gpu["lse"][valid] - gold["lse"][valid]))
+    assert lse_err <= U.LSE_ABS_TOL, lse_err
+    assert np.all(gpu["lse"][~valid] == 0.0)
+
+    # whole-output properties on the GPU
+    ign = torch.from_numpy(~valid).to(h.device)
+    assert torch.count_nonzero(dh_t[ign]).item() == 0
+    assert torch.isfinite(dh_t.float()).all().item() and torch.isfinite(dw_t.float()).all().item()
+    col = dw_t.float().sum(0)
+    budget = 4 * 2.0 ** -8 * dw_t.float().abs().sum(0)
+    assert bool((col.abs() <= budget).all().item())
+
+    # sampled dH rows (valid and ignored)
+    rng = np.random.default_rng(7)
+    vrows = np.nonzero(valid)[0]
+    irows = np.nonzero(~valid)[0]
+    rows = np.concatenate([rng.choice(vrows, 6, replace=False), vrows[[0, -1]], irows[:2]])
+    _say(f"[{name}] oracle dH rows {rows.tolist()}")
+    ref_dh = O.dh_of_rows(inp.h_bits, inp.w_bits, inp.targets, rows, int(gold["n_valid"]))
+    got_dh = dh_t[torch.from_numpy(rows).to(h.device)].float().cpu().numpy().astype(np.float64)
+    e = U.rel_fro(got_dh, ref_dh)
+    assert e <= U.GRAD_REL_TOL, ("dH", e)
+    assert np.all(got_dh[-2:] == 0.0)
+
+    # sampled dW rows: most frequent ids, tile and slab edges, the last id, random ids
+    v = wl.v
+    ids = [0, 1, 2, 255, 256, 4095, 4096, 8191, 8192, v - 1] + rng.integers(3, v, 4).tolist()
+    ids = np.array(sorted(set(i for i in ids if i < v)))
+    _say(f"[{name}] oracle dW rows {ids.tolist()}")
+    ref_dw = O.dw_of_rows(inp.h_bits, inp.w_bits, inp.targets, ids, gold["lse"])
+    got_dw = dw_t[torch.from_numpy(ids).to(h.device)].float().cpu().numpy().astype(np.float64)
+    e = U.rel_fro(got_dw, ref_dw)
+    assert e <= U.GRAD_REL_TOL, ("dW", e)
+    _say(f"[{name}] ok: loss {gpu['loss']:.6f} (oracle {float(gold['loss']):.6f}), lse err {lse_err:.2e}")
