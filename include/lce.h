@@ -79,7 +79,7 @@ typedef struct lce_problem {
 
 /*
  * Workspace sizes, in bytes, for lce_forward (*fwd_bytes) and lce_backward
- * (*bwd_bytes). They grow as O(N*D + D*V_slab) with V_slab <= max(4096, 2*D)
+ * (*bwd_bytes). They grow as O(N*D + D*V_slab) with V_slab <= max(8192, 4*D)
  * rounded to 256: never O(N*V). Either output pointer may be NULL.
  */
 lce_status_t lce_workspace_size(const lce_problem_t* p, size_t* fwd_bytes, size_t* bwd_bytes);

@@ -314,7 +314,19 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_fwd_stats(const uint16_t* __res
                                                            float* __restrict__ part_m, float* __restrict__ part_s,
                                                            int npad) {
   __shared__ __attribute__((aligned(16))) char smem[LDS_BYTES];
-  const int nt = blockIdx.x % nt_max, p = blockIdx.x / nt_max;
+  // Workgroups are dispatched round-robin over the 8 XCDs (block b runs on XCD b % 8). Give each
+  // XCD whole vocabulary partitions (p = xcd + 8 i) and walk all token tiles of one partition
+  // before the next, so the workgroups resident on one XCD stream the same W tiles through that
+  // XCD's L2 at about the same time.
+  int nt, p;
+  if (nparts % 8 == 0) {
+    const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
+    p = xcd + 8 * (slot / nt_max);
+    nt = slot % nt_max;
+  } else {
+    nt = blockIdx.x % nt_max;
+    p = blockIdx.x / nt_max;
+  }
   const int nv = *nv_ptr;
   const int n0 = nt * TILE;
   if (n0 >= nv) return;
@@ -511,6 +523,22 @@ __global__ __launch_bounds__(256) void k_transpose(const uint16_t* __restrict__ 
   }
 }
 
+// Tile scheduling for the backward contractions. Workgroups are dispatched round-robin over the
+// 8 XCDs (block b runs on XCD b % 8), each with its own L2. XCD x owns the band of row tiles
+// [x T / 8, (x + 1) T / 8) (T = live row tiles) and walks it column by column, so the ~32
+// workgroups resident on one XCD share the band's A tiles and a few B tiles in its L2, and each
+// large A operand is fetched by one XCD only. The grid is 8 * ceil(T_max / 8) * tn_count blocks;
+// blocks past the live tiles return false.
+__device__ __forceinline__ bool band_tile(int tm_live, int tn_count, int& tm, int& tn) {
+  const int x = blockIdx.x & 7, k = blockIdx.x >> 3;
+  const int r0 = (x * tm_live) >> 3, r1 = ((x + 1) * tm_live) >> 3;
+  const int rows = r1 - r0;
+  if (rows <= 0 || k >= rows * tn_count) return false;
+  tm = r0 + k % rows;
+  tn = k / rows;
+  return true;
+}
+
 // scale c = g / n_norm (mean) or g (sum); 0 when the count is 0
 __device__ __forceinline__ float grad_scale(const float* grad, const int* n_norm, int reduction) {
   const float g = *grad;
@@ -534,8 +562,8 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_bwd_g(const uint16_t* __restric
                                                        const int* __restrict__ n_norm, int reduction, int d, int tm_count,
                                                        uint16_t* __restrict__ G, int vc, uint16_t* __restrict__ Gt, int ldt) {
   __shared__ __attribute__((aligned(16))) char smem[LDS_BYTES];
-  const int tm = blockIdx.x % tm_count, tn = blockIdx.x / tm_count;
   const int nv = *nv_ptr;
+  const int tm = blockIdx.x % tm_count, tn = blockIdx.x / tm_count;
   const int n0 = tn * TILE;
   if (n0 >= nv) return;
   const int vt0 = tm * TILE;                 // slab-relative
@@ -612,7 +640,8 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_bwd_dw(const uint16_t* __restri
                                                         const int* __restrict__ nv_ptr, int tm_count,
                                                         uint16_t* __restrict__ dW, int64_t v0) {
   __shared__ __attribute__((aligned(16))) char smem[LDS_BYTES];
-  const int tm = blockIdx.x % tm_count, tn = blockIdx.x / tm_count;
+  int tm, tn;
+  if (!band_tile(tm_count, (d + TILE - 1) / TILE, tm, tn)) return;
   const int m0 = tm * TILE, d0 = tn * TILE;
   const int nv = *nv_ptr;
   const int kpad = ((nv + KPAD - 1) / KPAD) * KPAD;
@@ -646,10 +675,10 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_bwd_dh(const uint16_t* __restri
                                                         const int* __restrict__ nv_ptr, int tm_count,
                                                         float* __restrict__ dH32, int accumulate) {
   __shared__ __attribute__((aligned(16))) char smem[LDS_BYTES];
-  const int tm = blockIdx.x % tm_count, tn = blockIdx.x / tm_count;
-  const int m0 = tm * TILE, d0 = tn * TILE;
   const int nv = *nv_ptr;
-  if (m0 >= nv) return;
+  int tm, tn;
+  if (!band_tile((nv + TILE - 1) / TILE, (d + TILE - 1) / TILE, tm, tn)) return;
+  const int m0 = tm * TILE, d0 = tn * TILE;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, wr = wave >> 2, wc = wave & 3;
   __amdgpu_buffer_rsrc_t ra = make_rsrc(G + (int64_t)m0 * vc, (uint64_t)(nv - m0) * vc * 2);
   __amdgpu_buffer_rsrc_t rb = make_rsrc(WsT + (int64_t)d0 * vc, (uint64_t)(d - d0) * vc * 2);
@@ -658,21 +687,56 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_bwd_dh(const uint16_t* __restri
   dense_offsets(boff, d - d0, vc);
   f32x16_t acc[4][2];
   mma_mainloop(acc, ra, aoff, rb, boff, kpad, smem);
+  // Read-modify-write of the fp32 accumulator, one 32-row block (32 values per lane) at a time
+  // so that its 32 loads are in flight together; interior tiles skip the bounds tests.
   const int mb = m0 + wr * 128 + (lane >> 5) * 4;
   const int dc = d0 + wc * 64 + (lane & 31);
+  const bool interior = (m0 + TILE <= nv) && (d0 + TILE <= d);
+  float* base = dH32 + (int64_t)mb * d + dc;
+  if (interior) {
+    if (accumulate) {
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    const int col = dc + j * 32;
-    if (col >= d) continue;
+      for (int i = 0; i < 4; ++i) {
+        float old[2][16];
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            old[j][r] = base[(int64_t)(i * 32 + (r >> 2) * 8 + (r & 3)) * d + j * 32];
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            base[(int64_t)(i * 32 + (r >> 2) * 8 + (r & 3)) * d + j * 32] = old[j][r] + acc[i][j][r];
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            base[(int64_t)(i * 32 + (r >> 2) * 8 + (r & 3)) * d + j * 32] = acc[i][j][r];
+    }
+    return;
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    float old[2][16];
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int m = mb + i * 32 + (r >> 2) * 8 + (r & 3);
-        if (m < nv) {
-          float* p = dH32 + (int64_t)m * d + col;
-          *p = accumulate ? *p + acc[i][j][r] : acc[i][j][r];
-        }
+        const bool ok = accumulate && m < nv && dc + j * 32 < d;
+        old[j][r] = ok ? dH32[(int64_t)m * d + dc + j * 32] : 0.f;
+      }
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int m = mb + i * 32 + (r >> 2) * 8 + (r & 3);
+        if (m < nv && dc + j * 32 < d) dH32[(int64_t)m * d + dc + j * 32] = old[j][r] + acc[i][j][r];
       }
   }
 }
@@ -746,8 +810,10 @@ lce_status_t make_plan(const lce_problem_t* p, Plan* pl) {
   pl->nt_max = (int)(pl->npad / TILE);
   pl->vt_count = (int)((p->v + TILE - 1) / TILE);
   pl->nparts = pl->vt_count < MAX_PARTS ? pl->vt_count : MAX_PARTS;
-  int64_t vc = 2 * p->d;
-  if (vc < 4096) vc = 4096;
+  // backward vocabulary slab: 4 D columns (at least 8192) keeps G and Gt at O(N D) while
+  // halving the dH accumulator passes of a 2 D slab
+  int64_t vc = 4 * p->d;
+  if (vc < 8192) vc = 8192;
   vc = round_up(vc, TILE);
   const int64_t vround = round_up(p->v, TILE);
   if (vc > vround) vc = vround;
@@ -908,9 +974,9 @@ lce_status_t lce_backward(const lce_problem_t* p, const void* H, const void* W, 
     L(K_BWD_G, k_bwd_g, dim3((unsigned)(tm * pl.nt_max)), dim3(NTHREADS), w, pl.ldw, v0, vs, h, pl.ldh, pl.n,
       targets, p->target_bytes, (const int*)idx, (const int*)nv, lse, grad_loss, (const int*)n_valid,
       p->reduction, d, tm, g, vc, gt, npad);
-    L(K_BWD_DW, k_bwd_dw, dim3((unsigned)(tm * dt)), dim3(NTHREADS), (const uint16_t*)gt, npad, vs,
+    L(K_BWD_DW, k_bwd_dw, dim3((unsigned)(8 * ((tm + 7) / 8) * dt)), dim3(NTHREADS), (const uint16_t*)gt, npad, vs,
       (const uint16_t*)hvt, d, (const int*)nv, tm, (uint16_t*)dW, v0);
-    L(K_BWD_DH, k_bwd_dh, dim3((unsigned)(pl.nt_max * dt)), dim3(NTHREADS), (const uint16_t*)g, vc, vs64,
+    L(K_BWD_DH, k_bwd_dh, dim3((unsigned)(8 * ((pl.nt_max + 7) / 8) * dt)), dim3(NTHREADS), (const uint16_t*)g, vc, vs64,
       (const uint16_t*)wst, d, (const int*)nv, pl.nt_max, dh32, (int)(s > 0));
   }
   const int64_t nthr = pl.n * pl.d / 8;
