@@ -36,21 +36,51 @@ def _cpu_baseline(inp, seconds_target=10.0):
     except Exception:  # pragma: no cover
         threads = os.cpu_count() or 1
     valid = np.nonzero(inp.targets != inp.ignore_index)[0]
-    sample = 16
-    t0 = time.perf_counter()
-    O.lce(inp.h_bits[valid[:sample]], inp.w_bits, inp.targets[valid[:sample]])
-    dt = time.perf_counter() - t0
-    # grow the sample to roughly the target duration (one more run, not timed twice)
-    per_tok = dt / sample
-    sample2 = int(min(len(valid), max(sample, seconds_target / max(per_tok, 1e-9))))
-    if sample2 > sample:
+    # double the token sample until one oracle run takes at least `seconds_target`
+    sample = 32
+    while True:
         t0 = time.perf_counter()
-        O.lce(inp.h_bits[valid[:sample2]], inp.w_bits, inp.targets[valid[:sample2]])
+        O.lce(inp.h_bits[valid[:sample]], inp.w_bits, inp.targets[valid[:sample]])
         dt = time.perf_counter() - t0
-        sample = sample2
+        if dt >= seconds_target or sample >= len(valid):
+            break
+        sample = min(len(valid), max(2 * sample, int(sample * 1.2 * seconds_target / max(dt, 1e-3))))
     return {"value": sample / dt, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
             "sample": f"{sample} valid tokens of the {inp.workload.name} batch, full D and V, "
                       f"fp64 forward+backward ({dt:.1f} s)"}
+
+
+def _copy_calibration(gib=1.0, reps=3):
+    """A plain device copy of a known size, for scaling the HBM byte counters (FETCH_SIZE,
+    WRITE_SIZE) of a profiled run: each copy reads and writes exactly `gib` GiB."""
+    import torch
+    n = int(gib * (1 << 30))
+    a = torch.empty(n, dtype=torch.uint8, device="cuda:0").fill_(1)
+    b = torch.empty_like(a)
+    torch.cuda.synchronize()
+    for _ in range(reps):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_per_launch": n, "launches": reps}), flush=True)
+
+
+def _traffic(kernel):
+    """HBM bytes per launch of `kernel` from the committed counter summary, or None when that
+    summary was taken on a different kernel source."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "traffic_llama8b.txt")
+    src = os.path.join(ROOT, "paper_2605_21442_amd", "csrc", "lce.hip")
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    for line in open(path):
+        if ":" in line and not line.startswith("#"):
+            k, v = line.split(":", 1)
+            kv[k.strip()] = v.strip()
+    if kv.get("lce.hip sha256") != hashlib.sha256(open(src, "rb").read()).hexdigest():
+        return None
+    key = f"{kernel} bytes per launch"
+    return float(kv[key]) if key in kv else None
 
 
 def main():
@@ -61,7 +91,12 @@ def main():
     ap.add_argument("--workload", default="llama8b")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="run only a 1 GiB device copy (for scaling HBM byte counters)")
     args = ap.parse_args()
+    if args.copy_calibration:
+        _copy_calibration()
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for {args.gpus}); the LCE path here has no "
               f"multi-GPU mode", file=sys.stderr)
@@ -165,7 +200,7 @@ def main():
         "workspace_bytes": int(max(fwd_bytes, bwd_bytes)),
         "logits_bytes_avoided_fp32": int(n) * int(v) * 4,
         "roofline": {"bound": "mfma", "kernel": dom, "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
-                     "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
+                     "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS, "traffic": _traffic(dom),
                      "flops_per_launch": flops_launch, "avg_launch_ms": kernels[dom]["avg_ms"]},
         "kernels_ms_per_step": {k: r["total_ms"] / args.steps for k, r in kernels.items()},
     }
