@@ -37,6 +37,8 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef int i32x4_t __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
+typedef short s16x4_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4_t lds_s16x4_t;
 
 constexpr int TILE = 256;         // output tile edge (rows of A and of B per workgroup)
 constexpr int KPAD = 64;          // K padding granularity of the backward's staged operands
@@ -593,44 +595,68 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_bwd_g(const uint16_t* __restric
       tgt[j] = -1;
     }
   }
+  // G values in place, then the bf16 tile goes through LDS (free after the main loop) as
+  // T[token][v], 512-byte rows whose 16-byte chunk c sits at c ^ (token & 31), so that both the
+  // token-major rows of G and the vocabulary-major rows of Gt leave with wide coalesced stores.
   const int vb = wr * 128 + (lane >> 5) * 4;  // tile-relative vocabulary row base of this lane
+  char* T = smem;
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
     const bool tok_ok = tok[j] < nv;
+    const int nl = wc * 64 + j * 32 + (lane & 31);
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int vr = vb + i * 32 + (r >> 2) * 8 + (r & 3);
-        float g = 0.f;
-        if (tok_ok && vr < vleft) {
-          g = c * __builtin_amdgcn_exp2f(fmaf(acc[i][j][r], kLog2e, -l2[j]));
-          if (vr == tgt[j]) g -= c;
+      for (int q = 0; q < 4; ++q) {
+        float gq[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int r = q * 4 + e;
+          const int vr = vb + i * 32 + q * 8 + e;
+          float g = 0.f;
+          if (tok_ok && vr < vleft) {
+            g = c * __builtin_amdgcn_exp2f(fmaf(acc[i][j][r], kLog2e, -l2[j]));
+            if (vr == tgt[j]) g -= c;
+          }
+          gq[e] = g;
         }
-        acc[i][j][r] = g;
+        const int vl = vb + i * 32 + q * 8;
+        u32x2_t pk;
+        pk.x = pack_bf16x2(gq[0], gq[1]);
+        pk.y = pack_bf16x2(gq[2], gq[3]);
+        const uint32_t a = (uint32_t)(nl * 512 + ((((vl >> 3) ^ (nl & 31))) << 4) + ((vl & 7) << 1));
+        *reinterpret_cast<u32x2_t*>(T + a) = pk;
       }
-    // G[token][v]: 4 consecutive v per register group -> 8-byte stores
-    if (tok_ok) {
-      uint16_t* grow = G + (int64_t)tok[j] * vc + vt0;
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int vr = vb + i * 32 + q * 8;
-          u32x2_t pk;
-          pk.x = pack_bf16x2(acc[i][j][q * 4 + 0], acc[i][j][q * 4 + 1]);
-          pk.y = pack_bf16x2(acc[i][j][q * 4 + 2], acc[i][j][q * 4 + 3]);
-          *reinterpret_cast<u32x2_t*>(grow + vr) = pk;
-        }
+  }
+  __syncthreads();
+  // G rows (tokens < Nv): 16-byte chunks, one 512-byte row per 32 threads
+#pragma unroll 4
+  for (int it = 0; it < 16; ++it) {
+    const int q = threadIdx.x + NTHREADS * it;
+    const int nl = q >> 5, ch = q & 31;
+    if (n0 + nl < nv) {
+      const i32x4_t val = *reinterpret_cast<const i32x4_t*>(T + nl * 512 + ((ch ^ (nl & 31)) << 4));
+      *reinterpret_cast<i32x4_t*>(G + (int64_t)(n0 + nl) * vc + vt0 + ch * 8) = val;
     }
-    // Gt[v][token]: lanes hold consecutive tokens -> 2-byte stores, 64 contiguous bytes per row
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int vr = vb + i * 32 + (r >> 2) * 8 + (r & 3);
-        if (vr < vleft) Gt[(int64_t)(vt0 + vr) * ldt + tok[j]] = to_bf16(acc[i][j][r]);
-      }
+  }
+  // Gt rows (vocabulary rows < slab width): a transposing LDS read gives each lane 4 consecutive
+  // tokens of one vocabulary row. In a 16-lane group, lane i reads 8 bytes (4 vocabulary ids) of
+  // token row nb + 4 (i % 4) + i / 4; lane j receives vocabulary id vq + j % 4 of tokens
+  // nb + 4 (j / 4) .. +3. One wave instruction covers 4 vocabulary rows x 64 tokens.
+  {
+    const int grp = lane >> 4, i16 = lane & 15;
+#pragma unroll 4
+    for (int kk = 0; kk < 32; ++kk) {
+      const int item = wave * 32 + kk;
+      const int vq = (item >> 2) * 4;
+      const int nb = (item & 3) * 64 + grp * 16;
+      const int nl = nb + 4 * (i16 & 3) + (i16 >> 2);
+      const uint32_t a = (uint32_t)(nl * 512 + ((((vq >> 3) ^ (nl & 31))) << 4) + ((vq & 7) << 1));
+      const s16x4_t t4 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(T + a));
+      const int vrow = vq + (i16 & 3);
+      if (vrow < vleft)
+        *reinterpret_cast<s16x4_t*>(Gt + (int64_t)(vt0 + vrow) * ldt + n0 + nb + 4 * (i16 >> 2)) = t4;
+    }
   }
 }
 
