@@ -11,8 +11,11 @@
  *   M   = { n : t_n != ignore_index and 0 <= t_n < V },  Nv = |M|
  *   s   = H W^T (per row; never stored whole)
  *   lse_n = log sum_v exp(s[n, v]),   l_n = lse_n - s[n, t_n]            (n in M)
- *   L   = (1/Nv) sum_{n in M} l_n  (mean)   or   sum_{n in M} l_n  (sum)
- *   G   = c (softmax(s) - onehot(t)) on rows in M, 0 elsewhere;  c = g/Nv (mean) or g (sum)
+ *   L   = (1/Nv) sum_{n in M} l_n  (mean),  sum_{n in M} l_n  (sum),
+ *         or the per-token vector l_n, 0 outside M  (none: minus the per-token
+ *         log-probability of the target, the quantity DPO / GRPO style losses consume)
+ *   G   = c_n (softmax(s) - onehot(t)) on rows in M, 0 elsewhere;
+ *         c_n = g/Nv (mean), g (sum) or g_n (none, one upstream gradient per token)
  *   dH  = G W,   dW = G^T H
  *
  * Conventions shared by every entry point
@@ -59,7 +62,8 @@ typedef enum lce_status {
 
 typedef enum lce_reduction {
   LCE_REDUCE_MEAN = 0,      /* divide by the valid-token count Nv of this call */
-  LCE_REDUCE_SUM = 1
+  LCE_REDUCE_SUM = 1,
+  LCE_REDUCE_NONE = 2       /* per-token losses; loss and grad_loss are [N] arrays */
 } lce_reduction_t;
 
 /* Bit set in *dev_status by lce_forward when some target is neither ignore_index nor in [0, V). */
@@ -87,7 +91,8 @@ lce_status_t lce_workspace_size(const lce_problem_t* p, size_t* fwd_bytes, size_
 /*
  * Forward pass (paper Sec. 4.2): computes the loss without materialising the
  * logits. Outputs, all device memory:
- *   loss        [1] fp32: L (mean or sum; 0 when Nv = 0)
+ *   loss        fp32: [1] L for mean / sum (0 when Nv = 0); [N] per-token losses
+ *               for LCE_REDUCE_NONE (0.0 on ignored / bad rows)
  *   lse         [N] fp32: lse_n for valid rows, 0.0 for ignored / bad rows;
  *               keep it for lce_backward
  *   n_valid     [1] int32: Nv
@@ -105,8 +110,9 @@ lce_status_t lce_forward(const lce_problem_t* p,
  *   lse         [N] fp32 from lce_forward on the same inputs
  *   n_valid     [1] int32: the count that "mean" divides by (lce_forward's
  *               n_valid on one device; a global count when the tokens of one
- *               batch are spread over several calls)
- *   grad_loss   [1] fp32: upstream gradient g of L (read on the device)
+ *               batch are spread over several calls); unused for NONE
+ *   grad_loss   fp32, read on the device: [1] upstream gradient g of L for mean /
+ *               sum; [N] upstream gradients g_n of the per-token losses for NONE
  *   dH          [N, D] bf16, overwritten; rows of ignored tokens are +0.0
  *   dW          [V, D] bf16, overwritten
  */

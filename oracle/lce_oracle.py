@@ -16,9 +16,12 @@ representable in float64), materialising each row's full-vocabulary logits:
   logits           s[n, v] = sum_d H[n, d] * W[v, d]
   log-sum-exp      lse_n = m_n + ln sum_v exp(s[n, v] - m_n),  m_n = max_v s[n, v]
   per-row loss     l_n = lse_n - s[n, t_n]                        (n in M)
-  reduction        L = (1 / Nv) sum_{n in M} l_n   ("mean")  or  sum_{n in M} l_n  ("sum")
-  softmax grad     G[n, v] = c * (exp(s[n, v] - lse_n) - [v == t_n])  (n in M; 0 otherwise)
-                   c = g / Nv for "mean", c = g for "sum"; g = upstream gradient of L
+  reduction        L = (1 / Nv) sum_{n in M} l_n   ("mean"),  sum_{n in M} l_n  ("sum"),
+                   or the vector of l_n with 0 on rows outside M ("none": per-token losses, i.e.
+                   minus the per-token log-probabilities of the targets)
+  softmax grad     G[n, v] = c_n * (exp(s[n, v] - lse_n) - [v == t_n])  (n in M; 0 otherwise)
+                   c_n = g / Nv for "mean", c_n = g for "sum" (g = upstream gradient of L),
+                   c_n = g_n for "none" (g = vector of upstream gradients of the l_n)
   gradients        dH = G W,  dW = G^T H
 
 Readings where the paper is silent (each is also listed in the design notes):
@@ -64,8 +67,11 @@ def row_lse(h_rows: np.ndarray, w: np.ndarray) -> np.ndarray:
     return m + np.log(np.exp(s - m[:, None]).sum(axis=1))
 
 
-def scale_c(n_valid: int, reduction: str, grad: float) -> float:
-    """Scale of the softmax gradient: g / Nv for "mean", g for "sum" (0 when Nv = 0)."""
+def scale_c(n_valid: int, reduction: str, grad):
+    """Scale of the softmax gradient: g / Nv for "mean", g for "sum" (0 when Nv = 0), and the
+    per-row upstream gradients for "none" (an array, returned as float64)."""
+    if reduction == "none":
+        return np.asarray(grad, dtype=np.float64)
     if reduction not in ("mean", "sum"):
         raise ValueError(f"unknown reduction {reduction!r}")
     if n_valid == 0:
@@ -89,25 +95,28 @@ def forward(h, w, targets, ignore_index=-100, reduction="mean", block=512):
         lse[r] = lse_r
         per_row[r] = lse_r - s[np.arange(r.size), t[r]]
     nv = int(rows.size)
-    if nv == 0:
+    if reduction == "none":
+        loss = per_row.copy()
+    elif nv == 0:
         loss = 0.0
     elif reduction == "mean":
-        loss = per_row[rows].sum() / nv
+        loss = float(per_row[rows].sum() / nv)
     elif reduction == "sum":
-        loss = per_row[rows].sum()
+        loss = float(per_row[rows].sum())
     else:
         raise ValueError(f"unknown reduction {reduction!r}")
-    return {"loss": float(loss), "lse": lse, "per_row": per_row, "n_valid": nv, "status": status}
+    return {"loss": loss, "lse": lse, "per_row": per_row, "n_valid": nv, "status": status}
 
 
 def softmax_grad_rows(h_rows, w, t_rows, c):
-    """G rows c * (softmax(s) - onehot(t)) for valid float64 rows of H."""
+    """G rows c * (softmax(s) - onehot(t)) for valid float64 rows of H (c scalar or per row)."""
     s = h_rows @ w.T
     m = s.max(axis=1)
     lse = m + np.log(np.exp(s - m[:, None]).sum(axis=1))
     g = np.exp(s - lse[:, None])
     g[np.arange(len(t_rows)), t_rows] -= 1.0
-    return c * g
+    c = np.asarray(c, dtype=np.float64)
+    return (c[:, None] if c.ndim == 1 else c) * g
 
 
 def backward(h, w, targets, ignore_index=-100, reduction="mean", grad=1.0, block=512):
@@ -121,7 +130,7 @@ def backward(h, w, targets, ignore_index=-100, reduction="mean", grad=1.0, block
     dw = np.zeros_like(w)
     for s0 in range(0, rows.size, block):
         r = rows[s0:s0 + block]
-        g = softmax_grad_rows(h[r], w, t[r], c)
+        g = softmax_grad_rows(h[r], w, t[r], c[r] if reduction == "none" else c)
         dh[r] = g @ w
         dw += g.T @ h[r]
     return {"dH": dh, "dW": dw}
@@ -159,7 +168,8 @@ def dh_of_rows(h_bits, w_bits, targets, rows, n_valid, ignore_index=-100,
     out = np.zeros((len(rows), w.shape[1]), dtype=np.float64)
     for i, r in enumerate(rows):
         if ok[r]:
-            g = softmax_grad_rows(bf16_to_f64(h_bits[r:r + 1]), w, t[r:r + 1], c)
+            g = softmax_grad_rows(bf16_to_f64(h_bits[r:r + 1]), w, t[r:r + 1],
+                                  c[r:r + 1] if reduction == "none" else c)
             out[i] = (g @ w)[0]
     return out
 
@@ -179,5 +189,5 @@ def dw_of_rows(h_bits, w_bits, targets, vrows, lse_valid, ignore_index=-100,
         hr = bf16_to_f64(h_bits[r])                            # [b, D]
         p = np.exp(hr @ wv.T - lse_valid[r][:, None])          # softmax columns of these ids
         p -= (t[r][:, None] == np.asarray(vrows)[None, :])
-        out += (c * p).T @ hr
+        out += ((c[r][:, None] if reduction == "none" else c) * p).T @ hr
     return out

@@ -42,7 +42,8 @@ def _stream(dev: torch.device) -> int:
 
 def forward(hidden: torch.Tensor, weight: torch.Tensor, targets: torch.Tensor,
             ignore_index: int = -100, reduction: str = "mean"):
-    """(loss fp32 [], lse fp32 [N], n_valid int32 [1], status int32 [1]) computed by lce_forward."""
+    """(loss, lse fp32 [N], n_valid int32 [1], status int32 [1]) computed by lce_forward; loss is
+    a fp32 scalar for "mean" / "sum" and the fp32 per-token losses [N] for "none"."""
     h, ldh = _as_rows(hidden, "hidden")
     w, ldw = _as_rows(weight, "weight")
     n, d = h.shape
@@ -54,7 +55,7 @@ def forward(hidden: torch.Tensor, weight: torch.Tensor, targets: torch.Tensor,
                   target_bytes=tb)
     fwd_bytes, _ = B.lce_workspace_size(p)
     dev = h.device
-    loss = torch.empty((), dtype=torch.float32, device=dev)
+    loss = torch.empty((n,) if reduction == "none" else (), dtype=torch.float32, device=dev)
     lse = torch.empty(n, dtype=torch.float32, device=dev)
     nv = torch.empty(1, dtype=torch.int32, device=dev)
     status = torch.empty(1, dtype=torch.int32, device=dev)
@@ -77,8 +78,10 @@ def backward(hidden: torch.Tensor, weight: torch.Tensor, targets: torch.Tensor, 
                   target_bytes=tb)
     _, bwd_bytes = B.lce_workspace_size(p)
     dev = h.device
-    if grad_loss.dtype != torch.float32 or grad_loss.numel() != 1 or not grad_loss.is_cuda:
-        raise ValueError("grad_loss must be a one-element float32 GPU tensor")
+    want = n if reduction == "none" else 1
+    if grad_loss.dtype != torch.float32 or grad_loss.numel() != want or not grad_loss.is_cuda:
+        raise ValueError(f"grad_loss must be a {want}-element float32 GPU tensor")
+    grad_loss = grad_loss.contiguous()
     if lse.dtype != torch.float32 or lse.numel() != n or not lse.is_contiguous():
         raise ValueError("lse must be the contiguous float32 [N] tensor from forward")
     dh = torch.empty((n, d), dtype=torch.bfloat16, device=dev)
@@ -99,12 +102,12 @@ class LinearCrossEntropy(torch.autograd.Function):
         ctx.save_for_backward(hidden, weight, targets, lse, nv)
         ctx.ignore_index = ignore_index
         ctx.reduction = reduction
-        return loss
+        return loss.view(targets.shape) if reduction == "none" else loss
 
     @staticmethod
     def backward(ctx, grad):
         hidden, weight, targets, lse, nv = ctx.saved_tensors
-        g = grad.reshape(1)
+        g = grad.reshape(-1)
         if g.dtype != torch.float32:
             g = g.float()
         dh, dw = backward(hidden, weight, targets, lse, nv, g, ctx.ignore_index, ctx.reduction)
@@ -113,5 +116,6 @@ class LinearCrossEntropy(torch.autograd.Function):
 
 def linear_cross_entropy(hidden: torch.Tensor, weight: torch.Tensor, targets: torch.Tensor,
                          ignore_index: int = -100, reduction: str = "mean") -> torch.Tensor:
-    """Mean (or sum) cross-entropy of ``hidden @ weight.T`` against ``targets``, without the logits."""
+    """Cross-entropy of ``hidden @ weight.T`` against ``targets`` without the logits: the mean over
+    valid tokens, their sum, or (``reduction="none"``) the per-token losses, shaped like targets."""
     return LinearCrossEntropy.apply(hidden, weight, targets, ignore_index, reduction)

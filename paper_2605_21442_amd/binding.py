@@ -26,9 +26,10 @@ LCE_ERR_ARG = 7
 
 LCE_REDUCE_MEAN = 0
 LCE_REDUCE_SUM = 1
+LCE_REDUCE_NONE = 2
 LCE_STATUS_TARGET_OUT_OF_RANGE = 1
 
-REDUCTIONS = {"mean": LCE_REDUCE_MEAN, "sum": LCE_REDUCE_SUM}
+REDUCTIONS = {"mean": LCE_REDUCE_MEAN, "sum": LCE_REDUCE_SUM, "none": LCE_REDUCE_NONE}
 
 # every symbol include/lce.h declares
 EXPORTED = ("lce_workspace_size", "lce_forward", "lce_backward", "lce_status_string",

@@ -256,7 +256,8 @@ __device__ __forceinline__ void gather_offsets(uint32_t (&off)[4], const int* id
 // ---------------------------------------------------------------------------------------------
 __global__ __launch_bounds__(1024) void k_compact(const void* targets, int tbytes, int64_t n, int64_t v,
                                                   int ignore, int* idx, int* pos, int* nv_ws,
-                                                  int* nv_user, int* status, float* lse_zero) {
+                                                  int* nv_user, int* status, float* lse_zero,
+                                                  float* loss_zero) {
   __shared__ int scan[1024];
   __shared__ int bad_any;
   const int t = threadIdx.x;
@@ -292,6 +293,7 @@ __global__ __launch_bounds__(1024) void k_compact(const void* targets, int tbyte
     } else {
       pos[i] = -1;
       if (lse_zero) lse_zero[i] = 0.0f;
+      if (loss_zero) loss_zero[i] = 0.0f;
     }
   }
   if (t == 1023) {
@@ -406,7 +408,8 @@ __global__ __launch_bounds__(256) void k_combine(const uint16_t* __restrict__ H,
                                                  const int* __restrict__ idx, const int* __restrict__ nv_ptr,
                                                  int d, int nparts2, const float* __restrict__ part_m,
                                                  const float* __restrict__ part_s, int npad,
-                                                 float* __restrict__ lse_out, float* __restrict__ terms) {
+                                                 float* __restrict__ lse_out, float* __restrict__ terms,
+                                                 float* __restrict__ per_token) {
   const int lane = threadIdx.x & 63;
   const int i = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int nv = *nv_ptr;
@@ -435,6 +438,7 @@ __global__ __launch_bounds__(256) void k_combine(const uint16_t* __restrict__ H,
   if (lane == 0) {
     lse_out[row] = lse;
     terms[i] = lse - dot;
+    if (per_token) per_token[row] = lse - dot;
   }
 }
 
@@ -462,7 +466,7 @@ __global__ __launch_bounds__(1024) void k_loss(const float* __restrict__ terms, 
 
 __global__ void k_fwd_empty(float* loss, int* nv_user, int* status) {
   if (threadIdx.x == 0) {
-    *loss = 0.f;
+    if (loss) *loss = 0.f;
     *nv_user = 0;
     if (status) *status = 0;
   }
@@ -541,8 +545,10 @@ __device__ __forceinline__ bool band_tile(int tm_live, int tn_count, int& tm, in
   return true;
 }
 
-// scale c = g / n_norm (mean) or g (sum); 0 when the count is 0
+// scale c = g / n_norm (mean) or g (sum), 0 when the count is 0; for NONE the caller reads
+// the per-token gradient instead
 __device__ __forceinline__ float grad_scale(const float* grad, const int* n_norm, int reduction) {
+  if (reduction == LCE_REDUCE_NONE) return 0.f;
   const float g = *grad;
   if (reduction == LCE_REDUCE_SUM) return g;
   const int nn = *n_norm;
@@ -580,9 +586,9 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_bwd_g(const uint16_t* __restric
   f32x16_t acc[4][2];
   mma_mainloop(acc, ra, aoff, rb, boff, d, smem);
 
-  const float c = grad_scale(grad, n_norm, reduction);
+  const float c_all = grad_scale(grad, n_norm, reduction);
   int tok[2], tgt[2];
-  float l2[2];
+  float l2[2], cj[2];
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
     tok[j] = n0 + wc * 64 + j * 32 + (lane & 31);
@@ -590,9 +596,11 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_bwd_g(const uint16_t* __restric
       const int row = idx[tok[j]];
       l2[j] = lse[row] * kLog2e;
       tgt[j] = (int)(load_target(targets, tbytes, row) - v0) - vt0;   // tile-relative target row
+      cj[j] = reduction == LCE_REDUCE_NONE ? grad[row] : c_all;
     } else {
       l2[j] = 0.f;
       tgt[j] = -1;
+      cj[j] = 0.f;
     }
   }
   // G values in place, then the bf16 tile goes through LDS (free after the main loop) as
@@ -615,8 +623,8 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_bwd_g(const uint16_t* __restric
           const int vr = vb + i * 32 + q * 8 + e;
           float g = 0.f;
           if (tok_ok && vr < vleft) {
-            g = c * __builtin_amdgcn_exp2f(fmaf(acc[i][j][r], kLog2e, -l2[j]));
-            if (vr == tgt[j]) g -= c;
+            g = cj[j] * __builtin_amdgcn_exp2f(fmaf(acc[i][j][r], kLog2e, -l2[j]));
+            if (vr == tgt[j]) g -= cj[j];
           }
           gq[e] = g;
         }
@@ -823,7 +831,8 @@ lce_status_t make_plan(const lce_problem_t* p, Plan* pl) {
   if (p->reserved != 0) return LCE_ERR_ARG;
   if (p->n < 0 || p->d < 1 || p->v < 1) return LCE_ERR_SHAPE;
   if (p->d % 8 != 0) return LCE_ERR_UNSUPPORTED;
-  if (p->reduction != LCE_REDUCE_MEAN && p->reduction != LCE_REDUCE_SUM) return LCE_ERR_UNSUPPORTED;
+  if (p->reduction != LCE_REDUCE_MEAN && p->reduction != LCE_REDUCE_SUM && p->reduction != LCE_REDUCE_NONE)
+    return LCE_ERR_UNSUPPORTED;
   if (p->target_bytes != 4 && p->target_bytes != 8) return LCE_ERR_UNSUPPORTED;
   const int64_t ldh = p->ld_h ? p->ld_h : p->d, ldw = p->ld_w ? p->ld_w : p->d;
   if (ldh < p->d || ldw < p->d) return LCE_ERR_SHAPE;
@@ -929,8 +938,9 @@ lce_status_t lce_forward(const lce_problem_t* p, const void* H, const void* W, c
   if (pl.n > 0 && (!aligned16(H) || !aligned16(W) || ((uintptr_t)workspace & 255) != 0)) return LCE_ERR_ALIGN;
   if (pl.n > 0 && workspace_bytes < pl.fwd_bytes) return LCE_ERR_WORKSPACE;
   Launcher L{(hipStream_t)stream};
+  const bool none = p->reduction == LCE_REDUCE_NONE;
   if (pl.n == 0) {
-    L(K_MISC, k_fwd_empty, dim3(1), dim3(64), loss, n_valid, dev_status);
+    L(K_MISC, k_fwd_empty, dim3(1), dim3(64), none ? (float*)nullptr : loss, n_valid, dev_status);
     return L.st;
   }
   char* ws = (char*)workspace;
@@ -944,13 +954,13 @@ lce_status_t lce_forward(const lce_problem_t* p, const void* H, const void* W, c
   const uint16_t* w = (const uint16_t*)W;
 
   L(K_COMPACT, k_compact, dim3(1), dim3(1024), targets, p->target_bytes, pl.n, pl.v, p->ignore_index,
-    idx, pos, nv, n_valid, dev_status, lse);
+    idx, pos, nv, n_valid, dev_status, lse, none ? loss : (float*)nullptr);
   L(K_FWD_STATS, k_fwd_stats, dim3(pl.nt_max * pl.nparts), dim3(NTHREADS), w, pl.ldw, (int)pl.v, h, pl.ldh,
     pl.n, (const int*)idx, (const int*)nv, (int)pl.d, pl.nparts, pl.nt_max, pl.vt_count, pm, ps, (int)pl.npad);
   L(K_COMBINE, k_combine, dim3((unsigned)((pl.n + 3) / 4)), dim3(256), h, pl.ldh, w, pl.ldw, targets,
     p->target_bytes, (const int*)idx, (const int*)nv, (int)pl.d, 2 * pl.nparts, (const float*)pm,
-    (const float*)ps, (int)pl.npad, lse, terms);
-  L(K_LOSS, k_loss, dim3(1), dim3(1024), (const float*)terms, (const int*)nv, p->reduction, loss);
+    (const float*)ps, (int)pl.npad, lse, terms, none ? loss : (float*)nullptr);
+  if (!none) L(K_LOSS, k_loss, dim3(1), dim3(1024), (const float*)terms, (const int*)nv, p->reduction, loss);
   return L.st;
 }
 
@@ -960,7 +970,7 @@ lce_status_t lce_backward(const lce_problem_t* p, const void* H, const void* W, 
   Plan pl;
   lce_status_t st = make_plan(p, &pl);
   if (st != LCE_OK) return st;
-  if (!W || !dW || !n_valid || !grad_loss) return LCE_ERR_NULL;
+  if (!W || !dW || !grad_loss || (!n_valid && p->reduction == LCE_REDUCE_MEAN)) return LCE_ERR_NULL;
   if (pl.n > 0 && (!H || !targets || !lse || !dH || !workspace)) return LCE_ERR_NULL;
   if (!aligned16(W) || !aligned16(dW)) return LCE_ERR_ALIGN;
   if (pl.n > 0 && (!aligned16(H) || !aligned16(dH) || ((uintptr_t)workspace & 255) != 0)) return LCE_ERR_ALIGN;
@@ -985,7 +995,7 @@ lce_status_t lce_backward(const lce_problem_t* p, const void* H, const void* W, 
   const int d = (int)pl.d, npad = (int)pl.npad, vc = (int)pl.vc;
 
   L(K_COMPACT, k_compact, dim3(1), dim3(1024), targets, p->target_bytes, pl.n, pl.v, p->ignore_index,
-    idx, pos, nv, (int*)nullptr, (int*)nullptr, (float*)nullptr);
+    idx, pos, nv, (int*)nullptr, (int*)nullptr, (float*)nullptr, (float*)nullptr);
   // Hvt[d][i] = H[idx[i]][d] for i < Nv, zero up to round_up(Nv, 64)
   L(K_TRANSPOSE_H, k_transpose, dim3((unsigned)(npad / 64), (unsigned)((d + 63) / 64)), dim3(256), h, pl.ldh,
     (const int*)idx, (int64_t)0, (const int*)nv, 0, d, hvt, (int64_t)npad, npad);

@@ -25,11 +25,14 @@ def run_gpu(h, w, t, ignore_index=-100, reduction="mean", grad=1.0, backward=Tru
     loss, lse, nv, status = A.forward(h, w, t, ignore_index, reduction)
     out = {"loss_t": loss, "lse_t": lse, "nv_t": nv}
     if backward:
-        g = torch.tensor([grad], dtype=torch.float32, device=h.device)
+        if reduction == "none":
+            g = torch.as_tensor(np.asarray(grad, dtype=np.float32), device=h.device)
+        else:
+            g = torch.tensor([grad], dtype=torch.float32, device=h.device)
         dh, dw = A.backward(h, w, t, lse, nv, g, ignore_index, reduction)
         out["dH_t"], out["dW_t"] = dh, dw
     torch.cuda.synchronize()
-    out["loss"] = float(loss.item())
+    out["loss"] = loss.cpu().numpy().astype(np.float64) if reduction == "none" else float(loss.item())
     out["lse"] = lse.cpu().numpy().astype(np.float64)
     out["n_valid"] = int(nv.item())
     out["status"] = int(status.item())
@@ -47,7 +50,10 @@ def rel_fro(x, ref):
 def assert_parity(gpu, ref, *, grads=True, abs_zero_tol=1e-6):
     assert gpu["n_valid"] == ref["n_valid"], (gpu["n_valid"], ref["n_valid"])
     assert gpu["status"] == ref["status"]
-    assert abs(gpu["loss"] - ref["loss"]) <= LOSS_ABS_TOL, (gpu["loss"], ref["loss"])
+    if isinstance(ref["loss"], np.ndarray):      # per-token losses
+        assert np.max(np.abs(gpu["loss"] - ref["loss"]), initial=0.0) <= LSE_ABS_TOL
+    else:
+        assert abs(gpu["loss"] - ref["loss"]) <= LOSS_ABS_TOL, (gpu["loss"], ref["loss"])
     assert np.max(np.abs(gpu["lse"] - ref["lse"]), initial=0.0) <= LSE_ABS_TOL
     if grads:
         for k in ("dH", "dW"):

@@ -55,6 +55,7 @@ def test_workspace_is_linear_in_tokens_and_never_tokens_times_vocab():
     (dict(n=4, d=64, v=10, ld_h=32), B.LCE_ERR_SHAPE),
     (dict(n=4, d=64, v=10, ld_w=68), B.LCE_ERR_ALIGN),
     (dict(n=4, d=64, v=10, reduction=7), B.LCE_ERR_UNSUPPORTED),
+    (dict(n=4, d=64, v=10, reduction=3), B.LCE_ERR_UNSUPPORTED),
     (dict(n=4, d=64, v=10, target_bytes=2), B.LCE_ERR_UNSUPPORTED),
     (dict(n=1 << 22, d=1024, v=10), B.LCE_ERR_SHAPE),       # H beyond 32-bit byte offsets
 ])

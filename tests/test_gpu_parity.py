@@ -142,3 +142,29 @@ def test_autograd_function_matches_oracle():
     assert abs(loss.item() - ref["loss"]) <= U.LOSS_ABS_TOL
     assert U.rel_fro(h3.grad.view(300, 128).float().cpu().numpy(), ref["dH"]) <= U.GRAD_REL_TOL
     assert U.rel_fro(w1.grad.float().cpu().numpy(), ref["dW"]) <= U.GRAD_REL_TOL
+
+
+@pytest.mark.parametrize("n,d,v", [(300, 264, 1000), (600, 128, 9000), (1, 8, 5)])
+def test_per_token_losses_and_gradients(n, d, v):
+    inp = WL.custom(n, d, v, seed=n + 3, mask_frac=0.2, sigma_w=0.3)
+    g = np.random.default_rng(n).standard_normal(n).astype(np.float32)
+    gpu, ref = _case(inp, reduction="none", grad=g)
+    assert np.all(gpu["loss"][inp.targets == -100] == 0.0)
+
+
+def test_per_token_autograd_shape():
+    import torch
+    from paper_2605_21442_amd import linear_cross_entropy
+    inp = WL.custom(2 * 150, 96, 700, seed=31, mask_frac=0.1)
+    h, w, t = U.to_device(inp)
+    h3 = h.view(2, 150, 96).clone().requires_grad_(True)
+    w1 = w.clone().requires_grad_(True)
+    per = linear_cross_entropy(h3, w1, t.view(2, 150), reduction="none")
+    assert per.shape == (2, 150)
+    g = torch.linspace(-1, 1, 300, device=h.device).view(2, 150)
+    (per * g).sum().backward()
+    ref = O.lce(inp.h_bits, inp.w_bits, inp.targets, reduction="none",
+                grad=g.view(-1).cpu().numpy().astype(np.float64))
+    assert np.max(np.abs(per.detach().view(-1).cpu().numpy() - ref["loss"])) <= U.LSE_ABS_TOL
+    assert U.rel_fro(h3.grad.view(300, 96).float().cpu().numpy(), ref["dH"]) <= U.GRAD_REL_TOL
+    assert U.rel_fro(w1.grad.float().cpu().numpy(), ref["dW"]) <= U.GRAD_REL_TOL

@@ -284,3 +284,49 @@ def test_expected_loss_of_random_head():
     expect = math.log(wl.v) + wl.sigma_w ** 2 * wl.d / 2
     assert abs(out["loss"] - expect) < 0.05
     assert out["n_valid"] == wl.n_valid()
+
+
+# ---- per-token losses (reduction "none") ------------------------------------------------------
+
+def test_none_reduction_matches_torch_per_token_losses():
+    n, d, v = 41, 16, 77
+    h, w, t = _f64(n, d, v, seed=21, mask=np.arange(0, n, 5))
+    g = np.random.default_rng(3).standard_normal(n)
+    ours = _oracle_f64(h, w, t, "none", grad=g)
+    H = torch.tensor(h, requires_grad=True)
+    W = torch.tensor(w, requires_grad=True)
+    per = torch.nn.functional.cross_entropy(H @ W.T, torch.tensor(t), ignore_index=-100,
+                                            reduction="none")
+    (per * torch.tensor(g)).sum().backward()
+    np.testing.assert_allclose(ours["loss"], per.detach().numpy(), rtol=1e-12, atol=1e-14)
+    np.testing.assert_allclose(ours["dH"], H.grad.numpy(), rtol=1e-11, atol=1e-14)
+    np.testing.assert_allclose(ours["dW"], W.grad.numpy(), rtol=1e-11, atol=1e-14)
+    assert np.all(ours["loss"][t == -100] == 0.0)
+
+
+def test_none_reduction_sums_to_sum_reduction():
+    h, w, t = _f64(30, 12, 50, seed=22, mask=[3, 4])
+    per = _oracle_f64(h, w, t, "none", grad=np.ones(30))
+    tot = _oracle_f64(h, w, t, "sum", grad=1.0)
+    assert per["loss"].sum() == pytest.approx(tot["loss"], rel=1e-13)
+    np.testing.assert_allclose(per["dW"], tot["dW"], rtol=1e-12, atol=1e-15)
+    np.testing.assert_allclose(per["dH"], tot["dH"], rtol=1e-12, atol=1e-15)
+
+
+def test_none_reduction_gradient_of_one_token_is_central_difference():
+    n, d, v = 5, 6, 9
+    h, w, t = _f64(n, d, v, seed=23)
+    g = np.zeros(n)
+    g[2] = 1.0                                    # gradient of token 2's loss alone
+    out = _oracle_f64(h, w, t, "none", grad=g)
+    eps = 1e-6
+    num = np.zeros_like(w)
+    for i in range(v):
+        for j in range(d):
+            wp, wm = w.copy(), w.copy()
+            wp[i, j] += eps
+            wm[i, j] -= eps
+            num[i, j] = (O.forward(h, wp, t, -100, "none")["loss"][2]
+                         - O.forward(h, wm, t, -100, "none")["loss"][2]) / (2 * eps)
+    assert np.abs(num - out["dW"]).max() <= 1e-7 * np.abs(out["dW"]).max() + 1e-10
+    assert np.all(out["dH"][[0, 1, 3, 4]] == 0.0)
