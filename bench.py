@@ -1,12 +1,19 @@
 """Benchmark of the LCE hot path (forward + backward) on one MI355X.
 
 python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload llama8b] [--no-cpu-baseline]
+                [--variant lce|adamw_fused|adamw_two_phase]
 
 One step is one lce_forward + lce_backward over the whole batch of the named
 workload (default: the Llama-3.1-8B vocabulary head, N = 8 x 2048 tokens,
 D = 4096, V = 128256, 25% of targets masked). Inputs are seeded synthetic
 tensors already resident in HBM; outputs and workspace are allocated once
 before the timed region. The script prints one JSON line on stdout.
+
+The optimizer variants add one AdamW step on W per step (paper Sec. 4.1):
+``adamw_fused`` runs lce_forward + lce_backward_adamw (the step inside the
+backward, no dW buffer), ``adamw_two_phase`` runs lce_forward + lce_backward +
+lce_adamw_step (the standard path). Both keep fp32 moments and an fp32 master
+copy of W.
 """
 from __future__ import annotations
 
@@ -91,6 +98,7 @@ def main():
     ap.add_argument("--workload", default="llama8b")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--variant", default="lce", choices=("lce", "adamw_fused", "adamw_two_phase"))
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a 1 GiB device copy (for scaling HBM byte counters)")
     args = ap.parse_args()
@@ -128,22 +136,43 @@ def main():
     status = torch.empty(1, dtype=torch.int32, device=dev)
     grad = torch.ones(1, dtype=torch.float32, device=dev)
     dh = torch.empty((n, d), dtype=torch.bfloat16, device=dev)
-    dw = torch.empty((v, d), dtype=torch.bfloat16, device=dev)
+    fused = args.variant == "adamw_fused"
+    dw = None if fused else torch.empty((v, d), dtype=torch.bfloat16, device=dev)
     ws = torch.empty(max(fwd_bytes, bwd_bytes), dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream(dev).cuda_stream
+    opt_ptrs = None
+    if args.variant != "lce":
+        m1 = torch.zeros((v, d), dtype=torch.float32, device=dev)
+        m2 = torch.zeros((v, d), dtype=torch.float32, device=dev)
+        master = w.float()
+        opt_ptrs = (m1.data_ptr(), m2.data_ptr(), master.data_ptr())
+        step_no = [0]
+
+    def adamw():
+        step_no[0] += 1
+        return B.adamw(1e-5, 0.9, 0.95, 1e-8, 0.1, step_no[0])
 
     def step():
         B.lce_forward(p, h.data_ptr(), w.data_ptr(), t.data_ptr(), loss.data_ptr(), lse.data_ptr(),
                       nv.data_ptr(), status.data_ptr(), ws.data_ptr(), fwd_bytes, stream)
+        if fused:
+            B.lce_backward_adamw(p, h.data_ptr(), w.data_ptr(), t.data_ptr(), lse.data_ptr(), nv.data_ptr(),
+                                 grad.data_ptr(), dh.data_ptr(), *opt_ptrs, adamw(), ws.data_ptr(), bwd_bytes,
+                                 stream)
+            return
         B.lce_backward(p, h.data_ptr(), w.data_ptr(), t.data_ptr(), lse.data_ptr(), nv.data_ptr(),
                        grad.data_ptr(), dh.data_ptr(), dw.data_ptr(), ws.data_ptr(), bwd_bytes, stream)
+        if opt_ptrs is not None:
+            B.lce_adamw_step(v, d, 0, w.data_ptr(), dw.data_ptr(), *opt_ptrs, adamw(), stream)
 
     for i in range(args.warmup):
         step()
         torch.cuda.synchronize()
         print(f"[bench] warmup {i + 1}/{args.warmup} done", file=sys.stderr, flush=True)
     peak = torch.cuda.max_memory_allocated()
-    resident = (h.numel() + w.numel() + dh.numel() + dw.numel()) * 2 + t.numel() * 4 + n * 4
+    # inputs, outputs and (optimizer variants) the optimizer state; dW only where it exists
+    resident = (h.numel() + w.numel() + dh.numel() + (dw.numel() if dw is not None else 0)) * 2 \
+        + t.numel() * 4 + n * 4 + (3 * v * d * 4 if opt_ptrs is not None else 0)
 
     B.lce_timing_enable(True)
     torch.cuda.synchronize()
@@ -192,7 +221,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": wl.name, "n_tokens": n, "hidden": d, "vocab": v, "n_valid": nvalid,
                    "global_batch": wl.batch, "seq_len": wl.seq_len, "parallelism": "none",
-                   "reduction": "mean", "ignore_index": inp.ignore_index},
+                   "reduction": "mean", "ignore_index": inp.ignore_index, "variant": args.variant},
         "valid_tokens_per_s": nvalid * args.steps / elapsed,
         "mfma_frac_step": flops_step / (ms_step * 1e-3) / (PEAK_BF16_TFLOPS * 1e12),
         "peak_hbm_bytes": int(peak),

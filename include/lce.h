@@ -78,8 +78,32 @@ typedef struct lce_problem {
   int32_t ignore_index;     /* targets equal to this are ignored (e.g. -100) */
   int32_t reduction;        /* lce_reduction_t */
   int32_t target_bytes;     /* 4 (int32 targets) or 8 (int64 targets) */
-  int32_t reserved;         /* must be 0 */
+  int32_t flags;            /* bitwise OR of LCE_FLAG_* (0 for none); unknown bits are rejected */
 } lce_problem_t;
+
+/* lce_backward adds this call's dW to the values already in dW instead of overwriting it:
+ * dW = bf16(float(dW) + fp32 contribution). This is gradient accumulation over micro-batches,
+ * which the paper's benchmark settings use (performance benchmarks) and which its Sec. 4.1
+ * names as the case the fused optimizer step cannot serve. lce_forward ignores the flag;
+ * lce_backward_adamw rejects it (one update per backward pass). */
+#define LCE_FLAG_ACCUMULATE_DW 1
+
+/*
+ * Hyper-parameters of one AdamW step (decoupled weight decay, bias-corrected moments), the
+ * optimizer that paper Sec. 4.1 fuses into the backward pass. With t = step:
+ *   theta <- theta (1 - lr weight_decay)
+ *   m <- beta1 m + (1 - beta1) g,     v <- beta2 v + (1 - beta2) g^2
+ *   theta <- theta - lr / (1 - beta1^t) * m / (sqrt(v) / sqrt(1 - beta2^t) + eps)
+ * The constants are formed on the host in double precision and used in fp32 on the device.
+ */
+typedef struct lce_adamw {
+  float lr;                 /* >= 0 */
+  float beta1, beta2;       /* in [0, 1) */
+  float eps;                /* >= 0 */
+  float weight_decay;       /* >= 0 */
+  int32_t step;             /* t >= 1: the 1-based index of this update */
+  int32_t reserved;         /* must be 0 */
+} lce_adamw_t;
 
 /*
  * Workspace sizes, in bytes, for lce_forward (*fwd_bytes) and lce_backward
@@ -114,13 +138,46 @@ lce_status_t lce_forward(const lce_problem_t* p,
  *   grad_loss   fp32, read on the device: [1] upstream gradient g of L for mean /
  *               sum; [N] upstream gradients g_n of the per-token losses for NONE
  *   dH          [N, D] bf16, overwritten; rows of ignored tokens are +0.0
- *   dW          [V, D] bf16, overwritten
+ *   dW          [V, D] bf16, overwritten (or added to, with LCE_FLAG_ACCUMULATE_DW)
  */
 lce_status_t lce_backward(const lce_problem_t* p,
                           const void* H, const void* W, const void* targets,
                           const float* lse, const int32_t* n_valid, const float* grad_loss,
                           void* dH, void* dW,
                           void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Two-phase optimizer step (the standard path that in-backward fusion replaces, paper Sec.
+ * 4.1): one AdamW step on the bf16 parameter W [V, D] (row stride ld_w, 0 means d) with the
+ * bf16 gradient dW [V, D] (dense, as lce_backward writes it; NULL means a zero gradient).
+ *   exp_avg, exp_avg_sq  [V, D] fp32, dense, updated in place (start at 0 for step 1)
+ *   W_master             [V, D] fp32 or NULL. If given, it is the parameter: it is updated and
+ *                        W receives its bf16 rounding (nearest, ties to even). If NULL, the
+ *                        parameter is W itself, read as fp32 and rounded back to bf16.
+ * Element by element the arithmetic is exactly that of lce_backward_adamw, so the two paths
+ * give the same bits. All pointers 16-byte aligned; v >= 1, d >= 8 and a multiple of 8.
+ */
+lce_status_t lce_adamw_step(int64_t v, int64_t d, int64_t ld_w, void* W, const void* dW,
+                            float* exp_avg, float* exp_avg_sq, float* W_master,
+                            const lce_adamw_t* opt, void* stream);
+
+/*
+ * Backward pass with the optimizer step fused in (paper Sec. 4.1 applied to the LCE weight of
+ * Sec. 4.2): as lce_backward, but instead of writing dW, each vocabulary slab's dW block
+ * (rounded to bf16 exactly as lce_backward would store it) is consumed at once by an AdamW step
+ * on that slab of W, so no [V, D] gradient buffer ever exists. W, exp_avg, exp_avg_sq and
+ * W_master are as in lce_adamw_step and are updated in place; dH is written as by
+ * lce_backward (it uses the weights from before the step). The result is bitwise identical to
+ * lce_backward followed by lce_adamw_step with the same opt. W must not be read or written by
+ * other work while the call runs. p->flags must not contain LCE_FLAG_ACCUMULATE_DW. The
+ * workspace is lce_backward's (bwd_bytes).
+ */
+lce_status_t lce_backward_adamw(const lce_problem_t* p,
+                                const void* H, void* W, const void* targets,
+                                const float* lse, const int32_t* n_valid, const float* grad_loss,
+                                void* dH, float* exp_avg, float* exp_avg_sq, float* W_master,
+                                const lce_adamw_t* opt,
+                                void* workspace, size_t workspace_bytes, void* stream);
 
 /* Static, human-readable name of a status code. */
 const char* lce_status_string(lce_status_t s);

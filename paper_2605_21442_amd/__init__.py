@@ -7,11 +7,11 @@ Importing this package does not load the library; the first call does, and
 raises if it was not built.
 """
 
-__all__ = ["linear_cross_entropy", "LinearCrossEntropy"]
+__all__ = ["linear_cross_entropy", "LinearCrossEntropy", "AdamWState"]
 
 
 def __getattr__(name):
-    if name in ("linear_cross_entropy", "LinearCrossEntropy"):
+    if name in __all__:
         from . import autograd
         return getattr(autograd, name)
     raise AttributeError(name)

@@ -65,32 +65,118 @@ def forward(hidden: torch.Tensor, weight: torch.Tensor, targets: torch.Tensor,
     return loss, lse, nv, status
 
 
-def backward(hidden: torch.Tensor, weight: torch.Tensor, targets: torch.Tensor, lse: torch.Tensor,
-             n_valid: torch.Tensor, grad_loss: torch.Tensor, ignore_index: int = -100,
-             reduction: str = "mean"):
-    """(dH bf16 [N, D], dW bf16 [V, D]) computed by lce_backward."""
+def _backward_args(hidden, weight, targets, lse, grad_loss, ignore_index, reduction, flags=0):
     h, ldh = _as_rows(hidden, "hidden")
     w, ldw = _as_rows(weight, "weight")
     n, d = h.shape
     v = w.shape[0]
     t, tb = _targets(targets, n)
     p = B.problem(n, d, v, ld_h=ldh, ld_w=ldw, ignore_index=ignore_index, reduction=reduction,
-                  target_bytes=tb)
-    _, bwd_bytes = B.lce_workspace_size(p)
-    dev = h.device
+                  target_bytes=tb, flags=flags)
     want = n if reduction == "none" else 1
     if grad_loss.dtype != torch.float32 or grad_loss.numel() != want or not grad_loss.is_cuda:
         raise ValueError(f"grad_loss must be a {want}-element float32 GPU tensor")
-    grad_loss = grad_loss.contiguous()
     if lse.dtype != torch.float32 or lse.numel() != n or not lse.is_contiguous():
         raise ValueError("lse must be the contiguous float32 [N] tensor from forward")
-    dh = torch.empty((n, d), dtype=torch.bfloat16, device=dev)
-    dw = torch.empty((v, d), dtype=torch.bfloat16, device=dev)
+    return p, h, w, t, grad_loss.contiguous()
+
+
+def backward(hidden: torch.Tensor, weight: torch.Tensor, targets: torch.Tensor, lse: torch.Tensor,
+             n_valid: torch.Tensor, grad_loss: torch.Tensor, ignore_index: int = -100,
+             reduction: str = "mean", accumulate_into: torch.Tensor | None = None):
+    """(dH bf16 [N, D], dW bf16 [V, D]) computed by lce_backward. With ``accumulate_into`` (a
+    dense bf16 [V, D] tensor) this call's dW is added to it in place and it is returned as dW."""
+    flags = B.LCE_FLAG_ACCUMULATE_DW if accumulate_into is not None else 0
+    p, h, w, t, g = _backward_args(hidden, weight, targets, lse, grad_loss, ignore_index, reduction, flags)
+    _, bwd_bytes = B.lce_workspace_size(p)
+    dev = h.device
+    dh = torch.empty((p.n, p.d), dtype=torch.bfloat16, device=dev)
+    if accumulate_into is None:
+        dw = torch.empty((p.v, p.d), dtype=torch.bfloat16, device=dev)
+    else:
+        dw = accumulate_into
+        if dw.dtype != torch.bfloat16 or tuple(dw.shape) != (p.v, p.d) or not dw.is_contiguous():
+            raise ValueError("accumulate_into must be a contiguous bf16 [V, D] tensor")
     ws = torch.empty(max(bwd_bytes, 1), dtype=torch.uint8, device=dev)
     B.lce_backward(p, h.data_ptr(), w.data_ptr(), t.data_ptr(), lse.data_ptr(), n_valid.data_ptr(),
-                   grad_loss.data_ptr(), dh.data_ptr(), dw.data_ptr(), ws.data_ptr(), bwd_bytes,
-                   _stream(dev))
+                   g.data_ptr(), dh.data_ptr(), dw.data_ptr(), ws.data_ptr(), bwd_bytes, _stream(dev))
     return dh, dw
+
+
+class AdamWState:
+    """AdamW state of one bf16 weight [V, D] (paper Sec. 4.1): fp32 moments, an optional fp32
+    master copy, the hyper-parameters and the step count. ``step_with(dW)`` is the two-phase
+    optimizer step (lce_adamw_step); passed as ``optimizer=`` to ``linear_cross_entropy`` it
+    is instead applied inside the backward pass (lce_backward_adamw), which never forms dW."""
+
+    def __init__(self, weight: torch.Tensor, lr: float = 1e-3, betas=(0.9, 0.999), eps: float = 1e-8,
+                 weight_decay: float = 0.01, master_weights: bool = False):
+        if weight.dtype != torch.bfloat16 or weight.dim() != 2 or not weight.is_cuda:
+            raise ValueError("weight must be a 2-D bf16 GPU tensor")
+        if weight.stride(-1) != 1 or weight.stride(0) % 8 or weight.data_ptr() % 16:
+            raise ValueError("weight must have unit column stride, a row stride divisible by 8 and "
+                             "16-byte alignment, since it is updated in place")
+        self.weight = weight
+        self.lr, self.betas, self.eps, self.weight_decay = lr, tuple(betas), eps, weight_decay
+        self.exp_avg = torch.zeros(weight.shape, dtype=torch.float32, device=weight.device)
+        self.exp_avg_sq = torch.zeros_like(self.exp_avg)
+        self.master = weight.float().contiguous() if master_weights else None
+        self.step = 0
+
+    def state_dict(self) -> dict:
+        """Per-parameter state for checkpointing (tensors are shared, not copied)."""
+        return {"step": self.step, "exp_avg": self.exp_avg, "exp_avg_sq": self.exp_avg_sq,
+                "master": self.master, "lr": self.lr, "betas": self.betas, "eps": self.eps,
+                "weight_decay": self.weight_decay}
+
+    def load_state_dict(self, sd: dict) -> None:
+        """Restore a state_dict: moments (and master copy) are copied into this state's tensors."""
+        self.exp_avg.copy_(sd["exp_avg"])
+        self.exp_avg_sq.copy_(sd["exp_avg_sq"])
+        if (sd.get("master") is None) != (self.master is None):
+            raise ValueError("master-weight setting differs from the checkpoint")
+        if self.master is not None:
+            self.master.copy_(sd["master"])
+        self.step = int(sd["step"])
+        for k in ("lr", "betas", "eps", "weight_decay"):
+            if k in sd:
+                setattr(self, k, tuple(sd[k]) if k == "betas" else sd[k])
+
+    def next_opt(self) -> B.LceAdamW:
+        return B.adamw(self.lr, self.betas[0], self.betas[1], self.eps, self.weight_decay, self.step + 1)
+
+    def _ptrs(self):
+        m = self.master.data_ptr() if self.master is not None else 0
+        return self.exp_avg.data_ptr(), self.exp_avg_sq.data_ptr(), m
+
+    def step_with(self, dW: torch.Tensor | None) -> None:
+        """Two-phase step: one AdamW update of the weight with the bf16 gradient dW [V, D]."""
+        w = self.weight
+        if dW is not None and (dW.dtype != torch.bfloat16 or dW.shape != w.shape or not dW.is_contiguous()):
+            raise ValueError("dW must be a contiguous bf16 tensor shaped like the weight")
+        opt = self.next_opt()
+        B.lce_adamw_step(w.shape[0], w.shape[1], w.stride(0), w.data_ptr(), dW.data_ptr() if dW is not None else 0,
+                         *self._ptrs(), opt, _stream(w.device))
+        self.step += 1
+
+
+def backward_adamw(hidden: torch.Tensor, targets: torch.Tensor, lse: torch.Tensor, n_valid: torch.Tensor,
+                   grad_loss: torch.Tensor, state: AdamWState, ignore_index: int = -100,
+                   reduction: str = "mean") -> torch.Tensor:
+    """dH bf16 [N, D] from lce_backward_adamw; the weight of ``state`` takes one AdamW step
+    with its gradient inside the call."""
+    p, h, w, t, g = _backward_args(hidden, state.weight, targets, lse, grad_loss, ignore_index, reduction)
+    if w.data_ptr() != state.weight.data_ptr():
+        raise ValueError("the weight must be usable in place")
+    _, bwd_bytes = B.lce_workspace_size(p)
+    dev = h.device
+    dh = torch.empty((p.n, p.d), dtype=torch.bfloat16, device=dev)
+    ws = torch.empty(max(bwd_bytes, 1), dtype=torch.uint8, device=dev)
+    B.lce_backward_adamw(p, h.data_ptr(), w.data_ptr(), t.data_ptr(), lse.data_ptr(), n_valid.data_ptr(),
+                         g.data_ptr(), dh.data_ptr(), *state._ptrs(), state.next_opt(), ws.data_ptr(),
+                         bwd_bytes, _stream(dev))
+    state.step += 1
+    return dh
 
 
 class LinearCrossEntropy(torch.autograd.Function):
@@ -114,8 +200,38 @@ class LinearCrossEntropy(torch.autograd.Function):
         return dh.view(hidden.shape), dw, None, None, None
 
 
+class LinearCrossEntropyAdamW(torch.autograd.Function):
+    """As LinearCrossEntropy, but the backward steps the weight with AdamW in place (paper
+    Sec. 4.1) and returns no weight gradient."""
+
+    @staticmethod
+    def forward(ctx, hidden, weight, targets, state, ignore_index=-100, reduction="mean"):
+        loss, lse, nv, _ = forward(hidden, weight, targets, ignore_index, reduction)
+        ctx.save_for_backward(hidden, targets, lse, nv)
+        ctx.state = state
+        ctx.ignore_index = ignore_index
+        ctx.reduction = reduction
+        return loss.view(targets.shape) if reduction == "none" else loss
+
+    @staticmethod
+    def backward(ctx, grad):
+        hidden, targets, lse, nv = ctx.saved_tensors
+        g = grad.reshape(-1)
+        if g.dtype != torch.float32:
+            g = g.float()
+        dh = backward_adamw(hidden, targets, lse, nv, g, ctx.state, ctx.ignore_index, ctx.reduction)
+        return dh.view(hidden.shape), None, None, None, None, None
+
+
 def linear_cross_entropy(hidden: torch.Tensor, weight: torch.Tensor, targets: torch.Tensor,
-                         ignore_index: int = -100, reduction: str = "mean") -> torch.Tensor:
+                         ignore_index: int = -100, reduction: str = "mean",
+                         optimizer: AdamWState | None = None) -> torch.Tensor:
     """Cross-entropy of ``hidden @ weight.T`` against ``targets`` without the logits: the mean over
-    valid tokens, their sum, or (``reduction="none"``) the per-token losses, shaped like targets."""
+    valid tokens, their sum, or (``reduction="none"``) the per-token losses, shaped like targets.
+    With ``optimizer`` (an AdamWState of this weight) the backward pass applies the AdamW step
+    to the weight itself instead of producing its gradient."""
+    if optimizer is not None:
+        if optimizer.weight.data_ptr() != weight.data_ptr() or optimizer.weight.shape != weight.shape:
+            raise ValueError("optimizer state belongs to another weight")
+        return LinearCrossEntropyAdamW.apply(hidden, weight, targets, optimizer, ignore_index, reduction)
     return LinearCrossEntropy.apply(hidden, weight, targets, ignore_index, reduction)

@@ -28,13 +28,14 @@ LCE_REDUCE_MEAN = 0
 LCE_REDUCE_SUM = 1
 LCE_REDUCE_NONE = 2
 LCE_STATUS_TARGET_OUT_OF_RANGE = 1
+LCE_FLAG_ACCUMULATE_DW = 1
 
 REDUCTIONS = {"mean": LCE_REDUCE_MEAN, "sum": LCE_REDUCE_SUM, "none": LCE_REDUCE_NONE}
 
 # every symbol include/lce.h declares
 EXPORTED = ("lce_workspace_size", "lce_forward", "lce_backward", "lce_status_string",
             "lce_timing_enable", "lce_timing_kernel_count", "lce_timing_kernel_name",
-            "lce_timing_read")
+            "lce_timing_read", "lce_adamw_step", "lce_backward_adamw")
 
 
 class LceError(RuntimeError):
@@ -47,13 +48,23 @@ class LceProblem(ctypes.Structure):
     _fields_ = [("n", ctypes.c_int64), ("d", ctypes.c_int64), ("v", ctypes.c_int64),
                 ("ld_h", ctypes.c_int64), ("ld_w", ctypes.c_int64),
                 ("ignore_index", ctypes.c_int32), ("reduction", ctypes.c_int32),
-                ("target_bytes", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+                ("target_bytes", ctypes.c_int32), ("flags", ctypes.c_int32)]
+
+
+class LceAdamW(ctypes.Structure):
+    _fields_ = [("lr", ctypes.c_float), ("beta1", ctypes.c_float), ("beta2", ctypes.c_float),
+                ("eps", ctypes.c_float), ("weight_decay", ctypes.c_float), ("step", ctypes.c_int32),
+                ("reserved", ctypes.c_int32)]
 
 
 def problem(n: int, d: int, v: int, *, ld_h: int = 0, ld_w: int = 0, ignore_index: int = -100,
-            reduction: str | int = "mean", target_bytes: int = 4) -> LceProblem:
+            reduction: str | int = "mean", target_bytes: int = 4, flags: int = 0) -> LceProblem:
     red = REDUCTIONS[reduction] if isinstance(reduction, str) else int(reduction)
-    return LceProblem(n, d, v, ld_h, ld_w, ignore_index, red, target_bytes, 0)
+    return LceProblem(n, d, v, ld_h, ld_w, ignore_index, red, target_bytes, flags)
+
+
+def adamw(lr: float, beta1: float, beta2: float, eps: float, weight_decay: float, step: int) -> LceAdamW:
+    return LceAdamW(lr, beta1, beta2, eps, weight_decay, step, 0)
 
 
 _lib = None
@@ -75,6 +86,9 @@ def load() -> ctypes.CDLL:
         lib.lce_workspace_size.argtypes = [P, ctypes.POINTER(sz), ctypes.POINTER(sz)]
         lib.lce_forward.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
         lib.lce_backward.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+        A = ctypes.POINTER(LceAdamW)
+        lib.lce_adamw_step.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, vp, vp, vp, vp, vp, A, vp]
+        lib.lce_backward_adamw.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, A, vp, sz, vp]
         lib.lce_status_string.argtypes = [ctypes.c_int]
         lib.lce_status_string.restype = ctypes.c_char_p
         lib.lce_timing_enable.argtypes = [ctypes.c_int]
@@ -84,7 +98,7 @@ def load() -> ctypes.CDLL:
         lib.lce_timing_read.argtypes = [ctypes.c_int, ctypes.POINTER(ctypes.c_double),
                                         ctypes.POINTER(ctypes.c_int64)]
         for name in ("lce_workspace_size", "lce_forward", "lce_backward", "lce_timing_enable",
-                     "lce_timing_read", "lce_timing_kernel_count"):
+                     "lce_timing_read", "lce_timing_kernel_count", "lce_adamw_step", "lce_backward_adamw"):
             getattr(lib, name).restype = ctypes.c_int
         _lib = lib
         return lib
@@ -116,6 +130,20 @@ def lce_backward(p: LceProblem, H: int, W: int, targets: int, lse: int, n_valid:
                  dH: int, dW: int, workspace: int, workspace_bytes: int, stream: int) -> None:
     _check(load().lce_backward(ctypes.byref(p), H, W, targets, lse, n_valid, grad_loss, dH, dW,
                                workspace, workspace_bytes, stream or None), "lce_backward")
+
+
+def lce_adamw_step(v: int, d: int, ld_w: int, W: int, dW: int, exp_avg: int, exp_avg_sq: int,
+                   W_master: int, opt: LceAdamW, stream: int) -> None:
+    _check(load().lce_adamw_step(v, d, ld_w, W, dW or None, exp_avg, exp_avg_sq, W_master or None,
+                                 ctypes.byref(opt), stream or None), "lce_adamw_step")
+
+
+def lce_backward_adamw(p: LceProblem, H: int, W: int, targets: int, lse: int, n_valid: int,
+                       grad_loss: int, dH: int, exp_avg: int, exp_avg_sq: int, W_master: int,
+                       opt: LceAdamW, workspace: int, workspace_bytes: int, stream: int) -> None:
+    _check(load().lce_backward_adamw(ctypes.byref(p), H, W, targets, lse, n_valid, grad_loss, dH, exp_avg,
+                                     exp_avg_sq, W_master or None, ctypes.byref(opt), workspace,
+                                     workspace_bytes, stream or None), "lce_backward_adamw")
 
 
 def lce_timing_enable(on: bool) -> None:

@@ -64,6 +64,40 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 
 __device__ __forceinline__ uint16_t to_bf16(float x) { return __builtin_bit_cast(uint16_t, (__bf16)x); }
 
+// ---------------------------------------------------------------------------------------------
+// AdamW (decoupled weight decay, bias-corrected moments): the optimizer that paper Sec. 4.1
+// runs inside the backward pass. The per-call constants are formed once on the host; the
+// element update is one function shared by the fused dW epilogue and the standalone step, with
+// floating-point contraction off so both give the same bits.
+// ---------------------------------------------------------------------------------------------
+struct AdamWConst {
+  float keep;           // 1 - lr * weight_decay
+  float beta1, omb1;    // beta1, 1 - beta1
+  float beta2, omb2;    // beta2, 1 - beta2
+  float step_size;      // lr / (1 - beta1^t)
+  float inv_sqrt_bc2;   // 1 / sqrt(1 - beta2^t)
+  float eps;
+};
+
+// Parameter and moments of W [V, D]: W bf16 with row stride ldw; m, v (and master, if not null)
+// fp32 dense with row stride d.
+struct AdamWState {
+  uint16_t* W;
+  int64_t ldw;
+  float* m;
+  float* v;
+  float* master;
+};
+
+__device__ __forceinline__ void adamw_update(float& p, float& m, float& v, float g, const AdamWConst& c) {
+#pragma clang fp contract(off)
+  p = p * c.keep;
+  m = c.beta1 * m + c.omb1 * g;
+  v = c.beta2 * v + c.omb2 * (g * g);
+  const float denom = sqrtf(v) * c.inv_sqrt_bc2 + c.eps;
+  p = p - c.step_size * (m / denom);
+}
+
 __device__ __forceinline__ int64_t load_target(const void* t, int tbytes, int64_t i) {
   return tbytes == 8 ? ((const int64_t*)t)[i] : (int64_t)((const int32_t*)t)[i];
 }
@@ -668,11 +702,17 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_bwd_g(const uint16_t* __restric
   }
 }
 
-// K5: dW[v0 + m][dd] = sum_k Gt[m][k] Hvt[dd][k] over k < round_up(Nv, 64), written once in bf16.
+// K5: dW[v0 + m][dd] = sum_k Gt[m][k] Hvt[dd][k] over k < round_up(Nv, 64). The epilogue either
+// writes the block in bf16 (each element once), adds it to the bf16 values already there, or
+// hands each bf16-rounded element straight to the AdamW update of W (the in-backward step).
+enum DwMode { DW_STORE = 0, DW_ACCUMULATE = 1, DW_ADAMW = 2 };
+
+template <int kMode>
 __global__ __launch_bounds__(NTHREADS, 2) void k_bwd_dw(const uint16_t* __restrict__ Gt, int ldt, int vs,
                                                         const uint16_t* __restrict__ Hvt, int d,
                                                         const int* __restrict__ nv_ptr, int tm_count,
-                                                        uint16_t* __restrict__ dW, int64_t v0) {
+                                                        uint16_t* __restrict__ dW, int64_t v0,
+                                                        AdamWState st, AdamWConst oc) {
   __shared__ __attribute__((aligned(16))) char smem[LDS_BYTES];
   int tm, tn;
   if (!band_tile(tm_count, (d + TILE - 1) / TILE, tm, tn)) return;
@@ -694,12 +734,55 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_bwd_dw(const uint16_t* __restri
     const int col = dc + j * 32;
     if (col >= d) continue;
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < 4; ++i) {
+      if constexpr (kMode == DW_STORE) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int m = mb + i * 32 + (r >> 2) * 8 + (r & 3);
-        if (m < vs) dW[(v0 + m) * d + col] = to_bf16(acc[i][j][r]);
+        for (int r = 0; r < 16; ++r) {
+          const int m = mb + i * 32 + (r >> 2) * 8 + (r & 3);
+          if (m < vs) dW[(v0 + m) * d + col] = to_bf16(acc[i][j][r]);
+        }
+      } else if constexpr (kMode == DW_ACCUMULATE) {
+        float old[16];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int m = mb + i * 32 + (r >> 2) * 8 + (r & 3);
+          old[r] = m < vs ? bf16_to_f32(dW[(v0 + m) * d + col]) : 0.f;
+        }
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int m = mb + i * 32 + (r >> 2) * 8 + (r & 3);
+          if (m < vs) dW[(v0 + m) * d + col] = to_bf16(old[r] + acc[i][j][r]);
+        }
+      } else {
+        // four consecutive rows at a time: all their loads first, then the updates and stores
+#pragma unroll
+        for (int rq = 0; rq < 4; ++rq) {
+          const int mq = mb + i * 32 + rq * 8;
+          const int64_t base = (v0 + mq) * d + col;
+          const int64_t wbase = (v0 + mq) * st.ldw + col;
+          float p[4], mo[4], vo[4];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            if (mq + r < vs) {
+              mo[r] = st.m[base + r * d];
+              vo[r] = st.v[base + r * d];
+              p[r] = st.master ? st.master[base + r * d] : bf16_to_f32(st.W[wbase + r * st.ldw]);
+            }
+          }
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            if (mq + r < vs) {
+              const float g = bf16_to_f32(to_bf16(acc[i][j][rq * 4 + r]));
+              adamw_update(p[r], mo[r], vo[r], g, oc);
+              st.m[base + r * d] = mo[r];
+              st.v[base + r * d] = vo[r];
+              if (st.master) st.master[base + r * d] = p[r];
+              st.W[wbase + r * st.ldw] = to_bf16(p[r]);
+            }
+          }
+        }
       }
+    }
   }
 }
 
@@ -797,13 +880,60 @@ __global__ __launch_bounds__(256) void k_zero16(uint4* __restrict__ p, int64_t n
   if (i < n16) p[i] = make_uint4(0, 0, 0, 0);
 }
 
+// Standalone AdamW step over W [V, D] with the bf16 gradient dW (dense [V, D]; null = zero
+// gradient): eight consecutive elements of one row per thread and iteration, 16-byte accesses.
+__global__ __launch_bounds__(256) void k_adamw(int64_t v, int d, const uint16_t* __restrict__ dW,
+                                               AdamWState st, AdamWConst oc) {
+  const int cpr = d >> 3;
+  const int64_t total = v * cpr;
+  for (int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x; q < total; q += (int64_t)gridDim.x * 256) {
+    const int64_t row = q / cpr;
+    const int col = (int)(q - row * cpr) * 8;
+    const int64_t o = row * d + col;
+    const i32x4_t wv = *reinterpret_cast<const i32x4_t*>(st.W + row * st.ldw + col);
+    i32x4_t gv = {0, 0, 0, 0};
+    if (dW) gv = *reinterpret_cast<const i32x4_t*>(dW + o);
+    float p[8], mo[8], vo[8];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const float4 a = *reinterpret_cast<const float4*>(st.m + o + 4 * h);
+      const float4 b = *reinterpret_cast<const float4*>(st.v + o + 4 * h);
+      mo[4 * h] = a.x; mo[4 * h + 1] = a.y; mo[4 * h + 2] = a.z; mo[4 * h + 3] = a.w;
+      vo[4 * h] = b.x; vo[4 * h + 1] = b.y; vo[4 * h + 2] = b.z; vo[4 * h + 3] = b.w;
+      if (st.master) {
+        const float4 c = *reinterpret_cast<const float4*>(st.master + o + 4 * h);
+        p[4 * h] = c.x; p[4 * h + 1] = c.y; p[4 * h + 2] = c.z; p[4 * h + 3] = c.w;
+      }
+    }
+    uint32_t wout[4];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const uint32_t w2 = (uint32_t)wv[e >> 1], g2 = (uint32_t)gv[e >> 1];
+      if (!st.master) p[e] = bf16_to_f32((e & 1) ? (w2 >> 16) : (w2 & 0xFFFFu));
+      const float g = bf16_to_f32((e & 1) ? (g2 >> 16) : (g2 & 0xFFFFu));
+      adamw_update(p[e], mo[e], vo[e], g, oc);
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      wout[e] = (uint32_t)to_bf16(p[2 * e]) | ((uint32_t)to_bf16(p[2 * e + 1]) << 16);
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      *reinterpret_cast<float4*>(st.m + o + 4 * h) = make_float4(mo[4 * h], mo[4 * h + 1], mo[4 * h + 2], mo[4 * h + 3]);
+      *reinterpret_cast<float4*>(st.v + o + 4 * h) = make_float4(vo[4 * h], vo[4 * h + 1], vo[4 * h + 2], vo[4 * h + 3]);
+      if (st.master)
+        *reinterpret_cast<float4*>(st.master + o + 4 * h) = make_float4(p[4 * h], p[4 * h + 1], p[4 * h + 2], p[4 * h + 3]);
+    }
+    *reinterpret_cast<i32x4_t*>(st.W + row * st.ldw + col) = i32x4_t{(int)wout[0], (int)wout[1], (int)wout[2], (int)wout[3]};
+  }
+}
+
 // ---------------------------------------------------------------------------------------------
 // Host side: validation, plan, workspace carve-up, launches, optional timing.
 // ---------------------------------------------------------------------------------------------
 enum KernelId { K_COMPACT = 0, K_FWD_STATS, K_COMBINE, K_LOSS, K_TRANSPOSE_H, K_TRANSPOSE_W, K_BWD_G,
-                K_BWD_DW, K_BWD_DH, K_DH_FINAL, K_MISC, K_COUNT };
+                K_BWD_DW, K_BWD_DH, K_DH_FINAL, K_ADAMW, K_MISC, K_COUNT };
 const char* const kKernelNames[K_COUNT] = {"compact", "fwd_stats", "combine", "loss", "transpose_h",
-                                           "transpose_w", "bwd_g", "bwd_dw", "bwd_dh", "dh_finalize", "misc"};
+                                           "transpose_w", "bwd_g", "bwd_dw", "bwd_dh", "dh_finalize", "adamw", "misc"};
 
 struct Timing {
   std::mutex mu;
@@ -828,7 +958,7 @@ inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 
 lce_status_t make_plan(const lce_problem_t* p, Plan* pl) {
   if (!p) return LCE_ERR_NULL;
-  if (p->reserved != 0) return LCE_ERR_ARG;
+  if ((p->flags & ~LCE_FLAG_ACCUMULATE_DW) != 0) return LCE_ERR_ARG;
   if (p->n < 0 || p->d < 1 || p->v < 1) return LCE_ERR_SHAPE;
   if (p->d % 8 != 0) return LCE_ERR_UNSUPPORTED;
   if (p->reduction != LCE_REDUCE_MEAN && p->reduction != LCE_REDUCE_SUM && p->reduction != LCE_REDUCE_NONE)
@@ -878,6 +1008,31 @@ lce_status_t make_plan(const lce_problem_t* p, Plan* pl) {
 
 inline bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
 
+lce_status_t make_adamw(const lce_adamw_t* o, AdamWConst* c) {
+  if (!o) return LCE_ERR_NULL;
+  if (o->reserved != 0 || o->step < 1) return LCE_ERR_ARG;
+  if (!(o->lr >= 0.f && o->lr < INFINITY) || !(o->beta1 >= 0.f && o->beta1 < 1.f) ||
+      !(o->beta2 >= 0.f && o->beta2 < 1.f) || !(o->eps >= 0.f && o->eps < INFINITY) ||
+      !(o->weight_decay >= 0.f && o->weight_decay < INFINITY))
+    return LCE_ERR_ARG;
+  const double lr = o->lr, b1 = o->beta1, b2 = o->beta2;
+  c->keep = (float)(1.0 - lr * (double)o->weight_decay);
+  c->beta1 = o->beta1;
+  c->omb1 = (float)(1.0 - b1);
+  c->beta2 = o->beta2;
+  c->omb2 = (float)(1.0 - b2);
+  c->step_size = (float)(lr / (1.0 - pow(b1, (double)o->step)));
+  c->inv_sqrt_bc2 = (float)(1.0 / sqrt(1.0 - pow(b2, (double)o->step)));
+  c->eps = o->eps;
+  return LCE_OK;
+}
+
+unsigned adamw_grid(int64_t v, int64_t d) {
+  const int64_t chunks = v * (d / 8);
+  const int64_t blocks = (chunks + 255) / 256;
+  return (unsigned)(blocks < 4096 ? blocks : 4096);
+}
+
 struct Launcher {
   hipStream_t s;
   lce_status_t st = LCE_OK;
@@ -899,6 +1054,78 @@ struct Launcher {
     if (slot >= 0 && hipEventRecord(g_timing.ev[2 * slot + 1], s) != hipSuccess) st = LCE_ERR_HIP;
   }
 };
+
+// The backward pass behind lce_backward (dW != null) and lce_backward_adamw (adamw != null).
+lce_status_t backward_impl(const lce_problem_t* p, const void* H, const void* W, const void* targets,
+                           const float* lse, const int32_t* n_valid, const float* grad_loss, void* dH,
+                           uint16_t* dW, const AdamWState* adamw, const AdamWConst* oc,
+                           void* workspace, size_t workspace_bytes, void* stream) {
+  Plan pl;
+  lce_status_t st = make_plan(p, &pl);
+  if (st != LCE_OK) return st;
+  if (!W || !grad_loss || (!n_valid && p->reduction == LCE_REDUCE_MEAN)) return LCE_ERR_NULL;
+  if (pl.n > 0 && (!H || !targets || !lse || !dH || !workspace)) return LCE_ERR_NULL;
+  if (!aligned16(W)) return LCE_ERR_ALIGN;
+  if (pl.n > 0 && (!aligned16(H) || !aligned16(dH) || ((uintptr_t)workspace & 255) != 0)) return LCE_ERR_ALIGN;
+  if (pl.n > 0 && workspace_bytes < pl.bwd_bytes) return LCE_ERR_WORKSPACE;
+  const bool accumulate = (p->flags & LCE_FLAG_ACCUMULATE_DW) != 0;
+  const AdamWState as = adamw ? *adamw : AdamWState{nullptr, 0, nullptr, nullptr, nullptr};
+  const AdamWConst c = oc ? *oc : AdamWConst{};
+  Launcher L{(hipStream_t)stream};
+  if (pl.n == 0) {
+    // no tokens: dW is zero, so the fused step is a step with a zero gradient
+    if (adamw) {
+      L(K_ADAMW, k_adamw, dim3(adamw_grid(pl.v, pl.d)), dim3(256), pl.v, (int)pl.d, (const uint16_t*)nullptr, as, c);
+    } else if (!accumulate) {
+      const int64_t n16 = pl.v * pl.d / 8;
+      L(K_MISC, k_zero16, dim3((unsigned)((n16 + 255) / 256)), dim3(256), (uint4*)dW, n16);
+    }
+    return L.st;
+  }
+  char* ws = (char*)workspace;
+  int* idx = (int*)(ws + pl.o_idx);
+  int* pos = (int*)(ws + pl.o_pos);
+  int* nv = (int*)(ws + pl.o_nv);
+  uint16_t* hvt = (uint16_t*)(ws + pl.o_hvt);
+  uint16_t* g = (uint16_t*)(ws + pl.o_g);
+  uint16_t* gt = (uint16_t*)(ws + pl.o_gt);
+  uint16_t* wst = (uint16_t*)(ws + pl.o_wst);
+  float* dh32 = (float*)(ws + pl.o_dh32);
+  const uint16_t* h = (const uint16_t*)H;
+  const uint16_t* w = (const uint16_t*)W;
+  const int d = (int)pl.d, npad = (int)pl.npad, vc = (int)pl.vc;
+
+  L(K_COMPACT, k_compact, dim3(1), dim3(1024), targets, p->target_bytes, pl.n, pl.v, p->ignore_index,
+    idx, pos, nv, (int*)nullptr, (int*)nullptr, (float*)nullptr, (float*)nullptr);
+  // Hvt[d][i] = H[idx[i]][d] for i < Nv, zero up to round_up(Nv, 64)
+  L(K_TRANSPOSE_H, k_transpose, dim3((unsigned)(npad / 64), (unsigned)((d + 63) / 64)), dim3(256), h, pl.ldh,
+    (const int*)idx, (int64_t)0, (const int*)nv, 0, d, hvt, (int64_t)npad, npad);
+  const int dt = (d + TILE - 1) / TILE;
+  void (*dw_kernel)(const uint16_t*, int, int, const uint16_t*, int, const int*, int, uint16_t*, int64_t,
+                    AdamWState, AdamWConst) =
+      adamw ? k_bwd_dw<DW_ADAMW> : accumulate ? k_bwd_dw<DW_ACCUMULATE> : k_bwd_dw<DW_STORE>;
+  for (int64_t s = 0; s < pl.nslab; ++s) {
+    const int64_t v0 = s * pl.vc;
+    const int vs = (int)(pl.v - v0 < pl.vc ? pl.v - v0 : pl.vc);
+    const int vs64 = (int)round_up(vs, 64);
+    const int tm = (vs + TILE - 1) / TILE;
+    // W slab rows are read here (transposed copy, G tile) before the dW epilogue of the same slab
+    // may update them; later slabs read only their own rows, dH only the transposed copy
+    L(K_TRANSPOSE_W, k_transpose, dim3((unsigned)(vs64 / 64), (unsigned)((d + 63) / 64)), dim3(256), w, pl.ldw,
+      (const int*)nullptr, v0, (const int*)nullptr, vs, d, wst, (int64_t)vc, vs64);
+    L(K_BWD_G, k_bwd_g, dim3((unsigned)(tm * pl.nt_max)), dim3(NTHREADS), w, pl.ldw, v0, vs, h, pl.ldh, pl.n,
+      targets, p->target_bytes, (const int*)idx, (const int*)nv, lse, grad_loss, (const int*)n_valid,
+      p->reduction, d, tm, g, vc, gt, npad);
+    L(K_BWD_DW, dw_kernel, dim3((unsigned)(8 * ((tm + 7) / 8) * dt)), dim3(NTHREADS), (const uint16_t*)gt, npad,
+      vs, (const uint16_t*)hvt, d, (const int*)nv, tm, dW, v0, as, c);
+    L(K_BWD_DH, k_bwd_dh, dim3((unsigned)(8 * ((pl.nt_max + 7) / 8) * dt)), dim3(NTHREADS), (const uint16_t*)g, vc, vs64,
+      (const uint16_t*)wst, d, (const int*)nv, pl.nt_max, dh32, (int)(s > 0));
+  }
+  const int64_t nthr = pl.n * pl.d / 8;
+  L(K_DH_FINAL, k_dh_finalize, dim3((unsigned)((nthr + 255) / 256)), dim3(256), (const float*)dh32,
+    (const int*)pos, pl.n, d, (uint16_t*)dH, 1);
+  return L.st;
+}
 
 }  // namespace
 
@@ -967,58 +1194,45 @@ lce_status_t lce_forward(const lce_problem_t* p, const void* H, const void* W, c
 lce_status_t lce_backward(const lce_problem_t* p, const void* H, const void* W, const void* targets,
                           const float* lse, const int32_t* n_valid, const float* grad_loss,
                           void* dH, void* dW, void* workspace, size_t workspace_bytes, void* stream) {
-  Plan pl;
-  lce_status_t st = make_plan(p, &pl);
-  if (st != LCE_OK) return st;
-  if (!W || !dW || !grad_loss || (!n_valid && p->reduction == LCE_REDUCE_MEAN)) return LCE_ERR_NULL;
-  if (pl.n > 0 && (!H || !targets || !lse || !dH || !workspace)) return LCE_ERR_NULL;
-  if (!aligned16(W) || !aligned16(dW)) return LCE_ERR_ALIGN;
-  if (pl.n > 0 && (!aligned16(H) || !aligned16(dH) || ((uintptr_t)workspace & 255) != 0)) return LCE_ERR_ALIGN;
-  if (pl.n > 0 && workspace_bytes < pl.bwd_bytes) return LCE_ERR_WORKSPACE;
-  Launcher L{(hipStream_t)stream};
-  if (pl.n == 0) {
-    const int64_t n16 = pl.v * pl.d / 8;
-    L(K_MISC, k_zero16, dim3((unsigned)((n16 + 255) / 256)), dim3(256), (uint4*)dW, n16);
-    return L.st;
-  }
-  char* ws = (char*)workspace;
-  int* idx = (int*)(ws + pl.o_idx);
-  int* pos = (int*)(ws + pl.o_pos);
-  int* nv = (int*)(ws + pl.o_nv);
-  uint16_t* hvt = (uint16_t*)(ws + pl.o_hvt);
-  uint16_t* g = (uint16_t*)(ws + pl.o_g);
-  uint16_t* gt = (uint16_t*)(ws + pl.o_gt);
-  uint16_t* wst = (uint16_t*)(ws + pl.o_wst);
-  float* dh32 = (float*)(ws + pl.o_dh32);
-  const uint16_t* h = (const uint16_t*)H;
-  const uint16_t* w = (const uint16_t*)W;
-  const int d = (int)pl.d, npad = (int)pl.npad, vc = (int)pl.vc;
+  if (!dW) return LCE_ERR_NULL;
+  if (!aligned16(dW)) return LCE_ERR_ALIGN;
+  return backward_impl(p, H, W, targets, lse, n_valid, grad_loss, dH, (uint16_t*)dW, nullptr, nullptr,
+                       workspace, workspace_bytes, stream);
+}
 
-  L(K_COMPACT, k_compact, dim3(1), dim3(1024), targets, p->target_bytes, pl.n, pl.v, p->ignore_index,
-    idx, pos, nv, (int*)nullptr, (int*)nullptr, (float*)nullptr, (float*)nullptr);
-  // Hvt[d][i] = H[idx[i]][d] for i < Nv, zero up to round_up(Nv, 64)
-  L(K_TRANSPOSE_H, k_transpose, dim3((unsigned)(npad / 64), (unsigned)((d + 63) / 64)), dim3(256), h, pl.ldh,
-    (const int*)idx, (int64_t)0, (const int*)nv, 0, d, hvt, (int64_t)npad, npad);
-  const int dt = (d + TILE - 1) / TILE;
-  for (int64_t s = 0; s < pl.nslab; ++s) {
-    const int64_t v0 = s * pl.vc;
-    const int vs = (int)(pl.v - v0 < pl.vc ? pl.v - v0 : pl.vc);
-    const int vs64 = (int)round_up(vs, 64);
-    const int tm = (vs + TILE - 1) / TILE;
-    L(K_TRANSPOSE_W, k_transpose, dim3((unsigned)(vs64 / 64), (unsigned)((d + 63) / 64)), dim3(256), w, pl.ldw,
-      (const int*)nullptr, v0, (const int*)nullptr, vs, d, wst, (int64_t)vc, vs64);
-    L(K_BWD_G, k_bwd_g, dim3((unsigned)(tm * pl.nt_max)), dim3(NTHREADS), w, pl.ldw, v0, vs, h, pl.ldh, pl.n,
-      targets, p->target_bytes, (const int*)idx, (const int*)nv, lse, grad_loss, (const int*)n_valid,
-      p->reduction, d, tm, g, vc, gt, npad);
-    L(K_BWD_DW, k_bwd_dw, dim3((unsigned)(8 * ((tm + 7) / 8) * dt)), dim3(NTHREADS), (const uint16_t*)gt, npad, vs,
-      (const uint16_t*)hvt, d, (const int*)nv, tm, (uint16_t*)dW, v0);
-    L(K_BWD_DH, k_bwd_dh, dim3((unsigned)(8 * ((pl.nt_max + 7) / 8) * dt)), dim3(NTHREADS), (const uint16_t*)g, vc, vs64,
-      (const uint16_t*)wst, d, (const int*)nv, pl.nt_max, dh32, (int)(s > 0));
-  }
-  const int64_t nthr = pl.n * pl.d / 8;
-  L(K_DH_FINAL, k_dh_finalize, dim3((unsigned)((nthr + 255) / 256)), dim3(256), (const float*)dh32,
-    (const int*)pos, pl.n, d, (uint16_t*)dH, 1);
+lce_status_t lce_adamw_step(int64_t v, int64_t d, int64_t ld_w, void* W, const void* dW, float* exp_avg,
+                            float* exp_avg_sq, float* W_master, const lce_adamw_t* opt, void* stream) {
+  AdamWConst c;
+  lce_status_t st = make_adamw(opt, &c);
+  if (st != LCE_OK) return st;
+  const int64_t ldw = ld_w ? ld_w : d;
+  if (v < 1 || d < 8 || ldw < d || v >= (int64_t)1 << 30 || d >= (int64_t)1 << 20) return LCE_ERR_SHAPE;
+  if (d % 8 != 0) return LCE_ERR_UNSUPPORTED;
+  if (ldw % 8 != 0) return LCE_ERR_ALIGN;
+  if (!W || !exp_avg || !exp_avg_sq) return LCE_ERR_NULL;
+  if (!aligned16(W) || !aligned16(exp_avg) || !aligned16(exp_avg_sq) || (dW && !aligned16(dW)) ||
+      (W_master && !aligned16(W_master)))
+    return LCE_ERR_ALIGN;
+  AdamWState as{(uint16_t*)W, ldw, exp_avg, exp_avg_sq, W_master};
+  Launcher L{(hipStream_t)stream};
+  L(K_ADAMW, k_adamw, dim3(adamw_grid(v, d)), dim3(256), v, (int)d, (const uint16_t*)dW, as, c);
   return L.st;
+}
+
+lce_status_t lce_backward_adamw(const lce_problem_t* p, const void* H, void* W, const void* targets,
+                                const float* lse, const int32_t* n_valid, const float* grad_loss, void* dH,
+                                float* exp_avg, float* exp_avg_sq, float* W_master, const lce_adamw_t* opt,
+                                void* workspace, size_t workspace_bytes, void* stream) {
+  AdamWConst c;
+  lce_status_t st = make_adamw(opt, &c);
+  if (st != LCE_OK) return st;
+  if (!p) return LCE_ERR_NULL;
+  if (p->flags & LCE_FLAG_ACCUMULATE_DW) return LCE_ERR_ARG;
+  if (!exp_avg || !exp_avg_sq) return LCE_ERR_NULL;
+  if (!aligned16(exp_avg) || !aligned16(exp_avg_sq) || (W_master && !aligned16(W_master))) return LCE_ERR_ALIGN;
+  AdamWState as{(uint16_t*)W, p->ld_w ? p->ld_w : p->d, exp_avg, exp_avg_sq, W_master};
+  return backward_impl(p, H, W, targets, lse, n_valid, grad_loss, dH, nullptr, &as, &c, workspace,
+                       workspace_bytes, stream);
 }
 
 lce_status_t lce_timing_enable(int on) {

@@ -36,7 +36,7 @@ import numpy as np
 IGNORE_INDEX = -100
 
 # RNG stream ids
-_S_H, _S_W, _S_T, _S_MASK = 0, 1, 2, 3
+_S_H, _S_W, _S_T, _S_MASK, _S_OPT, _S_GRAD = 0, 1, 2, 3, 4, 5
 
 
 @dataclasses.dataclass(frozen=True)
@@ -191,3 +191,34 @@ def custom(n: int, d: int, v: int, *, seed: int = 0, sigma_w: float = 0.02,
         t = draw_targets(_rng(seed, case_id, _S_T), n, v, targets, 1.1)
         t = apply_mask(_rng(seed, case_id, _S_MASK), t, w, ignore_index)
     return Inputs(w, seed, h, wb, t, ignore_index)
+
+
+@dataclasses.dataclass
+class OptState:
+    """AdamW state of a [V, D] weight as a run would have left it (all float32)."""
+
+    m: np.ndarray               # first moments
+    v: np.ndarray               # second moments, >= 0
+    master: np.ndarray          # full-precision copy of the weight
+
+
+def opt_state(w_bits: np.ndarray, *, seed: int = 0, case_id: int = 99, g_scale: float = 1e-3,
+              cold: bool = False) -> OptState:
+    """Optimizer state for the bf16 weight ``w_bits``: zero moments (``cold``, a first step) or
+    moments of gradient scale ``g_scale`` (m ~ N(0, g_scale), v ~ g_scale^2 U(0.5, 1.5)); the master
+    copy is the weight plus a small float32 offset (below half a bf16 spacing of typical entries)."""
+    rng = _rng(seed, case_id, _S_OPT)
+    shape = w_bits.shape
+    if cold:
+        m = np.zeros(shape, np.float32)
+        v = np.zeros(shape, np.float32)
+    else:
+        m = (g_scale * rng.standard_normal(shape)).astype(np.float32)
+        v = ((g_scale * g_scale) * rng.uniform(0.5, 1.5, shape)).astype(np.float32)
+    master = bf16_bits_to_f32(w_bits) + (1e-5 * rng.standard_normal(shape)).astype(np.float32)
+    return OptState(m, v, master.astype(np.float32))
+
+
+def gradient_bits(v: int, d: int, *, seed: int = 0, case_id: int = 99, g_scale: float = 1e-3) -> np.ndarray:
+    """A bf16 gradient matrix [V, D] ~ N(0, g_scale) (input of a standalone optimizer step)."""
+    return draw_normal_bf16(_rng(seed, case_id, _S_GRAD), (v, d), g_scale)

@@ -65,12 +65,13 @@ def test_bad_problems_are_rejected(kw, code):
     assert e.value.code == code
 
 
-def test_reserved_field_must_be_zero():
-    p = B.problem(4, 64, 10)
-    p.reserved = 1
+@pytest.mark.parametrize("flags", [2, 4, 1 << 30, -1])
+def test_unknown_flag_bits_are_rejected(flags):
+    p = B.problem(4, 64, 10, flags=flags)
     with pytest.raises(B.LceError) as e:
         B.lce_workspace_size(p)
     assert e.value.code == B.LCE_ERR_ARG
+    B.lce_workspace_size(B.problem(4, 64, 10, flags=B.LCE_FLAG_ACCUMULATE_DW))
 
 
 def _fake(addr=0x100000):
@@ -117,3 +118,54 @@ def test_missing_library_fails_loudly(monkeypatch, tmp_path):
     monkeypatch.setattr(B, "LIB_PATH", str(tmp_path / "liblce.so"))
     with pytest.raises(RuntimeError, match="not built"):
         B.load()
+
+
+HP = dict(lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.01, step=1)
+
+
+def test_adamw_step_argument_checks_run_before_any_launch():
+    ok = dict(v=10, d=64, ld_w=0, W=_fake(0x200000), dW=_fake(0x300000), exp_avg=_fake(0x400000),
+              exp_avg_sq=_fake(0x500000), W_master=0, stream=0)
+    cases = [
+        (dict(W=0), {}, B.LCE_ERR_NULL), (dict(exp_avg=0), {}, B.LCE_ERR_NULL),
+        (dict(exp_avg_sq=0x500004), {}, B.LCE_ERR_ALIGN), (dict(W_master=0x600008), {}, B.LCE_ERR_ALIGN),
+        (dict(d=60), {}, B.LCE_ERR_UNSUPPORTED), (dict(v=0), {}, B.LCE_ERR_SHAPE),
+        (dict(ld_w=32), {}, B.LCE_ERR_SHAPE), (dict(ld_w=68), {}, B.LCE_ERR_ALIGN),
+        ({}, dict(step=0), B.LCE_ERR_ARG), ({}, dict(beta1=1.0), B.LCE_ERR_ARG),
+        ({}, dict(beta2=-0.1), B.LCE_ERR_ARG), ({}, dict(lr=float("nan")), B.LCE_ERR_ARG),
+        ({}, dict(eps=-1.0), B.LCE_ERR_ARG), ({}, dict(weight_decay=float("inf")), B.LCE_ERR_ARG),
+    ]
+    for change, hp, code in cases:
+        with pytest.raises(B.LceError) as e:
+            B.lce_adamw_step(**dict(ok, **change), opt=B.adamw(**dict(HP, **hp)))
+        assert e.value.code == code, (change, hp)
+    opt = B.adamw(**HP)
+    opt.reserved = 3
+    with pytest.raises(B.LceError) as e:
+        B.lce_adamw_step(**ok, opt=opt)
+    assert e.value.code == B.LCE_ERR_ARG
+
+
+def test_backward_adamw_argument_checks_run_before_any_launch():
+    p = B.problem(8, 64, 10)
+    _, bwd = B.lce_workspace_size(p)
+    ok = dict(H=_fake(), W=_fake(0x200000), targets=_fake(0x300000), lse=_fake(0x400000),
+              n_valid=_fake(0x500000), grad_loss=_fake(0x600000), dH=_fake(0x700000),
+              exp_avg=_fake(0x800000), exp_avg_sq=_fake(0x880000), W_master=0,
+              workspace=_fake(0x900000), workspace_bytes=bwd, stream=0)
+    cases = [
+        (dict(W=0), B.LCE_ERR_NULL), (dict(exp_avg=0), B.LCE_ERR_NULL),
+        (dict(exp_avg_sq=0x880008), B.LCE_ERR_ALIGN), (dict(dH=0x700004), B.LCE_ERR_ALIGN),
+        (dict(workspace_bytes=16), B.LCE_ERR_WORKSPACE),
+    ]
+    for change, code in cases:
+        with pytest.raises(B.LceError) as e:
+            B.lce_backward_adamw(p, **dict(ok, **change), opt=B.adamw(**HP))
+        assert e.value.code == code, change
+    # one update per backward pass: accumulation cannot be combined with the fused step
+    with pytest.raises(B.LceError) as e:
+        B.lce_backward_adamw(B.problem(8, 64, 10, flags=B.LCE_FLAG_ACCUMULATE_DW), **ok, opt=B.adamw(**HP))
+    assert e.value.code == B.LCE_ERR_ARG
+    with pytest.raises(B.LceError) as e:
+        B.lce_backward_adamw(p, **ok, opt=B.adamw(**dict(HP, step=-2)))
+    assert e.value.code == B.LCE_ERR_ARG

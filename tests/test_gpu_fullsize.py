@@ -81,3 +81,61 @@ def test_full_size_against_oracle(name):
     e = U.rel_fro(got_dw, ref_dw)
     assert e <= U.GRAD_REL_TOL, ("dW", e)
     _say(f"[{name}] ok: loss {gpu['loss']:.6f} (oracle {float(gold['loss']):.6f}), lse err {lse_err:.2e}")
+
+
+def test_full_size_fused_adamw_llama8b():
+    """lce_backward_adamw at the 8B head size, in the launch configuration the benchmark's
+    fused variant times: bit for bit the two-phase path (lce_backward, then lce_adamw_step), and
+    sampled rows of the updated parameter and moments against the oracle."""
+    import torch
+    from oracle import adamw_oracle as A
+    from paper_2605_21442_amd import autograd as AG
+    name = "llama8b"
+    path = MG.path_for(name, 0)
+    if not os.path.exists(path):
+        pytest.skip(f"{path} missing: run tests/golden/make_golden.py")
+    gold = np.load(path, allow_pickle=False)
+    wl = WL.WORKLOADS[name]
+    inp = WL.generate(wl, 0)
+    h, _, t = U.to_device(inp)
+    hp = dict(lr=1e-4, beta1=0.9, beta2=0.95, eps=1e-8, weight_decay=0.1)
+    g_scale = 2e-5                                   # typical |dW| of this head
+    results = []
+    for fused in (False, True):
+        _say(f"[{name}] {'fused' if fused else 'two-phase'} backward + AdamW")
+        w = torch.from_numpy(inp.w_bits.view(np.int16)).view(torch.bfloat16).to(h.device)
+        st = AG.AdamWState(w, lr=hp["lr"], betas=(hp["beta1"], hp["beta2"]), eps=hp["eps"],
+                           weight_decay=hp["weight_decay"], master_weights=True)
+        st.exp_avg_sq.fill_(g_scale * g_scale)       # a warm, uniform second moment
+        st.step = 9
+        loss, lse, nv, _ = AG.forward(h, w, t)
+        g = torch.ones(1, dtype=torch.float32, device=h.device)
+        if fused:
+            AG.backward_adamw(h, t, lse, nv, g, st)
+        else:
+            _, dw = AG.backward(h, w, t, lse, nv, g)
+            st.step_with(dw)
+            del dw
+        torch.cuda.synchronize()
+        results.append((w, st))
+    (wa, sa), (wb, sb) = results
+    assert torch.equal(wa.view(torch.int16), wb.view(torch.int16))
+    for x, y in ((sa.exp_avg, sb.exp_avg), (sa.exp_avg_sq, sb.exp_avg_sq), (sa.master, sb.master)):
+        assert torch.equal(x.view(torch.int32), y.view(torch.int32))
+
+    rng = np.random.default_rng(3)
+    v = wl.v
+    ids = np.array(sorted(set([0, 1, 255, 256, 16383, 16384, v - 1] + rng.integers(2, v, 3).tolist())))
+    _say(f"[{name}] oracle AdamW rows {ids.tolist()}")
+    ref_dw = O.dw_of_rows(inp.h_bits, inp.w_bits, inp.targets, ids, gold["lse"])
+    w0 = O.bf16_to_f64(inp.w_bits[ids])
+    theta, m1, v1 = A.adamw_step(w0, ref_dw, np.zeros_like(w0), np.full(w0.shape, np.float32(g_scale * g_scale)),
+                                 step=10, **hp)
+    sel = torch.from_numpy(ids).to(h.device)
+    got_theta = sb.master[sel].cpu().numpy().astype(np.float64)
+    got_m = sb.exp_avg[sel].cpu().numpy().astype(np.float64)
+    got_v = sb.exp_avg_sq[sel].cpu().numpy().astype(np.float64)
+    assert U.rel_fro(got_theta - w0, theta - w0) <= U.GRAD_REL_TOL
+    assert U.rel_fro(got_m, m1) <= U.GRAD_REL_TOL
+    assert U.rel_fro(got_v, v1) <= U.GRAD_REL_TOL
+    _say(f"[{name}] fused AdamW ok")
