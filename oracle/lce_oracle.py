@@ -36,7 +36,9 @@ Pins: the oracle is checked (``tests/test_oracle.py``) against closed forms
 (zero weights give L = ln V; a geometric-series vocabulary; V = 1 and V = 2),
 central finite differences, an independent library routine (torch CPU float64
 cross-entropy with autograd), and invariants (softmax-grad rows sum to zero,
-masked rows contribute nothing, shift and permutation invariance).
+masked rows contribute nothing, shift and permutation invariance). The vocabulary-parallel
+helpers at the end are pinned by recombining their per-shard results over several partitions of
+the vocabulary into the full-vocabulary results above.
 """
 from __future__ import annotations
 
@@ -191,3 +193,70 @@ def dw_of_rows(h_bits, w_bits, targets, vrows, lse_valid, ignore_index=-100,
         p -= (t[r][:, None] == np.asarray(vrows)[None, :])
         out += ((c[r][:, None] if reduction == "none" else c) * p).T @ hr
     return out
+
+
+# ---- vocabulary-parallel (loss-parallel) decomposition --------------------------------------
+# With W split by rows (vocabulary ids) over shards, the softmax normaliser is a log-sum-exp of
+# the shards' log-sum-exps and the target logit is held by exactly one shard (paper Sec. 4.2 and
+# Sec. 5: the loss composes with loss-parallel sharding of the output projection).
+
+def shard_forward(h, w_shard, targets, v_begin, v_total, ignore_index=-100):
+    """Partials of one shard holding ids [v_begin, v_begin + rows of w_shard): per valid row the
+    log-sum-exp over the shard's ids and the target logit if the shard holds the target (else 0);
+    both 0 on rows that are not valid for the full vocabulary ``v_total``."""
+    n = h.shape[0]
+    ok, status = valid_rows(targets, v_total, ignore_index)
+    rows = np.nonzero(ok)[0]
+    t = np.asarray(targets, dtype=np.int64)
+    lse_part = np.zeros(n, dtype=np.float64)
+    tgt_part = np.zeros(n, dtype=np.float64)
+    if rows.size:
+        s = h[rows] @ w_shard.T
+        m = s.max(axis=1)
+        lse_part[rows] = m + np.log(np.exp(s - m[:, None]).sum(axis=1))
+        local = t[rows] - v_begin
+        own = (local >= 0) & (local < w_shard.shape[0])
+        tgt_part[rows[own]] = s[np.nonzero(own)[0], local[own]]
+    return {"lse_part": lse_part, "tgt_part": tgt_part, "n_valid": int(rows.size), "status": status}
+
+
+def combine_shards(lse_parts, tgt_parts, targets, v_total, ignore_index=-100, reduction="mean"):
+    """Full-vocabulary lse and loss from the shards' partials ([G, N] each)."""
+    ok, status = valid_rows(targets, v_total, ignore_index)
+    lp = np.asarray(lse_parts, dtype=np.float64)
+    m = lp.max(axis=0)
+    lse = np.where(ok, m + np.log(np.exp(lp - m[None, :]).sum(axis=0)), 0.0)
+    per_row = np.where(ok, lse - np.asarray(tgt_parts, dtype=np.float64).sum(axis=0), 0.0)
+    nv = int(ok.sum())
+    if reduction == "none":
+        loss = per_row
+    elif nv == 0:
+        loss = 0.0
+    else:
+        loss = float(per_row.sum() / nv) if reduction == "mean" else float(per_row.sum())
+    return {"loss": loss, "lse": lse, "per_row": per_row, "n_valid": nv, "status": status}
+
+
+def shard_backward(h, w_shard, targets, lse, v_begin, v_total, n_valid, ignore_index=-100,
+                   reduction="mean", grad=1.0):
+    """One shard's terms of the gradients, given the full-vocabulary lse: dH_part = G_s W_s (the
+    shards' parts sum to dH) and dW_s = G_s^T H (the shard's rows of dW), with
+    G_s = c (exp(s - lse) - onehot) over the shard's ids (the onehot only where the shard holds
+    the target)."""
+    ok, _ = valid_rows(targets, v_total, ignore_index)
+    rows = np.nonzero(ok)[0]
+    t = np.asarray(targets, dtype=np.int64)
+    c = scale_c(n_valid, reduction, grad)
+    dh = np.zeros((h.shape[0], w_shard.shape[1]), dtype=np.float64)
+    dw = np.zeros_like(w_shard, dtype=np.float64)
+    if rows.size:
+        s = h[rows] @ w_shard.T
+        g = np.exp(s - np.asarray(lse, dtype=np.float64)[rows][:, None])
+        local = t[rows] - v_begin
+        own = np.nonzero((local >= 0) & (local < w_shard.shape[0]))[0]
+        g[own, local[own]] -= 1.0
+        cr = (c[rows][:, None] if reduction == "none" else c)
+        g = cr * g
+        dh[rows] = g @ w_shard
+        dw = g.T @ h[rows]
+    return {"dH_part": dh, "dW": dw}

@@ -330,3 +330,29 @@ def test_none_reduction_gradient_of_one_token_is_central_difference():
                          - O.forward(h, wm, t, -100, "none")["loss"][2]) / (2 * eps)
     assert np.abs(num - out["dW"]).max() <= 1e-7 * np.abs(out["dW"]).max() + 1e-10
     assert np.all(out["dH"][[0, 1, 3, 4]] == 0.0)
+
+
+# ---- vocabulary-parallel decomposition ----------------------------------------------------------
+
+@pytest.mark.parametrize("reduction", ["mean", "sum", "none"])
+@pytest.mark.parametrize("cuts", [[0, 53], [0, 1, 20, 52, 53], [0, 52, 53]])
+def test_shard_partials_combine_to_the_full_objective(reduction, cuts):
+    n, d, v = 19, 7, 53
+    h, w, t = _f64(n, d, v, seed=11, mask=np.array([2, 5]))
+    t[7] = v + 3                                      # out of range: ignored and flagged
+    g = np.linspace(-1, 2, n) if reduction == "none" else 0.5
+    full = _oracle_f64(h, w, t, reduction, grad=g)
+    parts = [O.shard_forward(h, w[a:b], t, a, v) for a, b in zip(cuts[:-1], cuts[1:])]
+    comb = O.combine_shards(np.stack([p["lse_part"] for p in parts]),
+                            np.stack([p["tgt_part"] for p in parts]), t, v, reduction=reduction)
+    assert comb["n_valid"] == full["n_valid"] and comb["status"] == full["status"] == 1
+    np.testing.assert_allclose(comb["lse"], full["lse"], rtol=1e-13, atol=1e-13)
+    np.testing.assert_allclose(comb["loss"], full["loss"], rtol=1e-12, atol=1e-13)
+    # exactly one shard holds each valid target
+    owners = sum((t - a >= 0) & (t - a < b - a) for a, b in zip(cuts[:-1], cuts[1:]))
+    valid = (t != -100) & (t >= 0) & (t < v)
+    assert np.all(owners[valid] == 1)
+    bw = [O.shard_backward(h, w[a:b], t, comb["lse"], a, v, comb["n_valid"], reduction=reduction, grad=g)
+          for a, b in zip(cuts[:-1], cuts[1:])]
+    np.testing.assert_allclose(sum(b["dH_part"] for b in bw), full["dH"], rtol=1e-11, atol=1e-14)
+    np.testing.assert_allclose(np.concatenate([b["dW"] for b in bw]), full["dW"], rtol=1e-11, atol=1e-14)
