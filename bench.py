@@ -1,7 +1,7 @@
 """Benchmark of the LCE hot path (forward + backward) on one MI355X.
 
 python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload llama8b] [--no-cpu-baseline]
-                [--variant lce|adamw_fused|adamw_two_phase]
+                [--variant lce|adamw_fused|adamw_two_phase|vocab_shard] [--shards 8]
 
 One step is one lce_forward + lce_backward over the whole batch of the named
 workload (default: the Llama-3.1-8B vocabulary head, N = 8 x 2048 tokens,
@@ -14,6 +14,13 @@ The optimizer variants add one AdamW step on W per step (paper Sec. 4.1):
 backward, no dW buffer), ``adamw_two_phase`` runs lce_forward + lce_backward +
 lce_adamw_step (the standard path). Both keep fp32 moments and an fp32 master
 copy of W.
+
+``vocab_shard`` times one device's share of G-way vocabulary parallelism (loss
+parallel, paper Sec. 5): lce_forward_shard + lce_combine_shards +
+lce_backward_shard on N tokens x V/G ids (shard 0). The [G, N] partials that
+an all-gather would bring from the other devices are stood in for by copies of
+this shard's own, and no collective runs; the line reports N / step time, the
+whole job's rate when G devices each run their share in parallel.
 """
 from __future__ import annotations
 
@@ -98,7 +105,8 @@ def main():
     ap.add_argument("--workload", default="llama8b")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--variant", default="lce", choices=("lce", "adamw_fused", "adamw_two_phase"))
+    ap.add_argument("--variant", default="lce", choices=("lce", "adamw_fused", "adamw_two_phase", "vocab_shard"))
+    ap.add_argument("--shards", type=int, default=8, help="vocabulary shards (vocab_shard variant)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a 1 GiB device copy (for scaling HBM byte counters)")
     args = ap.parse_args()
@@ -121,11 +129,22 @@ def main():
           f"(inputs drawn in {time.perf_counter() - t_gen:.1f} s)", file=sys.stderr, flush=True)
     dev = torch.device("cuda:0")
     h = torch.from_numpy(inp.h_bits.view(np.int16)).view(torch.bfloat16).to(dev)
-    w = torch.from_numpy(inp.w_bits.view(np.int16)).view(torch.bfloat16).to(dev)
+    sharded = args.variant == "vocab_shard"
+    # shard 0 of the vocabulary-parallel variant holds ids [0, ceil(V / G)); only its rows go to the GPU
+    v_rows = (wl.v + args.shards - 1) // args.shards if sharded else wl.v
+    w = torch.from_numpy(inp.w_bits[:v_rows].view(np.int16)).view(torch.bfloat16).to(dev)
     t = torch.from_numpy(inp.targets).to(dev)
     n, d, v = wl.n, wl.d, wl.v
+    v_total = v
+    if sharded:
+        v = v_rows
+        shard = B.LceShard(v_total, 0)
+        p_full = B.problem(n, d, v_total, ignore_index=inp.ignore_index, reduction="mean", target_bytes=4)
+        comb_bytes, _ = B.lce_workspace_size(p_full)
     p = B.problem(n, d, v, ignore_index=inp.ignore_index, reduction="mean", target_bytes=4)
     fwd_bytes, bwd_bytes = B.lce_workspace_size(p)
+    if sharded:
+        fwd_bytes = max(fwd_bytes, comb_bytes)
     torch.cuda.synchronize()
     base_alloc = torch.cuda.memory_allocated()
     torch.cuda.reset_peak_memory_stats()
@@ -138,6 +157,12 @@ def main():
     dh = torch.empty((n, d), dtype=torch.bfloat16, device=dev)
     fused = args.variant == "adamw_fused"
     dw = None if fused else torch.empty((v, d), dtype=torch.bfloat16, device=dev)
+    if sharded:
+        dh = torch.empty((n, d), dtype=torch.float32, device=dev)      # this shard's fp32 dH term
+        lse_part = torch.empty(n, dtype=torch.float32, device=dev)
+        tgt_part = torch.empty(n, dtype=torch.float32, device=dev)
+        lse_parts = torch.empty((args.shards, n), dtype=torch.float32, device=dev)
+        tgt_parts = torch.empty((args.shards, n), dtype=torch.float32, device=dev)
     ws = torch.empty(max(fwd_bytes, bwd_bytes), dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream(dev).cuda_stream
     opt_ptrs = None
@@ -152,7 +177,22 @@ def main():
         step_no[0] += 1
         return B.adamw(1e-5, 0.9, 0.95, 1e-8, 0.1, step_no[0])
 
+    def shard_step():
+        B.lce_forward_shard(p, shard, h.data_ptr(), w.data_ptr(), t.data_ptr(), lse_part.data_ptr(),
+                            tgt_part.data_ptr(), nv.data_ptr(), status.data_ptr(), ws.data_ptr(), fwd_bytes, stream)
+        # stand-in for the all-gather of every shard's partials
+        lse_parts.copy_(lse_part.expand(args.shards, n))
+        tgt_parts.copy_(tgt_part.expand(args.shards, n))
+        B.lce_combine_shards(p_full, args.shards, lse_parts.data_ptr(), tgt_parts.data_ptr(), t.data_ptr(),
+                             loss.data_ptr(), lse.data_ptr(), nv.data_ptr(), status.data_ptr(), ws.data_ptr(),
+                             fwd_bytes, stream)
+        B.lce_backward_shard(p, shard, h.data_ptr(), w.data_ptr(), t.data_ptr(), lse.data_ptr(), nv.data_ptr(),
+                             grad.data_ptr(), dh.data_ptr(), dw.data_ptr(), ws.data_ptr(), bwd_bytes, stream)
+
     def step():
+        if sharded:
+            shard_step()
+            return
         B.lce_forward(p, h.data_ptr(), w.data_ptr(), t.data_ptr(), loss.data_ptr(), lse.data_ptr(),
                       nv.data_ptr(), status.data_ptr(), ws.data_ptr(), fwd_bytes, stream)
         if fused:
@@ -171,8 +211,10 @@ def main():
         print(f"[bench] warmup {i + 1}/{args.warmup} done", file=sys.stderr, flush=True)
     peak = torch.cuda.max_memory_allocated()
     # inputs, outputs and (optimizer variants) the optimizer state; dW only where it exists
-    resident = (h.numel() + w.numel() + dh.numel() + (dw.numel() if dw is not None else 0)) * 2 \
-        + t.numel() * 4 + n * 4 + (3 * v * d * 4 if opt_ptrs is not None else 0)
+    def nbytes(x):
+        return x.numel() * x.element_size() if x is not None else 0
+    resident = nbytes(h) + nbytes(w) + nbytes(t) + nbytes(dh) + nbytes(dw) + n * 4 \
+        + (3 * v * d * 4 if opt_ptrs is not None else 0)
 
     B.lce_timing_enable(True)
     torch.cuda.synchronize()
@@ -221,7 +263,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": wl.name, "n_tokens": n, "hidden": d, "vocab": v, "n_valid": nvalid,
                    "global_batch": wl.batch, "seq_len": wl.seq_len, "parallelism": "none",
-                   "reduction": "mean", "ignore_index": inp.ignore_index, "variant": args.variant},
+                   "reduction": "mean", "ignore_index": inp.ignore_index, "variant": args.variant,
+                   **({"shards": args.shards, "vocab_total": v_total} if sharded else {})},
         "valid_tokens_per_s": nvalid * args.steps / elapsed,
         "mfma_frac_step": flops_step / (ms_step * 1e-3) / (PEAK_BF16_TFLOPS * 1e12),
         "peak_hbm_bytes": int(peak),

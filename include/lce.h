@@ -179,6 +179,63 @@ lce_status_t lce_backward_adamw(const lce_problem_t* p,
                                 const lce_adamw_t* opt,
                                 void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * Vocabulary-parallel ("loss parallel") mode. The paper composes the loss with loss-parallel
+ * sharding of the output projection over the vocabulary (Sec. 4.2, Sec. 5): each of G shards
+ * holds the rows of W for ids [v_begin, v_begin + p->v) of a vocabulary of v_total ids. Then
+ *   lse_n = log sum_g exp(lse_n^g)       (lse_n^g: log-sum-exp over shard g's ids)
+ *   s[n, t_n] = sum_g tgt_n^g            (tgt_n^g: the target logit if shard g holds t_n, else 0)
+ * so a forward needs only O(N) numbers per shard, and each shard's backward, given the global
+ * lse, yields its rows of dW and its term G_g W_g of dH (the terms sum to dH).
+ * The collectives that move these numbers between devices belong to the caller: gather the
+ * [N] partials of every shard into [G, N] arrays for lce_combine_shards, and sum the dH terms.
+ */
+typedef struct lce_shard {
+  int64_t v_total;          /* ids of the whole vocabulary; targets are ids in [0, v_total) */
+  int64_t v_begin;          /* first id of this shard: W row r is id v_begin + r */
+} lce_shard_t;
+
+/*
+ * Forward of one shard (p->v = rows of this shard; p->reduction is not used). Outputs:
+ *   lse_part  [N] fp32: log-sum-exp over this shard's ids for valid rows, 0.0 elsewhere
+ *   tgt_part  [N] fp32: s[n, t_n] if this shard holds t_n, else 0.0
+ *   n_valid, dev_status as lce_forward (validity is judged against v_total)
+ * Workspace: lce_workspace_size(p) forward bytes. Errors: LCE_ERR_SHAPE if the shard range is
+ * not inside [0, v_total) or v_total >= 2^30.
+ */
+lce_status_t lce_forward_shard(const lce_problem_t* p, const lce_shard_t* shard,
+                               const void* H, const void* W, const void* targets,
+                               float* lse_part, float* tgt_part, int32_t* n_valid, int32_t* dev_status,
+                               void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Combine of G = n_shards shards' partials into the full-vocabulary results (p->v = v_total;
+ * p->d is checked as elsewhere but not used). lse_parts and tgt_parts are [G, N] fp32, row g
+ * holding shard g's lse_part / tgt_part (any shard order). Outputs loss, lse, n_valid and
+ * dev_status exactly as lce_forward defines them. The combine runs over shards in row order,
+ * so every device that combines the same arrays gets the same bits. 1 <= n_shards <= 4096.
+ * Workspace: lce_workspace_size(p) forward bytes.
+ */
+lce_status_t lce_combine_shards(const lce_problem_t* p, int32_t n_shards,
+                                const float* lse_parts, const float* tgt_parts, const void* targets,
+                                float* loss, float* lse, int32_t* n_valid, int32_t* dev_status,
+                                void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Backward of one shard, given the full-vocabulary lse (from lce_combine_shards) and the global
+ * n_valid: G_g = c (exp(s - lse) - onehot) over this shard's ids (onehot only where the shard
+ * holds the target).
+ *   dH_part   [N, D] fp32 dense, overwritten: G_g W_g (rows of invalid tokens 0.0); the sum over
+ *             shards is dH, kept in fp32 so that the sum loses nothing to bf16 rounding
+ *   dW        [p->v, D] bf16 dense: this shard's rows of dW (LCE_FLAG_ACCUMULATE_DW applies)
+ * Workspace: lce_workspace_size(p) backward bytes.
+ */
+lce_status_t lce_backward_shard(const lce_problem_t* p, const lce_shard_t* shard,
+                                const void* H, const void* W, const void* targets,
+                                const float* lse, const int32_t* n_valid, const float* grad_loss,
+                                float* dH_part, void* dW,
+                                void* workspace, size_t workspace_bytes, void* stream);
+
 /* Static, human-readable name of a status code. */
 const char* lce_status_string(lce_status_t s);
 

@@ -179,6 +179,68 @@ def backward_adamw(hidden: torch.Tensor, targets: torch.Tensor, lse: torch.Tenso
     return dh
 
 
+# ---- vocabulary-parallel (loss-parallel) pieces ---------------------------------------------
+# Each function runs one library call for one vocabulary shard; moving the [N] partials and the
+# dH terms between devices (all-gather, all-reduce) is the caller's collective.
+
+def forward_shard(hidden, weight_shard, targets, v_begin: int, v_total: int, ignore_index: int = -100):
+    """(lse_part fp32 [N], tgt_part fp32 [N], n_valid, status) of the shard holding ids
+    [v_begin, v_begin + rows of weight_shard) of a v_total-id vocabulary (lce_forward_shard)."""
+    h, ldh = _as_rows(hidden, "hidden")
+    w, ldw = _as_rows(weight_shard, "weight")
+    n, d = h.shape
+    t, tb = _targets(targets, n)
+    p = B.problem(n, d, w.shape[0], ld_h=ldh, ld_w=ldw, ignore_index=ignore_index, target_bytes=tb)
+    fwd_bytes, _ = B.lce_workspace_size(p)
+    dev = h.device
+    lse_part = torch.empty(n, dtype=torch.float32, device=dev)
+    tgt_part = torch.empty(n, dtype=torch.float32, device=dev)
+    nv = torch.empty(1, dtype=torch.int32, device=dev)
+    status = torch.empty(1, dtype=torch.int32, device=dev)
+    ws = torch.empty(max(fwd_bytes, 1), dtype=torch.uint8, device=dev)
+    B.lce_forward_shard(p, B.LceShard(v_total, v_begin), h.data_ptr(), w.data_ptr(), t.data_ptr(),
+                        lse_part.data_ptr(), tgt_part.data_ptr(), nv.data_ptr(), status.data_ptr(),
+                        ws.data_ptr(), fwd_bytes, _stream(dev))
+    return lse_part, tgt_part, nv, status
+
+
+def combine_shards(lse_parts: torch.Tensor, tgt_parts: torch.Tensor, targets: torch.Tensor, v_total: int,
+                   d: int, ignore_index: int = -100, reduction: str = "mean"):
+    """(loss, lse [N], n_valid, status) of the whole vocabulary from [G, N] shard partials."""
+    g, n = lse_parts.shape
+    for x in (lse_parts, tgt_parts):
+        if x.dtype != torch.float32 or not x.is_contiguous() or tuple(x.shape) != (g, n):
+            raise ValueError("partials must be contiguous float32 [G, N] tensors")
+    t, tb = _targets(targets, n)
+    p = B.problem(n, d, v_total, ignore_index=ignore_index, reduction=reduction, target_bytes=tb)
+    fwd_bytes, _ = B.lce_workspace_size(p)
+    dev = lse_parts.device
+    loss = torch.empty((n,) if reduction == "none" else (), dtype=torch.float32, device=dev)
+    lse = torch.empty(n, dtype=torch.float32, device=dev)
+    nv = torch.empty(1, dtype=torch.int32, device=dev)
+    status = torch.empty(1, dtype=torch.int32, device=dev)
+    ws = torch.empty(max(fwd_bytes, 1), dtype=torch.uint8, device=dev)
+    B.lce_combine_shards(p, g, lse_parts.data_ptr(), tgt_parts.data_ptr(), t.data_ptr(), loss.data_ptr(),
+                         lse.data_ptr(), nv.data_ptr(), status.data_ptr(), ws.data_ptr(), fwd_bytes, _stream(dev))
+    return loss, lse, nv, status
+
+
+def backward_shard(hidden, weight_shard, targets, lse, n_valid, grad_loss, v_begin: int, v_total: int,
+                   ignore_index: int = -100, reduction: str = "mean"):
+    """(dH term fp32 [N, D], dW rows bf16 [V_shard, D]) of one shard, given the global lse
+    (lce_backward_shard); the dH terms of all shards sum to dH."""
+    p, h, w, t, g = _backward_args(hidden, weight_shard, targets, lse, grad_loss, ignore_index, reduction)
+    _, bwd_bytes = B.lce_workspace_size(p)
+    dev = h.device
+    dh = torch.empty((p.n, p.d), dtype=torch.float32, device=dev)
+    dw = torch.empty((p.v, p.d), dtype=torch.bfloat16, device=dev)
+    ws = torch.empty(max(bwd_bytes, 1), dtype=torch.uint8, device=dev)
+    B.lce_backward_shard(p, B.LceShard(v_total, v_begin), h.data_ptr(), w.data_ptr(), t.data_ptr(),
+                         lse.data_ptr(), n_valid.data_ptr(), g.data_ptr(), dh.data_ptr(), dw.data_ptr(),
+                         ws.data_ptr(), bwd_bytes, _stream(dev))
+    return dh, dw
+
+
 class LinearCrossEntropy(torch.autograd.Function):
     """Fused projection + cross-entropy; backward returns gradients for hidden and weight."""
 

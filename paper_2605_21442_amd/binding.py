@@ -35,7 +35,8 @@ REDUCTIONS = {"mean": LCE_REDUCE_MEAN, "sum": LCE_REDUCE_SUM, "none": LCE_REDUCE
 # every symbol include/lce.h declares
 EXPORTED = ("lce_workspace_size", "lce_forward", "lce_backward", "lce_status_string",
             "lce_timing_enable", "lce_timing_kernel_count", "lce_timing_kernel_name",
-            "lce_timing_read", "lce_adamw_step", "lce_backward_adamw")
+            "lce_timing_read", "lce_adamw_step", "lce_backward_adamw", "lce_forward_shard",
+            "lce_combine_shards", "lce_backward_shard")
 
 
 class LceError(RuntimeError):
@@ -55,6 +56,10 @@ class LceAdamW(ctypes.Structure):
     _fields_ = [("lr", ctypes.c_float), ("beta1", ctypes.c_float), ("beta2", ctypes.c_float),
                 ("eps", ctypes.c_float), ("weight_decay", ctypes.c_float), ("step", ctypes.c_int32),
                 ("reserved", ctypes.c_int32)]
+
+
+class LceShard(ctypes.Structure):
+    _fields_ = [("v_total", ctypes.c_int64), ("v_begin", ctypes.c_int64)]
 
 
 def problem(n: int, d: int, v: int, *, ld_h: int = 0, ld_w: int = 0, ignore_index: int = -100,
@@ -89,6 +94,10 @@ def load() -> ctypes.CDLL:
         A = ctypes.POINTER(LceAdamW)
         lib.lce_adamw_step.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int64, vp, vp, vp, vp, vp, A, vp]
         lib.lce_backward_adamw.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, A, vp, sz, vp]
+        S = ctypes.POINTER(LceShard)
+        lib.lce_forward_shard.argtypes = [P, S, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+        lib.lce_combine_shards.argtypes = [P, ctypes.c_int32, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+        lib.lce_backward_shard.argtypes = [P, S, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
         lib.lce_status_string.argtypes = [ctypes.c_int]
         lib.lce_status_string.restype = ctypes.c_char_p
         lib.lce_timing_enable.argtypes = [ctypes.c_int]
@@ -98,7 +107,8 @@ def load() -> ctypes.CDLL:
         lib.lce_timing_read.argtypes = [ctypes.c_int, ctypes.POINTER(ctypes.c_double),
                                         ctypes.POINTER(ctypes.c_int64)]
         for name in ("lce_workspace_size", "lce_forward", "lce_backward", "lce_timing_enable",
-                     "lce_timing_read", "lce_timing_kernel_count", "lce_adamw_step", "lce_backward_adamw"):
+                     "lce_timing_read", "lce_timing_kernel_count", "lce_adamw_step", "lce_backward_adamw",
+                     "lce_forward_shard", "lce_combine_shards", "lce_backward_shard"):
             getattr(lib, name).restype = ctypes.c_int
         _lib = lib
         return lib
@@ -144,6 +154,30 @@ def lce_backward_adamw(p: LceProblem, H: int, W: int, targets: int, lse: int, n_
     _check(load().lce_backward_adamw(ctypes.byref(p), H, W, targets, lse, n_valid, grad_loss, dH, exp_avg,
                                      exp_avg_sq, W_master or None, ctypes.byref(opt), workspace,
                                      workspace_bytes, stream or None), "lce_backward_adamw")
+
+
+def lce_forward_shard(p: LceProblem, shard: LceShard, H: int, W: int, targets: int, lse_part: int,
+                      tgt_part: int, n_valid: int, dev_status: int, workspace: int, workspace_bytes: int,
+                      stream: int) -> None:
+    _check(load().lce_forward_shard(ctypes.byref(p), ctypes.byref(shard), H, W, targets, lse_part, tgt_part,
+                                    n_valid, dev_status or None, workspace, workspace_bytes, stream or None),
+           "lce_forward_shard")
+
+
+def lce_combine_shards(p: LceProblem, n_shards: int, lse_parts: int, tgt_parts: int, targets: int, loss: int,
+                       lse: int, n_valid: int, dev_status: int, workspace: int, workspace_bytes: int,
+                       stream: int) -> None:
+    _check(load().lce_combine_shards(ctypes.byref(p), n_shards, lse_parts, tgt_parts, targets, loss, lse,
+                                     n_valid, dev_status or None, workspace, workspace_bytes, stream or None),
+           "lce_combine_shards")
+
+
+def lce_backward_shard(p: LceProblem, shard: LceShard, H: int, W: int, targets: int, lse: int, n_valid: int,
+                       grad_loss: int, dH_part: int, dW: int, workspace: int, workspace_bytes: int,
+                       stream: int) -> None:
+    _check(load().lce_backward_shard(ctypes.byref(p), ctypes.byref(shard), H, W, targets, lse, n_valid,
+                                     grad_loss, dH_part, dW, workspace, workspace_bytes, stream or None),
+           "lce_backward_shard")
 
 
 def lce_timing_enable(on: bool) -> None:

@@ -438,31 +438,35 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_fwd_stats(const uint16_t* __res
 // ---------------------------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void k_combine(const uint16_t* __restrict__ H, int64_t ldh,
                                                  const uint16_t* __restrict__ W, int64_t ldw,
-                                                 const void* targets, int tbytes,
+                                                 const void* targets, int tbytes, int64_t id0, int64_t v_local,
                                                  const int* __restrict__ idx, const int* __restrict__ nv_ptr,
                                                  int d, int nparts2, const float* __restrict__ part_m,
                                                  const float* __restrict__ part_s, int npad,
                                                  float* __restrict__ lse_out, float* __restrict__ terms,
-                                                 float* __restrict__ per_token) {
+                                                 float* __restrict__ per_token, float* __restrict__ tgt_part) {
   const int lane = threadIdx.x & 63;
   const int i = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int nv = *nv_ptr;
   if (i >= nv) return;
   const int row = idx[i];
-  const int64_t tg = load_target(targets, tbytes, row);
-  const uint4* hr = reinterpret_cast<const uint4*>(H + (int64_t)row * ldh);
-  const uint4* wt = reinterpret_cast<const uint4*>(W + tg * ldw);
+  // target id relative to this W's first row (id0 > 0 only for a vocabulary shard, which may
+  // not hold the target: then its target logit is 0)
+  const int64_t tl = load_target(targets, tbytes, row) - id0;
   float dot = 0.f;
-  for (int c = lane; c < d / 8; c += 64) {
-    const uint4 a = hr[c], b = wt[c];
-    const uint32_t av[4] = {a.x, a.y, a.z, a.w}, bv[4] = {b.x, b.y, b.z, b.w};
+  if (tl >= 0 && tl < v_local) {
+    const uint4* hr = reinterpret_cast<const uint4*>(H + (int64_t)row * ldh);
+    const uint4* wt = reinterpret_cast<const uint4*>(W + tl * ldw);
+    for (int c = lane; c < d / 8; c += 64) {
+      const uint4 a = hr[c], b = wt[c];
+      const uint32_t av[4] = {a.x, a.y, a.z, a.w}, bv[4] = {b.x, b.y, b.z, b.w};
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      dot = fmaf(bf16_to_f32(av[q] & 0xFFFF), bf16_to_f32(bv[q] & 0xFFFF), dot);
-      dot = fmaf(bf16_to_f32(av[q] >> 16), bf16_to_f32(bv[q] >> 16), dot);
+      for (int q = 0; q < 4; ++q) {
+        dot = fmaf(bf16_to_f32(av[q] & 0xFFFF), bf16_to_f32(bv[q] & 0xFFFF), dot);
+        dot = fmaf(bf16_to_f32(av[q] >> 16), bf16_to_f32(bv[q] >> 16), dot);
+      }
     }
+    dot = wave_sum(dot);
   }
-  dot = wave_sum(dot);
   const float m = lane < nparts2 ? part_m[(int64_t)lane * npad + i] : -INFINITY;
   const float s = lane < nparts2 ? part_s[(int64_t)lane * npad + i] : 0.f;
   const float mm = wave_max(m);
@@ -471,9 +475,36 @@ __global__ __launch_bounds__(256) void k_combine(const uint16_t* __restrict__ H,
   const float lse = (mm + log2f(se)) * kLn2;
   if (lane == 0) {
     lse_out[row] = lse;
-    terms[i] = lse - dot;
-    if (per_token) per_token[row] = lse - dot;
+    if (tgt_part) {
+      tgt_part[row] = dot;
+    } else {
+      terms[i] = lse - dot;
+      if (per_token) per_token[row] = lse - dot;
+    }
   }
+}
+
+// Combine of vocabulary shards: lse = log sum_g exp(lse_g) (max-shifted, shards in order) and the
+// target logit sum_g tgt_g (one shard holds it), per valid token; one thread per token.
+__global__ __launch_bounds__(256) void k_shard_combine(int g_count, const float* __restrict__ lse_parts,
+                                                       const float* __restrict__ tgt_parts, int64_t ld,
+                                                       const int* __restrict__ idx, const int* __restrict__ nv_ptr,
+                                                       float* __restrict__ lse_out, float* __restrict__ terms,
+                                                       float* __restrict__ per_token) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i >= *nv_ptr) return;
+  const int row = idx[i];
+  float mm = -INFINITY;
+  for (int g = 0; g < g_count; ++g) mm = fmaxf(mm, lse_parts[g * ld + row]);
+  float se = 0.f, z = 0.f;
+  for (int g = 0; g < g_count; ++g) {
+    se += exp2f((lse_parts[g * ld + row] - mm) * kLog2e);
+    z += tgt_parts[g * ld + row];
+  }
+  const float lse = mm + log2f(se) * kLn2;
+  lse_out[row] = lse;
+  terms[i] = lse - z;
+  if (per_token) per_token[row] = lse - z;
 }
 
 // K3b: loss = sum or mean of the per-row terms, fixed-order fp64 tree.
@@ -598,7 +629,7 @@ __device__ __forceinline__ float grad_scale(const float* grad, const int* n_norm
 // ---------------------------------------------------------------------------------------------
 __global__ __launch_bounds__(NTHREADS, 2) void k_bwd_g(const uint16_t* __restrict__ W, int64_t ldw, int64_t v0, int vs,
                                                        const uint16_t* __restrict__ H, int64_t ldh, int64_t n,
-                                                       const void* targets, int tbytes,
+                                                       const void* targets, int tbytes, int64_t id0,
                                                        const int* __restrict__ idx, const int* __restrict__ nv_ptr,
                                                        const float* __restrict__ lse, const float* __restrict__ grad,
                                                        const int* __restrict__ n_norm, int reduction, int d, int tm_count,
@@ -629,7 +660,7 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_bwd_g(const uint16_t* __restric
     if (tok[j] < nv) {
       const int row = idx[tok[j]];
       l2[j] = lse[row] * kLog2e;
-      tgt[j] = (int)(load_target(targets, tbytes, row) - v0) - vt0;   // tile-relative target row
+      tgt[j] = (int)(load_target(targets, tbytes, row) - id0 - v0) - vt0;   // tile-relative target row
       cj[j] = reduction == LCE_REDUCE_NONE ? grad[row] : c_all;
     } else {
       l2[j] = 0.f;
@@ -860,19 +891,25 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_bwd_dh(const uint16_t* __restri
 
 // K7: dH[row] = bf16(dH32[pos[row]]) for valid rows, +0.0 for the others. 8 elements per thread.
 __global__ __launch_bounds__(256) void k_dh_finalize(const float* __restrict__ dH32, const int* __restrict__ pos,
-                                                     int64_t n, int d, uint16_t* __restrict__ dH, int has_slabs) {
+                                                     int64_t n, int d, uint16_t* __restrict__ dH,
+                                                     float* __restrict__ dHf, int has_slabs) {
   const int64_t e = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 8;
   if (e >= n * d) return;
   const int64_t row = e / d;
   const int col = (int)(e - row * d);
   const int p = pos[row];
-  uint4 out = make_uint4(0, 0, 0, 0);
+  float4 a = make_float4(0.f, 0.f, 0.f, 0.f), b = a;
   if (p >= 0 && has_slabs) {
-    const float4 a = *reinterpret_cast<const float4*>(dH32 + (int64_t)p * d + col);
-    const float4 b = *reinterpret_cast<const float4*>(dH32 + (int64_t)p * d + col + 4);
-    out = make_uint4(pack_bf16x2(a.x, a.y), pack_bf16x2(a.z, a.w), pack_bf16x2(b.x, b.y), pack_bf16x2(b.z, b.w));
+    a = *reinterpret_cast<const float4*>(dH32 + (int64_t)p * d + col);
+    b = *reinterpret_cast<const float4*>(dH32 + (int64_t)p * d + col + 4);
   }
-  *reinterpret_cast<uint4*>(dH + e) = out;
+  if (dHf) {   // fp32 rows (a vocabulary shard's term of dH, to be summed over shards)
+    *reinterpret_cast<float4*>(dHf + e) = a;
+    *reinterpret_cast<float4*>(dHf + e + 4) = b;
+  } else {
+    *reinterpret_cast<uint4*>(dH + e) =
+        make_uint4(pack_bf16x2(a.x, a.y), pack_bf16x2(a.z, a.w), pack_bf16x2(b.x, b.y), pack_bf16x2(b.z, b.w));
+  }
 }
 
 __global__ __launch_bounds__(256) void k_zero16(uint4* __restrict__ p, int64_t n16) {
@@ -931,9 +968,9 @@ __global__ __launch_bounds__(256) void k_adamw(int64_t v, int d, const uint16_t*
 // Host side: validation, plan, workspace carve-up, launches, optional timing.
 // ---------------------------------------------------------------------------------------------
 enum KernelId { K_COMPACT = 0, K_FWD_STATS, K_COMBINE, K_LOSS, K_TRANSPOSE_H, K_TRANSPOSE_W, K_BWD_G,
-                K_BWD_DW, K_BWD_DH, K_DH_FINAL, K_ADAMW, K_MISC, K_COUNT };
+                K_BWD_DW, K_BWD_DH, K_DH_FINAL, K_ADAMW, K_SHARD_COMBINE, K_MISC, K_COUNT };
 const char* const kKernelNames[K_COUNT] = {"compact", "fwd_stats", "combine", "loss", "transpose_h",
-                                           "transpose_w", "bwd_g", "bwd_dw", "bwd_dh", "dh_finalize", "adamw", "misc"};
+                                           "transpose_w", "bwd_g", "bwd_dw", "bwd_dh", "dh_finalize", "adamw", "shard_combine", "misc"};
 
 struct Timing {
   std::mutex mu;
@@ -1055,18 +1092,77 @@ struct Launcher {
   }
 };
 
-// The backward pass behind lce_backward (dW != null) and lce_backward_adamw (adamw != null).
-lce_status_t backward_impl(const lce_problem_t* p, const void* H, const void* W, const void* targets,
-                           const float* lse, const int32_t* n_valid, const float* grad_loss, void* dH,
-                           uint16_t* dW, const AdamWState* adamw, const AdamWConst* oc,
+// Which part of the vocabulary W holds: ids [v_begin, v_begin + p->v) of v_total (the whole
+// vocabulary: v_begin = 0, v_total = p->v).
+struct ShardInfo {
+  int64_t v_total, v_begin;
+};
+
+lce_status_t shard_info(const lce_problem_t* p, const lce_shard_t* sh, ShardInfo* si) {
+  if (!p || !sh) return LCE_ERR_NULL;
+  if (sh->v_total < 1 || sh->v_total >= (int64_t)1 << 30 || sh->v_begin < 0 || p->v < 1 ||
+      sh->v_begin + p->v > sh->v_total)
+    return LCE_ERR_SHAPE;
+  si->v_total = sh->v_total;
+  si->v_begin = sh->v_begin;
+  return LCE_OK;
+}
+
+// The forward pass behind lce_forward and (tgt_part != null) lce_forward_shard.
+lce_status_t forward_impl(const lce_problem_t* p, const ShardInfo* shard, const void* H, const void* W,
+                          const void* targets, float* loss, float* lse, float* tgt_part, int32_t* n_valid,
+                          int32_t* dev_status, void* workspace, size_t workspace_bytes, void* stream) {
+  Plan pl;
+  lce_status_t st = make_plan(p, &pl);
+  if (st != LCE_OK) return st;
+  const ShardInfo si = shard ? *shard : ShardInfo{pl.v, 0};
+  if ((!shard && !loss) || (shard && !tgt_part) || !n_valid) return LCE_ERR_NULL;
+  if (pl.n > 0 && (!H || !W || !targets || !lse || !workspace)) return LCE_ERR_NULL;
+  if (pl.n > 0 && (!aligned16(H) || !aligned16(W) || ((uintptr_t)workspace & 255) != 0)) return LCE_ERR_ALIGN;
+  if (pl.n > 0 && workspace_bytes < pl.fwd_bytes) return LCE_ERR_WORKSPACE;
+  Launcher L{(hipStream_t)stream};
+  const bool none = !shard && p->reduction == LCE_REDUCE_NONE;
+  if (pl.n == 0) {
+    L(K_MISC, k_fwd_empty, dim3(1), dim3(64), (none || shard) ? (float*)nullptr : loss, n_valid, dev_status);
+    return L.st;
+  }
+  char* ws = (char*)workspace;
+  int* idx = (int*)(ws + pl.o_idx);
+  int* pos = (int*)(ws + pl.o_pos);
+  int* nv = (int*)(ws + pl.o_nv);
+  float* pm = (float*)(ws + pl.o_pm);
+  float* ps = (float*)(ws + pl.o_ps);
+  float* terms = (float*)(ws + pl.o_terms);
+  const uint16_t* h = (const uint16_t*)H;
+  const uint16_t* w = (const uint16_t*)W;
+
+  // rows that are not valid get lse 0 and a zero per-token loss (or shard target logit)
+  L(K_COMPACT, k_compact, dim3(1), dim3(1024), targets, p->target_bytes, pl.n, si.v_total, p->ignore_index,
+    idx, pos, nv, n_valid, dev_status, lse, none ? loss : tgt_part);
+  L(K_FWD_STATS, k_fwd_stats, dim3(pl.nt_max * pl.nparts), dim3(NTHREADS), w, pl.ldw, (int)pl.v, h, pl.ldh,
+    pl.n, (const int*)idx, (const int*)nv, (int)pl.d, pl.nparts, pl.nt_max, pl.vt_count, pm, ps, (int)pl.npad);
+  L(K_COMBINE, k_combine, dim3((unsigned)((pl.n + 3) / 4)), dim3(256), h, pl.ldh, w, pl.ldw, targets,
+    p->target_bytes, si.v_begin, pl.v, (const int*)idx, (const int*)nv, (int)pl.d, 2 * pl.nparts,
+    (const float*)pm, (const float*)ps, (int)pl.npad, lse, terms, none ? loss : (float*)nullptr, tgt_part);
+  if (!none && !shard) L(K_LOSS, k_loss, dim3(1), dim3(1024), (const float*)terms, (const int*)nv, p->reduction, loss);
+  return L.st;
+}
+
+// The backward pass behind lce_backward (dW != null), lce_backward_adamw (adamw != null) and
+// lce_backward_shard (shard != null, fp32 dH term in dHf).
+lce_status_t backward_impl(const lce_problem_t* p, const ShardInfo* shard, const void* H, const void* W,
+                           const void* targets, const float* lse, const int32_t* n_valid, const float* grad_loss,
+                           void* dH, float* dHf, uint16_t* dW, const AdamWState* adamw, const AdamWConst* oc,
                            void* workspace, size_t workspace_bytes, void* stream) {
   Plan pl;
   lce_status_t st = make_plan(p, &pl);
   if (st != LCE_OK) return st;
+  const ShardInfo si = shard ? *shard : ShardInfo{pl.v, 0};
+  void* dH_any = dHf ? (void*)dHf : dH;
   if (!W || !grad_loss || (!n_valid && p->reduction == LCE_REDUCE_MEAN)) return LCE_ERR_NULL;
-  if (pl.n > 0 && (!H || !targets || !lse || !dH || !workspace)) return LCE_ERR_NULL;
+  if (pl.n > 0 && (!H || !targets || !lse || !dH_any || !workspace)) return LCE_ERR_NULL;
   if (!aligned16(W)) return LCE_ERR_ALIGN;
-  if (pl.n > 0 && (!aligned16(H) || !aligned16(dH) || ((uintptr_t)workspace & 255) != 0)) return LCE_ERR_ALIGN;
+  if (pl.n > 0 && (!aligned16(H) || !aligned16(dH_any) || ((uintptr_t)workspace & 255) != 0)) return LCE_ERR_ALIGN;
   if (pl.n > 0 && workspace_bytes < pl.bwd_bytes) return LCE_ERR_WORKSPACE;
   const bool accumulate = (p->flags & LCE_FLAG_ACCUMULATE_DW) != 0;
   const AdamWState as = adamw ? *adamw : AdamWState{nullptr, 0, nullptr, nullptr, nullptr};
@@ -1095,7 +1191,7 @@ lce_status_t backward_impl(const lce_problem_t* p, const void* H, const void* W,
   const uint16_t* w = (const uint16_t*)W;
   const int d = (int)pl.d, npad = (int)pl.npad, vc = (int)pl.vc;
 
-  L(K_COMPACT, k_compact, dim3(1), dim3(1024), targets, p->target_bytes, pl.n, pl.v, p->ignore_index,
+  L(K_COMPACT, k_compact, dim3(1), dim3(1024), targets, p->target_bytes, pl.n, si.v_total, p->ignore_index,
     idx, pos, nv, (int*)nullptr, (int*)nullptr, (float*)nullptr, (float*)nullptr);
   // Hvt[d][i] = H[idx[i]][d] for i < Nv, zero up to round_up(Nv, 64)
   L(K_TRANSPOSE_H, k_transpose, dim3((unsigned)(npad / 64), (unsigned)((d + 63) / 64)), dim3(256), h, pl.ldh,
@@ -1114,7 +1210,7 @@ lce_status_t backward_impl(const lce_problem_t* p, const void* H, const void* W,
     L(K_TRANSPOSE_W, k_transpose, dim3((unsigned)(vs64 / 64), (unsigned)((d + 63) / 64)), dim3(256), w, pl.ldw,
       (const int*)nullptr, v0, (const int*)nullptr, vs, d, wst, (int64_t)vc, vs64);
     L(K_BWD_G, k_bwd_g, dim3((unsigned)(tm * pl.nt_max)), dim3(NTHREADS), w, pl.ldw, v0, vs, h, pl.ldh, pl.n,
-      targets, p->target_bytes, (const int*)idx, (const int*)nv, lse, grad_loss, (const int*)n_valid,
+      targets, p->target_bytes, si.v_begin, (const int*)idx, (const int*)nv, lse, grad_loss, (const int*)n_valid,
       p->reduction, d, tm, g, vc, gt, npad);
     L(K_BWD_DW, dw_kernel, dim3((unsigned)(8 * ((tm + 7) / 8) * dt)), dim3(NTHREADS), (const uint16_t*)gt, npad,
       vs, (const uint16_t*)hvt, d, (const int*)nv, tm, dW, v0, as, c);
@@ -1123,7 +1219,7 @@ lce_status_t backward_impl(const lce_problem_t* p, const void* H, const void* W,
   }
   const int64_t nthr = pl.n * pl.d / 8;
   L(K_DH_FINAL, k_dh_finalize, dim3((unsigned)((nthr + 255) / 256)), dim3(256), (const float*)dh32,
-    (const int*)pos, pl.n, d, (uint16_t*)dH, 1);
+    (const int*)pos, pl.n, d, (uint16_t*)dH, dHf, 1);
   return L.st;
 }
 
@@ -1157,12 +1253,31 @@ lce_status_t lce_workspace_size(const lce_problem_t* p, size_t* fwd_bytes, size_
 lce_status_t lce_forward(const lce_problem_t* p, const void* H, const void* W, const void* targets,
                          float* loss, float* lse, int32_t* n_valid, int32_t* dev_status,
                          void* workspace, size_t workspace_bytes, void* stream) {
+  return forward_impl(p, nullptr, H, W, targets, loss, lse, nullptr, n_valid, dev_status, workspace,
+                      workspace_bytes, stream);
+}
+
+lce_status_t lce_forward_shard(const lce_problem_t* p, const lce_shard_t* shard, const void* H, const void* W,
+                               const void* targets, float* lse_part, float* tgt_part, int32_t* n_valid,
+                               int32_t* dev_status, void* workspace, size_t workspace_bytes, void* stream) {
+  ShardInfo si;
+  lce_status_t st = shard_info(p, shard, &si);
+  if (st != LCE_OK) return st;
+  return forward_impl(p, &si, H, W, targets, nullptr, lse_part, tgt_part, n_valid, dev_status, workspace,
+                      workspace_bytes, stream);
+}
+
+lce_status_t lce_combine_shards(const lce_problem_t* p, int32_t n_shards, const float* lse_parts,
+                                const float* tgt_parts, const void* targets, float* loss, float* lse,
+                                int32_t* n_valid, int32_t* dev_status, void* workspace, size_t workspace_bytes,
+                                void* stream) {
   Plan pl;
   lce_status_t st = make_plan(p, &pl);
   if (st != LCE_OK) return st;
+  if (n_shards < 1 || n_shards > 4096) return LCE_ERR_ARG;
   if (!loss || !n_valid) return LCE_ERR_NULL;
-  if (pl.n > 0 && (!H || !W || !targets || !lse || !workspace)) return LCE_ERR_NULL;
-  if (pl.n > 0 && (!aligned16(H) || !aligned16(W) || ((uintptr_t)workspace & 255) != 0)) return LCE_ERR_ALIGN;
+  if (pl.n > 0 && (!lse_parts || !tgt_parts || !targets || !lse || !workspace)) return LCE_ERR_NULL;
+  if (pl.n > 0 && ((uintptr_t)workspace & 255) != 0) return LCE_ERR_ALIGN;
   if (pl.n > 0 && workspace_bytes < pl.fwd_bytes) return LCE_ERR_WORKSPACE;
   Launcher L{(hipStream_t)stream};
   const bool none = p->reduction == LCE_REDUCE_NONE;
@@ -1174,19 +1289,11 @@ lce_status_t lce_forward(const lce_problem_t* p, const void* H, const void* W, c
   int* idx = (int*)(ws + pl.o_idx);
   int* pos = (int*)(ws + pl.o_pos);
   int* nv = (int*)(ws + pl.o_nv);
-  float* pm = (float*)(ws + pl.o_pm);
-  float* ps = (float*)(ws + pl.o_ps);
   float* terms = (float*)(ws + pl.o_terms);
-  const uint16_t* h = (const uint16_t*)H;
-  const uint16_t* w = (const uint16_t*)W;
-
   L(K_COMPACT, k_compact, dim3(1), dim3(1024), targets, p->target_bytes, pl.n, pl.v, p->ignore_index,
     idx, pos, nv, n_valid, dev_status, lse, none ? loss : (float*)nullptr);
-  L(K_FWD_STATS, k_fwd_stats, dim3(pl.nt_max * pl.nparts), dim3(NTHREADS), w, pl.ldw, (int)pl.v, h, pl.ldh,
-    pl.n, (const int*)idx, (const int*)nv, (int)pl.d, pl.nparts, pl.nt_max, pl.vt_count, pm, ps, (int)pl.npad);
-  L(K_COMBINE, k_combine, dim3((unsigned)((pl.n + 3) / 4)), dim3(256), h, pl.ldh, w, pl.ldw, targets,
-    p->target_bytes, (const int*)idx, (const int*)nv, (int)pl.d, 2 * pl.nparts, (const float*)pm,
-    (const float*)ps, (int)pl.npad, lse, terms, none ? loss : (float*)nullptr);
+  L(K_SHARD_COMBINE, k_shard_combine, dim3((unsigned)((pl.n + 255) / 256)), dim3(256), (int)n_shards, lse_parts,
+    tgt_parts, pl.n, (const int*)idx, (const int*)nv, lse, terms, none ? loss : (float*)nullptr);
   if (!none) L(K_LOSS, k_loss, dim3(1), dim3(1024), (const float*)terms, (const int*)nv, p->reduction, loss);
   return L.st;
 }
@@ -1196,8 +1303,21 @@ lce_status_t lce_backward(const lce_problem_t* p, const void* H, const void* W, 
                           void* dH, void* dW, void* workspace, size_t workspace_bytes, void* stream) {
   if (!dW) return LCE_ERR_NULL;
   if (!aligned16(dW)) return LCE_ERR_ALIGN;
-  return backward_impl(p, H, W, targets, lse, n_valid, grad_loss, dH, (uint16_t*)dW, nullptr, nullptr,
-                       workspace, workspace_bytes, stream);
+  return backward_impl(p, nullptr, H, W, targets, lse, n_valid, grad_loss, dH, nullptr, (uint16_t*)dW, nullptr,
+                       nullptr, workspace, workspace_bytes, stream);
+}
+
+lce_status_t lce_backward_shard(const lce_problem_t* p, const lce_shard_t* shard, const void* H, const void* W,
+                                const void* targets, const float* lse, const int32_t* n_valid,
+                                const float* grad_loss, float* dH_part, void* dW, void* workspace,
+                                size_t workspace_bytes, void* stream) {
+  ShardInfo si;
+  lce_status_t st = shard_info(p, shard, &si);
+  if (st != LCE_OK) return st;
+  if (!dW || (p->n > 0 && !dH_part)) return LCE_ERR_NULL;
+  if (!aligned16(dW)) return LCE_ERR_ALIGN;
+  return backward_impl(p, &si, H, W, targets, lse, n_valid, grad_loss, nullptr, dH_part, (uint16_t*)dW, nullptr,
+                       nullptr, workspace, workspace_bytes, stream);
 }
 
 lce_status_t lce_adamw_step(int64_t v, int64_t d, int64_t ld_w, void* W, const void* dW, float* exp_avg,
@@ -1231,8 +1351,8 @@ lce_status_t lce_backward_adamw(const lce_problem_t* p, const void* H, void* W, 
   if (!exp_avg || !exp_avg_sq) return LCE_ERR_NULL;
   if (!aligned16(exp_avg) || !aligned16(exp_avg_sq) || (W_master && !aligned16(W_master))) return LCE_ERR_ALIGN;
   AdamWState as{(uint16_t*)W, p->ld_w ? p->ld_w : p->d, exp_avg, exp_avg_sq, W_master};
-  return backward_impl(p, H, W, targets, lse, n_valid, grad_loss, dH, nullptr, &as, &c, workspace,
-                       workspace_bytes, stream);
+  return backward_impl(p, nullptr, H, W, targets, lse, n_valid, grad_loss, dH, nullptr, nullptr, &as, &c,
+                       workspace, workspace_bytes, stream);
 }
 
 lce_status_t lce_timing_enable(int on) {

@@ -169,3 +169,38 @@ def test_backward_adamw_argument_checks_run_before_any_launch():
     with pytest.raises(B.LceError) as e:
         B.lce_backward_adamw(p, **ok, opt=B.adamw(**dict(HP, step=-2)))
     assert e.value.code == B.LCE_ERR_ARG
+
+
+def test_shard_argument_checks_run_before_any_launch():
+    p = B.problem(8, 64, 10)
+    fwd, bwd = B.lce_workspace_size(p)
+    fok = dict(H=_fake(), W=_fake(0x200000), targets=_fake(0x300000), lse_part=_fake(0x400000),
+               tgt_part=_fake(0x500000), n_valid=_fake(0x600000), dev_status=0,
+               workspace=_fake(0x700000), workspace_bytes=fwd, stream=0)
+    for shard, code in [(B.LceShard(20, 11), B.LCE_ERR_SHAPE),     # rows 11..20 leave [0, 20)
+                        (B.LceShard(20, -1), B.LCE_ERR_SHAPE),
+                        (B.LceShard(1 << 30, 0), B.LCE_ERR_SHAPE),
+                        (B.LceShard(9, 0), B.LCE_ERR_SHAPE)]:
+        with pytest.raises(B.LceError) as e:
+            B.lce_forward_shard(p, shard, **fok)
+        assert e.value.code == code, (shard.v_total, shard.v_begin)
+    with pytest.raises(B.LceError) as e:
+        B.lce_forward_shard(p, B.LceShard(20, 10), **dict(fok, tgt_part=0))
+    assert e.value.code == B.LCE_ERR_NULL
+    cok = dict(lse_parts=_fake(0x200000), tgt_parts=_fake(0x300000), targets=_fake(0x400000),
+               loss=_fake(0x500000), lse=_fake(0x600000), n_valid=_fake(0x700000), dev_status=0,
+               workspace=_fake(0x800000), workspace_bytes=fwd, stream=0)
+    for n_shards, change, code in [(0, {}, B.LCE_ERR_ARG), (5000, {}, B.LCE_ERR_ARG),
+                                   (2, dict(tgt_parts=0), B.LCE_ERR_NULL),
+                                   (2, dict(workspace_bytes=64), B.LCE_ERR_WORKSPACE)]:
+        with pytest.raises(B.LceError) as e:
+            B.lce_combine_shards(p, n_shards, **dict(cok, **change))
+        assert e.value.code == code, (n_shards, change)
+    bok = dict(H=_fake(), W=_fake(0x200000), targets=_fake(0x300000), lse=_fake(0x400000),
+               n_valid=_fake(0x500000), grad_loss=_fake(0x600000), dH_part=_fake(0x700000),
+               dW=_fake(0x800000), workspace=_fake(0x900000), workspace_bytes=bwd, stream=0)
+    for change, code in [(dict(dH_part=0), B.LCE_ERR_NULL), (dict(dW=0x800008), B.LCE_ERR_ALIGN),
+                         (dict(workspace_bytes=16), B.LCE_ERR_WORKSPACE)]:
+        with pytest.raises(B.LceError) as e:
+            B.lce_backward_shard(p, B.LceShard(20, 10), **dict(bok, **change))
+        assert e.value.code == code, change

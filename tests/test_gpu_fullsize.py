@@ -139,3 +139,55 @@ def test_full_size_fused_adamw_llama8b():
     assert U.rel_fro(got_m, m1) <= U.GRAD_REL_TOL
     assert U.rel_fro(got_v, v1) <= U.GRAD_REL_TOL
     _say(f"[{name}] fused AdamW ok")
+
+
+def test_full_size_vocabulary_shards_llama8b():
+    """The 8B head split into 8 vocabulary shards (each the per-device shape of 8-way loss
+    parallelism, N tokens x V/8 ids), combined on the one GPU: loss and every lse against the
+    stored oracle forward, sampled dH rows (sum of the shards' fp32 terms) and dW rows against
+    the oracle."""
+    import torch
+    from paper_2605_21442_amd import autograd as AG
+    name = "llama8b"
+    path = MG.path_for(name, 0)
+    if not os.path.exists(path):
+        pytest.skip(f"{path} missing: run tests/golden/make_golden.py")
+    gold = np.load(path, allow_pickle=False)
+    wl = WL.WORKLOADS[name]
+    inp = WL.generate(wl, 0)
+    h, w, t = U.to_device(inp)
+    v, g_count = wl.v, 8
+    cuts = [round(i * v / g_count) for i in range(g_count + 1)]
+    _say(f"[{name}] {g_count} vocabulary shards, cuts {cuts}")
+    parts = [AG.forward_shard(h, w[a:b], t, a, v) for a, b in zip(cuts[:-1], cuts[1:])]
+    lse_parts = torch.stack([q[0] for q in parts]).contiguous()
+    tgt_parts = torch.stack([q[1] for q in parts]).contiguous()
+    del parts
+    loss, lse, nv, status = AG.combine_shards(lse_parts, tgt_parts, t, v, wl.d)
+    assert int(nv.item()) == int(gold["n_valid"]) and int(status.item()) == 0
+    assert abs(float(loss.item()) - float(gold["loss"])) <= U.LOSS_ABS_TOL
+    valid = inp.targets != inp.ignore_index
+    lse_err = np.max(np.abs(lse.cpu().numpy()[valid] - gold["lse"][valid]))
+    assert lse_err <= U.LSE_ABS_TOL, lse_err
+
+    g = torch.ones(1, dtype=torch.float32, device=h.device)
+    dh = torch.zeros((wl.n, wl.d), dtype=torch.float32, device=h.device)
+    dws = []
+    for a, b in zip(cuts[:-1], cuts[1:]):
+        term, dw = AG.backward_shard(h, w[a:b], t, lse, nv, g, a, v)
+        dh += term
+        dws.append(dw)
+        del term
+    dw = torch.cat(dws)
+    rng = np.random.default_rng(11)
+    vrows = np.nonzero(valid)[0]
+    rows = np.concatenate([rng.choice(vrows, 5, replace=False), np.nonzero(~valid)[0][:1]])
+    ref_dh = O.dh_of_rows(inp.h_bits, inp.w_bits, inp.targets, rows, int(gold["n_valid"]))
+    got_dh = dh[torch.from_numpy(rows).to(h.device)].cpu().numpy().astype(np.float64)
+    assert U.rel_fro(got_dh, ref_dh) <= U.GRAD_REL_TOL
+    assert np.all(got_dh[-1] == 0.0)
+    ids = np.array(sorted(set([0, 1, cuts[1] - 1, cuts[1], cuts[4], v - 1] + rng.integers(2, v, 3).tolist())))
+    ref_dw = O.dw_of_rows(inp.h_bits, inp.w_bits, inp.targets, ids, gold["lse"])
+    got_dw = dw[torch.from_numpy(ids).to(h.device)].float().cpu().numpy().astype(np.float64)
+    assert U.rel_fro(got_dw, ref_dw) <= U.GRAD_REL_TOL
+    _say(f"[{name}] shards ok: loss {float(loss.item()):.6f} (oracle {float(gold['loss']):.6f})")
