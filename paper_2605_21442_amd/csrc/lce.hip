@@ -130,9 +130,12 @@ __device__ __forceinline__ float wave_max(float x) {
 // in that order.
 //
 // Schedule of slice j (four 16-wide substeps, fragments read one substep ahead): after the
-// third substep's MFMAs are issued, one barrier both publishes slice j+1 (its loads were issued a
-// whole slice earlier) and frees slice j's buffer, into which slice j+2 is then loaded while the
-// fourth substep runs and the first fragments of slice j+1 are read.
+// third substep's MFMAs are issued, one barrier both publishes slice j+1 (its loads were issued
+// about a slice earlier) and frees slice j's buffer, into which slice j+2 is then loaded while
+// the fourth substep runs and the first fragments of slice j+1 are read. Waves 0..3 issue their
+// loads at the barrier, waves 4..7 one or two substeps later (kLateGroups): on this part a whole
+// workgroup's 64 load instructions at once fill the texture-address queues and stall the
+// issuing waves (measured: 3-9 % per kernel; the better delay depends on the operand stream).
 //
 // aoff/boff: byte offset (row start + this lane's chunk) of the 4 rows this lane loads per slice
 // and operand. K must be a multiple of 8; a ragged last slice is zero-filled by pointing the
@@ -197,6 +200,7 @@ __device__ __forceinline__ void load_slice(__amdgpu_buffer_rsrc_t ra, const uint
 // s_waitcnt with only the vector-memory counter constrained (expcnt / lgkmcnt left at max)
 #define LCE_WAIT_VM(n) __builtin_amdgcn_s_waitcnt((((n) & 15) | (7 << 4) | (15 << 8) | (((n) >> 4) << 14)))
 
+template <int kLateGroups>
 __device__ __forceinline__ void mma_mainloop(f32x16_t (&acc)[4][2],
                                              __amdgpu_buffer_rsrc_t ra, const uint32_t (&aoff)[4],
                                              __amdgpu_buffer_rsrc_t rb, const uint32_t (&boff)[4],
@@ -234,6 +238,11 @@ __device__ __forceinline__ void mma_mainloop(f32x16_t (&acc)[4][2],
   }
   __builtin_amdgcn_s_barrier();
 
+  // The second wave of each SIMD (waves 4..7) issues its share of a slice's loads kLateGroups
+  // MFMA substeps after the barrier instead of right at it: half the load burst, and one wave
+  // per SIMD goes straight back to MFMA work.
+  const bool late = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6) >= 4;
+  int pend = -1;
   FragSet f0, f1;
   read_frags(f0, smem, a_rd, b_rd, kofs[0]);
   for (int j = 0; j < S; ++j) {
@@ -241,6 +250,10 @@ __device__ __forceinline__ void mma_mainloop(f32x16_t (&acc)[4][2],
     const char* nxt = smem + ((j + 1) & 1) * SLICE_BYTES;
     read_frags(f1, cur, a_rd, b_rd, kofs[1]);
     mma_substep(acc, f0);
+    if (kLateGroups == 2 && pend >= 0) {
+      load(pend);
+      pend = -1;
+    }
     read_frags(f0, cur, a_rd, b_rd, kofs[2]);
     mma_substep(acc, f1);
     read_frags(f1, cur, a_rd, b_rd, kofs[3]);
@@ -249,10 +262,17 @@ __device__ __forceinline__ void mma_mainloop(f32x16_t (&acc)[4][2],
       // slice j+1 landed (own loads) and every wave is done with slice j's buffer
       __builtin_amdgcn_s_waitcnt(0);
       __builtin_amdgcn_s_barrier();
-      if (j + 2 < S) load(j + 2);
+      if (j + 2 < S) {
+        if (!late) load(j + 2);
+        else pend = j + 2;
+      }
       read_frags(f0, nxt, a_rd, b_rd, kofs[0]);
     }
     mma_substep(acc, f1);
+    if (kLateGroups == 1 && pend >= 0) {
+      load(pend);
+      pend = -1;
+    }
   }
   // every wave is done reading LDS before the caller reuses it
   __syncthreads();
@@ -386,7 +406,7 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_fwd_stats(const uint16_t* __res
     __amdgpu_buffer_rsrc_t ra = make_rsrc(W + (int64_t)v0 * ldw, (uint64_t)vleft * ldw * 2);
     uint32_t aoff[4];
     dense_offsets(aoff, vleft, ldw);
-    mma_mainloop(acc, ra, aoff, rb, boff, d, smem);
+    mma_mainloop<2>(acc, ra, aoff, rb, boff, d, smem);
 
     // rows (vocabulary ids) of this lane: v0 + wr*128 + 32 bi + 8 (r/4) + 4 (lane/32) + r%4
     const int vb = wr * 128 + (lane >> 5) * 4;
@@ -649,7 +669,7 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_bwd_g(const uint16_t* __restric
   dense_offsets(aoff, vleft, ldw);
   gather_offsets(boff, idx, n0, nv, ldh);
   f32x16_t acc[4][2];
-  mma_mainloop(acc, ra, aoff, rb, boff, d, smem);
+  mma_mainloop<2>(acc, ra, aoff, rb, boff, d, smem);
 
   const float c_all = grad_scale(grad, n_norm, reduction);
   int tok[2], tgt[2];
@@ -757,7 +777,7 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_bwd_dw(const uint16_t* __restri
   dense_offsets(aoff, vs - m0, ldt);
   dense_offsets(boff, d - d0, ldt);
   f32x16_t acc[4][2];
-  mma_mainloop(acc, ra, aoff, rb, boff, kpad, smem);
+  mma_mainloop<1>(acc, ra, aoff, rb, boff, kpad, smem);
   const int mb = m0 + wr * 128 + (lane >> 5) * 4;
   const int dc = d0 + wc * 64 + (lane & 31);
 #pragma unroll
@@ -834,7 +854,7 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_bwd_dh(const uint16_t* __restri
   dense_offsets(aoff, nv - m0, vc);
   dense_offsets(boff, d - d0, vc);
   f32x16_t acc[4][2];
-  mma_mainloop(acc, ra, aoff, rb, boff, kpad, smem);
+  mma_mainloop<2>(acc, ra, aoff, rb, boff, kpad, smem);
   // Read-modify-write of the fp32 accumulator, one 32-row block (32 values per lane) at a time
   // so that its 32 loads are in flight together; interior tiles skip the bounds tests.
   const int mb = m0 + wr * 128 + (lane >> 5) * 4;
