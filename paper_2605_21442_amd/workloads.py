@@ -222,3 +222,57 @@ def opt_state(w_bits: np.ndarray, *, seed: int = 0, case_id: int = 99, g_scale: 
 def gradient_bits(v: int, d: int, *, seed: int = 0, case_id: int = 99, g_scale: float = 1e-3) -> np.ndarray:
     """A bf16 gradient matrix [V, D] ~ N(0, g_scale) (input of a standalone optimizer step)."""
     return draw_normal_bf16(_rng(seed, case_id, _S_GRAD), (v, d), g_scale)
+
+
+# ---- knowledge distillation: a student head and a teacher head over the same tokens -----------
+
+_S_HT, _S_WT = 6, 7
+
+
+@dataclasses.dataclass
+class KdInputs:
+    """Student (hs, ws) and teacher (ht, wt) bf16 bit patterns and int32 labels (mask only)."""
+
+    name: str
+    hs_bits: np.ndarray         # uint16 [N, Ds]
+    ws_bits: np.ndarray         # uint16 [V, Ds]
+    ht_bits: np.ndarray         # uint16 [N, Dt]
+    wt_bits: np.ndarray         # uint16 [V, Dt]
+    targets: np.ndarray         # int32 [N]
+    ignore_index: int = IGNORE_INDEX
+
+
+# Distilling a Llama-3.1-8B head (teacher) into a Llama-3.2-1B head (student): same 128256-id
+# vocabulary, 8 x 2048 tokens, 25 % of positions masked as prompt.
+KD_WORKLOADS = {
+    "kd_tiny": dict(n=256, ds=256, dt=512, v=4096, batch=1, seq=256, sigma_s=0.02, sigma_t=0.02,
+                    mask_frac=0.10, targets="uniform", case_id=11),
+    "kd_8b_to_1b": dict(n=16384, ds=2048, dt=4096, v=128256, batch=8, seq=2048, sigma_s=0.02,
+                        sigma_t=0.02, mask_frac=0.25, targets="zipf", case_id=12),
+}
+
+
+def kd_generate(name: str, seed: int = 0, **over) -> KdInputs:
+    """Draw the inputs of a KD workload (KD_WORKLOADS entry, fields overridable)."""
+    k = dict(KD_WORKLOADS[name], **over)
+    n, v, cid = k["n"], k["v"], k["case_id"]
+    w = Workload(name, n=n, d=k["ds"], v=v, batch=k["batch"], seq=k["seq"], sigma_w=k["sigma_s"],
+                 targets=k["targets"], mask_frac=k["mask_frac"], case_id=cid)
+    hs = draw_normal_bf16(_rng(seed, cid, _S_H), (n, k["ds"]), 1.0)
+    ws = draw_normal_bf16(_rng(seed, cid, _S_W), (v, k["ds"]), k["sigma_s"])
+    ht = draw_normal_bf16(_rng(seed, cid, _S_HT), (n, k["dt"]), 1.0)
+    wt = draw_normal_bf16(_rng(seed, cid, _S_WT), (v, k["dt"]), k["sigma_t"])
+    t = draw_targets(_rng(seed, cid, _S_T), n, v, k["targets"], 1.1)
+    t = apply_mask(_rng(seed, cid, _S_MASK), t, w)
+    return KdInputs(name, hs, ws, ht, wt, t)
+
+
+def kd_custom(n: int, ds: int, dt: int, v: int, *, seed: int = 0, sigma_s: float = 0.3,
+              sigma_t: float = 0.3, mask_frac: float = 0.1, target_override=None) -> KdInputs:
+    """Small ad-hoc KD inputs (ragged shapes, edge cases)."""
+    over = dict(n=n, ds=ds, dt=dt, v=v, batch=1, seq=n, sigma_s=sigma_s, sigma_t=sigma_t,
+                mask_frac=mask_frac, targets="uniform", case_id=13)
+    inp = kd_generate("kd_tiny", seed, **over)
+    if target_override is not None:
+        inp.targets = np.asarray(target_override, dtype=np.int32).copy()
+    return inp
