@@ -236,6 +236,58 @@ lce_status_t lce_backward_shard(const lce_problem_t* p, const lce_shard_t* shard
                                 float* dH_part, void* dW,
                                 void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * Fused linear knowledge-distillation loss. The paper's recipes include knowledge distillation
+ * with dedicated KD losses (Sec. 3.2, after Hinton et al., cited in Sec. 2); here it is built on
+ * the LCE tiling for a student head (Hs [N, Ds], Ws [V, Ds]) and a teacher head (Ht [N, Dt],
+ * Wt [V, Dt]) over the same tokens and vocabulary, with temperature T:
+ *   p_t = softmax(Ht Wt^T / T),  zs = Hs Ws^T / T
+ *   l_n = lse(zs_n) - sum_v p_t(v) zs_n(v)       soft-target cross-entropy, n in M
+ *   L   = mean / sum over M, or the per-token l_n (0 outside M), as for lce_forward
+ *   G   = c (softmax(zs) - p_t) / T,  dHs = G Ws,  dWs = G^T Hs     (no teacher gradient)
+ * Labels only define the valid set M (as for LCE: not ignore_index and in [0, V)). The loss
+ * is not multiplied by T^2; neither logit matrix is ever held whole (the teacher's
+ * probabilities exist one vocabulary slab at a time, in the workspace).
+ */
+typedef struct lce_kd_problem {
+  int64_t n;                /* tokens */
+  int64_t ds, dt;           /* student / teacher hidden sizes (multiples of 8) */
+  int64_t v;                /* vocabulary size shared by both heads */
+  int64_t ld_hs, ld_ws, ld_ht, ld_wt;   /* row strides in elements; 0 means dense */
+  float temperature;        /* T > 0 */
+  int32_t ignore_index;
+  int32_t reduction;        /* lce_reduction_t */
+  int32_t target_bytes;     /* 4 or 8 */
+  int32_t flags;            /* LCE_FLAG_ACCUMULATE_DW applies to dWs */
+  int32_t reserved;         /* must be 0 */
+} lce_kd_problem_t;
+
+/* Workspace bytes of lce_kd_forward / lce_kd_backward: O(N (Ds + Dt) + N V_slab) with the
+ * student's slab width, never O(N V). */
+lce_status_t lce_kd_workspace_size(const lce_kd_problem_t* p, size_t* fwd_bytes, size_t* bwd_bytes);
+
+/*
+ * KD forward. Outputs (device): loss ([1], or [N] per token for LCE_REDUCE_NONE), lse_s and
+ * lse_t ([N] fp32: log-sum-exp of zs and of the teacher's logits / T on valid rows, 0.0
+ * elsewhere; keep both for the backward), n_valid, dev_status (nullable) as for lce_forward.
+ */
+lce_status_t lce_kd_forward(const lce_kd_problem_t* p,
+                            const void* Hs, const void* Ws, const void* Ht, const void* Wt,
+                            const void* targets, float* loss, float* lse_s, float* lse_t,
+                            int32_t* n_valid, int32_t* dev_status,
+                            void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * KD backward: dHs [N, Ds] bf16 (overwritten, 0 on rows outside M) and dWs [V, Ds] bf16
+ * (overwritten, or added to with LCE_FLAG_ACCUMULATE_DW); grad_loss and n_valid as for
+ * lce_backward; lse_s / lse_t from lce_kd_forward on the same inputs.
+ */
+lce_status_t lce_kd_backward(const lce_kd_problem_t* p,
+                             const void* Hs, const void* Ws, const void* Ht, const void* Wt,
+                             const void* targets, const float* lse_s, const float* lse_t,
+                             const int32_t* n_valid, const float* grad_loss, void* dHs, void* dWs,
+                             void* workspace, size_t workspace_bytes, void* stream);
+
 /* Static, human-readable name of a status code. */
 const char* lce_status_string(lce_status_t s);
 

@@ -7,7 +7,7 @@ Importing this package does not load the library; the first call does, and
 raises if it was not built.
 """
 
-__all__ = ["linear_cross_entropy", "LinearCrossEntropy", "AdamWState"]
+__all__ = ["linear_cross_entropy", "LinearCrossEntropy", "AdamWState", "linear_kd_loss", "LinearKD"]
 
 
 def __getattr__(name):

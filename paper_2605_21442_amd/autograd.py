@@ -297,3 +297,100 @@ def linear_cross_entropy(hidden: torch.Tensor, weight: torch.Tensor, targets: to
             raise ValueError("optimizer state belongs to another weight")
         return LinearCrossEntropyAdamW.apply(hidden, weight, targets, optimizer, ignore_index, reduction)
     return LinearCrossEntropy.apply(hidden, weight, targets, ignore_index, reduction)
+
+
+# ---- fused linear knowledge distillation ------------------------------------------------------
+
+def _kd_problem(hs, ws, ht, wt, targets, temperature, ignore_index, reduction, flags=0):
+    h_s, ldhs = _as_rows(hs, "student hidden")
+    w_s, ldws = _as_rows(ws, "student weight")
+    h_t, ldht = _as_rows(ht, "teacher hidden")
+    w_t, ldwt = _as_rows(wt, "teacher weight")
+    n, ds = h_s.shape
+    dt = h_t.shape[1]
+    v = w_s.shape[0]
+    if h_t.shape[0] != n or w_s.shape[1] != ds or w_t.shape != (v, dt):
+        raise ValueError("student/teacher shapes disagree")
+    t, tb = _targets(targets, n)
+    p = B.kd_problem(n, ds, dt, v, ld_hs=ldhs, ld_ws=ldws, ld_ht=ldht, ld_wt=ldwt, temperature=temperature,
+                     ignore_index=ignore_index, reduction=reduction, target_bytes=tb, flags=flags)
+    return p, h_s, w_s, h_t, w_t, t
+
+
+def kd_forward(hs, ws, ht, wt, targets, temperature: float = 1.0, ignore_index: int = -100,
+               reduction: str = "mean"):
+    """(loss, lse_s [N], lse_t [N], n_valid, status) from lce_kd_forward."""
+    p, h_s, w_s, h_t, w_t, t = _kd_problem(hs, ws, ht, wt, targets, temperature, ignore_index, reduction)
+    fwd_bytes, _ = B.lce_kd_workspace_size(p)
+    dev = h_s.device
+    n = p.n
+    loss = torch.empty((n,) if reduction == "none" else (), dtype=torch.float32, device=dev)
+    lse_s = torch.empty(n, dtype=torch.float32, device=dev)
+    lse_t = torch.empty(n, dtype=torch.float32, device=dev)
+    nv = torch.empty(1, dtype=torch.int32, device=dev)
+    status = torch.empty(1, dtype=torch.int32, device=dev)
+    ws_ = torch.empty(max(fwd_bytes, 1), dtype=torch.uint8, device=dev)
+    B.lce_kd_forward(p, h_s.data_ptr(), w_s.data_ptr(), h_t.data_ptr(), w_t.data_ptr(), t.data_ptr(),
+                     loss.data_ptr(), lse_s.data_ptr(), lse_t.data_ptr(), nv.data_ptr(), status.data_ptr(),
+                     ws_.data_ptr(), fwd_bytes, _stream(dev))
+    return loss, lse_s, lse_t, nv, status
+
+
+def kd_backward(hs, ws, ht, wt, targets, lse_s, lse_t, n_valid, grad_loss, temperature: float = 1.0,
+                ignore_index: int = -100, reduction: str = "mean", accumulate_into: torch.Tensor | None = None):
+    """(dHs bf16 [N, Ds], dWs bf16 [V, Ds]) from lce_kd_backward."""
+    flags = B.LCE_FLAG_ACCUMULATE_DW if accumulate_into is not None else 0
+    p, h_s, w_s, h_t, w_t, t = _kd_problem(hs, ws, ht, wt, targets, temperature, ignore_index, reduction, flags)
+    n, ds, v = p.n, p.ds, p.v
+    want = n if reduction == "none" else 1
+    if grad_loss.dtype != torch.float32 or grad_loss.numel() != want or not grad_loss.is_cuda:
+        raise ValueError(f"grad_loss must be a {want}-element float32 GPU tensor")
+    for x in (lse_s, lse_t):
+        if x.dtype != torch.float32 or x.numel() != n or not x.is_contiguous():
+            raise ValueError("lse_s / lse_t must be the contiguous float32 [N] tensors from kd_forward")
+    _, bwd_bytes = B.lce_kd_workspace_size(p)
+    dev = h_s.device
+    dh = torch.empty((n, ds), dtype=torch.bfloat16, device=dev)
+    if accumulate_into is None:
+        dw = torch.empty((v, ds), dtype=torch.bfloat16, device=dev)
+    else:
+        dw = accumulate_into
+        if dw.dtype != torch.bfloat16 or tuple(dw.shape) != (v, ds) or not dw.is_contiguous():
+            raise ValueError("accumulate_into must be a contiguous bf16 [V, Ds] tensor")
+    g = grad_loss.contiguous()
+    ws_ = torch.empty(max(bwd_bytes, 1), dtype=torch.uint8, device=dev)
+    B.lce_kd_backward(p, h_s.data_ptr(), w_s.data_ptr(), h_t.data_ptr(), w_t.data_ptr(), t.data_ptr(),
+                      lse_s.data_ptr(), lse_t.data_ptr(), n_valid.data_ptr(), g.data_ptr(), dh.data_ptr(),
+                      dw.data_ptr(), ws_.data_ptr(), bwd_bytes, _stream(dev))
+    return dh, dw
+
+
+class LinearKD(torch.autograd.Function):
+    """Soft-target cross-entropy of a student head against a teacher head; gradients for the
+    student's hidden states and weight only."""
+
+    @staticmethod
+    def forward(ctx, hs, ws, ht, wt, targets, temperature=1.0, ignore_index=-100, reduction="mean"):
+        loss, lse_s, lse_t, nv, _ = kd_forward(hs, ws, ht, wt, targets, temperature, ignore_index, reduction)
+        ctx.save_for_backward(hs, ws, ht, wt, targets, lse_s, lse_t, nv)
+        ctx.opts = (temperature, ignore_index, reduction)
+        return loss.view(targets.shape) if reduction == "none" else loss
+
+    @staticmethod
+    def backward(ctx, grad):
+        hs, ws, ht, wt, targets, lse_s, lse_t, nv = ctx.saved_tensors
+        temperature, ignore_index, reduction = ctx.opts
+        g = grad.reshape(-1)
+        if g.dtype != torch.float32:
+            g = g.float()
+        dh, dw = kd_backward(hs, ws, ht, wt, targets, lse_s, lse_t, nv, g, temperature, ignore_index, reduction)
+        return dh.view(hs.shape), dw, None, None, None, None, None, None
+
+
+def linear_kd_loss(student_hidden, student_weight, teacher_hidden, teacher_weight, targets,
+                   temperature: float = 1.0, ignore_index: int = -100, reduction: str = "mean"):
+    """Knowledge-distillation loss between two output heads without either logit matrix: the
+    soft-target cross-entropy of softmax(student / T) against softmax(teacher / T), averaged (or
+    summed, or per token) over the tokens whose label is not ignored."""
+    return LinearKD.apply(student_hidden, student_weight, teacher_hidden, teacher_weight, targets,
+                          temperature, ignore_index, reduction)

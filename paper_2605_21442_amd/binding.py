@@ -36,7 +36,8 @@ REDUCTIONS = {"mean": LCE_REDUCE_MEAN, "sum": LCE_REDUCE_SUM, "none": LCE_REDUCE
 EXPORTED = ("lce_workspace_size", "lce_forward", "lce_backward", "lce_status_string",
             "lce_timing_enable", "lce_timing_kernel_count", "lce_timing_kernel_name",
             "lce_timing_read", "lce_adamw_step", "lce_backward_adamw", "lce_forward_shard",
-            "lce_combine_shards", "lce_backward_shard")
+            "lce_combine_shards", "lce_backward_shard", "lce_kd_workspace_size", "lce_kd_forward",
+            "lce_kd_backward")
 
 
 class LceError(RuntimeError):
@@ -56,6 +57,22 @@ class LceAdamW(ctypes.Structure):
     _fields_ = [("lr", ctypes.c_float), ("beta1", ctypes.c_float), ("beta2", ctypes.c_float),
                 ("eps", ctypes.c_float), ("weight_decay", ctypes.c_float), ("step", ctypes.c_int32),
                 ("reserved", ctypes.c_int32)]
+
+
+class LceKdProblem(ctypes.Structure):
+    _fields_ = [("n", ctypes.c_int64), ("ds", ctypes.c_int64), ("dt", ctypes.c_int64), ("v", ctypes.c_int64),
+                ("ld_hs", ctypes.c_int64), ("ld_ws", ctypes.c_int64), ("ld_ht", ctypes.c_int64),
+                ("ld_wt", ctypes.c_int64), ("temperature", ctypes.c_float), ("ignore_index", ctypes.c_int32),
+                ("reduction", ctypes.c_int32), ("target_bytes", ctypes.c_int32), ("flags", ctypes.c_int32),
+                ("reserved", ctypes.c_int32)]
+
+
+def kd_problem(n: int, ds: int, dt: int, v: int, *, ld_hs: int = 0, ld_ws: int = 0, ld_ht: int = 0,
+               ld_wt: int = 0, temperature: float = 1.0, ignore_index: int = -100,
+               reduction: str | int = "mean", target_bytes: int = 4, flags: int = 0) -> LceKdProblem:
+    red = REDUCTIONS[reduction] if isinstance(reduction, str) else int(reduction)
+    return LceKdProblem(n, ds, dt, v, ld_hs, ld_ws, ld_ht, ld_wt, temperature, ignore_index, red, target_bytes,
+                        flags, 0)
 
 
 class LceShard(ctypes.Structure):
@@ -98,6 +115,10 @@ def load() -> ctypes.CDLL:
         lib.lce_forward_shard.argtypes = [P, S, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
         lib.lce_combine_shards.argtypes = [P, ctypes.c_int32, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
         lib.lce_backward_shard.argtypes = [P, S, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+        KP = ctypes.POINTER(LceKdProblem)
+        lib.lce_kd_workspace_size.argtypes = [KP, ctypes.POINTER(sz), ctypes.POINTER(sz)]
+        lib.lce_kd_forward.argtypes = [KP, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+        lib.lce_kd_backward.argtypes = [KP, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
         lib.lce_status_string.argtypes = [ctypes.c_int]
         lib.lce_status_string.restype = ctypes.c_char_p
         lib.lce_timing_enable.argtypes = [ctypes.c_int]
@@ -108,7 +129,8 @@ def load() -> ctypes.CDLL:
                                         ctypes.POINTER(ctypes.c_int64)]
         for name in ("lce_workspace_size", "lce_forward", "lce_backward", "lce_timing_enable",
                      "lce_timing_read", "lce_timing_kernel_count", "lce_adamw_step", "lce_backward_adamw",
-                     "lce_forward_shard", "lce_combine_shards", "lce_backward_shard"):
+                     "lce_forward_shard", "lce_combine_shards", "lce_backward_shard", "lce_kd_workspace_size",
+                     "lce_kd_forward", "lce_kd_backward"):
             getattr(lib, name).restype = ctypes.c_int
         _lib = lib
         return lib
@@ -178,6 +200,26 @@ def lce_backward_shard(p: LceProblem, shard: LceShard, H: int, W: int, targets: 
     _check(load().lce_backward_shard(ctypes.byref(p), ctypes.byref(shard), H, W, targets, lse, n_valid,
                                      grad_loss, dH_part, dW, workspace, workspace_bytes, stream or None),
            "lce_backward_shard")
+
+
+def lce_kd_workspace_size(p: LceKdProblem) -> tuple[int, int]:
+    f, b = ctypes.c_size_t(0), ctypes.c_size_t(0)
+    _check(load().lce_kd_workspace_size(ctypes.byref(p), ctypes.byref(f), ctypes.byref(b)), "lce_kd_workspace_size")
+    return f.value, b.value
+
+
+def lce_kd_forward(p: LceKdProblem, Hs: int, Ws: int, Ht: int, Wt: int, targets: int, loss: int, lse_s: int,
+                   lse_t: int, n_valid: int, dev_status: int, workspace: int, workspace_bytes: int,
+                   stream: int) -> None:
+    _check(load().lce_kd_forward(ctypes.byref(p), Hs, Ws, Ht, Wt, targets, loss, lse_s, lse_t, n_valid,
+                                 dev_status or None, workspace, workspace_bytes, stream or None), "lce_kd_forward")
+
+
+def lce_kd_backward(p: LceKdProblem, Hs: int, Ws: int, Ht: int, Wt: int, targets: int, lse_s: int, lse_t: int,
+                    n_valid: int, grad_loss: int, dHs: int, dWs: int, workspace: int, workspace_bytes: int,
+                    stream: int) -> None:
+    _check(load().lce_kd_backward(ctypes.byref(p), Hs, Ws, Ht, Wt, targets, lse_s, lse_t, n_valid, grad_loss,
+                                  dHs, dWs, workspace, workspace_bytes, stream or None), "lce_kd_backward")
 
 
 def lce_timing_enable(on: bool) -> None:

@@ -370,7 +370,8 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_fwd_stats(const uint16_t* __res
                                                            const int* __restrict__ idx, const int* __restrict__ nv_ptr,
                                                            int d, int nparts, int nt_max, int vt_count,
                                                            float* __restrict__ part_m, float* __restrict__ part_s,
-                                                           int npad) {
+                                                           int npad, float scale2) {
+  // scale2 = log2(e) / T: partials are kept in base-2 units of the logits divided by T
   __shared__ __attribute__((aligned(16))) char smem[LDS_BYTES];
   // Workgroups are dispatched round-robin over the 8 XCDs (block b runs on XCD b % 8). Give each
   // XCD whole vocabulary partitions (p = xcd + 8 i) and walk all token tiles of one partition
@@ -421,13 +422,13 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_fwd_stats(const uint16_t* __res
           if (ragged && (vb + i * 32 + (r >> 2) * 8 + (r & 3)) >= vleft) acc[i][j][r] = -INFINITY;
           mx = fmaxf(mx, acc[i][j][r]);
         }
-      const float nm = fmaxf(m2[j], mx * kLog2e);
+      const float nm = fmaxf(m2[j], mx * scale2);
       if (nm == -INFINITY) continue;
       float s = 0.f;
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) s += __builtin_amdgcn_exp2f(fmaf(acc[i][j][r], kLog2e, -nm));
+        for (int r = 0; r < 16; ++r) s += __builtin_amdgcn_exp2f(fmaf(acc[i][j][r], scale2, -nm));
       ss[j] = (m2[j] == -INFINITY ? 0.f : ss[j] * __builtin_amdgcn_exp2f(m2[j] - nm)) + s;
       m2[j] = nm;
     }
@@ -647,13 +648,24 @@ __device__ __forceinline__ float grad_scale(const float* grad, const int* n_norm
 // Entries outside the valid tokens / slab columns are written as zeros where the later
 // contractions read them (K padding), so those loops need no masking.
 // ---------------------------------------------------------------------------------------------
+// The same kernel serves the distillation loss (KD) with soft targets, in four modes:
+//   G_ONEHOT  LCE: G = c (softmax - onehot(t))
+//   G_SOFT    KD student: G = c (softmax(z/T) - P) / T, P the teacher's probabilities of this slab
+//   Q_SOFT    KD student forward: per token, sum over the tile's ids of P * z / T (partials qpart)
+//   P_WRITE   KD teacher: P = softmax(z/T) of this slab, fp32, P[v][token] (row stride ldt)
+// scale2 = log2(e) / T (log2(e) for LCE), inv_t = 1 / T; lse is that of the scaled logits.
+enum GMode { G_ONEHOT = 0, G_SOFT = 1, Q_SOFT = 2, P_WRITE = 3 };
+
+template <int kMode>
 __global__ __launch_bounds__(NTHREADS, 2) void k_bwd_g(const uint16_t* __restrict__ W, int64_t ldw, int64_t v0, int vs,
                                                        const uint16_t* __restrict__ H, int64_t ldh, int64_t n,
                                                        const void* targets, int tbytes, int64_t id0,
                                                        const int* __restrict__ idx, const int* __restrict__ nv_ptr,
                                                        const float* __restrict__ lse, const float* __restrict__ grad,
                                                        const int* __restrict__ n_norm, int reduction, int d, int tm_count,
-                                                       uint16_t* __restrict__ G, int vc, uint16_t* __restrict__ Gt, int ldt) {
+                                                       uint16_t* __restrict__ G, int vc, uint16_t* __restrict__ Gt, int ldt,
+                                                       float scale2, float inv_t, float* __restrict__ P,
+                                                       float* __restrict__ qpart, int64_t qrow) {
   __shared__ __attribute__((aligned(16))) char smem[LDS_BYTES];
   const int nv = *nv_ptr;
   const int tm = blockIdx.x % tm_count, tn = blockIdx.x / tm_count;
@@ -680,7 +692,7 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_bwd_g(const uint16_t* __restric
     if (tok[j] < nv) {
       const int row = idx[tok[j]];
       l2[j] = lse[row] * kLog2e;
-      tgt[j] = (int)(load_target(targets, tbytes, row) - id0 - v0) - vt0;   // tile-relative target row
+      tgt[j] = kMode == G_ONEHOT ? (int)(load_target(targets, tbytes, row) - id0 - v0) - vt0 : -1;
       cj[j] = reduction == LCE_REDUCE_NONE ? grad[row] : c_all;
     } else {
       l2[j] = 0.f;
@@ -688,10 +700,38 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_bwd_g(const uint16_t* __restric
       cj[j] = 0.f;
     }
   }
+  const int vb = wr * 128 + (lane >> 5) * 4;  // tile-relative vocabulary row base of this lane
+  if constexpr (kMode == P_WRITE || kMode == Q_SOFT) {
+    // P[v][token] rows of this tile: lanes of a half-wave hold 32 consecutive tokens of one row
+    float q[2] = {0.f, 0.f};
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      if (tok[j] >= nv) continue;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int vr = vb + i * 32 + (r >> 2) * 8 + (r & 3);
+          if (vr < vleft) {
+            float* pp = P + (int64_t)(vt0 + vr) * ldt + tok[j];
+            if constexpr (kMode == P_WRITE) *pp = __builtin_amdgcn_exp2f(fmaf(acc[i][j][r], scale2, -l2[j]));
+            else q[j] = fmaf(*pp, acc[i][j][r] * inv_t, q[j]);
+          }
+        }
+    }
+    if constexpr (kMode == Q_SOFT) {
+      // the two lane halves hold disjoint vocabulary rows of the same tokens
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        q[j] += __shfl_xor(q[j], 32);
+        if (lane < 32 && tok[j] < nv) qpart[(qrow + 2 * tm + wr) * ldt + tok[j]] = q[j];
+      }
+    }
+    return;
+  }
   // G values in place, then the bf16 tile goes through LDS (free after the main loop) as
   // T[token][v], 512-byte rows whose 16-byte chunk c sits at c ^ (token & 31), so that both the
   // token-major rows of G and the vocabulary-major rows of Gt leave with wide coalesced stores.
-  const int vb = wr * 128 + (lane >> 5) * 4;  // tile-relative vocabulary row base of this lane
   char* T = smem;
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
@@ -708,8 +748,13 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_bwd_g(const uint16_t* __restric
           const int vr = vb + i * 32 + q * 8 + e;
           float g = 0.f;
           if (tok_ok && vr < vleft) {
-            g = cj[j] * __builtin_amdgcn_exp2f(fmaf(acc[i][j][r], kLog2e, -l2[j]));
-            if (vr == tgt[j]) g -= cj[j];
+            const float e2 = __builtin_amdgcn_exp2f(fmaf(acc[i][j][r], scale2, -l2[j]));
+            if constexpr (kMode == G_SOFT) {
+              g = cj[j] * inv_t * (e2 - P[(int64_t)(vt0 + vr) * ldt + tok[j]]);
+            } else {
+              g = cj[j] * e2;
+              if (vr == tgt[j]) g -= cj[j];
+            }
           }
           gq[e] = g;
         }
@@ -984,13 +1029,35 @@ __global__ __launch_bounds__(256) void k_adamw(int64_t v, int d, const uint16_t*
   }
 }
 
+// KD per-token loss: l = lse_s - sum of the token's Q partials (fixed order), for valid rows; terms
+// (compact order) feed the mean / sum, per_token (row order, 0 on rows outside M) is the "none"
+// output.
+__global__ __launch_bounds__(256) void k_kd_terms(const float* __restrict__ qpart, int nq, int64_t ldq,
+                                                  const int* __restrict__ pos, int64_t n,
+                                                  const float* __restrict__ lse_s, float* __restrict__ terms,
+                                                  float* __restrict__ per_token) {
+  const int64_t row = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (row >= n) return;
+  const int i = pos[row];
+  if (i < 0) {
+    if (per_token) per_token[row] = 0.f;
+    return;
+  }
+  float q = 0.f;
+  for (int k = 0; k < nq; ++k) q += qpart[k * ldq + i];
+  const float l = lse_s[row] - q;
+  terms[i] = l;
+  if (per_token) per_token[row] = l;
+}
+
 // ---------------------------------------------------------------------------------------------
 // Host side: validation, plan, workspace carve-up, launches, optional timing.
 // ---------------------------------------------------------------------------------------------
 enum KernelId { K_COMPACT = 0, K_FWD_STATS, K_COMBINE, K_LOSS, K_TRANSPOSE_H, K_TRANSPOSE_W, K_BWD_G,
-                K_BWD_DW, K_BWD_DH, K_DH_FINAL, K_ADAMW, K_SHARD_COMBINE, K_MISC, K_COUNT };
+                K_BWD_DW, K_BWD_DH, K_DH_FINAL, K_ADAMW, K_SHARD_COMBINE, K_KD_P, K_KD_Q, K_KD_TERMS, K_MISC,
+                K_COUNT };
 const char* const kKernelNames[K_COUNT] = {"compact", "fwd_stats", "combine", "loss", "transpose_h",
-                                           "transpose_w", "bwd_g", "bwd_dw", "bwd_dh", "dh_finalize", "adamw", "shard_combine", "misc"};
+                                           "transpose_w", "bwd_g", "bwd_dw", "bwd_dh", "dh_finalize", "adamw", "shard_combine", "kd_teacher_p", "kd_q", "kd_terms", "misc"};
 
 struct Timing {
   std::mutex mu;
@@ -1160,7 +1227,8 @@ lce_status_t forward_impl(const lce_problem_t* p, const ShardInfo* shard, const 
   L(K_COMPACT, k_compact, dim3(1), dim3(1024), targets, p->target_bytes, pl.n, si.v_total, p->ignore_index,
     idx, pos, nv, n_valid, dev_status, lse, none ? loss : tgt_part);
   L(K_FWD_STATS, k_fwd_stats, dim3(pl.nt_max * pl.nparts), dim3(NTHREADS), w, pl.ldw, (int)pl.v, h, pl.ldh,
-    pl.n, (const int*)idx, (const int*)nv, (int)pl.d, pl.nparts, pl.nt_max, pl.vt_count, pm, ps, (int)pl.npad);
+    pl.n, (const int*)idx, (const int*)nv, (int)pl.d, pl.nparts, pl.nt_max, pl.vt_count, pm, ps, (int)pl.npad,
+    kLog2e);
   L(K_COMBINE, k_combine, dim3((unsigned)((pl.n + 3) / 4)), dim3(256), h, pl.ldh, w, pl.ldw, targets,
     p->target_bytes, si.v_begin, pl.v, (const int*)idx, (const int*)nv, (int)pl.d, 2 * pl.nparts,
     (const float*)pm, (const float*)ps, (int)pl.npad, lse, terms, none ? loss : (float*)nullptr, tgt_part);
@@ -1168,12 +1236,27 @@ lce_status_t forward_impl(const lce_problem_t* p, const ShardInfo* shard, const 
   return L.st;
 }
 
-// The backward pass behind lce_backward (dW != null), lce_backward_adamw (adamw != null) and
-// lce_backward_shard (shard != null, fp32 dH term in dHf).
+// Teacher head of the distillation loss, as the student's backward needs it: the teacher's
+// probabilities are recomputed slab by slab into an fp32 buffer P [Vc][Npad] placed after the
+// student's backward workspace.
+struct KdArgs {
+  const uint16_t* ht;
+  int64_t ldht;
+  const uint16_t* wt;
+  int64_t ldwt;
+  int dt;
+  const float* lse_t;
+  float scale2, inv_t;
+};
+
+inline size_t kd_p_bytes(const Plan& pl) { return (size_t)4 * pl.vc * pl.npad; }
+
+// The backward pass behind lce_backward (dW != null), lce_backward_adamw (adamw != null),
+// lce_backward_shard (shard != null, fp32 dH term in dHf) and lce_kd_backward (kd != null).
 lce_status_t backward_impl(const lce_problem_t* p, const ShardInfo* shard, const void* H, const void* W,
                            const void* targets, const float* lse, const int32_t* n_valid, const float* grad_loss,
                            void* dH, float* dHf, uint16_t* dW, const AdamWState* adamw, const AdamWConst* oc,
-                           void* workspace, size_t workspace_bytes, void* stream) {
+                           void* workspace, size_t workspace_bytes, void* stream, const KdArgs* kd = nullptr) {
   Plan pl;
   lce_status_t st = make_plan(p, &pl);
   if (st != LCE_OK) return st;
@@ -1183,7 +1266,8 @@ lce_status_t backward_impl(const lce_problem_t* p, const ShardInfo* shard, const
   if (pl.n > 0 && (!H || !targets || !lse || !dH_any || !workspace)) return LCE_ERR_NULL;
   if (!aligned16(W)) return LCE_ERR_ALIGN;
   if (pl.n > 0 && (!aligned16(H) || !aligned16(dH_any) || ((uintptr_t)workspace & 255) != 0)) return LCE_ERR_ALIGN;
-  if (pl.n > 0 && workspace_bytes < pl.bwd_bytes) return LCE_ERR_WORKSPACE;
+  const size_t need = pl.bwd_bytes + (kd ? kd_p_bytes(pl) : 0);
+  if (pl.n > 0 && workspace_bytes < need) return LCE_ERR_WORKSPACE;
   const bool accumulate = (p->flags & LCE_FLAG_ACCUMULATE_DW) != 0;
   const AdamWState as = adamw ? *adamw : AdamWState{nullptr, 0, nullptr, nullptr, nullptr};
   const AdamWConst c = oc ? *oc : AdamWConst{};
@@ -1229,9 +1313,23 @@ lce_status_t backward_impl(const lce_problem_t* p, const ShardInfo* shard, const
     // may update them; later slabs read only their own rows, dH only the transposed copy
     L(K_TRANSPOSE_W, k_transpose, dim3((unsigned)(vs64 / 64), (unsigned)((d + 63) / 64)), dim3(256), w, pl.ldw,
       (const int*)nullptr, v0, (const int*)nullptr, vs, d, wst, (int64_t)vc, vs64);
-    L(K_BWD_G, k_bwd_g, dim3((unsigned)(tm * pl.nt_max)), dim3(NTHREADS), w, pl.ldw, v0, vs, h, pl.ldh, pl.n,
-      targets, p->target_bytes, si.v_begin, (const int*)idx, (const int*)nv, lse, grad_loss, (const int*)n_valid,
-      p->reduction, d, tm, g, vc, gt, npad);
+    if (kd) {
+      // teacher probabilities of this slab, then G = c (softmax(zs / T) - P) / T
+      float* P = (float*)(ws + pl.bwd_bytes);
+      L(K_KD_P, k_bwd_g<P_WRITE>, dim3((unsigned)(tm * pl.nt_max)), dim3(NTHREADS), kd->wt, kd->ldwt, v0, vs,
+        kd->ht, kd->ldht, pl.n, targets, p->target_bytes, (int64_t)0, (const int*)idx, (const int*)nv, kd->lse_t,
+        grad_loss, (const int*)n_valid, p->reduction, kd->dt, tm, (uint16_t*)nullptr, vc, (uint16_t*)nullptr, npad,
+        kd->scale2, kd->inv_t, P, (float*)nullptr, (int64_t)0);
+      L(K_BWD_G, k_bwd_g<G_SOFT>, dim3((unsigned)(tm * pl.nt_max)), dim3(NTHREADS), w, pl.ldw, v0, vs, h, pl.ldh,
+        pl.n, targets, p->target_bytes, (int64_t)0, (const int*)idx, (const int*)nv, lse, grad_loss,
+        (const int*)n_valid, p->reduction, d, tm, g, vc, gt, npad, kd->scale2, kd->inv_t, P, (float*)nullptr,
+        (int64_t)0);
+    } else {
+      L(K_BWD_G, k_bwd_g<G_ONEHOT>, dim3((unsigned)(tm * pl.nt_max)), dim3(NTHREADS), w, pl.ldw, v0, vs, h, pl.ldh,
+        pl.n, targets, p->target_bytes, si.v_begin, (const int*)idx, (const int*)nv, lse, grad_loss,
+        (const int*)n_valid, p->reduction, d, tm, g, vc, gt, npad, kLog2e, 1.f, (float*)nullptr, (float*)nullptr,
+        (int64_t)0);
+    }
     L(K_BWD_DW, dw_kernel, dim3((unsigned)(8 * ((tm + 7) / 8) * dt)), dim3(NTHREADS), (const uint16_t*)gt, npad,
       vs, (const uint16_t*)hvt, d, (const int*)nv, tm, dW, v0, as, c);
     L(K_BWD_DH, k_bwd_dh, dim3((unsigned)(8 * ((pl.nt_max + 7) / 8) * dt)), dim3(NTHREADS), (const uint16_t*)g, vc, vs64,
@@ -1240,6 +1338,111 @@ lce_status_t backward_impl(const lce_problem_t* p, const ShardInfo* shard, const
   const int64_t nthr = pl.n * pl.d / 8;
   L(K_DH_FINAL, k_dh_finalize, dim3((unsigned)((nthr + 255) / 256)), dim3(256), (const float*)dh32,
     (const int*)pos, pl.n, d, (uint16_t*)dH, dHf, 1);
+  return L.st;
+}
+
+// ---- knowledge distillation --------------------------------------------------------------------
+struct KdPlan {
+  lce_problem_t ps, pt;   // student and teacher heads as LCE problems
+  Plan s, t;
+  float scale2, inv_t;
+  size_t o_tgt, o_q, o_p, fwd_bytes, bwd_bytes;
+};
+
+lce_status_t make_kd_plan(const lce_kd_problem_t* p, KdPlan* k) {
+  if (!p) return LCE_ERR_NULL;
+  if (p->reserved != 0) return LCE_ERR_ARG;
+  if (!(p->temperature > 0.f && p->temperature < INFINITY)) return LCE_ERR_ARG;
+  k->ps = lce_problem_t{p->n, p->ds, p->v, p->ld_hs, p->ld_ws, p->ignore_index, p->reduction, p->target_bytes, p->flags};
+  k->pt = lce_problem_t{p->n, p->dt, p->v, p->ld_ht, p->ld_wt, p->ignore_index, p->reduction, p->target_bytes, 0};
+  lce_status_t st = make_plan(&k->ps, &k->s);
+  if (st != LCE_OK) return st;
+  st = make_plan(&k->pt, &k->t);
+  if (st != LCE_OK) return st;
+  k->scale2 = (float)(1.4426950408889634 / (double)p->temperature);
+  k->inv_t = (float)(1.0 / (double)p->temperature);
+  // forward: the student plan's forward regions (index arrays, partials, terms; the teacher's
+  // partials have the same shape), then target-logit scratch, Q partials and P
+  auto up = [](size_t x) { return (x + 255) / 256 * 256; };
+  size_t cur = up(k->s.fwd_bytes);
+  k->o_tgt = cur;
+  cur += up(4 * (size_t)k->s.npad);
+  k->o_q = cur;
+  cur += up((size_t)4 * 2 * k->s.vt_count * k->s.npad);
+  k->o_p = cur;
+  cur += up(kd_p_bytes(k->s));
+  k->fwd_bytes = cur;
+  k->bwd_bytes = k->s.bwd_bytes + kd_p_bytes(k->s);
+  return LCE_OK;
+}
+
+lce_status_t kd_forward_impl(const lce_kd_problem_t* p, const void* Hs, const void* Ws, const void* Ht,
+                             const void* Wt, const void* targets, float* loss, float* lse_s, float* lse_t,
+                             int32_t* n_valid, int32_t* dev_status, void* workspace, size_t workspace_bytes,
+                             void* stream) {
+  KdPlan k;
+  lce_status_t st = make_kd_plan(p, &k);
+  if (st != LCE_OK) return st;
+  const Plan& pl = k.s;
+  if (!loss || !n_valid) return LCE_ERR_NULL;
+  if (pl.n > 0 && (!Hs || !Ws || !Ht || !Wt || !targets || !lse_s || !lse_t || !workspace)) return LCE_ERR_NULL;
+  if (pl.n > 0 && (!aligned16(Hs) || !aligned16(Ws) || !aligned16(Ht) || !aligned16(Wt) ||
+                   ((uintptr_t)workspace & 255) != 0))
+    return LCE_ERR_ALIGN;
+  if (pl.n > 0 && workspace_bytes < k.fwd_bytes) return LCE_ERR_WORKSPACE;
+  Launcher L{(hipStream_t)stream};
+  const bool none = p->reduction == LCE_REDUCE_NONE;
+  if (pl.n == 0) {
+    L(K_MISC, k_fwd_empty, dim3(1), dim3(64), none ? (float*)nullptr : loss, n_valid, dev_status);
+    return L.st;
+  }
+  char* ws = (char*)workspace;
+  int* idx = (int*)(ws + pl.o_idx);
+  int* pos = (int*)(ws + pl.o_pos);
+  int* nv = (int*)(ws + pl.o_nv);
+  float* pm = (float*)(ws + pl.o_pm);
+  float* ps = (float*)(ws + pl.o_ps);
+  float* terms = (float*)(ws + pl.o_terms);
+  float* tgt = (float*)(ws + k.o_tgt);
+  float* qpart = (float*)(ws + k.o_q);
+  float* P = (float*)(ws + k.o_p);
+  const uint16_t* hs = (const uint16_t*)Hs;
+  const uint16_t* wsm = (const uint16_t*)Ws;
+  const uint16_t* ht = (const uint16_t*)Ht;
+  const uint16_t* wt = (const uint16_t*)Wt;
+  const int npad = (int)pl.npad, vc = (int)pl.vc;
+
+  L(K_COMPACT, k_compact, dim3(1), dim3(1024), targets, p->target_bytes, pl.n, pl.v, p->ignore_index,
+    idx, pos, nv, n_valid, dev_status, lse_s, lse_t);
+  // log-sum-exp of both heads' logits / T (no target logit: an empty id range)
+  const Plan& tp = k.t;
+  L(K_FWD_STATS, k_fwd_stats, dim3(tp.nt_max * tp.nparts), dim3(NTHREADS), wt, tp.ldw, (int)tp.v, ht, tp.ldh,
+    tp.n, (const int*)idx, (const int*)nv, (int)tp.d, tp.nparts, tp.nt_max, tp.vt_count, pm, ps, npad, k.scale2);
+  L(K_COMBINE, k_combine, dim3((unsigned)((pl.n + 3) / 4)), dim3(256), ht, tp.ldh, wt, tp.ldw, targets,
+    p->target_bytes, (int64_t)0, (int64_t)0, (const int*)idx, (const int*)nv, (int)tp.d, 2 * tp.nparts,
+    (const float*)pm, (const float*)ps, npad, lse_t, terms, (float*)nullptr, tgt);
+  L(K_FWD_STATS, k_fwd_stats, dim3(pl.nt_max * pl.nparts), dim3(NTHREADS), wsm, pl.ldw, (int)pl.v, hs, pl.ldh,
+    pl.n, (const int*)idx, (const int*)nv, (int)pl.d, pl.nparts, pl.nt_max, pl.vt_count, pm, ps, npad, k.scale2);
+  L(K_COMBINE, k_combine, dim3((unsigned)((pl.n + 3) / 4)), dim3(256), hs, pl.ldh, wsm, pl.ldw, targets,
+    p->target_bytes, (int64_t)0, (int64_t)0, (const int*)idx, (const int*)nv, (int)pl.d, 2 * pl.nparts,
+    (const float*)pm, (const float*)ps, npad, lse_s, terms, (float*)nullptr, tgt);
+  // per slab: teacher probabilities P, then the student's sum_v P zs / T per token and tile
+  for (int64_t s = 0; s < pl.nslab; ++s) {
+    const int64_t v0 = s * pl.vc;
+    const int vs = (int)(pl.v - v0 < pl.vc ? pl.v - v0 : pl.vc);
+    const int tm = (vs + TILE - 1) / TILE;
+    L(K_KD_P, k_bwd_g<P_WRITE>, dim3((unsigned)(tm * pl.nt_max)), dim3(NTHREADS), wt, tp.ldw, v0, vs, ht, tp.ldh,
+      pl.n, targets, p->target_bytes, (int64_t)0, (const int*)idx, (const int*)nv, (const float*)lse_t,
+      (const float*)nullptr, (const int*)nullptr, p->reduction, (int)tp.d, tm, (uint16_t*)nullptr, vc,
+      (uint16_t*)nullptr, npad, k.scale2, k.inv_t, P, (float*)nullptr, (int64_t)0);
+    L(K_KD_Q, k_bwd_g<Q_SOFT>, dim3((unsigned)(tm * pl.nt_max)), dim3(NTHREADS), wsm, pl.ldw, v0, vs, hs, pl.ldh,
+      pl.n, targets, p->target_bytes, (int64_t)0, (const int*)idx, (const int*)nv, (const float*)lse_s,
+      (const float*)nullptr, (const int*)nullptr, p->reduction, (int)pl.d, tm, (uint16_t*)nullptr, vc,
+      (uint16_t*)nullptr, npad, k.scale2, k.inv_t, P, qpart, (int64_t)(2 * (v0 / TILE)));
+  }
+  L(K_KD_TERMS, k_kd_terms, dim3((unsigned)((pl.n + 255) / 256)), dim3(256), (const float*)qpart,
+    2 * pl.vt_count, (int64_t)npad, (const int*)pos, pl.n, (const float*)lse_s, terms, none ? loss : (float*)nullptr);
+  if (!none) L(K_LOSS, k_loss, dim3(1), dim3(1024), (const float*)terms, (const int*)nv, p->reduction, loss);
   return L.st;
 }
 
@@ -1373,6 +1576,39 @@ lce_status_t lce_backward_adamw(const lce_problem_t* p, const void* H, void* W, 
   AdamWState as{(uint16_t*)W, p->ld_w ? p->ld_w : p->d, exp_avg, exp_avg_sq, W_master};
   return backward_impl(p, nullptr, H, W, targets, lse, n_valid, grad_loss, dH, nullptr, nullptr, &as, &c,
                        workspace, workspace_bytes, stream);
+}
+
+lce_status_t lce_kd_workspace_size(const lce_kd_problem_t* p, size_t* fwd_bytes, size_t* bwd_bytes) {
+  KdPlan k;
+  lce_status_t st = make_kd_plan(p, &k);
+  if (st != LCE_OK) return st;
+  if (fwd_bytes) *fwd_bytes = k.fwd_bytes;
+  if (bwd_bytes) *bwd_bytes = k.bwd_bytes;
+  return LCE_OK;
+}
+
+lce_status_t lce_kd_forward(const lce_kd_problem_t* p, const void* Hs, const void* Ws, const void* Ht,
+                            const void* Wt, const void* targets, float* loss, float* lse_s, float* lse_t,
+                            int32_t* n_valid, int32_t* dev_status, void* workspace, size_t workspace_bytes,
+                            void* stream) {
+  return kd_forward_impl(p, Hs, Ws, Ht, Wt, targets, loss, lse_s, lse_t, n_valid, dev_status, workspace,
+                         workspace_bytes, stream);
+}
+
+lce_status_t lce_kd_backward(const lce_kd_problem_t* p, const void* Hs, const void* Ws, const void* Ht,
+                             const void* Wt, const void* targets, const float* lse_s, const float* lse_t,
+                             const int32_t* n_valid, const float* grad_loss, void* dHs, void* dWs,
+                             void* workspace, size_t workspace_bytes, void* stream) {
+  KdPlan k;
+  lce_status_t st = make_kd_plan(p, &k);
+  if (st != LCE_OK) return st;
+  if (!dWs) return LCE_ERR_NULL;
+  if (!aligned16(dWs)) return LCE_ERR_ALIGN;
+  if (p->n > 0 && (!Ht || !Wt || !lse_t)) return LCE_ERR_NULL;
+  if (p->n > 0 && (!aligned16(Ht) || !aligned16(Wt))) return LCE_ERR_ALIGN;
+  const KdArgs kd{(const uint16_t*)Ht, k.t.ldh, (const uint16_t*)Wt, k.t.ldw, (int)k.t.d, lse_t, k.scale2, k.inv_t};
+  return backward_impl(&k.ps, nullptr, Hs, Ws, targets, lse_s, n_valid, grad_loss, dHs, nullptr, (uint16_t*)dWs,
+                       nullptr, nullptr, workspace, workspace_bytes, stream, &kd);
 }
 
 lce_status_t lce_timing_enable(int on) {

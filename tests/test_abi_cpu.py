@@ -204,3 +204,38 @@ def test_shard_argument_checks_run_before_any_launch():
         with pytest.raises(B.LceError) as e:
             B.lce_backward_shard(p, B.LceShard(20, 10), **dict(bok, **change))
         assert e.value.code == code, change
+
+
+def test_kd_argument_checks_run_before_any_launch():
+    p = B.kd_problem(8, 64, 96, 10)
+    fwd, bwd = B.lce_kd_workspace_size(p)
+    assert fwd > 0 and bwd > 0
+    for kw, code in [(dict(temperature=0.0), B.LCE_ERR_ARG), (dict(temperature=float("nan")), B.LCE_ERR_ARG),
+                     (dict(flags=4), B.LCE_ERR_ARG)]:
+        with pytest.raises(B.LceError) as e:
+            B.lce_kd_workspace_size(B.kd_problem(8, 64, 96, 10, **kw))
+        assert e.value.code == code, kw
+    with pytest.raises(B.LceError) as e:
+        B.lce_kd_workspace_size(B.kd_problem(8, 64, 90, 10))            # teacher width not a multiple of 8
+    assert e.value.code == B.LCE_ERR_UNSUPPORTED
+    q = B.kd_problem(8, 64, 96, 10)
+    q.reserved = 1
+    with pytest.raises(B.LceError) as e:
+        B.lce_kd_workspace_size(q)
+    assert e.value.code == B.LCE_ERR_ARG
+    fok = dict(Hs=_fake(), Ws=_fake(0x200000), Ht=_fake(0x300000), Wt=_fake(0x400000), targets=_fake(0x500000),
+               loss=_fake(0x600000), lse_s=_fake(0x700000), lse_t=_fake(0x800000), n_valid=_fake(0x900000),
+               dev_status=0, workspace=_fake(0xA00000), workspace_bytes=fwd, stream=0)
+    for change, code in [(dict(Ht=0), B.LCE_ERR_NULL), (dict(lse_t=0), B.LCE_ERR_NULL),
+                         (dict(Wt=0x400008), B.LCE_ERR_ALIGN), (dict(workspace_bytes=fwd - 1), B.LCE_ERR_WORKSPACE)]:
+        with pytest.raises(B.LceError) as e:
+            B.lce_kd_forward(p, **dict(fok, **change))
+        assert e.value.code == code, change
+    bok = dict(Hs=_fake(), Ws=_fake(0x200000), Ht=_fake(0x300000), Wt=_fake(0x400000), targets=_fake(0x500000),
+               lse_s=_fake(0x600000), lse_t=_fake(0x700000), n_valid=_fake(0x800000), grad_loss=_fake(0x900000),
+               dHs=_fake(0xA00000), dWs=_fake(0xB00000), workspace=_fake(0xC00000), workspace_bytes=bwd, stream=0)
+    for change, code in [(dict(dWs=0), B.LCE_ERR_NULL), (dict(lse_t=0), B.LCE_ERR_NULL),
+                         (dict(Ht=0x300004), B.LCE_ERR_ALIGN), (dict(workspace_bytes=bwd - 1), B.LCE_ERR_WORKSPACE)]:
+        with pytest.raises(B.LceError) as e:
+            B.lce_kd_backward(p, **dict(bok, **change))
+        assert e.value.code == code, change
