@@ -1,7 +1,7 @@
 """Benchmark of the LCE hot path (forward + backward) on one MI355X.
 
 python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload llama8b] [--no-cpu-baseline]
-                [--variant lce|adamw_fused|adamw_two_phase|vocab_shard] [--shards 8]
+                [--variant lce|adamw_fused|adamw_two_phase|vocab_shard|kd] [--shards 8]
 
 One step is one lce_forward + lce_backward over the whole batch of the named
 workload (default: the Llama-3.1-8B vocabulary head, N = 8 x 2048 tokens,
@@ -21,6 +21,12 @@ lce_backward_shard on N tokens x V/G ids (shard 0). The [G, N] partials that
 an all-gather would bring from the other devices are stood in for by copies of
 this shard's own, and no collective runs; the line reports N / step time, the
 whole job's rate when G devices each run their share in parallel.
+
+``kd`` times the fused linear knowledge-distillation loss (lce_kd_forward +
+lce_kd_backward, temperature 2) distilling the Llama-3.1-8B head (teacher,
+D = 4096) into the Llama-3.2-1B head (student, D = 2048) over 8 x 2048 tokens;
+its MFMA work per step is 6 Nv V Dt + 8 Nv V Ds (teacher statistics and two
+probability passes; student statistics, Q pass, G recompute, dW and dH).
 """
 from __future__ import annotations
 
@@ -105,7 +111,8 @@ def main():
     ap.add_argument("--workload", default="llama8b")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--variant", default="lce", choices=("lce", "adamw_fused", "adamw_two_phase", "vocab_shard"))
+    ap.add_argument("--variant", default="lce",
+                    choices=("lce", "adamw_fused", "adamw_two_phase", "vocab_shard", "kd"))
     ap.add_argument("--shards", type=int, default=8, help="vocabulary shards (vocab_shard variant)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a 1 GiB device copy (for scaling HBM byte counters)")
@@ -117,6 +124,10 @@ def main():
         print(f"bench.py measures one GPU only (asked for {args.gpus}); the LCE path here has no "
               f"multi-GPU mode", file=sys.stderr)
         sys.exit(2)
+
+    if args.variant == "kd":
+        bench_kd(args)
+        return
 
     import torch
     from paper_2605_21442_amd import binding as B
@@ -281,6 +292,121 @@ def main():
         out["cpu_baseline"] = _cpu_baseline(inp)
     else:
         out["cpu_baseline"] = None
+    print(json.dumps(out), flush=True)
+
+
+def _kd_cpu_baseline(inp, temperature, seconds_target=10.0):
+    """The KD oracle, as it stands, on a bounded token sample (forward + backward)."""
+    from oracle import kd_oracle as K
+    try:
+        import threadpoolctl
+        threads = max(i.get("num_threads", 1) for i in threadpoolctl.threadpool_info()) or 1
+    except Exception:  # pragma: no cover
+        threads = os.cpu_count() or 1
+    valid = np.nonzero(inp.targets != inp.ignore_index)[0]
+    sample = 16
+    while True:
+        r = valid[:sample]
+        t0 = time.perf_counter()
+        K.kd_bits(inp.hs_bits[r], inp.ws_bits, inp.ht_bits[r], inp.wt_bits, inp.targets[r], temperature=temperature)
+        dt = time.perf_counter() - t0
+        if dt >= seconds_target or sample >= len(valid):
+            break
+        sample = min(len(valid), max(2 * sample, int(sample * 1.2 * seconds_target / max(dt, 1e-3))))
+    return {"value": sample / dt, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{sample} valid tokens of the {inp.name} batch, full Ds, Dt and V, fp64 KD "
+                      f"forward+backward ({dt:.1f} s)"}
+
+
+def bench_kd(args):
+    """The KD variant: one step = lce_kd_forward + lce_kd_backward on the 8B-to-1B heads."""
+    import torch
+    from paper_2605_21442_amd import binding as B
+    from paper_2605_21442_amd import workloads as WL
+
+    name, T = "kd_8b_to_1b", 2.0
+    inp = WL.kd_generate(name, args.seed)
+    k = WL.KD_WORKLOADS[name]
+    n, ds, dt, v = k["n"], k["ds"], k["dt"], k["v"]
+    dev = torch.device("cuda:0")
+    to = lambda b: torch.from_numpy(b.view(np.int16)).view(torch.bfloat16).to(dev)
+    hs, ws, ht, wt = to(inp.hs_bits), to(inp.ws_bits), to(inp.ht_bits), to(inp.wt_bits)
+    t = torch.from_numpy(inp.targets).to(dev)
+    p = B.kd_problem(n, ds, dt, v, temperature=T, ignore_index=inp.ignore_index)
+    fwd_bytes, bwd_bytes = B.lce_kd_workspace_size(p)
+    torch.cuda.synchronize()
+    torch.cuda.reset_peak_memory_stats()
+    loss = torch.empty((), dtype=torch.float32, device=dev)
+    lse_s = torch.empty(n, dtype=torch.float32, device=dev)
+    lse_t = torch.empty(n, dtype=torch.float32, device=dev)
+    nv = torch.empty(1, dtype=torch.int32, device=dev)
+    status = torch.empty(1, dtype=torch.int32, device=dev)
+    grad = torch.ones(1, dtype=torch.float32, device=dev)
+    dh = torch.empty((n, ds), dtype=torch.bfloat16, device=dev)
+    dw = torch.empty((v, ds), dtype=torch.bfloat16, device=dev)
+    wsp = torch.empty(max(fwd_bytes, bwd_bytes), dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream(dev).cuda_stream
+
+    def step():
+        B.lce_kd_forward(p, hs.data_ptr(), ws.data_ptr(), ht.data_ptr(), wt.data_ptr(), t.data_ptr(),
+                         loss.data_ptr(), lse_s.data_ptr(), lse_t.data_ptr(), nv.data_ptr(), status.data_ptr(),
+                         wsp.data_ptr(), fwd_bytes, stream)
+        B.lce_kd_backward(p, hs.data_ptr(), ws.data_ptr(), ht.data_ptr(), wt.data_ptr(), t.data_ptr(),
+                          lse_s.data_ptr(), lse_t.data_ptr(), nv.data_ptr(), grad.data_ptr(), dh.data_ptr(),
+                          dw.data_ptr(), wsp.data_ptr(), bwd_bytes, stream)
+
+    for i in range(args.warmup):
+        step()
+        torch.cuda.synchronize()
+        print(f"[bench] kd warmup {i + 1}/{args.warmup} done", file=sys.stderr, flush=True)
+    peak = torch.cuda.max_memory_allocated()
+    B.lce_timing_enable(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    kernels = {}
+    for kk, kname in enumerate(B.lce_timing_kernel_names()):
+        ms, cnt = B.lce_timing_read(kk)
+        if cnt:
+            kernels[kname] = {"total_ms": ms, "launches": cnt, "avg_ms": ms / cnt}
+    B.lce_timing_enable(False)
+    nvalid = int(nv.item())
+    # MFMA work per step and kernel (see the module docstring)
+    work = {"fwd_stats": 2.0 * nvalid * v * (ds + dt), "kd_teacher_p": 4.0 * nvalid * v * dt,
+            "kd_q": 2.0 * nvalid * v * ds, "bwd_g": 2.0 * nvalid * v * ds, "bwd_dw": 2.0 * nvalid * v * ds,
+            "bwd_dh": 2.0 * nvalid * v * ds}
+    flops_step = sum(work.values())
+    ms_step = elapsed * 1e3 / args.steps
+    for kname, r in sorted(kernels.items(), key=lambda kv: -kv[1]["total_ms"]):
+        extra = ""
+        if kname in work:
+            tf = work[kname] / (r["total_ms"] / args.steps * 1e-3) / 1e12
+            extra = f" {tf:7.1f} TFLOP/s ({100 * tf / PEAK_BF16_TFLOPS:4.1f}% of peak)"
+        print(f"[bench]   {kname:12s} {r['total_ms'] / args.steps:8.3f} ms/step  {r['launches']:5d} launches"
+              f"  avg {r['avg_ms']:.4f} ms{extra}", file=sys.stderr)
+    dom = max((kk for kk in kernels if kk in work), key=lambda kk: kernels[kk]["total_ms"])
+    per_launch = work[dom] / (kernels[dom]["launches"] / args.steps)
+    achieved = per_launch / (kernels[dom]["avg_ms"] * 1e-3) / 1e12
+    out = {
+        "metric": METRIC, "value": n * args.steps / elapsed, "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": name, "n_tokens": n, "student_hidden": ds, "teacher_hidden": dt, "vocab": v,
+                   "n_valid": nvalid, "temperature": T, "parallelism": "none", "reduction": "mean",
+                   "variant": "kd"},
+        "valid_tokens_per_s": nvalid * args.steps / elapsed,
+        "mfma_frac_step": flops_step / (ms_step * 1e-3) / (PEAK_BF16_TFLOPS * 1e12),
+        "peak_hbm_bytes": int(peak), "workspace_bytes": int(max(fwd_bytes, bwd_bytes)),
+        "logits_bytes_avoided_fp32": 2 * int(n) * int(v) * 4,
+        "roofline": {"bound": "mfma", "kernel": dom, "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
+                     "flops_per_launch": per_launch, "avg_launch_ms": kernels[dom]["avg_ms"]},
+        "kernels_ms_per_step": {kk: r["total_ms"] / args.steps for kk, r in kernels.items()},
+        "cpu_baseline": None if args.no_cpu_baseline else _kd_cpu_baseline(inp, T),
+    }
     print(json.dumps(out), flush=True)
 
 

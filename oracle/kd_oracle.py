@@ -42,8 +42,9 @@ def _lse(z):
 
 
 def kd(hs, ws, ht, wt, targets, temperature=1.0, ignore_index=-100, reduction="mean", grad=1.0,
-       block=512):
-    """Loss, lse of both heads (0 outside M), Nv, status, dHs and dWs, all float64."""
+       block=512, grads=True):
+    """Loss, lse of both heads (0 outside M), Nv, status, dHs and dWs (unless grads=False), all
+    float64."""
     n, v = hs.shape[0], ws.shape[0]
     ok, status = valid_rows(targets, v, ignore_index)
     rows = np.nonzero(ok)[0]
@@ -65,6 +66,8 @@ def kd(hs, ws, ht, wt, targets, temperature=1.0, ignore_index=-100, reduction="m
         pt = np.exp(zt - lt[:, None])
         ps = np.exp(zs - ls[:, None])
         per_row[r] = ls - (pt * zs).sum(axis=1)
+        if not grads:
+            continue
         cr = c[r][:, None] if reduction == "none" else c
         g = cr * (ps - pt) / temperature
         dhs[r] = g @ ws
@@ -101,4 +104,44 @@ def kd_rows(hs_bits, ws_bits, ht_bits, wt_bits, targets, rows, temperature=1.0, 
         pt = np.exp(zt[0] - lt)
         out["per_row"][i] = ls - float(pt @ zs[0])
         out["lse_s"][i], out["lse_t"][i] = ls, lt
+    return out
+
+
+def kd_dh_rows(hs_bits, ws_bits, ht_bits, wt_bits, targets, rows, n_valid, temperature=1.0,
+               ignore_index=-100, grad=1.0):
+    """Rows of dHs = G Ws for the mean reduction (zero for rows outside M)."""
+    v = ws_bits.shape[0]
+    ok, _ = valid_rows(targets, v, ignore_index)
+    ws = bf16_to_f64(ws_bits)
+    wt = bf16_to_f64(wt_bits)
+    c = scale_c(n_valid, "mean", grad)
+    out = np.zeros((len(rows), ws.shape[1]))
+    for i, r in enumerate(rows):
+        if not ok[r]:
+            continue
+        zs = bf16_to_f64(hs_bits[r:r + 1]) @ ws.T / temperature
+        zt = bf16_to_f64(ht_bits[r:r + 1]) @ wt.T / temperature
+        ps = np.exp(zs - _lse(zs)[:, None])
+        pt = np.exp(zt - _lse(zt)[:, None])
+        out[i] = ((c * (ps - pt) / temperature) @ ws)[0]
+    return out
+
+
+def kd_dw_rows(hs_bits, ws_bits, ht_bits, wt_bits, targets, vrows, lse_s, lse_t, temperature=1.0,
+               ignore_index=-100, grad=1.0, block=4096):
+    """Rows of dWs = G^T Hs (mean reduction) for vocabulary ids ``vrows``, given the oracle's lse of
+    both heads for every row."""
+    v = ws_bits.shape[0]
+    ok, _ = valid_rows(targets, v, ignore_index)
+    rows = np.nonzero(ok)[0]
+    c = scale_c(int(rows.size), "mean", grad)
+    wsv = bf16_to_f64(ws_bits[np.asarray(vrows)])
+    wtv = bf16_to_f64(wt_bits[np.asarray(vrows)])
+    out = np.zeros((len(vrows), ws_bits.shape[1]))
+    for s0 in range(0, rows.size, block):
+        r = rows[s0:s0 + block]
+        hs = bf16_to_f64(hs_bits[r])
+        ps = np.exp(hs @ wsv.T / temperature - lse_s[r][:, None])
+        pt = np.exp(bf16_to_f64(ht_bits[r]) @ wtv.T / temperature - lse_t[r][:, None])
+        out += (c * (ps - pt) / temperature).T @ hs
     return out

@@ -708,16 +708,26 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_bwd_g(const uint16_t* __restric
     for (int j = 0; j < 2; ++j) {
       if (tok[j] >= nv) continue;
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < 4; ++i) {
+        if constexpr (kMode == P_WRITE) {
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int vr = vb + i * 32 + (r >> 2) * 8 + (r & 3);
-          if (vr < vleft) {
-            float* pp = P + (int64_t)(vt0 + vr) * ldt + tok[j];
-            if constexpr (kMode == P_WRITE) *pp = __builtin_amdgcn_exp2f(fmaf(acc[i][j][r], scale2, -l2[j]));
-            else q[j] = fmaf(*pp, acc[i][j][r] * inv_t, q[j]);
+          for (int r = 0; r < 16; ++r) {
+            const int vr = vb + i * 32 + (r >> 2) * 8 + (r & 3);
+            if (vr < vleft)
+              P[(int64_t)(vt0 + vr) * ldt + tok[j]] = __builtin_amdgcn_exp2f(fmaf(acc[i][j][r], scale2, -l2[j]));
           }
+        } else {
+          // the block's 16 probabilities are loaded together, then used
+          float pt[16];
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int vr = vb + i * 32 + (r >> 2) * 8 + (r & 3);
+            pt[r] = vr < vleft ? P[(int64_t)(vt0 + vr) * ldt + tok[j]] : 0.f;
+          }
+#pragma unroll
+          for (int r = 0; r < 16; ++r) q[j] = fmaf(pt[r], acc[i][j][r] * inv_t, q[j]);
         }
+      }
     }
     if constexpr (kMode == Q_SOFT) {
       // the two lane halves hold disjoint vocabulary rows of the same tokens
@@ -738,7 +748,16 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_bwd_g(const uint16_t* __restric
     const bool tok_ok = tok[j] < nv;
     const int nl = wc * 64 + j * 32 + (lane & 31);
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < 4; ++i) {
+      float pt[16];
+      if constexpr (kMode == G_SOFT) {
+        // the block's 16 teacher probabilities are loaded together, then used
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int vr = vb + i * 32 + (r >> 2) * 8 + (r & 3);
+          pt[r] = (tok_ok && vr < vleft) ? P[(int64_t)(vt0 + vr) * ldt + tok[j]] : 0.f;
+        }
+      }
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         float gq[4];
@@ -750,7 +769,7 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_bwd_g(const uint16_t* __restric
           if (tok_ok && vr < vleft) {
             const float e2 = __builtin_amdgcn_exp2f(fmaf(acc[i][j][r], scale2, -l2[j]));
             if constexpr (kMode == G_SOFT) {
-              g = cj[j] * inv_t * (e2 - P[(int64_t)(vt0 + vr) * ldt + tok[j]]);
+              g = cj[j] * inv_t * (e2 - pt[r]);
             } else {
               g = cj[j] * e2;
               if (vr == tgt[j]) g -= cj[j];
@@ -765,6 +784,7 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_bwd_g(const uint16_t* __restric
         const uint32_t a = (uint32_t)(nl * 512 + ((((vl >> 3) ^ (nl & 31))) << 4) + ((vl & 7) << 1));
         *reinterpret_cast<u32x2_t*>(T + a) = pk;
       }
+    }
   }
   __syncthreads();
   // G rows (tokens < Nv): 16-byte chunks, one 512-byte row per 32 threads

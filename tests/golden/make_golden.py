@@ -18,6 +18,7 @@ import numpy as np
 ROOT = os.path.dirname(os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
 sys.path.insert(0, ROOT)
 
+from oracle import kd_oracle as K  # noqa: E402
 from oracle import lce_oracle as O  # noqa: E402
 from paper_2605_21442_amd import workloads as WL  # noqa: E402
 
@@ -50,7 +51,30 @@ def make(name: str, seed: int = 0) -> None:
           flush=True)
 
 
+def kd_fingerprint(inp: WL.KdInputs) -> str:
+    h = hashlib.sha256()
+    for a in (inp.hs_bits[:2], inp.ws_bits[-2:], inp.ht_bits[:2], inp.wt_bits[-2:], inp.targets):
+        h.update(np.ascontiguousarray(a).tobytes())
+    return h.hexdigest()
+
+
+KD_TEMPERATURE = 2.0
+
+
+def make_kd(name: str, seed: int = 0) -> None:
+    """KD forward of a full-size distillation workload at temperature 2."""
+    t0 = time.time()
+    inp = WL.kd_generate(name, seed)
+    out = K.kd_bits(inp.hs_bits, inp.ws_bits, inp.ht_bits, inp.wt_bits, inp.targets,
+                    temperature=KD_TEMPERATURE, grads=False)
+    np.savez_compressed(path_for(name, seed), loss=np.float64(out["loss"]), lse_s=out["lse_s"],
+                        lse_t=out["lse_t"], n_valid=np.int64(out["n_valid"]), status=np.int64(out["status"]),
+                        temperature=np.float64(KD_TEMPERATURE), fingerprint=np.array(kd_fingerprint(inp)),
+                        workload=np.array(name), seed=np.int64(seed))
+    print(f"{name}: loss={out['loss']:.9f} Nv={out['n_valid']} ({time.time() - t0:.0f} s)", flush=True)
+
+
 if __name__ == "__main__":
-    names = sys.argv[1:] or [k for k in WL.WORKLOADS if k != "tiny"]
+    names = sys.argv[1:] or [k for k in WL.WORKLOADS if k != "tiny"] + ["kd_8b_to_1b"]
     for k in names:
-        make(k)
+        make_kd(k) if k in WL.KD_WORKLOADS else make(k)

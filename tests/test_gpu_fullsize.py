@@ -191,3 +191,52 @@ def test_full_size_vocabulary_shards_llama8b():
     got_dw = dw[torch.from_numpy(ids).to(h.device)].float().cpu().numpy().astype(np.float64)
     assert U.rel_fro(got_dw, ref_dw) <= U.GRAD_REL_TOL
     _say(f"[{name}] shards ok: loss {float(loss.item()):.6f} (oracle {float(gold['loss']):.6f})")
+
+
+def test_full_size_kd_8b_to_1b():
+    """Distilling the 8B head into the 1B head (N = 16384, Ds = 2048, Dt = 4096, V = 128256, T = 2)
+    in the launch configuration the benchmark's KD variant times: loss and every row's lse of both
+    heads against the stored oracle forward, sampled dHs / dWs rows against the oracle."""
+    import torch
+    from oracle import kd_oracle as K
+    from paper_2605_21442_amd import autograd as AG
+    name = "kd_8b_to_1b"
+    path = MG.path_for(name, 0)
+    if not os.path.exists(path):
+        pytest.skip(f"{path} missing: run tests/golden/make_golden.py")
+    gold = np.load(path, allow_pickle=False)
+    inp = WL.kd_generate(name, 0)
+    assert str(gold["fingerprint"]) == MG.kd_fingerprint(inp), "golden file is stale"
+    T = float(gold["temperature"])
+    dev = "cuda:0"
+    to = lambda b: torch.from_numpy(b.view(np.int16)).view(torch.bfloat16).to(dev)
+    hs, ws, ht, wt = to(inp.hs_bits), to(inp.ws_bits), to(inp.ht_bits), to(inp.wt_bits)
+    t = torch.from_numpy(inp.targets).to(dev)
+    _say(f"[{name}] kd forward + backward")
+    loss, lse_s, lse_t, nv, status = AG.kd_forward(hs, ws, ht, wt, t, T)
+    g = torch.ones(1, dtype=torch.float32, device=dev)
+    dh, dw = AG.kd_backward(hs, ws, ht, wt, t, lse_s, lse_t, nv, g, T)
+    torch.cuda.synchronize()
+    assert int(nv.item()) == int(gold["n_valid"]) and int(status.item()) == 0
+    assert abs(float(loss.item()) - float(gold["loss"])) <= U.LOSS_ABS_TOL, (float(loss.item()), float(gold["loss"]))
+    valid = inp.targets != inp.ignore_index
+    for k, got in (("lse_s", lse_s), ("lse_t", lse_t)):
+        err = np.max(np.abs(got.cpu().numpy()[valid] - gold[k][valid]))
+        assert err <= U.LSE_ABS_TOL, (k, err)
+    rng = np.random.default_rng(5)
+    vrows = np.nonzero(valid)[0]
+    rows = np.concatenate([rng.choice(vrows, 4, replace=False), np.nonzero(~valid)[0][:1]])
+    _say(f"[{name}] oracle dHs rows {rows.tolist()}")
+    ref = K.kd_dh_rows(inp.hs_bits, inp.ws_bits, inp.ht_bits, inp.wt_bits, inp.targets, rows,
+                       int(gold["n_valid"]), temperature=T)
+    got = dh[torch.from_numpy(rows).to(dev)].float().cpu().numpy().astype(np.float64)
+    assert U.rel_fro(got, ref) <= U.GRAD_REL_TOL
+    assert np.all(got[-1] == 0.0)
+    v = inp.ws_bits.shape[0]
+    ids = np.array(sorted(set([0, 1, 8191, 8192, v - 1] + rng.integers(2, v, 3).tolist())))
+    _say(f"[{name}] oracle dWs rows {ids.tolist()}")
+    ref = K.kd_dw_rows(inp.hs_bits, inp.ws_bits, inp.ht_bits, inp.wt_bits, inp.targets, ids, gold["lse_s"],
+                       gold["lse_t"], temperature=T)
+    got = dw[torch.from_numpy(ids).to(dev)].float().cpu().numpy().astype(np.float64)
+    assert U.rel_fro(got, ref) <= U.GRAD_REL_TOL
+    _say(f"[{name}] ok: loss {float(loss.item()):.6f} (oracle {float(gold['loss']):.6f})")

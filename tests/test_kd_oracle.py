@@ -101,3 +101,17 @@ def test_sampled_rows_helper_matches_whole_oracle():
     part = K.kd_rows(hs_b, ws_b, ht_b, wt_b, t, rows, temperature=2.0)
     np.testing.assert_allclose(part["per_row"], whole["loss"][rows], rtol=1e-13, atol=1e-15)
     np.testing.assert_allclose(part["lse_t"], whole["lse_t"][rows], rtol=1e-13, atol=1e-15)
+
+
+def test_sampled_gradient_rows_match_whole_oracle():
+    bits = lambda a: (np.asarray(a, np.float32).view(np.uint32) >> 16).astype(np.uint16)
+    hs, ws, ht, wt, t = _heads(n=40, v=50, seed=10)
+    hs_b, ws_b, ht_b, wt_b = bits(hs), bits(ws), bits(ht), bits(wt)
+    whole = K.kd_bits(hs_b, ws_b, ht_b, wt_b, t, temperature=2.0, grad=1.5)
+    rows = np.array([0, 1, 4, 39])
+    dh = K.kd_dh_rows(hs_b, ws_b, ht_b, wt_b, t, rows, whole["n_valid"], temperature=2.0, grad=1.5)
+    np.testing.assert_allclose(dh, whole["dHs"][rows], rtol=1e-11, atol=1e-15)
+    ids = np.array([0, 7, 49])
+    dw = K.kd_dw_rows(hs_b, ws_b, ht_b, wt_b, t, ids, whole["lse_s"], whole["lse_t"], temperature=2.0, grad=1.5,
+                      block=16)
+    np.testing.assert_allclose(dw, whole["dWs"][ids], rtol=1e-11, atol=1e-15)
