@@ -1,7 +1,7 @@
 """Benchmark of the LCE hot path (forward + backward) on one MI355X.
 
 python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload llama8b] [--no-cpu-baseline]
-                [--variant lce|adamw_fused|adamw_two_phase|vocab_shard|kd] [--shards 8]
+                [--variant lce|adamw_fused|adamw_two_phase|vocab_shard|kd|kd_fused] [--shards 8]
 
 One step is one lce_forward + lce_backward over the whole batch of the named
 workload (default: the Llama-3.1-8B vocabulary head, N = 8 x 2048 tokens,
@@ -25,8 +25,10 @@ whole job's rate when G devices each run their share in parallel.
 ``kd`` times the fused linear knowledge-distillation loss (lce_kd_forward +
 lce_kd_backward, temperature 2) distilling the Llama-3.1-8B head (teacher,
 D = 4096) into the Llama-3.2-1B head (student, D = 2048) over 8 x 2048 tokens;
-its MFMA work per step is 6 Nv V Dt + 8 Nv V Ds (teacher statistics and two
+its MFMA work per step is 6 Nv V Dt + 10 Nv V Ds (teacher statistics and two
 probability passes; student statistics, Q pass, G recompute, dW and dH).
+``kd_fused`` runs the same step as one lce_kd_forward_backward call: 4 Nv V Dt
++ 8 Nv V Ds (one teacher probability pass, one student pass for G and Q).
 """
 from __future__ import annotations
 
@@ -112,7 +114,7 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--variant", default="lce",
-                    choices=("lce", "adamw_fused", "adamw_two_phase", "vocab_shard", "kd"))
+                    choices=("lce", "adamw_fused", "adamw_two_phase", "vocab_shard", "kd", "kd_fused"))
     ap.add_argument("--shards", type=int, default=8, help="vocabulary shards (vocab_shard variant)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a 1 GiB device copy (for scaling HBM byte counters)")
@@ -125,8 +127,8 @@ def main():
               f"multi-GPU mode", file=sys.stderr)
         sys.exit(2)
 
-    if args.variant == "kd":
-        bench_kd(args)
+    if args.variant in ("kd", "kd_fused"):
+        bench_kd(args, fused=args.variant == "kd_fused")
         return
 
     import torch
@@ -318,8 +320,9 @@ def _kd_cpu_baseline(inp, temperature, seconds_target=10.0):
                       f"forward+backward ({dt:.1f} s)"}
 
 
-def bench_kd(args):
-    """The KD variant: one step = lce_kd_forward + lce_kd_backward on the 8B-to-1B heads."""
+def bench_kd(args, fused=False):
+    """The KD variants: one step = lce_kd_forward + lce_kd_backward (or one lce_kd_forward_backward)
+    on the 8B-to-1B heads."""
     import torch
     from paper_2605_21442_amd import binding as B
     from paper_2605_21442_amd import workloads as WL
@@ -334,6 +337,8 @@ def bench_kd(args):
     t = torch.from_numpy(inp.targets).to(dev)
     p = B.kd_problem(n, ds, dt, v, temperature=T, ignore_index=inp.ignore_index)
     fwd_bytes, bwd_bytes = B.lce_kd_workspace_size(p)
+    if fused:
+        fwd_bytes = bwd_bytes = B.lce_kd_workspace_size_fused(p)
     torch.cuda.synchronize()
     torch.cuda.reset_peak_memory_stats()
     loss = torch.empty((), dtype=torch.float32, device=dev)
@@ -348,6 +353,12 @@ def bench_kd(args):
     stream = torch.cuda.current_stream(dev).cuda_stream
 
     def step():
+        if fused:
+            B.lce_kd_forward_backward(p, hs.data_ptr(), ws.data_ptr(), ht.data_ptr(), wt.data_ptr(), t.data_ptr(),
+                                      grad.data_ptr(), loss.data_ptr(), lse_s.data_ptr(), lse_t.data_ptr(),
+                                      nv.data_ptr(), status.data_ptr(), dh.data_ptr(), dw.data_ptr(), wsp.data_ptr(),
+                                      fwd_bytes, stream)
+            return
         B.lce_kd_forward(p, hs.data_ptr(), ws.data_ptr(), ht.data_ptr(), wt.data_ptr(), t.data_ptr(),
                          loss.data_ptr(), lse_s.data_ptr(), lse_t.data_ptr(), nv.data_ptr(), status.data_ptr(),
                          wsp.data_ptr(), fwd_bytes, stream)
@@ -375,9 +386,10 @@ def bench_kd(args):
     B.lce_timing_enable(False)
     nvalid = int(nv.item())
     # MFMA work per step and kernel (see the module docstring)
-    work = {"fwd_stats": 2.0 * nvalid * v * (ds + dt), "kd_teacher_p": 4.0 * nvalid * v * dt,
-            "kd_q": 2.0 * nvalid * v * ds, "bwd_g": 2.0 * nvalid * v * ds, "bwd_dw": 2.0 * nvalid * v * ds,
-            "bwd_dh": 2.0 * nvalid * v * ds}
+    work = {"fwd_stats": 2.0 * nvalid * v * (ds + dt), "kd_teacher_p": (2.0 if fused else 4.0) * nvalid * v * dt,
+            "bwd_g": 2.0 * nvalid * v * ds, "bwd_dw": 2.0 * nvalid * v * ds, "bwd_dh": 2.0 * nvalid * v * ds}
+    if not fused:
+        work["kd_q"] = 2.0 * nvalid * v * ds
     flops_step = sum(work.values())
     ms_step = elapsed * 1e3 / args.steps
     for kname, r in sorted(kernels.items(), key=lambda kv: -kv[1]["total_ms"]):
@@ -396,7 +408,7 @@ def bench_kd(args):
         "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": name, "n_tokens": n, "student_hidden": ds, "teacher_hidden": dt, "vocab": v,
                    "n_valid": nvalid, "temperature": T, "parallelism": "none", "reduction": "mean",
-                   "variant": "kd"},
+                   "variant": "kd_fused" if fused else "kd"},
         "valid_tokens_per_s": nvalid * args.steps / elapsed,
         "mfma_frac_step": flops_step / (ms_step * 1e-3) / (PEAK_BF16_TFLOPS * 1e12),
         "peak_hbm_bytes": int(peak), "workspace_bytes": int(max(fwd_bytes, bwd_bytes)),

@@ -288,6 +288,22 @@ lce_status_t lce_kd_backward(const lce_kd_problem_t* p,
                              const int32_t* n_valid, const float* grad_loss, void* dHs, void* dWs,
                              void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * KD forward and backward in one call, for the usual case where the KD loss is the objective
+ * being differentiated: grad_loss is read on the device when the gradient kernels run. The
+ * teacher's probabilities are formed once per slab (not once in the forward and again in the
+ * backward) and one student pass per slab yields both G and the loss's partial sums, so the MFMA
+ * work is 4 Nv V Dt + 8 Nv V Ds instead of 6 Nv V Dt + 10 Nv V Ds. Outputs are those of
+ * lce_kd_forward and lce_kd_backward, bit for bit. Workspace: lce_kd_workspace_size_fused.
+ */
+lce_status_t lce_kd_workspace_size_fused(const lce_kd_problem_t* p, size_t* bytes);
+lce_status_t lce_kd_forward_backward(const lce_kd_problem_t* p,
+                                     const void* Hs, const void* Ws, const void* Ht, const void* Wt,
+                                     const void* targets, const float* grad_loss,
+                                     float* loss, float* lse_s, float* lse_t,
+                                     int32_t* n_valid, int32_t* dev_status, void* dHs, void* dWs,
+                                     void* workspace, size_t workspace_bytes, void* stream);
+
 /* Static, human-readable name of a status code. */
 const char* lce_status_string(lce_status_t s);
 

@@ -365,6 +365,32 @@ def kd_backward(hs, ws, ht, wt, targets, lse_s, lse_t, n_valid, grad_loss, tempe
     return dh, dw
 
 
+def kd_forward_backward(hs, ws, ht, wt, targets, grad_loss, temperature: float = 1.0, ignore_index: int = -100,
+                        reduction: str = "mean"):
+    """(loss, lse_s, lse_t, n_valid, status, dHs, dWs) from lce_kd_forward_backward: the KD loss
+    and the student's gradients in one call, ``grad_loss`` being the upstream gradient."""
+    p, h_s, w_s, h_t, w_t, t = _kd_problem(hs, ws, ht, wt, targets, temperature, ignore_index, reduction)
+    n, ds, v = p.n, p.ds, p.v
+    want = n if reduction == "none" else 1
+    if grad_loss.dtype != torch.float32 or grad_loss.numel() != want or not grad_loss.is_cuda:
+        raise ValueError(f"grad_loss must be a {want}-element float32 GPU tensor")
+    g = grad_loss.contiguous()
+    nbytes = B.lce_kd_workspace_size_fused(p)
+    dev = h_s.device
+    loss = torch.empty((n,) if reduction == "none" else (), dtype=torch.float32, device=dev)
+    lse_s = torch.empty(n, dtype=torch.float32, device=dev)
+    lse_t = torch.empty(n, dtype=torch.float32, device=dev)
+    nv = torch.empty(1, dtype=torch.int32, device=dev)
+    status = torch.empty(1, dtype=torch.int32, device=dev)
+    dh = torch.empty((n, ds), dtype=torch.bfloat16, device=dev)
+    dw = torch.empty((v, ds), dtype=torch.bfloat16, device=dev)
+    ws_ = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
+    B.lce_kd_forward_backward(p, h_s.data_ptr(), w_s.data_ptr(), h_t.data_ptr(), w_t.data_ptr(), t.data_ptr(),
+                              g.data_ptr(), loss.data_ptr(), lse_s.data_ptr(), lse_t.data_ptr(), nv.data_ptr(),
+                              status.data_ptr(), dh.data_ptr(), dw.data_ptr(), ws_.data_ptr(), nbytes, _stream(dev))
+    return loss, lse_s, lse_t, nv, status, dh, dw
+
+
 class LinearKD(torch.autograd.Function):
     """Soft-target cross-entropy of a student head against a teacher head; gradients for the
     student's hidden states and weight only."""

@@ -37,7 +37,7 @@ EXPORTED = ("lce_workspace_size", "lce_forward", "lce_backward", "lce_status_str
             "lce_timing_enable", "lce_timing_kernel_count", "lce_timing_kernel_name",
             "lce_timing_read", "lce_adamw_step", "lce_backward_adamw", "lce_forward_shard",
             "lce_combine_shards", "lce_backward_shard", "lce_kd_workspace_size", "lce_kd_forward",
-            "lce_kd_backward")
+            "lce_kd_backward", "lce_kd_workspace_size_fused", "lce_kd_forward_backward")
 
 
 class LceError(RuntimeError):
@@ -119,6 +119,8 @@ def load() -> ctypes.CDLL:
         lib.lce_kd_workspace_size.argtypes = [KP, ctypes.POINTER(sz), ctypes.POINTER(sz)]
         lib.lce_kd_forward.argtypes = [KP, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
         lib.lce_kd_backward.argtypes = [KP, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+        lib.lce_kd_workspace_size_fused.argtypes = [KP, ctypes.POINTER(sz)]
+        lib.lce_kd_forward_backward.argtypes = [KP, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
         lib.lce_status_string.argtypes = [ctypes.c_int]
         lib.lce_status_string.restype = ctypes.c_char_p
         lib.lce_timing_enable.argtypes = [ctypes.c_int]
@@ -130,7 +132,7 @@ def load() -> ctypes.CDLL:
         for name in ("lce_workspace_size", "lce_forward", "lce_backward", "lce_timing_enable",
                      "lce_timing_read", "lce_timing_kernel_count", "lce_adamw_step", "lce_backward_adamw",
                      "lce_forward_shard", "lce_combine_shards", "lce_backward_shard", "lce_kd_workspace_size",
-                     "lce_kd_forward", "lce_kd_backward"):
+                     "lce_kd_forward", "lce_kd_backward", "lce_kd_workspace_size_fused", "lce_kd_forward_backward"):
             getattr(lib, name).restype = ctypes.c_int
         _lib = lib
         return lib
@@ -220,6 +222,20 @@ def lce_kd_backward(p: LceKdProblem, Hs: int, Ws: int, Ht: int, Wt: int, targets
                     stream: int) -> None:
     _check(load().lce_kd_backward(ctypes.byref(p), Hs, Ws, Ht, Wt, targets, lse_s, lse_t, n_valid, grad_loss,
                                   dHs, dWs, workspace, workspace_bytes, stream or None), "lce_kd_backward")
+
+
+def lce_kd_workspace_size_fused(p: LceKdProblem) -> int:
+    b = ctypes.c_size_t(0)
+    _check(load().lce_kd_workspace_size_fused(ctypes.byref(p), ctypes.byref(b)), "lce_kd_workspace_size_fused")
+    return b.value
+
+
+def lce_kd_forward_backward(p: LceKdProblem, Hs: int, Ws: int, Ht: int, Wt: int, targets: int, grad_loss: int,
+                            loss: int, lse_s: int, lse_t: int, n_valid: int, dev_status: int, dHs: int, dWs: int,
+                            workspace: int, workspace_bytes: int, stream: int) -> None:
+    _check(load().lce_kd_forward_backward(ctypes.byref(p), Hs, Ws, Ht, Wt, targets, grad_loss, loss, lse_s, lse_t,
+                                          n_valid, dev_status or None, dHs, dWs, workspace, workspace_bytes,
+                                          stream or None), "lce_kd_forward_backward")
 
 
 def lce_timing_enable(on: bool) -> None:

@@ -653,8 +653,9 @@ __device__ __forceinline__ float grad_scale(const float* grad, const int* n_norm
 //   G_SOFT    KD student: G = c (softmax(z/T) - P) / T, P the teacher's probabilities of this slab
 //   Q_SOFT    KD student forward: per token, sum over the tile's ids of P * z / T (partials qpart)
 //   P_WRITE   KD teacher: P = softmax(z/T) of this slab, fp32, P[v][token] (row stride ldt)
+//   G_SOFT_Q  KD student, forward and backward in one pass: G_SOFT and Q_SOFT together
 // scale2 = log2(e) / T (log2(e) for LCE), inv_t = 1 / T; lse is that of the scaled logits.
-enum GMode { G_ONEHOT = 0, G_SOFT = 1, Q_SOFT = 2, P_WRITE = 3 };
+enum GMode { G_ONEHOT = 0, G_SOFT = 1, Q_SOFT = 2, P_WRITE = 3, G_SOFT_Q = 4 };
 
 template <int kMode>
 __global__ __launch_bounds__(NTHREADS, 2) void k_bwd_g(const uint16_t* __restrict__ W, int64_t ldw, int64_t v0, int vs,
@@ -743,6 +744,7 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_bwd_g(const uint16_t* __restric
   // T[token][v], 512-byte rows whose 16-byte chunk c sits at c ^ (token & 31), so that both the
   // token-major rows of G and the vocabulary-major rows of Gt leave with wide coalesced stores.
   char* T = smem;
+  float qs[2] = {0.f, 0.f};
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
     const bool tok_ok = tok[j] < nv;
@@ -750,7 +752,7 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_bwd_g(const uint16_t* __restric
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       float pt[16];
-      if constexpr (kMode == G_SOFT) {
+      if constexpr (kMode == G_SOFT || kMode == G_SOFT_Q) {
         // the block's 16 teacher probabilities are loaded together, then used
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
@@ -768,8 +770,9 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_bwd_g(const uint16_t* __restric
           float g = 0.f;
           if (tok_ok && vr < vleft) {
             const float e2 = __builtin_amdgcn_exp2f(fmaf(acc[i][j][r], scale2, -l2[j]));
-            if constexpr (kMode == G_SOFT) {
+            if constexpr (kMode == G_SOFT || kMode == G_SOFT_Q) {
               g = cj[j] * inv_t * (e2 - pt[r]);
+              if constexpr (kMode == G_SOFT_Q) qs[j] = fmaf(pt[r], acc[i][j][r] * inv_t, qs[j]);
             } else {
               g = cj[j] * e2;
               if (vr == tgt[j]) g -= cj[j];
@@ -784,6 +787,13 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_bwd_g(const uint16_t* __restric
         const uint32_t a = (uint32_t)(nl * 512 + ((((vl >> 3) ^ (nl & 31))) << 4) + ((vl & 7) << 1));
         *reinterpret_cast<u32x2_t*>(T + a) = pk;
       }
+    }
+  }
+  if constexpr (kMode == G_SOFT_Q) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      qs[j] += __shfl_xor(qs[j], 32);
+      if (lane < 32 && tok[j] < nv) qpart[(qrow + 2 * tm + wr) * ldt + tok[j]] = qs[j];
     }
   }
   __syncthreads();
@@ -1267,6 +1277,7 @@ struct KdArgs {
   int dt;
   const float* lse_t;
   float scale2, inv_t;
+  float* qpart;   // non-null: the student pass also writes the loss's Q partials (fused KD call)
 };
 
 inline size_t kd_p_bytes(const Plan& pl) { return (size_t)4 * pl.vc * pl.npad; }
@@ -1340,10 +1351,16 @@ lce_status_t backward_impl(const lce_problem_t* p, const ShardInfo* shard, const
         kd->ht, kd->ldht, pl.n, targets, p->target_bytes, (int64_t)0, (const int*)idx, (const int*)nv, kd->lse_t,
         grad_loss, (const int*)n_valid, p->reduction, kd->dt, tm, (uint16_t*)nullptr, vc, (uint16_t*)nullptr, npad,
         kd->scale2, kd->inv_t, P, (float*)nullptr, (int64_t)0);
-      L(K_BWD_G, k_bwd_g<G_SOFT>, dim3((unsigned)(tm * pl.nt_max)), dim3(NTHREADS), w, pl.ldw, v0, vs, h, pl.ldh,
-        pl.n, targets, p->target_bytes, (int64_t)0, (const int*)idx, (const int*)nv, lse, grad_loss,
-        (const int*)n_valid, p->reduction, d, tm, g, vc, gt, npad, kd->scale2, kd->inv_t, P, (float*)nullptr,
-        (int64_t)0);
+      if (kd->qpart)
+        L(K_BWD_G, k_bwd_g<G_SOFT_Q>, dim3((unsigned)(tm * pl.nt_max)), dim3(NTHREADS), w, pl.ldw, v0, vs, h,
+          pl.ldh, pl.n, targets, p->target_bytes, (int64_t)0, (const int*)idx, (const int*)nv, lse, grad_loss,
+          (const int*)n_valid, p->reduction, d, tm, g, vc, gt, npad, kd->scale2, kd->inv_t, P, kd->qpart,
+          (int64_t)(2 * (v0 / TILE)));
+      else
+        L(K_BWD_G, k_bwd_g<G_SOFT>, dim3((unsigned)(tm * pl.nt_max)), dim3(NTHREADS), w, pl.ldw, v0, vs, h,
+          pl.ldh, pl.n, targets, p->target_bytes, (int64_t)0, (const int*)idx, (const int*)nv, lse, grad_loss,
+          (const int*)n_valid, p->reduction, d, tm, g, vc, gt, npad, kd->scale2, kd->inv_t, P, (float*)nullptr,
+          (int64_t)0);
     } else {
       L(K_BWD_G, k_bwd_g<G_ONEHOT>, dim3((unsigned)(tm * pl.nt_max)), dim3(NTHREADS), w, pl.ldw, v0, vs, h, pl.ldh,
         pl.n, targets, p->target_bytes, si.v_begin, (const int*)idx, (const int*)nv, lse, grad_loss,
@@ -1367,6 +1384,7 @@ struct KdPlan {
   Plan s, t;
   float scale2, inv_t;
   size_t o_tgt, o_q, o_p, fwd_bytes, bwd_bytes;
+  size_t f_q, f_tgt, fused_bytes;   // fused call: backward regions, P, then Q partials and scratch
 };
 
 lce_status_t make_kd_plan(const lce_kd_problem_t* p, KdPlan* k) {
@@ -1393,7 +1411,84 @@ lce_status_t make_kd_plan(const lce_kd_problem_t* p, KdPlan* k) {
   cur += up(kd_p_bytes(k->s));
   k->fwd_bytes = cur;
   k->bwd_bytes = k->s.bwd_bytes + kd_p_bytes(k->s);
+  cur = up(k->bwd_bytes);
+  k->f_q = cur;
+  cur += up((size_t)4 * 2 * k->s.vt_count * k->s.npad);
+  k->f_tgt = cur;
+  cur += up(4 * (size_t)k->s.npad);
+  k->fused_bytes = cur;
   return LCE_OK;
+}
+
+// Forward and backward of the KD loss in one call (the upstream gradient is read on the device
+// when the gradient kernels run): both heads' statistics, then per slab one teacher pass and one
+// student pass that writes G and the loss's Q partials together.
+lce_status_t kd_fused_impl(const lce_kd_problem_t* p, const void* Hs, const void* Ws, const void* Ht,
+                           const void* Wt, const void* targets, const float* grad_loss, float* loss, float* lse_s,
+                           float* lse_t, int32_t* n_valid, int32_t* dev_status, void* dHs, void* dWs,
+                           void* workspace, size_t workspace_bytes, void* stream) {
+  KdPlan k;
+  lce_status_t st = make_kd_plan(p, &k);
+  if (st != LCE_OK) return st;
+  const Plan& pl = k.s;
+  if (!loss || !n_valid || !grad_loss || !dWs) return LCE_ERR_NULL;
+  if (!aligned16(dWs)) return LCE_ERR_ALIGN;
+  if (pl.n > 0 && (!Hs || !Ws || !Ht || !Wt || !targets || !lse_s || !lse_t || !dHs || !workspace))
+    return LCE_ERR_NULL;
+  if (pl.n > 0 && (!aligned16(Hs) || !aligned16(Ws) || !aligned16(Ht) || !aligned16(Wt) || !aligned16(dHs) ||
+                   ((uintptr_t)workspace & 255) != 0))
+    return LCE_ERR_ALIGN;
+  if (pl.n > 0 && workspace_bytes < k.fused_bytes) return LCE_ERR_WORKSPACE;
+  const bool none = p->reduction == LCE_REDUCE_NONE;
+  if (pl.n == 0) {
+    Launcher L{(hipStream_t)stream};
+    L(K_MISC, k_fwd_empty, dim3(1), dim3(64), none ? (float*)nullptr : loss, n_valid, dev_status);
+    if (L.st != LCE_OK) return L.st;
+    return backward_impl(&k.ps, nullptr, Hs, Ws, targets, lse_s, n_valid, grad_loss, dHs, nullptr,
+                         (uint16_t*)dWs, nullptr, nullptr, workspace, workspace_bytes, stream);
+  }
+  char* ws = (char*)workspace;
+  int* idx = (int*)(ws + pl.o_idx);
+  int* pos = (int*)(ws + pl.o_pos);
+  int* nv = (int*)(ws + pl.o_nv);
+  float* pm = (float*)(ws + pl.o_pm);
+  float* ps = (float*)(ws + pl.o_ps);
+  float* tgt = (float*)(ws + k.f_tgt);
+  float* qpart = (float*)(ws + k.f_q);
+  const uint16_t* hs = (const uint16_t*)Hs;
+  const uint16_t* wsm = (const uint16_t*)Ws;
+  const uint16_t* ht = (const uint16_t*)Ht;
+  const uint16_t* wt = (const uint16_t*)Wt;
+  const Plan& tp = k.t;
+  const int npad = (int)pl.npad;
+  {
+    Launcher L{(hipStream_t)stream};
+    L(K_COMPACT, k_compact, dim3(1), dim3(1024), targets, p->target_bytes, pl.n, pl.v, p->ignore_index,
+      idx, pos, nv, n_valid, dev_status, lse_s, lse_t);
+    L(K_FWD_STATS, k_fwd_stats, dim3(tp.nt_max * tp.nparts), dim3(NTHREADS), wt, tp.ldw, (int)tp.v, ht, tp.ldh,
+      tp.n, (const int*)idx, (const int*)nv, (int)tp.d, tp.nparts, tp.nt_max, tp.vt_count, pm, ps, npad, k.scale2);
+    L(K_COMBINE, k_combine, dim3((unsigned)((pl.n + 3) / 4)), dim3(256), ht, tp.ldh, wt, tp.ldw, targets,
+      p->target_bytes, (int64_t)0, (int64_t)0, (const int*)idx, (const int*)nv, (int)tp.d, 2 * tp.nparts,
+      (const float*)pm, (const float*)ps, npad, lse_t, (float*)nullptr, (float*)nullptr, tgt);
+    L(K_FWD_STATS, k_fwd_stats, dim3(pl.nt_max * pl.nparts), dim3(NTHREADS), wsm, pl.ldw, (int)pl.v, hs, pl.ldh,
+      pl.n, (const int*)idx, (const int*)nv, (int)pl.d, pl.nparts, pl.nt_max, pl.vt_count, pm, ps, npad, k.scale2);
+    L(K_COMBINE, k_combine, dim3((unsigned)((pl.n + 3) / 4)), dim3(256), hs, pl.ldh, wsm, pl.ldw, targets,
+      p->target_bytes, (int64_t)0, (int64_t)0, (const int*)idx, (const int*)nv, (int)pl.d, 2 * pl.nparts,
+      (const float*)pm, (const float*)ps, npad, lse_s, (float*)nullptr, (float*)nullptr, tgt);
+    if (L.st != LCE_OK) return L.st;
+  }
+  const KdArgs kd{ht, tp.ldh, wt, tp.ldw, (int)tp.d, lse_t, k.scale2, k.inv_t, qpart};
+  st = backward_impl(&k.ps, nullptr, Hs, Ws, targets, lse_s, n_valid, grad_loss, dHs, nullptr, (uint16_t*)dWs,
+                     nullptr, nullptr, workspace, workspace_bytes, stream, &kd);
+  if (st != LCE_OK) return st;
+  // the backward's workspace (idx, pos, Nv) is still valid; the per-token terms reuse the
+  // student-statistics region, free again
+  Launcher L{(hipStream_t)stream};
+  float* terms = (float*)(ws + pl.o_terms);
+  L(K_KD_TERMS, k_kd_terms, dim3((unsigned)((pl.n + 255) / 256)), dim3(256), (const float*)qpart,
+    2 * pl.vt_count, (int64_t)npad, (const int*)pos, pl.n, (const float*)lse_s, terms, none ? loss : (float*)nullptr);
+  if (!none) L(K_LOSS, k_loss, dim3(1), dim3(1024), (const float*)terms, (const int*)nv, p->reduction, loss);
+  return L.st;
 }
 
 lce_status_t kd_forward_impl(const lce_kd_problem_t* p, const void* Hs, const void* Ws, const void* Ht,
@@ -1615,6 +1710,22 @@ lce_status_t lce_kd_forward(const lce_kd_problem_t* p, const void* Hs, const voi
                          workspace_bytes, stream);
 }
 
+lce_status_t lce_kd_forward_backward(const lce_kd_problem_t* p, const void* Hs, const void* Ws, const void* Ht,
+                                     const void* Wt, const void* targets, const float* grad_loss, float* loss,
+                                     float* lse_s, float* lse_t, int32_t* n_valid, int32_t* dev_status, void* dHs,
+                                     void* dWs, void* workspace, size_t workspace_bytes, void* stream) {
+  return kd_fused_impl(p, Hs, Ws, Ht, Wt, targets, grad_loss, loss, lse_s, lse_t, n_valid, dev_status, dHs, dWs,
+                       workspace, workspace_bytes, stream);
+}
+
+lce_status_t lce_kd_workspace_size_fused(const lce_kd_problem_t* p, size_t* bytes) {
+  KdPlan k;
+  lce_status_t st = make_kd_plan(p, &k);
+  if (st != LCE_OK) return st;
+  if (bytes) *bytes = k.fused_bytes;
+  return LCE_OK;
+}
+
 lce_status_t lce_kd_backward(const lce_kd_problem_t* p, const void* Hs, const void* Ws, const void* Ht,
                              const void* Wt, const void* targets, const float* lse_s, const float* lse_t,
                              const int32_t* n_valid, const float* grad_loss, void* dHs, void* dWs,
@@ -1626,7 +1737,8 @@ lce_status_t lce_kd_backward(const lce_kd_problem_t* p, const void* Hs, const vo
   if (!aligned16(dWs)) return LCE_ERR_ALIGN;
   if (p->n > 0 && (!Ht || !Wt || !lse_t)) return LCE_ERR_NULL;
   if (p->n > 0 && (!aligned16(Ht) || !aligned16(Wt))) return LCE_ERR_ALIGN;
-  const KdArgs kd{(const uint16_t*)Ht, k.t.ldh, (const uint16_t*)Wt, k.t.ldw, (int)k.t.d, lse_t, k.scale2, k.inv_t};
+  const KdArgs kd{(const uint16_t*)Ht, k.t.ldh, (const uint16_t*)Wt, k.t.ldw, (int)k.t.d, lse_t, k.scale2, k.inv_t,
+                  nullptr};
   return backward_impl(&k.ps, nullptr, Hs, Ws, targets, lse_s, n_valid, grad_loss, dHs, nullptr, (uint16_t*)dWs,
                        nullptr, nullptr, workspace, workspace_bytes, stream, &kd);
 }

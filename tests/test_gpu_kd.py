@@ -120,3 +120,33 @@ def test_kd_autograd_function():
     assert abs(loss.item() - ref["loss"]) <= U.LOSS_ABS_TOL
     assert U.rel_fro(hs.grad.view(300, 96).float().cpu().numpy(), ref["dHs"]) <= U.GRAD_REL_TOL
     assert U.rel_fro(ws.grad.float().cpu().numpy(), ref["dWs"]) <= U.GRAD_REL_TOL
+
+
+@pytest.mark.parametrize("n,ds,dt,v,reduction", [(600, 128, 256, 9000, "mean"), (300, 264, 136, 1000, "none"),
+                                                 (1, 8, 16, 5, "sum"), (40, 16, 32, 300, "mean")])
+def test_fused_forward_backward_is_bitwise_the_two_calls(n, ds, dt, v, reduction):
+    import torch
+    from paper_2605_21442_amd import autograd as AG
+    inp = WL.kd_custom(n, ds, dt, v, seed=n + 1, mask_frac=0.2)
+    hs, ws, ht, wt = (_dev(x) for x in (inp.hs_bits, inp.ws_bits, inp.ht_bits, inp.wt_bits))
+    t = torch.from_numpy(inp.targets).to("cuda:0")
+    g = torch.from_numpy(np.random.default_rng(n).standard_normal(n if reduction == "none" else 1)
+                         .astype(np.float32)).to("cuda:0")
+    loss, lse_s, lse_t, nv, _ = AG.kd_forward(hs, ws, ht, wt, t, 1.5, -100, reduction)
+    dh, dw = AG.kd_backward(hs, ws, ht, wt, t, lse_s, lse_t, nv, g, 1.5, -100, reduction)
+    f = AG.kd_forward_backward(hs, ws, ht, wt, t, g, 1.5, -100, reduction)
+    torch.cuda.synchronize()
+    for a, b in ((loss, f[0]), (lse_s, f[1]), (lse_t, f[2]), (nv, f[3]), (dh, f[5]), (dw, f[6])):
+        assert torch.equal(a.view(-1).view(torch.int8) if a.dtype != torch.int32 else a,
+                           b.view(-1).view(torch.int8) if b.dtype != torch.int32 else b)
+
+
+def test_fused_without_tokens():
+    import torch
+    from paper_2605_21442_amd import autograd as AG
+    inp = WL.kd_custom(0, 32, 48, 300, seed=1, target_override=np.zeros(0, np.int32))
+    hs, ws, ht, wt = (_dev(x) for x in (inp.hs_bits, inp.ws_bits, inp.ht_bits, inp.wt_bits))
+    t = torch.from_numpy(inp.targets).to("cuda:0")
+    f = AG.kd_forward_backward(hs, ws, ht, wt, t, torch.ones(1, device="cuda:0"))
+    torch.cuda.synchronize()
+    assert float(f[0].item()) == 0.0 and int(f[3].item()) == 0 and not f[6].float().abs().sum().item()
