@@ -168,3 +168,17 @@ def test_per_token_autograd_shape():
     assert np.max(np.abs(per.detach().view(-1).cpu().numpy() - ref["loss"])) <= U.LSE_ABS_TOL
     assert U.rel_fro(h3.grad.view(300, 96).float().cpu().numpy(), ref["dH"]) <= U.GRAD_REL_TOL
     assert U.rel_fro(w1.grad.float().cpu().numpy(), ref["dW"]) <= U.GRAD_REL_TOL
+
+
+@pytest.mark.parametrize("case", range(12))
+def test_random_shapes_sweep(case):
+    """Seeded random shapes across tile, slab and partition boundaries (D multiple of 8)."""
+    rng = np.random.default_rng(1000 + case)
+    n = int(rng.integers(1, 900))
+    d = int(rng.integers(1, 80)) * 8
+    v = int(rng.choice([int(rng.integers(1, 600)), int(rng.integers(8000, 17000))]))
+    reduction = ["mean", "sum", "none"][case % 3]
+    grad = (rng.standard_normal(n).astype(np.float32) if reduction == "none" else float(rng.uniform(0.2, 2.0)))
+    inp = WL.custom(n, d, v, seed=case, mask_frac=float(rng.uniform(0, 0.5)), sigma_w=0.3)
+    print(f"sweep case {case}: n={n} d={d} v={v} {reduction}", flush=True)
+    _case(inp, reduction=reduction, grad=grad)
