@@ -14,6 +14,10 @@
 //   backward: compact -> gather/transpose H_valid -> per vocabulary slab:
 //             transpose W slab, G tile (recompute S^T, G = c (softmax - onehot)),
 //             dW slab = G^T H_valid, dH32 (+)= G W_slab -> finalise dH
+// Built on the same kernels: the backward with an AdamW step on each finished dW block
+// (paper Sec. 4.1), a vocabulary-shard (loss-parallel) forward / combine / backward, and a
+// fused linear knowledge-distillation loss whose G kernel takes the teacher's probabilities
+// as soft targets.
 //
 // Every contraction is a "both operands K-contiguous" product C = A B^T run by
 // one MFMA main loop: 256x256 output tiles, 8 waves of 128x64, bf16
@@ -915,7 +919,7 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_bwd_dw(const uint16_t* __restri
 // K6: dH32[m][dd] (+)= sum_k G[m][k] WsT[dd][k] over k < round_up(vs, 64); rows m < Nv.
 __global__ __launch_bounds__(NTHREADS, 2) void k_bwd_dh(const uint16_t* __restrict__ G, int vc, int kpad,
                                                         const uint16_t* __restrict__ WsT, int d,
-                                                        const int* __restrict__ nv_ptr, int tm_count,
+                                                        const int* __restrict__ nv_ptr,
                                                         float* __restrict__ dH32, int accumulate) {
   __shared__ __attribute__((aligned(16))) char smem[LDS_BYTES];
   const int nv = *nv_ptr;
@@ -1370,7 +1374,7 @@ lce_status_t backward_impl(const lce_problem_t* p, const ShardInfo* shard, const
     L(K_BWD_DW, dw_kernel, dim3((unsigned)(8 * ((tm + 7) / 8) * dt)), dim3(NTHREADS), (const uint16_t*)gt, npad,
       vs, (const uint16_t*)hvt, d, (const int*)nv, tm, dW, v0, as, c);
     L(K_BWD_DH, k_bwd_dh, dim3((unsigned)(8 * ((pl.nt_max + 7) / 8) * dt)), dim3(NTHREADS), (const uint16_t*)g, vc, vs64,
-      (const uint16_t*)wst, d, (const int*)nv, pl.nt_max, dh32, (int)(s > 0));
+      (const uint16_t*)wst, d, (const int*)nv, dh32, (int)(s > 0));
   }
   const int64_t nthr = pl.n * pl.d / 8;
   L(K_DH_FINAL, k_dh_finalize, dim3((unsigned)((nthr + 255) / 256)), dim3(256), (const float*)dh32,
