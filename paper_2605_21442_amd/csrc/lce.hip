@@ -42,6 +42,7 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef int i32x4_t __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
 typedef short s16x4_t __attribute__((ext_vector_type(4)));
+typedef short s16x8_t __attribute__((ext_vector_type(8)));
 typedef __attribute__((address_space(3))) s16x4_t lds_s16x4_t;
 
 constexpr int TILE = 256;         // output tile edge (rows of A and of B per workgroup)
@@ -811,23 +812,30 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_bwd_g(const uint16_t* __restric
       *reinterpret_cast<i32x4_t*>(G + (int64_t)(n0 + nl) * vc + vt0 + ch * 8) = val;
     }
   }
-  // Gt rows (vocabulary rows < slab width): a transposing LDS read gives each lane 4 consecutive
-  // tokens of one vocabulary row. In a 16-lane group, lane i reads 8 bytes (4 vocabulary ids) of
-  // token row nb + 4 (i % 4) + i / 4; lane j receives vocabulary id vq + j % 4 of tokens
-  // nb + 4 (j / 4) .. +3. One wave instruction covers 4 vocabulary rows x 64 tokens.
+  // Gt rows (vocabulary rows < slab width): two transposing LDS reads give each lane 8 consecutive
+  // tokens of one vocabulary row, stored as one 16-byte chunk. In a 16-lane group, lane i reads 8
+  // bytes (4 vocabulary ids) of token row nb + 8 (i % 4) + i / 4 (and 4 rows further for the
+  // second read); lane j receives vocabulary id vq + j % 4 of tokens nb + 8 (j / 4) .. +7. One
+  // pair of wave instructions covers 4 vocabulary rows x 128 tokens.
   {
     const int grp = lane >> 4, i16 = lane & 15;
 #pragma unroll 4
-    for (int kk = 0; kk < 32; ++kk) {
-      const int item = wave * 32 + kk;
-      const int vq = (item >> 2) * 4;
-      const int nb = (item & 3) * 64 + grp * 16;
-      const int nl = nb + 4 * (i16 & 3) + (i16 >> 2);
-      const uint32_t a = (uint32_t)(nl * 512 + ((((vq >> 3) ^ (nl & 31))) << 4) + ((vq & 7) << 1));
-      const s16x4_t t4 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(T + a));
+    for (int kk = 0; kk < 16; ++kk) {
+      const int item = wave * 16 + kk;
+      const int vq = (item >> 1) * 4;
+      const int nb = (item & 1) * 128 + grp * 32;
+      const int nl = nb + 8 * (i16 & 3) + (i16 >> 2);
+      const uint32_t a0 = (uint32_t)(nl * 512 + ((((vq >> 3) ^ (nl & 31))) << 4) + ((vq & 7) << 1));
+      const uint32_t a1 = (uint32_t)((nl + 4) * 512 + ((((vq >> 3) ^ ((nl + 4) & 31))) << 4) + ((vq & 7) << 1));
+      const s16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(T + a0));
+      const s16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(T + a1));
       const int vrow = vq + (i16 & 3);
-      if (vrow < vleft)
-        *reinterpret_cast<s16x4_t*>(Gt + (int64_t)(vt0 + vrow) * ldt + n0 + nb + 4 * (i16 >> 2)) = t4;
+      if (vrow < vleft) {
+        s16x8_t t8;
+        t8.lo = lo;
+        t8.hi = hi;
+        *reinterpret_cast<s16x8_t*>(Gt + (int64_t)(vt0 + vrow) * ldt + n0 + nb + 8 * (i16 >> 2)) = t8;
+      }
     }
   }
 }
