@@ -1034,7 +1034,8 @@ __global__ __launch_bounds__(256) void k_adamw(int64_t v, int d, const uint16_t*
     const int64_t row = q / cpr;
     const int col = (int)(q - row * cpr) * 8;
     const int64_t o = row * d + col;
-    const i32x4_t wv = *reinterpret_cast<const i32x4_t*>(st.W + row * st.ldw + col);
+    i32x4_t wv = {0, 0, 0, 0};
+    if (!st.master) wv = *reinterpret_cast<const i32x4_t*>(st.W + row * st.ldw + col);
     i32x4_t gv = {0, 0, 0, 0};
     if (dW) gv = *reinterpret_cast<const i32x4_t*>(dW + o);
     float p[8], mo[8], vo[8];
@@ -1196,7 +1197,7 @@ lce_status_t make_adamw(const lce_adamw_t* o, AdamWConst* c) {
 unsigned adamw_grid(int64_t v, int64_t d) {
   const int64_t chunks = v * (d / 8);
   const int64_t blocks = (chunks + 255) / 256;
-  return (unsigned)(blocks < 4096 ? blocks : 4096);
+  return (unsigned)(blocks < 16384 ? blocks : 16384);
 }
 
 struct Launcher {
