@@ -825,10 +825,16 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_bwd_g(const uint16_t* __restric
       const int vq = (item >> 1) * 4;
       const int nb = (item & 1) * 128 + grp * 32;
       const int nl = nb + 8 * (i16 & 3) + (i16 >> 2);
-      const uint32_t a0 = (uint32_t)(nl * 512 + ((((vq >> 3) ^ (nl & 31))) << 4) + ((vq & 7) << 1));
-      const uint32_t a1 = (uint32_t)((nl + 4) * 512 + ((((vq >> 3) ^ ((nl + 4) & 31))) << 4) + ((vq & 7) << 1));
-      const s16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(T + a0));
-      const s16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(T + a1));
+      // odd groups read their +4 rows first, so that each instruction's two groups of a half-wave
+      // touch 32 distinct token rows (mod 32) and hence distinct LDS banks
+      const int sw = (grp & 1) * 4;
+      const int r0 = nl + sw, r1 = nl + 4 - sw;
+      const uint32_t a0 = (uint32_t)(r0 * 512 + ((((vq >> 3) ^ (r0 & 31))) << 4) + ((vq & 7) << 1));
+      const uint32_t a1 = (uint32_t)(r1 * 512 + ((((vq >> 3) ^ (r1 & 31))) << 4) + ((vq & 7) << 1));
+      const s16x4_t x0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(T + a0));
+      const s16x4_t x1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(T + a1));
+      const s16x4_t lo = sw ? x1 : x0;
+      const s16x4_t hi = sw ? x0 : x1;
       const int vrow = vq + (i16 & 3);
       if (vrow < vleft) {
         s16x8_t t8;
