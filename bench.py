@@ -72,6 +72,33 @@ def _cpu_baseline(inp, seconds_target=10.0):
                       f"fp64 forward+backward ({dt:.1f} s)"}
 
 
+def _host_info():
+    """The host the CPU oracle ran on: CPU model, cores visible to this process, BLAS build."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            model = next((l.split(":", 1)[1].strip() for l in f if l.startswith("model name")), None)
+    except OSError:  # pragma: no cover
+        pass
+    try:
+        blas = np.show_config(mode="dicts")["Build Dependencies"]["blas"]
+        blas = f"{blas.get('name')} {blas.get('version')}"
+    except Exception:  # pragma: no cover
+        blas = None
+    return {"cpu_model": model, "affinity_cores": len(os.sched_getaffinity(0)), "os_cpu_count": os.cpu_count(),
+            "blas": blas}
+
+
+def _event_summary(events):
+    """Median / min step time and the median forward and backward parts, from per-step
+    (start, after forward, end) events recorded on the stream the step runs on."""
+    steps = [a.elapsed_time(c) for a, _, c in events]
+    fwd = [a.elapsed_time(b) for a, b, _ in events]
+    bwd = [b.elapsed_time(c) for _, b, c in events]
+    return {"median": float(np.median(steps)), "min": float(np.min(steps)),
+            "fwd_median": float(np.median(fwd)), "bwd_median": float(np.median(bwd))}
+
+
 def _copy_calibration(gib=1.0, reps=3):
     """A plain device copy of a known size, for scaling the HBM byte counters (FETCH_SIZE,
     WRITE_SIZE) of a profiled run: each copy reads and writes exactly `gib` GiB."""
@@ -190,7 +217,7 @@ def main():
         step_no[0] += 1
         return B.adamw(1e-5, 0.9, 0.95, 1e-8, 0.1, step_no[0])
 
-    def shard_step():
+    def shard_step(mid=None):
         B.lce_forward_shard(p, shard, h.data_ptr(), w.data_ptr(), t.data_ptr(), lse_part.data_ptr(),
                             tgt_part.data_ptr(), nv.data_ptr(), status.data_ptr(), ws.data_ptr(), fwd_bytes, stream)
         # stand-in for the all-gather of every shard's partials
@@ -199,15 +226,19 @@ def main():
         B.lce_combine_shards(p_full, args.shards, lse_parts.data_ptr(), tgt_parts.data_ptr(), t.data_ptr(),
                              loss.data_ptr(), lse.data_ptr(), nv.data_ptr(), status.data_ptr(), ws.data_ptr(),
                              fwd_bytes, stream)
+        if mid is not None:
+            mid.record()
         B.lce_backward_shard(p, shard, h.data_ptr(), w.data_ptr(), t.data_ptr(), lse.data_ptr(), nv.data_ptr(),
                              grad.data_ptr(), dh.data_ptr(), dw.data_ptr(), ws.data_ptr(), bwd_bytes, stream)
 
-    def step():
+    def step(mid=None):
         if sharded:
-            shard_step()
+            shard_step(mid)
             return
         B.lce_forward(p, h.data_ptr(), w.data_ptr(), t.data_ptr(), loss.data_ptr(), lse.data_ptr(),
                       nv.data_ptr(), status.data_ptr(), ws.data_ptr(), fwd_bytes, stream)
+        if mid is not None:
+            mid.record()
         if fused:
             B.lce_backward_adamw(p, h.data_ptr(), w.data_ptr(), t.data_ptr(), lse.data_ptr(), nv.data_ptr(),
                                  grad.data_ptr(), dh.data_ptr(), *opt_ptrs, adamw(), ws.data_ptr(), bwd_bytes,
@@ -230,10 +261,13 @@ def main():
         + (3 * v * d * 4 if opt_ptrs is not None else 0)
 
     B.lce_timing_enable(True)
+    events = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(3)) for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step()
+    for e0, e1, e2 in events:
+        e0.record()
+        step(e1)
+        e2.record()
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     names = B.lce_timing_kernel_names()
@@ -280,6 +314,9 @@ def main():
                    **({"shards": args.shards, "vocab_total": v_total} if sharded else {})},
         "valid_tokens_per_s": nvalid * args.steps / elapsed,
         "mfma_frac_step": flops_step / (ms_step * 1e-3) / (PEAK_BF16_TFLOPS * 1e12),
+        # the same step counted without the backward's recompute of the logits (6 Nv D V)
+        "mfma_frac_step_no_recompute": 0.75 * flops_step / (ms_step * 1e-3) / (PEAK_BF16_TFLOPS * 1e12),
+        "step_ms": _event_summary(events),
         "peak_hbm_bytes": int(peak),
         "peak_hbm_bytes_transient": int(peak - resident),
         "workspace_bytes": int(max(fwd_bytes, bwd_bytes)),
@@ -292,6 +329,7 @@ def main():
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a token sample ...", file=sys.stderr, flush=True)
         out["cpu_baseline"] = _cpu_baseline(inp)
+        out["host"] = _host_info()
     else:
         out["cpu_baseline"] = None
     print(json.dumps(out), flush=True)
@@ -352,7 +390,7 @@ def bench_kd(args, fused=False):
     wsp = torch.empty(max(fwd_bytes, bwd_bytes), dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream(dev).cuda_stream
 
-    def step():
+    def step(mid=None):
         if fused:
             B.lce_kd_forward_backward(p, hs.data_ptr(), ws.data_ptr(), ht.data_ptr(), wt.data_ptr(), t.data_ptr(),
                                       grad.data_ptr(), loss.data_ptr(), lse_s.data_ptr(), lse_t.data_ptr(),
@@ -362,6 +400,8 @@ def bench_kd(args, fused=False):
         B.lce_kd_forward(p, hs.data_ptr(), ws.data_ptr(), ht.data_ptr(), wt.data_ptr(), t.data_ptr(),
                          loss.data_ptr(), lse_s.data_ptr(), lse_t.data_ptr(), nv.data_ptr(), status.data_ptr(),
                          wsp.data_ptr(), fwd_bytes, stream)
+        if mid is not None:
+            mid.record()
         B.lce_kd_backward(p, hs.data_ptr(), ws.data_ptr(), ht.data_ptr(), wt.data_ptr(), t.data_ptr(),
                           lse_s.data_ptr(), lse_t.data_ptr(), nv.data_ptr(), grad.data_ptr(), dh.data_ptr(),
                           dw.data_ptr(), wsp.data_ptr(), bwd_bytes, stream)
@@ -372,10 +412,15 @@ def bench_kd(args, fused=False):
         print(f"[bench] kd warmup {i + 1}/{args.warmup} done", file=sys.stderr, flush=True)
     peak = torch.cuda.max_memory_allocated()
     B.lce_timing_enable(True)
+    events = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(3)) for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step()
+    for e0, e1, e2 in events:
+        e0.record()
+        step(e1)
+        if fused:           # one call: no forward / backward boundary to mark
+            e1.record()
+        e2.record()
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     kernels = {}
@@ -411,6 +456,7 @@ def bench_kd(args, fused=False):
                    "variant": "kd_fused" if fused else "kd"},
         "valid_tokens_per_s": nvalid * args.steps / elapsed,
         "mfma_frac_step": flops_step / (ms_step * 1e-3) / (PEAK_BF16_TFLOPS * 1e12),
+        "step_ms": _event_summary(events),
         "peak_hbm_bytes": int(peak), "workspace_bytes": int(max(fwd_bytes, bwd_bytes)),
         "logits_bytes_avoided_fp32": 2 * int(n) * int(v) * 4,
         "roofline": {"bound": "mfma", "kernel": dom, "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
@@ -419,6 +465,8 @@ def bench_kd(args, fused=False):
         "kernels_ms_per_step": {kk: r["total_ms"] / args.steps for kk, r in kernels.items()},
         "cpu_baseline": None if args.no_cpu_baseline else _kd_cpu_baseline(inp, T),
     }
+    if not args.no_cpu_baseline:
+        out["host"] = _host_info()
     print(json.dumps(out), flush=True)
 
 

@@ -33,6 +33,9 @@ def test_bench_prints_one_json_line_with_the_contract_fields(variant):
         assert k in d, k
     assert d["n_gpus"] == 1 and d["steps"] == 2 and d["warmup"] == 1 and d["value"] > 0
     assert "workload" in d["config"]
+    sm = d["step_ms"]
+    assert 0 < sm["min"] <= sm["median"] and sm["fwd_median"] > 0 and sm["bwd_median"] >= 0
+    assert abs(sm["median"] - d["ms_per_step"]) < 0.5 * d["ms_per_step"]
     rl = d["roofline"]
     assert rl["bound"] == "mfma" and rl["unit"] == "TFLOP/s" and 0 < rl["frac"] < 1
     assert abs(rl["frac"] - rl["achieved"] / rl["peak"]) < 1e-9

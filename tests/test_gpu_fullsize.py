@@ -240,3 +240,50 @@ def test_full_size_kd_8b_to_1b():
     got = dw[torch.from_numpy(ids).to(dev)].float().cpu().numpy().astype(np.float64)
     assert U.rel_fro(got, ref) <= U.GRAD_REL_TOL
     _say(f"[{name}] ok: loss {float(loss.item()):.6f} (oracle {float(gold['loss']):.6f})")
+
+
+def test_full_size_allocates_nothing_beyond_the_workspace():
+    """8B head: the library makes no allocation of its own (the driver's free memory is unchanged
+    across the calls), the caller-sized workspace stays below half a bf16 copy of the logits, and
+    no buffer of the path comes near the [N, V] size the method avoids."""
+    import torch
+    from paper_2605_21442_amd import binding as B
+    wl = WL.WORKLOADS["llama8b"]
+    inp = WL.generate(wl, 0)
+    h, w, t = U.to_device(inp)
+    dev = h.device
+    n, d, v = wl.n, wl.d, wl.v
+    p = B.problem(n, d, v, ignore_index=inp.ignore_index, reduction="mean", target_bytes=4)
+    fwd_bytes, bwd_bytes = B.lce_workspace_size(p)
+    ws = torch.empty(max(fwd_bytes, bwd_bytes), dtype=torch.uint8, device=dev)
+    loss = torch.empty((), dtype=torch.float32, device=dev)
+    lse = torch.empty(n, dtype=torch.float32, device=dev)
+    nv = torch.empty(1, dtype=torch.int32, device=dev)
+    status = torch.empty(1, dtype=torch.int32, device=dev)
+    grad = torch.ones(1, dtype=torch.float32, device=dev)
+    dh = torch.empty((n, d), dtype=torch.bfloat16, device=dev)
+    dw = torch.empty((v, d), dtype=torch.bfloat16, device=dev)
+    stream = torch.cuda.current_stream(dev).cuda_stream
+
+    def step():
+        B.lce_forward(p, h.data_ptr(), w.data_ptr(), t.data_ptr(), loss.data_ptr(), lse.data_ptr(),
+                      nv.data_ptr(), status.data_ptr(), ws.data_ptr(), fwd_bytes, stream)
+        B.lce_backward(p, h.data_ptr(), w.data_ptr(), t.data_ptr(), lse.data_ptr(), nv.data_ptr(),
+                       grad.data_ptr(), dh.data_ptr(), dw.data_ptr(), ws.data_ptr(), bwd_bytes, stream)
+
+    step()                                   # first call loads the code objects
+    torch.cuda.synchronize()
+    free0 = torch.cuda.mem_get_info(dev)[0]
+    alloc0 = torch.cuda.memory_allocated(dev)
+    torch.cuda.reset_peak_memory_stats(dev)
+    _say("[llama8b] second forward + backward, watching device memory")
+    step()
+    torch.cuda.synchronize()
+    free1 = torch.cuda.mem_get_info(dev)[0]
+    assert torch.cuda.max_memory_allocated(dev) == alloc0       # nothing through torch's allocator
+    assert abs(free1 - free0) <= (2 << 20), (free0, free1)      # nothing through the driver either
+    logits_bf16 = n * v * 2
+    assert max(fwd_bytes, bwd_bytes) < logits_bf16 // 2
+    for x in (h, w, dh, dw, ws):
+        assert x.numel() * x.element_size() < logits_bf16 // 2
+    assert int(nv.item()) == wl.n_valid() and int(status.item()) == 0
