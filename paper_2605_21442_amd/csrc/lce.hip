@@ -378,15 +378,20 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_fwd_stats(const uint16_t* __res
                                                            int npad, float scale2) {
   // scale2 = log2(e) / T: partials are kept in base-2 units of the logits divided by T
   __shared__ __attribute__((aligned(16))) char smem[LDS_BYTES];
-  // Workgroups are dispatched round-robin over the 8 XCDs (block b runs on XCD b % 8). Give each
-  // XCD whole vocabulary partitions (p = xcd + 8 i) and walk all token tiles of one partition
-  // before the next, so the workgroups resident on one XCD stream the same W tiles through that
-  // XCD's L2 at about the same time.
+  // Workgroups are dispatched round-robin over the 8 XCDs (block b runs on XCD b % 8). Each XCD
+  // owns whole vocabulary partitions (p = xcd + 8 k, k < ppx) and runs its workgroups in rounds of
+  // about 32 (one per CU): every round covers all ppx partitions for a group of 32 / ppx token
+  // tiles, so the resident workgroups share ppx W tiles and 32 / ppx H tiles through the XCD's L2
+  // (12 distinct tiles per 32 workgroups at ppx = 4, where one partition over 32 token tiles
+  // would stream 32 distinct H tiles). The last round takes the token tiles that are left.
   int nt, p;
   if (nparts % 8 == 0) {
     const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
-    p = xcd + 8 * (slot / nt_max);
-    nt = slot % nt_max;
+    const int ppx = nparts >> 3;
+    const int gn = ppx >= 32 ? 1 : 32 / ppx;
+    const int r = slot / (ppx * gn), rem = slot % (ppx * gn);
+    p = xcd + 8 * (rem % ppx);
+    nt = r * gn + rem / ppx;
   } else {
     nt = blockIdx.x % nt_max;
     p = blockIdx.x / nt_max;
@@ -748,6 +753,9 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_bwd_g(const uint16_t* __restric
   // G values in place, then the bf16 tile goes through LDS (free after the main loop) as
   // T[token][v], 512-byte rows whose 16-byte chunk c sits at c ^ (token & 31), so that both the
   // token-major rows of G and the vocabulary-major rows of Gt leave with wide coalesced stores.
+  // Within a chunk the two 8-byte halves (ids 0-3, 4-7) trade places in token rows with bit 4 set:
+  // the 32 lanes of a half-wave, which hold the same half of 32 consecutive token rows, then write
+  // (and the transposing reads below fetch) 32 distinct 8-byte bank slots.
   char* T = smem;
   float qs[2] = {0.f, 0.f};
 #pragma unroll
@@ -789,7 +797,8 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_bwd_g(const uint16_t* __restric
         u32x2_t pk;
         pk.x = pack_bf16x2(gq[0], gq[1]);
         pk.y = pack_bf16x2(gq[2], gq[3]);
-        const uint32_t a = (uint32_t)(nl * 512 + ((((vl >> 3) ^ (nl & 31))) << 4) + ((vl & 7) << 1));
+        const uint32_t a = (uint32_t)(nl * 512 + ((((vl >> 3) ^ (nl & 31))) << 4) +
+                                      ((((vl >> 2) & 1) ^ ((nl >> 4) & 1)) << 3));
         *reinterpret_cast<u32x2_t*>(T + a) = pk;
       }
     }
@@ -808,7 +817,8 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_bwd_g(const uint16_t* __restric
     const int q = threadIdx.x + NTHREADS * it;
     const int nl = q >> 5, ch = q & 31;
     if (n0 + nl < nv) {
-      const i32x4_t val = *reinterpret_cast<const i32x4_t*>(T + nl * 512 + ((ch ^ (nl & 31)) << 4));
+      i32x4_t val = *reinterpret_cast<const i32x4_t*>(T + nl * 512 + ((ch ^ (nl & 31)) << 4));
+      if (nl & 16) val = (i32x4_t){val.z, val.w, val.x, val.y};
       *reinterpret_cast<i32x4_t*>(G + (int64_t)(n0 + nl) * vc + vt0 + ch * 8) = val;
     }
   }
@@ -829,8 +839,10 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_bwd_g(const uint16_t* __restric
       // touch 32 distinct token rows (mod 32) and hence distinct LDS banks
       const int sw = (grp & 1) * 4;
       const int r0 = nl + sw, r1 = nl + 4 - sw;
-      const uint32_t a0 = (uint32_t)(r0 * 512 + ((((vq >> 3) ^ (r0 & 31))) << 4) + ((vq & 7) << 1));
-      const uint32_t a1 = (uint32_t)(r1 * 512 + ((((vq >> 3) ^ (r1 & 31))) << 4) + ((vq & 7) << 1));
+      const uint32_t a0 = (uint32_t)(r0 * 512 + ((((vq >> 3) ^ (r0 & 31))) << 4) +
+                                     ((((vq >> 2) & 1) ^ ((r0 >> 4) & 1)) << 3));
+      const uint32_t a1 = (uint32_t)(r1 * 512 + ((((vq >> 3) ^ (r1 & 31))) << 4) +
+                                     ((((vq >> 2) & 1) ^ ((r1 >> 4) & 1)) << 3));
       const s16x4_t x0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(T + a0));
       const s16x4_t x1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(T + a1));
       const s16x4_t lo = sw ? x1 : x0;
