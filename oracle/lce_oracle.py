@@ -121,8 +121,9 @@ def softmax_grad_rows(h_rows, w, t_rows, c):
     return (c[:, None] if c.ndim == 1 else c) * g
 
 
-def backward(h, w, targets, ignore_index=-100, reduction="mean", grad=1.0, block=512):
-    """dH = G W and dW = G^T H with G the scaled softmax-minus-onehot of the valid rows."""
+def backward(h, w, targets, ignore_index=-100, reduction="mean", grad=1.0, block=512, progress=None):
+    """dH = G W and dW = G^T H with G the scaled softmax-minus-onehot of the valid rows.
+    ``progress(done, total)``, if given, is called after each block of valid rows."""
     n, v = h.shape[0], w.shape[0]
     ok, _ = valid_rows(targets, v, ignore_index)
     rows = np.nonzero(ok)[0]
@@ -135,6 +136,8 @@ def backward(h, w, targets, ignore_index=-100, reduction="mean", grad=1.0, block
         g = softmax_grad_rows(h[r], w, t[r], c[r] if reduction == "none" else c)
         dh[r] = g @ w
         dw += g.T @ h[r]
+        if progress is not None:
+            progress(s0 + r.size, rows.size)
     return {"dH": dh, "dW": dw}
 
 
