@@ -12,17 +12,20 @@
 //             online max / sum-exp epilogue) -> combine (merge partials, target
 //             logit, per-row loss) -> loss (fixed-order reduction)
 //   backward: compact -> gather/transpose H_valid -> per vocabulary slab:
-//             transpose W slab, G tile (recompute S^T, G = c (softmax - onehot)),
-//             dW slab = G^T H_valid, dH32 (+)= G W_slab -> finalise dH
+//             G tile (recompute S^T, G = c (softmax - onehot)), dH32 (+)= G W_slab,
+//             dW slab = G^T H_valid -> finalise dH
 // Built on the same kernels: the backward with an AdamW step on each finished dW block
 // (paper Sec. 4.1), a vocabulary-shard (loss-parallel) forward / combine / backward, and a
 // fused linear knowledge-distillation loss whose G kernel takes the teacher's probabilities
 // as soft targets.
 //
-// Every contraction is a "both operands K-contiguous" product C = A B^T run by
-// one MFMA main loop: 256x256 output tiles, 8 waves of 128x64, bf16
-// v_mfma_f32_32x32x16 with fp32 accumulation, K streamed through two 64-wide LDS
-// slices filled by direct-to-LDS buffer loads (XOR-swizzled 16-byte chunks).
+// Every contraction C = A B^T (C [M, N], sum over K) runs one MFMA main loop:
+// 256x256 output tiles, 8 waves of 128x64, bf16 v_mfma_f32_32x32x16 with fp32
+// accumulation, K streamed through two 64-wide LDS slices filled by direct-to-LDS
+// buffer loads (XOR-swizzled 16-byte chunks). Each operand is either K-contiguous
+// (H, W in the forward and G kernels; G in dH) or K-major (G in dW, the W slab in
+// dH: the MFMA fragments then come from transposing LDS reads), so G is written
+// once, token-major, and W is never copied.
 
 #include <hip/hip_runtime.h>
 
@@ -31,6 +34,8 @@
 #include <string.h>
 
 #include <mutex>
+#include <type_traits>
+#include <utility>
 #include <vector>
 
 #include "lce.h"
@@ -53,11 +58,50 @@ constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 constexpr uint32_t kRsrcWord3 = 0x00020000u;  // gfx9 raw buffer: 32-bit data format
 
+// Raw buffer descriptor: base address, stride 0, num_records = bytes. num_records is capped below
+// 2^31 so that offset 2^31 is always out of range (the zero-fill trick for ragged K slices); every
+// access of a tile lies within its first 2^31 bytes (checked on the host, or the descriptor is
+// rebuilt per slice). Two forms: the compiler's buffer-resource type for the load builtin, and the
+// 4 descriptor words (in SGPRs) for the inline-asm load.
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint64_t bytes) {
-  // capped below 2^31 so that offset 2^31 is always out of range (the zero-fill trick for ragged
-  // K slices); every access of a tile lies within its first 2^31 bytes (checked on the host)
-  uint32_t n = bytes > 0x7FFFFFFFull ? 0x7FFFFFFFu : (uint32_t)bytes;
+  const uint32_t n = bytes > 0x7FFFFFFFull ? 0x7FFFFFFFu : (uint32_t)bytes;
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)n, (int)kRsrcWord3);
+}
+
+__device__ __forceinline__ i32x4_t make_rsrc_words(const void* base, uint64_t bytes) {
+  const uint64_t a = (uint64_t)(uintptr_t)base;
+  const uint32_t n = bytes > 0x7FFFFFFFull ? 0x7FFFFFFFu : (uint32_t)bytes;
+  i32x4_t w;
+  w.x = __builtin_amdgcn_readfirstlane((int)(uint32_t)a);
+  w.y = __builtin_amdgcn_readfirstlane((int)((a >> 32) & 0xFFFFu));
+  w.z = __builtin_amdgcn_readfirstlane((int)n);
+  w.w = (int)kRsrcWord3;
+  return w;
+}
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+// One direct-to-LDS load: 16 bytes per lane from the buffer at voffset + soffset into LDS at lds
+// + 16 * lane (lds wave-uniform; m0 is its LDS byte address).
+//  kAsm = false: the compiler builtin. The compiler tracks it as an LDS write and, before any LDS
+//    read it cannot prove disjoint, waits for every such load in flight; it proves this for the
+//    128-bit fragment reads but not for the transposing reads.
+//  kAsm = true: inline asm, which the compiler does not track, for the main loops that use
+//    transposing reads (a compiler wait there would stall each substep on the next slice's
+//    loads). The main loop orders the loads against the reads itself: a vmcnt wait and a barrier
+//    before a buffer is read, and a buffer is refilled only after the barrier that follows its
+//    last read. The s_nop is the wait state an M0 write needs before a load that writes LDS.
+template <bool kAsm>
+__device__ __forceinline__ void dma16(const __amdgpu_buffer_rsrc_t& rs, const i32x4_t& rw, const char* lds, int m0,
+                                      uint32_t voffset, uint32_t soffset) {
+  if constexpr (!kAsm) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void_t*)lds, 16, (int)voffset, (int)soffset, 0, 0);
+  } else {
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+                 :
+                 : "s"(m0), "v"(voffset), "s"(rw), "s"(soffset)
+                 : "memory", "m0");
+  }
 }
 
 __device__ __forceinline__ float bf16_to_f32(uint32_t bits16) { return __uint_as_float(bits16 << 16); }
@@ -126,13 +170,25 @@ __device__ __forceinline__ float wave_max(float x) {
 // for v_mfma_f32_32x32x16_bf16 is 8 consecutive K values of one row (lane l: row l % 32, K
 // chunk l / 32 of the 16-wide substep).
 //
-// K streams through two LDS buffers of 64-wide slices (A 256x64 and B 256x64 bf16: 64 KB per
-// buffer). A slice is copied global -> LDS by buffer loads that write LDS directly; each moves 8
-// rows x 128 bytes (one full cache line per row, which the memory pipeline turns into whole-line
-// requests), one 16-byte chunk per lane. In LDS a row is 128 bytes and chunk c of row r sits at
-// position c ^ swz(r), swz(r) = (r & 7) ^ ((r >> 3) & 1): the 128-bit fragment reads of any 8 or
-// 16 consecutive rows then hit distinct banks. Each load picks its source chunk so that it lands
-// in that order.
+// K streams through two LDS buffers of 64-wide slices (A and B 32 KB each: 64 KB per buffer),
+// copied global -> LDS by buffer loads that write LDS directly, one 16-byte chunk per lane and
+// 1 KB per instruction. An operand is stored in one of two ways:
+//
+//  * row-major (K contiguous, e.g. H [N, D], W [V, D]): a slice is 256 rows x 128 bytes; each
+//    load instruction moves 8 rows (one full cache line per row, which the memory pipeline turns
+//    into whole-line requests). Chunk c of row r sits at position c ^ swz(r), swz(r) = (r & 7) ^
+//    ((r >> 3) & 1), so that the 128-bit fragment reads of any 8 or 16 consecutive rows hit
+//    distinct banks;
+//  * K-major (the 256 tile elements contiguous, e.g. G [Nv, Vc] as the A operand of G^T H, or
+//    W [V, D] as the B operand of G W): a slice is 64 K-rows x 512 bytes; each load instruction
+//    moves 2 K-rows (4 whole lines each). Chunk c of K-row k sits at position c ^ kswz(k),
+//    kswz(k) = 4 (k & 3) + 16 ((k >> 3) & 1). Fragments come from pairs of transposing reads
+//    (ds_read_b64_tr_b16): in a 16-lane group, lane i reads 4 consecutive elements (8 bytes) of
+//    K-row i / 4 and lane j receives element j of the group's 16 columns from K-rows 0..3; the
+//    second read covers K-rows 4..7. The swizzle spreads the 4 K-rows x 64 bytes that a half-wave
+//    reads over all banks.
+//
+// Each load picks its source chunk so that it lands in the swizzled position.
 //
 // Schedule of slice j (four 16-wide substeps, fragments read one substep ahead): after the
 // third substep's MFMAs are issued, one barrier both publishes slice j+1 (its loads were issued
@@ -142,32 +198,90 @@ __device__ __forceinline__ float wave_max(float x) {
 // workgroup's 64 load instructions at once fill the texture-address queues and stall the
 // issuing waves (measured: 3-9 % per kernel; the better delay depends on the operand stream).
 //
-// aoff/boff: byte offset (row start + this lane's chunk) of the 4 rows this lane loads per slice
-// and operand. K must be a multiple of 8; a ragged last slice is zero-filled by pointing the
-// lanes past K outside the buffer resource (buffer loads return 0 there).
+// K must be a multiple of 8; a ragged last slice is zero-filled by pointing the lanes past K
+// outside the buffer resource (buffer loads return 0 there).
 // ---------------------------------------------------------------------------------------------
 constexpr int KSLICE = 64;
 constexpr int SLICE_BYTES = 65536;      // A (32 KB) + B (32 KB)
 constexpr int LDS_BYTES = 2 * SLICE_BYTES;
 constexpr uint32_t kOobOffset = 0x80000000u;
 
-typedef __attribute__((address_space(3))) void lds_void_t;
+// One operand of the main loop.
+//  row-major: rsrc covers the tile's 256 rows; off[q] is the byte offset of row
+//             wave*32 + 8q + lane/8 plus this lane's chunk (K offset 0).
+//  K-major:   base points at K-row 0, first column of the tile; rows are ld elements apart and
+//             the buffer holds `bytes` bytes from base on; off[q] is the byte offset of K-row
+//             wave*8 + 2q + lane/32 of a slice plus this lane's chunk. The buffer resource is
+//             rebuilt per slice at base + k0 * ld, so offsets stay small for any buffer size.
+struct Operand {
+  __amdgpu_buffer_rsrc_t rsrc;
+  i32x4_t rwords;
+  const uint16_t* base;
+  int64_t ld;
+  uint64_t bytes;
+  uint32_t off[4];
+};
 
 struct FragSet {
   bf16x8_t a[4], b[2];
 };
 
-// chunk this lane loads for its even-numbered rows (odd rows: ^ 1)
+// chunk this lane loads for its even-numbered rows (odd rows: ^ 1), row-major operands
 __device__ __forceinline__ int lane_chunk_even() {
   const int j = threadIdx.x & 63;
   return (j & 7) ^ ((j >> 3) & 7);
 }
 
-__device__ __forceinline__ void read_frags(FragSet& f, const char* buf, uint32_t a_rd, uint32_t b_rd, uint32_t kofs) {
+__device__ __forceinline__ int kswz(int k) { return ((k & 3) << 2) | (((k >> 3) & 1) << 4); }
+
+// LDS byte offset, within an operand's 32 KB, of this lane's first transposing read for the
+// 32-column block starting at column c0 of substep 0 (the second read is 2048 bytes further,
+// substep ks adds ks * 8192).
+__device__ __forceinline__ uint32_t kmajor_frag_addr(int c0) {
+  const int lane = threadIdx.x & 63, g = lane >> 4, i = lane & 15;
+  const int k = 8 * (g >> 1) + (i >> 2);
+  const int col = c0 + 16 * (g & 1) + 4 * (i & 3);
+  return (uint32_t)(k * 512 + (((col >> 3) ^ kswz(k)) << 4) + (col & 7) * 2);
+}
+
+__device__ __forceinline__ bf16x8_t read_tr_pair(const char* p) {
+  s16x8_t t;
+  t.lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)p);
+  t.hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(p + 2048));
+  return __builtin_bit_cast(bf16x8_t, t);
+}
+
+// Per-lane LDS read addresses of one operand: row-major uses rd (row base) + kofs[ks];
+// K-major uses tr[block] + ks * 8192.
+template <int kBlocks>
+struct FragAddr {
+  uint32_t rd;
+  uint32_t kofs[4];
+  uint32_t tr[kBlocks];
+};
+
+template <bool kKM, int kBlocks>
+__device__ __forceinline__ void frag_addr(FragAddr<kBlocks>& fa, int row0) {
+  const int lane = threadIdx.x & 63;
+  if constexpr (!kKM) {
+    const int swz = (lane & 7) ^ ((lane >> 3) & 1);
+    fa.rd = (uint32_t)((row0 + (lane & 31)) * 128);
 #pragma unroll
-  for (int i = 0; i < 4; ++i) f.a[i] = *reinterpret_cast<const bf16x8_t*>(buf + a_rd + i * 4096 + kofs);
+    for (int ks = 0; ks < 4; ++ks) fa.kofs[ks] = (uint32_t)((((ks * 2) + (lane >> 5)) ^ swz) * 16);
+  } else {
 #pragma unroll
-  for (int j = 0; j < 2; ++j) f.b[j] = *reinterpret_cast<const bf16x8_t*>(buf + 32768 + b_rd + j * 4096 + kofs);
+    for (int b = 0; b < kBlocks; ++b) fa.tr[b] = kmajor_frag_addr(row0 + 32 * b);
+  }
+}
+
+template <bool kKM, int kBlocks>
+__device__ __forceinline__ void read_operand(bf16x8_t (&f)[kBlocks], const char* reg, const FragAddr<kBlocks>& fa,
+                                             int ks) {
+#pragma unroll
+  for (int b = 0; b < kBlocks; ++b) {
+    if constexpr (!kKM) f[b] = *reinterpret_cast<const bf16x8_t*>(reg + fa.rd + b * 4096 + fa.kofs[ks]);
+    else f[b] = read_tr_pair(reg + fa.tr[b] + ks * 8192);
+  }
 }
 
 __device__ __forceinline__ void mma_substep(f32x16_t (&acc)[4][2], const FragSet& f) {
@@ -177,48 +291,62 @@ __device__ __forceinline__ void mma_substep(f32x16_t (&acc)[4][2], const FragSet
     for (int j = 0; j < 2; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[i], f.b[j], acc[i][j], 0, 0, 0);
 }
 
-template <bool kMasked>
-__device__ __forceinline__ void load_slice(__amdgpu_buffer_rsrc_t ra, const uint32_t (&aoff)[4],
-                                           __amdgpu_buffer_rsrc_t rb, const uint32_t (&boff)[4],
-                                           char* buf, int k0, int K) {
-  char* dst = buf + (threadIdx.x >> 6) * 4096;
-  if (!kMasked) {
+// This wave's 4 load instructions of one operand's slice k0 (dstp = the operand's region + 4 KB
+// per wave, dst its LDS byte address).
+template <bool kAsm, bool kKM, bool kMasked>
+__device__ __forceinline__ void load_operand(const Operand& op, const char* dstp, int dst, int k0, int K) {
+  if constexpr (!kKM) {
+    if (!kMasked) {
 #pragma unroll
-    for (int q = 0; q < 4; ++q)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_void_t*)(dst + q * 1024), 16, (int)aoff[q], k0 * 2, 0, 0);
+      for (int q = 0; q < 4; ++q)
+        dma16<kAsm>(op.rsrc, op.rwords, dstp + q * 1024, dst + q * 1024, op.off[q], (uint32_t)k0 * 2);
+    } else {
+      const int ce = lane_chunk_even();
 #pragma unroll
-    for (int q = 0; q < 4; ++q)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_void_t*)(dst + 32768 + q * 1024), 16, (int)boff[q], k0 * 2, 0, 0);
+      for (int q = 0; q < 4; ++q) {
+        const bool ok = k0 + (ce ^ (q & 1)) * 8 < K;
+        dma16<kAsm>(op.rsrc, op.rwords, dstp + q * 1024, dst + q * 1024, ok ? op.off[q] + (uint32_t)k0 * 2 : kOobOffset,
+                    0u);
+      }
+    }
   } else {
-    const int ce = lane_chunk_even();
+    const uint16_t* base = op.base + (int64_t)k0 * op.ld;
+    const uint64_t bytes = op.bytes - (uint64_t)k0 * op.ld * 2;
+    const __amdgpu_buffer_rsrc_t rs = make_rsrc(base, bytes);
+    const i32x4_t rw = make_rsrc_words(base, bytes);
+    const int krow = (threadIdx.x >> 6) * 8 + ((threadIdx.x & 63) >> 5);
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      const bool ok = k0 + (ce ^ (q & 1)) * 8 < K;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_void_t*)(dst + q * 1024), 16,
-                                               (int)(ok ? aoff[q] + (uint32_t)k0 * 2 : kOobOffset), 0, 0, 0);
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_void_t*)(dst + 32768 + q * 1024), 16,
-                                               (int)(ok ? boff[q] + (uint32_t)k0 * 2 : kOobOffset), 0, 0, 0);
+      const bool ok = !kMasked || k0 + krow + 2 * q < K;
+      dma16<kAsm>(rs, rw, dstp + q * 1024, dst + q * 1024, ok ? op.off[q] : kOobOffset, 0u);
     }
   }
+}
+
+template <bool kAsm, bool kAKM, bool kBKM, bool kMasked>
+__device__ __forceinline__ void load_slice(const Operand& A, const Operand& B, const char* buf, int k0, int K) {
+  const char* dstp = buf + (threadIdx.x >> 6) * 4096;
+  const int dst = kAsm ? __builtin_amdgcn_readfirstlane((int)(uint32_t)(uintptr_t)dstp) : 0;
+  load_operand<kAsm, kAKM, kMasked>(A, dstp, dst, k0, K);
+  load_operand<kAsm, kBKM, kMasked>(B, dstp + 32768, dst + 32768, k0, K);
 }
 
 // s_waitcnt with only the vector-memory counter constrained (expcnt / lgkmcnt left at max)
 #define LCE_WAIT_VM(n) __builtin_amdgcn_s_waitcnt((((n) & 15) | (7 << 4) | (15 << 8) | (((n) >> 4) << 14)))
 
-template <int kLateGroups>
-__device__ __forceinline__ void mma_mainloop(f32x16_t (&acc)[4][2],
-                                             __amdgpu_buffer_rsrc_t ra, const uint32_t (&aoff)[4],
-                                             __amdgpu_buffer_rsrc_t rb, const uint32_t (&boff)[4],
-                                             int K, char* smem) {
-  const int lane = threadIdx.x & 63;
+template <int kLateGroups, bool kAKM = false, bool kBKM = false>
+__device__ __forceinline__ void mma_mainloop(f32x16_t (&acc)[4][2], const Operand& A, const Operand& B, int K,
+                                             char* smem) {
   const int wave = threadIdx.x >> 6;
   const int wr = wave >> 2, wc = wave & 3;
-  const uint32_t a_rd = (uint32_t)((wr * 128 + (lane & 31)) * 128);
-  const uint32_t b_rd = (uint32_t)((wc * 64 + (lane & 31)) * 128);
-  const int swz = (lane & 7) ^ ((lane >> 3) & 1);
-  uint32_t kofs[4];
-#pragma unroll
-  for (int ks = 0; ks < 4; ++ks) kofs[ks] = (uint32_t)((((ks * 2) + (lane >> 5)) ^ swz) * 16);
+  FragAddr<4> fa;
+  FragAddr<2> fb;
+  frag_addr<kAKM>(fa, wr * 128);
+  frag_addr<kBKM>(fb, wc * 64);
+  auto read_frags = [&](FragSet& f, const char* buf, int ks) {
+    read_operand<kAKM>(f.a, buf, fa, ks);
+    read_operand<kBKM>(f.b, buf + 32768, fb, ks);
+  };
 
 #pragma unroll
   for (int i = 0; i < 4; ++i)
@@ -228,10 +356,12 @@ __device__ __forceinline__ void mma_mainloop(f32x16_t (&acc)[4][2],
   const int S = (K + KSLICE - 1) / KSLICE;
   if (S <= 0) return;
   const bool ragged = (K % KSLICE) != 0;
+  // loads as inline asm where transposing reads are used (see dma16)
+  constexpr bool kAsm = kAKM || kBKM;
   auto load = [&](int s) {
     char* buf = smem + (s & 1) * SLICE_BYTES;
-    if (ragged && s == S - 1) load_slice<true>(ra, aoff, rb, boff, buf, s * KSLICE, K);
-    else load_slice<false>(ra, aoff, rb, boff, buf, s * KSLICE, K);
+    if (ragged && s == S - 1) load_slice<kAsm, kAKM, kBKM, true>(A, B, buf, s * KSLICE, K);
+    else load_slice<kAsm, kAKM, kBKM, false>(A, B, buf, s * KSLICE, K);
   };
 
   load(0);
@@ -249,19 +379,19 @@ __device__ __forceinline__ void mma_mainloop(f32x16_t (&acc)[4][2],
   const bool late = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6) >= 4;
   int pend = -1;
   FragSet f0, f1;
-  read_frags(f0, smem, a_rd, b_rd, kofs[0]);
+  read_frags(f0, smem, 0);
   for (int j = 0; j < S; ++j) {
     const char* cur = smem + (j & 1) * SLICE_BYTES;
     const char* nxt = smem + ((j + 1) & 1) * SLICE_BYTES;
-    read_frags(f1, cur, a_rd, b_rd, kofs[1]);
+    read_frags(f1, cur, 1);
     mma_substep(acc, f0);
     if (kLateGroups == 2 && pend >= 0) {
       load(pend);
       pend = -1;
     }
-    read_frags(f0, cur, a_rd, b_rd, kofs[2]);
+    read_frags(f0, cur, 2);
     mma_substep(acc, f1);
-    read_frags(f1, cur, a_rd, b_rd, kofs[3]);
+    read_frags(f1, cur, 3);
     mma_substep(acc, f0);
     if (j + 1 < S) {
       // slice j+1 landed (own loads) and every wave is done with slice j's buffer
@@ -271,7 +401,7 @@ __device__ __forceinline__ void mma_mainloop(f32x16_t (&acc)[4][2],
         if (!late) load(j + 2);
         else pend = j + 2;
       }
-      read_frags(f0, nxt, a_rd, b_rd, kofs[0]);
+      read_frags(f0, nxt, 0);
     }
     mma_substep(acc, f1);
     if (kLateGroups == 1 && pend >= 0) {
@@ -283,29 +413,54 @@ __device__ __forceinline__ void mma_mainloop(f32x16_t (&acc)[4][2],
   __syncthreads();
 }
 
-// Byte offsets (row start + this lane's chunk) of the 4 rows this lane loads per slice of a dense
-// operand whose rows [row0, row0 + 256) are wanted; rows at or beyond `rows_left` are clamped.
-__device__ __forceinline__ void dense_offsets(uint32_t (&off)[4], int rows_left, int64_t ld) {
+// A row-major operand whose rows [row0, row0 + 256) are wanted (rsrc based at row0): the byte
+// offsets of the 4 rows this lane loads per slice; rows at or beyond `rows_left` are clamped.
+__device__ __forceinline__ Operand dense_operand(const uint16_t* tile, int rows_left, int64_t ld) {
+  Operand op;
+  op.rsrc = make_rsrc(tile, (uint64_t)rows_left * ld * 2);
+  op.rwords = make_rsrc_words(tile, (uint64_t)rows_left * ld * 2);
   const int j = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int ce = lane_chunk_even();
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     int r = w * 32 + q * 8 + (j >> 3);
     r = r < rows_left ? r : rows_left - 1;
-    off[q] = (uint32_t)((int64_t)r * ld * 2 + (ce ^ (q & 1)) * 16);
+    op.off[q] = (uint32_t)((int64_t)r * ld * 2 + (ce ^ (q & 1)) * 16);
   }
+  return op;
 }
 
-// Same for rows gathered through the compacted valid-row list idx[0..nv).
-__device__ __forceinline__ void gather_offsets(uint32_t (&off)[4], const int* idx, int n0, int nv, int64_t ld) {
+// Same for rows gathered through the compacted valid-row list idx[0..nv) of a buffer of n rows.
+__device__ __forceinline__ Operand gather_operand(const uint16_t* src, int64_t n, int64_t ld, const int* idx, int n0,
+                                                  int nv) {
+  Operand op;
+  op.rsrc = make_rsrc(src, (uint64_t)n * ld * 2);
+  op.rwords = make_rsrc_words(src, (uint64_t)n * ld * 2);
   const int j = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int ce = lane_chunk_even();
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     int r = n0 + w * 32 + q * 8 + (j >> 3);
     r = r < nv ? r : nv - 1;
-    off[q] = (uint32_t)((int64_t)idx[r] * ld * 2 + (ce ^ (q & 1)) * 16);
+    op.off[q] = (uint32_t)((int64_t)idx[r] * ld * 2 + (ce ^ (q & 1)) * 16);
   }
+  return op;
+}
+
+// A K-major operand: K-row 0 of the tile at `base` (its first column), rows `ld` elements apart,
+// `bytes` readable bytes from base on.
+__device__ __forceinline__ Operand kmajor_operand(const uint16_t* base, int64_t ld, uint64_t bytes) {
+  Operand op;
+  op.base = base;
+  op.ld = ld;
+  op.bytes = bytes;
+  const int j = threadIdx.x & 63, w = threadIdx.x >> 6;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int k = w * 8 + 2 * q + (j >> 5);
+    op.off[q] = (uint32_t)((int64_t)k * ld * 2 + (((j & 31) ^ kswz(k)) << 4));
+  }
+  return op;
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -402,9 +557,7 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_fwd_stats(const uint16_t* __res
   const int vt0 = (int)((int64_t)p * vt_count / nparts), vt1 = (int)((int64_t)(p + 1) * vt_count / nparts);
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, wr = wave >> 2, wc = wave & 3;
-  __amdgpu_buffer_rsrc_t rb = make_rsrc(H, (uint64_t)n * ldh * 2);
-  uint32_t boff[4];
-  gather_offsets(boff, idx, n0, nv, ldh);
+  const Operand opb = gather_operand(H, n, ldh, idx, n0, nv);
 
   float m2[2], ss[2];
 #pragma unroll
@@ -414,10 +567,8 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_fwd_stats(const uint16_t* __res
   for (int vt = vt0; vt < vt1; ++vt) {
     const int v0 = vt * TILE;
     const int vleft = v - v0;
-    __amdgpu_buffer_rsrc_t ra = make_rsrc(W + (int64_t)v0 * ldw, (uint64_t)vleft * ldw * 2);
-    uint32_t aoff[4];
-    dense_offsets(aoff, vleft, ldw);
-    mma_mainloop<2>(acc, ra, aoff, rb, boff, d, smem);
+    const Operand opa = dense_operand(W + (int64_t)v0 * ldw, vleft, ldw);
+    mma_mainloop<2>(acc, opa, opb, d, smem);
 
     // rows (vocabulary ids) of this lane: v0 + wr*128 + 32 bi + 8 (r/4) + 4 (lane/32) + r%4
     const int vb = wr * 128 + (lane >> 5) * 4;
@@ -654,9 +805,9 @@ __device__ __forceinline__ float grad_scale(const float* grad, const int* n_norm
 // ---------------------------------------------------------------------------------------------
 // K4: softmax-gradient tile for one vocabulary slab. Tile (vocabulary tile tm, token tile tn) of
 // S^T = W_slab H_valid^T is recomputed and turned into G = c (exp(s - lse) - onehot), rounded to
-// bf16 and written twice: G[token][v] (row stride vc) and Gt[v][token] (row stride ldt).
-// Entries outside the valid tokens / slab columns are written as zeros where the later
-// contractions read them (K padding), so those loops need no masking.
+// bf16 and written as G[token][v] (row stride vc). Every tile is written whole: entries of tokens
+// at or beyond Nv and of ids at or beyond the slab width are zeros, so the two contractions that
+// read G (dH with K = ids, dW with K = tokens, G read K-major) need no masking of G.
 // ---------------------------------------------------------------------------------------------
 // The same kernel serves the distillation loss (KD) with soft targets, in four modes:
 //   G_ONEHOT  LCE: G = c (softmax - onehot(t))
@@ -674,7 +825,7 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_bwd_g(const uint16_t* __restric
                                                        const int* __restrict__ idx, const int* __restrict__ nv_ptr,
                                                        const float* __restrict__ lse, const float* __restrict__ grad,
                                                        const int* __restrict__ n_norm, int reduction, int d, int tm_count,
-                                                       uint16_t* __restrict__ G, int vc, uint16_t* __restrict__ Gt, int ldt,
+                                                       uint16_t* __restrict__ G, int vc, int ldt,
                                                        float scale2, float inv_t, float* __restrict__ P,
                                                        float* __restrict__ qpart, int64_t qrow) {
   __shared__ __attribute__((aligned(16))) char smem[LDS_BYTES];
@@ -686,13 +837,10 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_bwd_g(const uint16_t* __restric
   const int vleft = vs - vt0;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, wr = wave >> 2, wc = wave & 3;
 
-  __amdgpu_buffer_rsrc_t ra = make_rsrc(W + (v0 + vt0) * ldw, (uint64_t)vleft * ldw * 2);
-  __amdgpu_buffer_rsrc_t rb = make_rsrc(H, (uint64_t)n * ldh * 2);
-  uint32_t aoff[4], boff[4];
-  dense_offsets(aoff, vleft, ldw);
-  gather_offsets(boff, idx, n0, nv, ldh);
+  const Operand opa = dense_operand(W + (v0 + vt0) * ldw, vleft, ldw);
+  const Operand opb = gather_operand(H, n, ldh, idx, n0, nv);
   f32x16_t acc[4][2];
-  mma_mainloop<2>(acc, ra, aoff, rb, boff, d, smem);
+  mma_mainloop<2>(acc, opa, opb, d, smem);
 
   const float c_all = grad_scale(grad, n_norm, reduction);
   int tok[2], tgt[2];
@@ -751,11 +899,10 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_bwd_g(const uint16_t* __restric
     return;
   }
   // G values in place, then the bf16 tile goes through LDS (free after the main loop) as
-  // T[token][v], 512-byte rows whose 16-byte chunk c sits at c ^ (token & 31), so that both the
-  // token-major rows of G and the vocabulary-major rows of Gt leave with wide coalesced stores.
-  // Within a chunk the two 8-byte halves (ids 0-3, 4-7) trade places in token rows with bit 4 set:
-  // the 32 lanes of a half-wave, which hold the same half of 32 consecutive token rows, then write
-  // (and the transposing reads below fetch) 32 distinct 8-byte bank slots.
+  // T[token][v], 512-byte rows whose 16-byte chunk c sits at c ^ (token & 31), so that the
+  // token-major rows of G leave with wide coalesced stores. Within a chunk the two 8-byte halves
+  // (ids 0-3, 4-7) trade places in token rows with bit 4 set: the 32 lanes of a half-wave, which
+  // hold the same half of 32 consecutive token rows, then write 32 distinct 8-byte bank slots.
   char* T = smem;
   float qs[2] = {0.f, 0.f};
 #pragma unroll
@@ -811,60 +958,26 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_bwd_g(const uint16_t* __restric
     }
   }
   __syncthreads();
-  // G rows (tokens < Nv): 16-byte chunks, one 512-byte row per 32 threads
+  // G rows, the whole tile (rows of tokens >= Nv are zeros): 16-byte chunks, one 512-byte row
+  // per 32 threads
 #pragma unroll 4
   for (int it = 0; it < 16; ++it) {
     const int q = threadIdx.x + NTHREADS * it;
     const int nl = q >> 5, ch = q & 31;
-    if (n0 + nl < nv) {
-      i32x4_t val = *reinterpret_cast<const i32x4_t*>(T + nl * 512 + ((ch ^ (nl & 31)) << 4));
-      if (nl & 16) val = (i32x4_t){val.z, val.w, val.x, val.y};
-      *reinterpret_cast<i32x4_t*>(G + (int64_t)(n0 + nl) * vc + vt0 + ch * 8) = val;
-    }
-  }
-  // Gt rows (vocabulary rows < slab width): two transposing LDS reads give each lane 8 consecutive
-  // tokens of one vocabulary row, stored as one 16-byte chunk. In a 16-lane group, lane i reads 8
-  // bytes (4 vocabulary ids) of token row nb + 8 (i % 4) + i / 4 (and 4 rows further for the
-  // second read); lane j receives vocabulary id vq + j % 4 of tokens nb + 8 (j / 4) .. +7. One
-  // pair of wave instructions covers 4 vocabulary rows x 128 tokens.
-  {
-    const int grp = lane >> 4, i16 = lane & 15;
-#pragma unroll 4
-    for (int kk = 0; kk < 16; ++kk) {
-      const int item = wave * 16 + kk;
-      const int vq = (item >> 1) * 4;
-      const int nb = (item & 1) * 128 + grp * 32;
-      const int nl = nb + 8 * (i16 & 3) + (i16 >> 2);
-      // odd groups read their +4 rows first, so that each instruction's two groups of a half-wave
-      // touch 32 distinct token rows (mod 32) and hence distinct LDS banks
-      const int sw = (grp & 1) * 4;
-      const int r0 = nl + sw, r1 = nl + 4 - sw;
-      const uint32_t a0 = (uint32_t)(r0 * 512 + ((((vq >> 3) ^ (r0 & 31))) << 4) +
-                                     ((((vq >> 2) & 1) ^ ((r0 >> 4) & 1)) << 3));
-      const uint32_t a1 = (uint32_t)(r1 * 512 + ((((vq >> 3) ^ (r1 & 31))) << 4) +
-                                     ((((vq >> 2) & 1) ^ ((r1 >> 4) & 1)) << 3));
-      const s16x4_t x0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(T + a0));
-      const s16x4_t x1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(T + a1));
-      const s16x4_t lo = sw ? x1 : x0;
-      const s16x4_t hi = sw ? x0 : x1;
-      const int vrow = vq + (i16 & 3);
-      if (vrow < vleft) {
-        s16x8_t t8;
-        t8.lo = lo;
-        t8.hi = hi;
-        *reinterpret_cast<s16x8_t*>(Gt + (int64_t)(vt0 + vrow) * ldt + n0 + nb + 8 * (i16 >> 2)) = t8;
-      }
-    }
+    i32x4_t val = *reinterpret_cast<const i32x4_t*>(T + nl * 512 + ((ch ^ (nl & 31)) << 4));
+    if (nl & 16) val = (i32x4_t){val.z, val.w, val.x, val.y};
+    *reinterpret_cast<i32x4_t*>(G + (int64_t)(n0 + nl) * vc + vt0 + ch * 8) = val;
   }
 }
 
-// K5: dW[v0 + m][dd] = sum_k Gt[m][k] Hvt[dd][k] over k < round_up(Nv, 64). The epilogue either
+// K5: dW[v0 + m][dd] = sum_k G[k][m] Hvt[dd][k] over k < round_up(Nv, 64), G [Npad][vc] read
+// K-major (transposing LDS reads), Hvt [D][Npad] row-major. The epilogue either
 // writes the block in bf16 (each element once), adds it to the bf16 values already there, or
 // hands each bf16-rounded element straight to the AdamW update of W (the in-backward step).
 enum DwMode { DW_STORE = 0, DW_ACCUMULATE = 1, DW_ADAMW = 2 };
 
 template <int kMode>
-__global__ __launch_bounds__(NTHREADS, 2) void k_bwd_dw(const uint16_t* __restrict__ Gt, int ldt, int vs,
+__global__ __launch_bounds__(NTHREADS, 2) void k_bwd_dw(const uint16_t* __restrict__ G, int vc, int ldt, int vs,
                                                         const uint16_t* __restrict__ Hvt, int d,
                                                         const int* __restrict__ nv_ptr, int tm_count,
                                                         uint16_t* __restrict__ dW, int64_t v0,
@@ -876,13 +989,11 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_bwd_dw(const uint16_t* __restri
   const int nv = *nv_ptr;
   const int kpad = ((nv + KPAD - 1) / KPAD) * KPAD;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, wr = wave >> 2, wc = wave & 3;
-  __amdgpu_buffer_rsrc_t ra = make_rsrc(Gt + (int64_t)m0 * ldt, (uint64_t)(vs - m0) * ldt * 2);
-  __amdgpu_buffer_rsrc_t rb = make_rsrc(Hvt + (int64_t)d0 * ldt, (uint64_t)(d - d0) * ldt * 2);
-  uint32_t aoff[4], boff[4];
-  dense_offsets(aoff, vs - m0, ldt);
-  dense_offsets(boff, d - d0, ldt);
+  // ldt = Npad: G has Npad rows of vc ids, Hvt D rows of Npad tokens
+  const Operand opa = kmajor_operand(G + m0, vc, ((uint64_t)ldt * vc - m0) * 2);
+  const Operand opb = dense_operand(Hvt + (int64_t)d0 * ldt, d - d0, ldt);
   f32x16_t acc[4][2];
-  mma_mainloop<1>(acc, ra, aoff, rb, boff, kpad, smem);
+  mma_mainloop<1, true, false>(acc, opa, opb, kpad, smem);
   const int mb = m0 + wr * 128 + (lane >> 5) * 4;
   const int dc = d0 + wc * 64 + (lane & 31);
 #pragma unroll
@@ -942,9 +1053,11 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_bwd_dw(const uint16_t* __restri
   }
 }
 
-// K6: dH32[m][dd] (+)= sum_k G[m][k] WsT[dd][k] over k < round_up(vs, 64); rows m < Nv.
-__global__ __launch_bounds__(NTHREADS, 2) void k_bwd_dh(const uint16_t* __restrict__ G, int vc, int kpad,
-                                                        const uint16_t* __restrict__ WsT, int d,
+// K6: dH32[m][dd] (+)= sum_k G[m][k] Ws[k][dd] over the slab's k < vs; rows m < Nv. Ws = W + v0 ldw
+// is the slab's first row, read K-major (transposing LDS reads); ws_rows = V - v0 rows follow.
+__global__ __launch_bounds__(NTHREADS, 2) void k_bwd_dh(const uint16_t* __restrict__ G, int vc, int vs,
+                                                        const uint16_t* __restrict__ Ws, int64_t ldw,
+                                                        int64_t ws_rows, int d,
                                                         const int* __restrict__ nv_ptr,
                                                         float* __restrict__ dH32, int accumulate) {
   __shared__ __attribute__((aligned(16))) char smem[LDS_BYTES];
@@ -953,13 +1066,10 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_bwd_dh(const uint16_t* __restri
   if (!band_tile((nv + TILE - 1) / TILE, (d + TILE - 1) / TILE, tm, tn)) return;
   const int m0 = tm * TILE, d0 = tn * TILE;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, wr = wave >> 2, wc = wave & 3;
-  __amdgpu_buffer_rsrc_t ra = make_rsrc(G + (int64_t)m0 * vc, (uint64_t)(nv - m0) * vc * 2);
-  __amdgpu_buffer_rsrc_t rb = make_rsrc(WsT + (int64_t)d0 * vc, (uint64_t)(d - d0) * vc * 2);
-  uint32_t aoff[4], boff[4];
-  dense_offsets(aoff, nv - m0, vc);
-  dense_offsets(boff, d - d0, vc);
+  const Operand opa = dense_operand(G + (int64_t)m0 * vc, nv - m0, vc);
+  const Operand opb = kmajor_operand(Ws + d0, ldw, ((uint64_t)ws_rows * ldw - d0) * 2);
   f32x16_t acc[4][2];
-  mma_mainloop<2>(acc, ra, aoff, rb, boff, kpad, smem);
+  mma_mainloop<2, false, true>(acc, opa, opb, vs, smem);
   // Read-modify-write of the fp32 accumulator, one 32-row block (32 values per lane) at a time
   // so that its 32 loads are in flight together; interior tiles skip the bounds tests.
   const int mb = m0 + wr * 128 + (lane >> 5) * 4;
@@ -1114,11 +1224,11 @@ __global__ __launch_bounds__(256) void k_kd_terms(const float* __restrict__ qpar
 // ---------------------------------------------------------------------------------------------
 // Host side: validation, plan, workspace carve-up, launches, optional timing.
 // ---------------------------------------------------------------------------------------------
-enum KernelId { K_COMPACT = 0, K_FWD_STATS, K_COMBINE, K_LOSS, K_TRANSPOSE_H, K_TRANSPOSE_W, K_BWD_G,
+enum KernelId { K_COMPACT = 0, K_FWD_STATS, K_COMBINE, K_LOSS, K_TRANSPOSE_H, K_BWD_G,
                 K_BWD_DW, K_BWD_DH, K_DH_FINAL, K_ADAMW, K_SHARD_COMBINE, K_KD_P, K_KD_Q, K_KD_TERMS, K_MISC,
                 K_COUNT };
 const char* const kKernelNames[K_COUNT] = {"compact", "fwd_stats", "combine", "loss", "transpose_h",
-                                           "transpose_w", "bwd_g", "bwd_dw", "bwd_dh", "dh_finalize", "adamw", "shard_combine", "kd_teacher_p", "kd_q", "kd_terms", "misc"};
+                                           "bwd_g", "bwd_dw", "bwd_dh", "dh_finalize", "adamw", "shard_combine", "kd_teacher_p", "kd_q", "kd_terms", "misc"};
 
 struct Timing {
   std::mutex mu;
@@ -1136,7 +1246,7 @@ struct Plan {
   int64_t vc, nslab;
   // workspace offsets
   size_t o_idx, o_pos, o_nv, o_pm, o_ps, o_terms, fwd_bytes;
-  size_t o_hvt, o_g, o_gt, o_wst, o_dh32, bwd_bytes;
+  size_t o_hvt, o_g, o_dh32, bwd_bytes;
 };
 
 inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
@@ -1160,7 +1270,7 @@ lce_status_t make_plan(const lce_problem_t* p, Plan* pl) {
   pl->nt_max = (int)(pl->npad / TILE);
   pl->vt_count = (int)((p->v + TILE - 1) / TILE);
   pl->nparts = pl->vt_count < MAX_PARTS ? pl->vt_count : MAX_PARTS;
-  // backward vocabulary slab: 4 D columns (at least 8192) keeps G and Gt at O(N D) while
+  // backward vocabulary slab: 4 D columns (at least 8192) keeps G at O(N D) while
   // halving the dH accumulator passes of a 2 D slab
   int64_t vc = 4 * p->d;
   if (vc < 8192) vc = 8192;
@@ -1184,8 +1294,6 @@ lce_status_t make_plan(const lce_problem_t* p, Plan* pl) {
   cur = common;
   pl->o_hvt = take(cur, 2 * (size_t)p->d * pl->npad);
   pl->o_g = take(cur, 2 * (size_t)pl->npad * vc);
-  pl->o_gt = take(cur, 2 * (size_t)vc * pl->npad);
-  pl->o_wst = take(cur, 2 * (size_t)p->d * vc);
   pl->o_dh32 = take(cur, 4 * (size_t)pl->npad * p->d);
   pl->bwd_bytes = cur;
   return LCE_OK;
@@ -1350,8 +1458,6 @@ lce_status_t backward_impl(const lce_problem_t* p, const ShardInfo* shard, const
   int* nv = (int*)(ws + pl.o_nv);
   uint16_t* hvt = (uint16_t*)(ws + pl.o_hvt);
   uint16_t* g = (uint16_t*)(ws + pl.o_g);
-  uint16_t* gt = (uint16_t*)(ws + pl.o_gt);
-  uint16_t* wst = (uint16_t*)(ws + pl.o_wst);
   float* dh32 = (float*)(ws + pl.o_dh32);
   const uint16_t* h = (const uint16_t*)H;
   const uint16_t* w = (const uint16_t*)W;
@@ -1363,45 +1469,42 @@ lce_status_t backward_impl(const lce_problem_t* p, const ShardInfo* shard, const
   L(K_TRANSPOSE_H, k_transpose, dim3((unsigned)(npad / 64), (unsigned)((d + 63) / 64)), dim3(256), h, pl.ldh,
     (const int*)idx, (int64_t)0, (const int*)nv, 0, d, hvt, (int64_t)npad, npad);
   const int dt = (d + TILE - 1) / TILE;
-  void (*dw_kernel)(const uint16_t*, int, int, const uint16_t*, int, const int*, int, uint16_t*, int64_t,
+  void (*dw_kernel)(const uint16_t*, int, int, int, const uint16_t*, int, const int*, int, uint16_t*, int64_t,
                     AdamWState, AdamWConst) =
       adamw ? k_bwd_dw<DW_ADAMW> : accumulate ? k_bwd_dw<DW_ACCUMULATE> : k_bwd_dw<DW_STORE>;
   for (int64_t s = 0; s < pl.nslab; ++s) {
     const int64_t v0 = s * pl.vc;
     const int vs = (int)(pl.v - v0 < pl.vc ? pl.v - v0 : pl.vc);
-    const int vs64 = (int)round_up(vs, 64);
     const int tm = (vs + TILE - 1) / TILE;
-    // W slab rows are read here (transposed copy, G tile) before the dW epilogue of the same slab
-    // may update them; later slabs read only their own rows, dH only the transposed copy
-    L(K_TRANSPOSE_W, k_transpose, dim3((unsigned)(vs64 / 64), (unsigned)((d + 63) / 64)), dim3(256), w, pl.ldw,
-      (const int*)nullptr, v0, (const int*)nullptr, vs, d, wst, (int64_t)vc, vs64);
     if (kd) {
       // teacher probabilities of this slab, then G = c (softmax(zs / T) - P) / T
       float* P = (float*)(ws + pl.bwd_bytes);
       L(K_KD_P, k_bwd_g<P_WRITE>, dim3((unsigned)(tm * pl.nt_max)), dim3(NTHREADS), kd->wt, kd->ldwt, v0, vs,
         kd->ht, kd->ldht, pl.n, targets, p->target_bytes, (int64_t)0, (const int*)idx, (const int*)nv, kd->lse_t,
-        grad_loss, (const int*)n_valid, p->reduction, kd->dt, tm, (uint16_t*)nullptr, vc, (uint16_t*)nullptr, npad,
+        grad_loss, (const int*)n_valid, p->reduction, kd->dt, tm, (uint16_t*)nullptr, vc, npad,
         kd->scale2, kd->inv_t, P, (float*)nullptr, (int64_t)0);
       if (kd->qpart)
         L(K_BWD_G, k_bwd_g<G_SOFT_Q>, dim3((unsigned)(tm * pl.nt_max)), dim3(NTHREADS), w, pl.ldw, v0, vs, h,
           pl.ldh, pl.n, targets, p->target_bytes, (int64_t)0, (const int*)idx, (const int*)nv, lse, grad_loss,
-          (const int*)n_valid, p->reduction, d, tm, g, vc, gt, npad, kd->scale2, kd->inv_t, P, kd->qpart,
+          (const int*)n_valid, p->reduction, d, tm, g, vc, npad, kd->scale2, kd->inv_t, P, kd->qpart,
           (int64_t)(2 * (v0 / TILE)));
       else
         L(K_BWD_G, k_bwd_g<G_SOFT>, dim3((unsigned)(tm * pl.nt_max)), dim3(NTHREADS), w, pl.ldw, v0, vs, h,
           pl.ldh, pl.n, targets, p->target_bytes, (int64_t)0, (const int*)idx, (const int*)nv, lse, grad_loss,
-          (const int*)n_valid, p->reduction, d, tm, g, vc, gt, npad, kd->scale2, kd->inv_t, P, (float*)nullptr,
+          (const int*)n_valid, p->reduction, d, tm, g, vc, npad, kd->scale2, kd->inv_t, P, (float*)nullptr,
           (int64_t)0);
     } else {
       L(K_BWD_G, k_bwd_g<G_ONEHOT>, dim3((unsigned)(tm * pl.nt_max)), dim3(NTHREADS), w, pl.ldw, v0, vs, h, pl.ldh,
         pl.n, targets, p->target_bytes, si.v_begin, (const int*)idx, (const int*)nv, lse, grad_loss,
-        (const int*)n_valid, p->reduction, d, tm, g, vc, gt, npad, kLog2e, 1.f, (float*)nullptr, (float*)nullptr,
+        (const int*)n_valid, p->reduction, d, tm, g, vc, npad, kLog2e, 1.f, (float*)nullptr, (float*)nullptr,
         (int64_t)0);
     }
-    L(K_BWD_DW, dw_kernel, dim3((unsigned)(8 * ((tm + 7) / 8) * dt)), dim3(NTHREADS), (const uint16_t*)gt, npad,
+    // dH reads the slab's W rows before the dW launch, whose AdamW epilogue (in-backward step)
+    // may update them; later slabs read only their own rows
+    L(K_BWD_DH, k_bwd_dh, dim3((unsigned)(8 * ((pl.nt_max + 7) / 8) * dt)), dim3(NTHREADS), (const uint16_t*)g, vc, vs,
+      w + v0 * pl.ldw, pl.ldw, pl.v - v0, d, (const int*)nv, dh32, (int)(s > 0));
+    L(K_BWD_DW, dw_kernel, dim3((unsigned)(8 * ((tm + 7) / 8) * dt)), dim3(NTHREADS), (const uint16_t*)g, vc, npad,
       vs, (const uint16_t*)hvt, d, (const int*)nv, tm, dW, v0, as, c);
-    L(K_BWD_DH, k_bwd_dh, dim3((unsigned)(8 * ((pl.nt_max + 7) / 8) * dt)), dim3(NTHREADS), (const uint16_t*)g, vc, vs64,
-      (const uint16_t*)wst, d, (const int*)nv, dh32, (int)(s > 0));
   }
   const int64_t nthr = pl.n * pl.d / 8;
   L(K_DH_FINAL, k_dh_finalize, dim3((unsigned)((nthr + 255) / 256)), dim3(256), (const float*)dh32,
@@ -1580,11 +1683,11 @@ lce_status_t kd_forward_impl(const lce_kd_problem_t* p, const void* Hs, const vo
     L(K_KD_P, k_bwd_g<P_WRITE>, dim3((unsigned)(tm * pl.nt_max)), dim3(NTHREADS), wt, tp.ldw, v0, vs, ht, tp.ldh,
       pl.n, targets, p->target_bytes, (int64_t)0, (const int*)idx, (const int*)nv, (const float*)lse_t,
       (const float*)nullptr, (const int*)nullptr, p->reduction, (int)tp.d, tm, (uint16_t*)nullptr, vc,
-      (uint16_t*)nullptr, npad, k.scale2, k.inv_t, P, (float*)nullptr, (int64_t)0);
+      npad, k.scale2, k.inv_t, P, (float*)nullptr, (int64_t)0);
     L(K_KD_Q, k_bwd_g<Q_SOFT>, dim3((unsigned)(tm * pl.nt_max)), dim3(NTHREADS), wsm, pl.ldw, v0, vs, hs, pl.ldh,
       pl.n, targets, p->target_bytes, (int64_t)0, (const int*)idx, (const int*)nv, (const float*)lse_s,
       (const float*)nullptr, (const int*)nullptr, p->reduction, (int)pl.d, tm, (uint16_t*)nullptr, vc,
-      (uint16_t*)nullptr, npad, k.scale2, k.inv_t, P, qpart, (int64_t)(2 * (v0 / TILE)));
+      npad, k.scale2, k.inv_t, P, qpart, (int64_t)(2 * (v0 / TILE)));
   }
   L(K_KD_TERMS, k_kd_terms, dim3((unsigned)((pl.n + 255) / 256)), dim3(256), (const float*)qpart,
     2 * pl.vt_count, (int64_t)npad, (const int*)pos, pl.n, (const float*)lse_s, terms, none ? loss : (float*)nullptr);
