@@ -322,7 +322,7 @@ def main():
         "workspace_bytes": int(max(fwd_bytes, bwd_bytes)),
         "logits_bytes_avoided_fp32": int(n) * int(v) * 4,
         "roofline": {"bound": "mfma", "kernel": dom, "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
-                     "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS, "traffic": _traffic(dom),
+                     "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS, "traffic": _traffic(dom) if (wl.name, args.variant) == ("llama8b", "lce") else None,
                      "flops_per_launch": flops_launch, "avg_launch_ms": kernels[dom]["avg_ms"]},
         "kernels_ms_per_step": {k: r["total_ms"] / args.steps for k, r in kernels.items()},
     }
