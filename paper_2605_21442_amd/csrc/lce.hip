@@ -202,17 +202,35 @@ __device__ __forceinline__ float wave_max(float x) {
 // outside the buffer resource (buffer loads return 0 there).
 // ---------------------------------------------------------------------------------------------
 constexpr int KSLICE = 64;
-constexpr int SLICE_BYTES = 65536;      // A (32 KB) + B (32 KB)
-constexpr int LDS_BYTES = 2 * SLICE_BYTES;
 constexpr uint32_t kOobOffset = 0x80000000u;
 
-// One operand of the main loop.
-//  row-major: rsrc covers the tile's 256 rows; off[q] is the byte offset of row
-//             wave*32 + 8q + lane/8 plus this lane's chunk (K offset 0).
-//  K-major:   base points at K-row 0, first column of the tile; rows are ld elements apart and
-//             the buffer holds `bytes` bytes from base on; off[q] is the byte offset of K-row
-//             wave*8 + 2q + lane/32 of a slice plus this lane's chunk. The buffer resource is
-//             rebuilt per slice at base + k0 * ld, so offsets stay small for any buffer size.
+// Tile geometry of the main loop with WM wave rows: the A tile has 128 WM rows (256 or 384), the
+// B tile 256; 4 WM waves (2 or 3 per SIMD). A slice buffer holds the A region (128 WM rows x 128
+// bytes) followed by the B region (32 KB); two buffers.
+template <int WM>
+struct Geo {
+  static constexpr int TM = 128 * WM;
+  static constexpr int NT = 256 * WM;
+  static constexpr int AREG = TM * 128;
+  static constexpr int SLICE = AREG + 32768;
+  static constexpr int LDS = 2 * SLICE;
+};
+constexpr int LDS_BYTES = Geo<2>::LDS;
+constexpr int kDhWM = 3;   // wave rows of the dH contraction
+
+// One operand of the main loop, kW (256 or 384) tile rows (row-major) or tile columns (K-major)
+// wide. Waves w < kW / 32 load it, 4 KB of the operand's region per wave and slice; the load of
+// the q-th kilobyte reads at voffset off[.] + soffset.
+//  OP_DENSE:  rsrc covers the tile's rows (rows past the tile's end read as zeros); off[0] /
+//             off[1] are the byte offsets of row w*32 + lane/8 plus this lane's even / odd-q chunk;
+//             row 8q adds q * qstride (scalar) and the slice's K offset 2 k0 (scalar).
+//  OP_GATHER: rsrc covers the source buffer; off[q] is the byte offset of the gathered row plus
+//             the chunk; the K offset is added as a scalar.
+//  OP_KMAJOR: base points at K-row 0, first column of the tile; rows are ld elements apart and
+//             the buffer holds `bytes` bytes from base on; the buffer resource is rebuilt per slice
+//             at base + k0 * ld, so offsets stay small for any buffer size. kW = 256: off[0] /
+//             off[1] are the offsets for q = 0 / 1, and q = 2 / 3 read 2 qstride (four K-rows)
+//             further; kW = 384: off[q] per q.
 struct Operand {
   __amdgpu_buffer_rsrc_t rsrc;
   i32x4_t rwords;
@@ -220,7 +238,12 @@ struct Operand {
   int64_t ld;
   uint64_t bytes;
   uint32_t off[4];
+  uint32_t qstride;
 };
+
+// How an operand is stored: row-major rows of a dense buffer, row-major rows gathered through a
+// row list, or K-major.
+enum OpKind { OP_DENSE = 0, OP_GATHER = 1, OP_KMAJOR = 2 };
 
 struct FragSet {
   bf16x8_t a[4], b[2];
@@ -232,55 +255,88 @@ __device__ __forceinline__ int lane_chunk_even() {
   return (j & 7) ^ ((j >> 3) & 7);
 }
 
+// K-major swizzle: position in LDS of 16-byte chunk c (of kW / 8) of K-row k, and its inverse.
+//  kW = 256: c ^ (4 (k & 3) + 16 ((k >> 3) & 1));
+//  kW = 384: within each group of 16 chunks c ^ 4 (k & 3), and the three groups rotated by one
+//            for K-rows with bit 3 set.
+// Either way the 4 K-rows x 64 bytes a half-wave reads in one transposing read land on all banks.
 __device__ __forceinline__ int kswz(int k) { return ((k & 3) << 2) | (((k >> 3) & 1) << 4); }
 
-// LDS byte offset, within an operand's 32 KB, of this lane's first transposing read for the
-// 32-column block starting at column c0 of substep 0 (the second read is 2048 bytes further,
-// substep ks adds ks * 8192).
+template <int kW>
+__device__ __forceinline__ int kpos(int k, int c) {
+  if constexpr (kW == 256) {
+    return c ^ kswz(k);
+  } else {
+    const int g = (c >> 4) + ((k >> 3) & 1);
+    return 16 * (g >= 3 ? g - 3 : g) + ((c & 15) ^ ((k & 3) << 2));
+  }
+}
+
+template <int kW>
+__device__ __forceinline__ int kchunk(int k, int pos) {
+  if constexpr (kW == 256) {
+    return pos ^ kswz(k);
+  } else {
+    const int g = (pos >> 4) - ((k >> 3) & 1);
+    return 16 * (g < 0 ? g + 3 : g) + ((pos & 15) ^ ((k & 3) << 2));
+  }
+}
+
+// LDS byte offset, within a kW-wide K-major operand region, of this lane's first transposing read
+// for the 32-column block starting at column c0 of substep 0 (the second read is 8 kW bytes
+// further: 4 K-rows; substep ks adds 32 kW ks: 16 K-rows).
+template <int kW>
 __device__ __forceinline__ uint32_t kmajor_frag_addr(int c0) {
   const int lane = threadIdx.x & 63, g = lane >> 4, i = lane & 15;
   const int k = 8 * (g >> 1) + (i >> 2);
   const int col = c0 + 16 * (g & 1) + 4 * (i & 3);
-  return (uint32_t)(k * 512 + (((col >> 3) ^ kswz(k)) << 4) + (col & 7) * 2);
+  return (uint32_t)(k * kW * 2 + (kpos<kW>(k, col >> 3) << 4) + (col & 7) * 2);
 }
 
+template <int kW>
 __device__ __forceinline__ bf16x8_t read_tr_pair(const char* p) {
   s16x8_t t;
   t.lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)p);
-  t.hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(p + 2048));
+  t.hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)(p + 8 * kW));
   return __builtin_bit_cast(bf16x8_t, t);
 }
 
-// Per-lane LDS read addresses of one operand: row-major uses rd (row base) + kofs[ks];
-// K-major uses tr[block] + ks * 8192.
+// Per-lane LDS read addresses of one operand.
+//  row-major: rk = row base | chunk of substep 0; substep ks reads at rk ^ 32 ks (the chunk index
+//             (2 ks + lane / 32) ^ swz is the substep-0 chunk ^ 2 ks), block b 4096 b further.
+//  K-major:   tr[b] for block b (+ 32 kW ks per substep); for kW = 256 the blocks of a wave's
+//             B columns differ by chunk ^ 4 in every K-row, so only tr[0] is kept.
 template <int kBlocks>
 struct FragAddr {
-  uint32_t rd;
-  uint32_t kofs[4];
+  uint32_t rk;
   uint32_t tr[kBlocks];
 };
 
-template <bool kKM, int kBlocks>
+template <bool kKM, int kW, int kBlocks>
 __device__ __forceinline__ void frag_addr(FragAddr<kBlocks>& fa, int row0) {
   const int lane = threadIdx.x & 63;
   if constexpr (!kKM) {
     const int swz = (lane & 7) ^ ((lane >> 3) & 1);
-    fa.rd = (uint32_t)((row0 + (lane & 31)) * 128);
-#pragma unroll
-    for (int ks = 0; ks < 4; ++ks) fa.kofs[ks] = (uint32_t)((((ks * 2) + (lane >> 5)) ^ swz) * 16);
+    fa.rk = (uint32_t)((row0 + (lane & 31)) * 128) | (uint32_t)(((lane >> 5) ^ swz) * 16);
   } else {
 #pragma unroll
-    for (int b = 0; b < kBlocks; ++b) fa.tr[b] = kmajor_frag_addr(row0 + 32 * b);
+    for (int b = 0; b < kBlocks; ++b) fa.tr[b] = kmajor_frag_addr<kW>(row0 + 32 * b);
   }
 }
 
-template <bool kKM, int kBlocks>
+template <bool kKM, int kW, int kBlocks>
 __device__ __forceinline__ void read_operand(bf16x8_t (&f)[kBlocks], const char* reg, const FragAddr<kBlocks>& fa,
                                              int ks) {
+  if constexpr (!kKM) {
+    const char* p = reg + (fa.rk ^ (uint32_t)(32 * ks));
 #pragma unroll
-  for (int b = 0; b < kBlocks; ++b) {
-    if constexpr (!kKM) f[b] = *reinterpret_cast<const bf16x8_t*>(reg + fa.rd + b * 4096 + fa.kofs[ks]);
-    else f[b] = read_tr_pair(reg + fa.tr[b] + ks * 8192);
+    for (int b = 0; b < kBlocks; ++b) f[b] = *reinterpret_cast<const bf16x8_t*>(p + b * 4096);
+  } else {
+#pragma unroll
+    for (int b = 0; b < kBlocks; ++b) {
+      const uint32_t a = (kW == 256 && kBlocks == 2) ? (b == 0 ? fa.tr[0] : (fa.tr[0] ^ 64u)) : fa.tr[b];
+      f[b] = read_tr_pair<kW>(reg + a + ks * 32 * kW);
+    }
   }
 }
 
@@ -291,61 +347,67 @@ __device__ __forceinline__ void mma_substep(f32x16_t (&acc)[4][2], const FragSet
     for (int j = 0; j < 2; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[i], f.b[j], acc[i][j], 0, 0, 0);
 }
 
-// This wave's 4 load instructions of one operand's slice k0 (dstp = the operand's region + 4 KB
-// per wave, dst its LDS byte address).
-template <bool kAsm, bool kKM, bool kMasked>
+// This wave's 4 load instructions of one kW-wide operand's slice k0 (dstp = the operand's region
+// + 4 KB per wave, dst its LDS byte address). Lanes that must read zeros (past K on a ragged last
+// slice) point outside the buffer resource.
+template <bool kAsm, int kKind, int kW, bool kMasked>
 __device__ __forceinline__ void load_operand(const Operand& op, const char* dstp, int dst, int k0, int K) {
-  if constexpr (!kKM) {
-    if (!kMasked) {
+  if constexpr (kKind != OP_KMAJOR) {
+    const int ce = lane_chunk_even();
 #pragma unroll
-      for (int q = 0; q < 4; ++q)
-        dma16<kAsm>(op.rsrc, op.rwords, dstp + q * 1024, dst + q * 1024, op.off[q], (uint32_t)k0 * 2);
-    } else {
-      const int ce = lane_chunk_even();
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const bool ok = k0 + (ce ^ (q & 1)) * 8 < K;
-        dma16<kAsm>(op.rsrc, op.rwords, dstp + q * 1024, dst + q * 1024, ok ? op.off[q] + (uint32_t)k0 * 2 : kOobOffset,
-                    0u);
-      }
+    for (int q = 0; q < 4; ++q) {
+      const bool ok = !kMasked || k0 + (ce ^ (q & 1)) * 8 < K;
+      const uint32_t v = kKind == OP_DENSE ? op.off[q & 1] : op.off[q];
+      const uint32_t so = (uint32_t)k0 * 2 + (kKind == OP_DENSE ? (uint32_t)q * op.qstride : 0u);
+      dma16<kAsm>(op.rsrc, op.rwords, dstp + q * 1024, dst + q * 1024, ok ? v : kOobOffset, so);
     }
   } else {
     const uint16_t* base = op.base + (int64_t)k0 * op.ld;
     const uint64_t bytes = op.bytes - (uint64_t)k0 * op.ld * 2;
     const __amdgpu_buffer_rsrc_t rs = make_rsrc(base, bytes);
     const i32x4_t rw = make_rsrc_words(base, bytes);
-    const int krow = (threadIdx.x >> 6) * 8 + ((threadIdx.x & 63) >> 5);
+    const int p0 = (threadIdx.x >> 6) * 256 + (threadIdx.x & 63);   // 16-byte unit of q = 0
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      const bool ok = !kMasked || k0 + krow + 2 * q < K;
-      dma16<kAsm>(rs, rw, dstp + q * 1024, dst + q * 1024, ok ? op.off[q] : kOobOffset, 0u);
+      const bool ok = !kMasked || k0 + (p0 + 64 * q) / (kW / 8) < K;
+      const uint32_t v = kW == 256 ? op.off[q & 1] : op.off[q];
+      const uint32_t so = kW == 256 ? (uint32_t)(q & 2) * op.qstride : 0u;   // off[1] holds q = 1's rows
+      dma16<kAsm>(rs, rw, dstp + q * 1024, dst + q * 1024, ok ? v : kOobOffset, so);
     }
   }
 }
 
-template <bool kAsm, bool kAKM, bool kBKM, bool kMasked>
-__device__ __forceinline__ void load_slice(const Operand& A, const Operand& B, const char* buf, int k0, int K) {
-  const char* dstp = buf + (threadIdx.x >> 6) * 4096;
-  const int dst = kAsm ? __builtin_amdgcn_readfirstlane((int)(uint32_t)(uintptr_t)dstp) : 0;
-  load_operand<kAsm, kAKM, kMasked>(A, dstp, dst, k0, K);
-  load_operand<kAsm, kBKM, kMasked>(B, dstp + 32768, dst + 32768, k0, K);
+template <bool kAsm, int kAKind, int kBKind, int WM, bool kMasked>
+__device__ __forceinline__ void load_slice(const Operand& A, const Operand& B, const char* buf, int bufoff, int k0,
+                                           int K) {
+  const int w = threadIdx.x >> 6;
+  const char* dstp = buf + w * 4096;
+  const int dst = bufoff + __builtin_amdgcn_readfirstlane(w) * 4096;   // LDS byte address (asm loads)
+  load_operand<kAsm, kAKind, Geo<WM>::TM, kMasked>(A, dstp, dst, k0, K);
+  if (WM == 2 || w < 8) load_operand<kAsm, kBKind, 256, kMasked>(B, dstp + Geo<WM>::AREG, dst + Geo<WM>::AREG, k0, K);
 }
 
 // s_waitcnt with only the vector-memory counter constrained (expcnt / lgkmcnt left at max)
 #define LCE_WAIT_VM(n) __builtin_amdgcn_s_waitcnt((((n) & 15) | (7 << 4) | (15 << 8) | (((n) >> 4) << 14)))
 
-template <int kLateGroups, bool kAKM = false, bool kBKM = false>
+// acc = A B^T for this workgroup's (128 WM) x 256 tile. WM = 2: 8 waves, fragments double-
+// buffered (read one substep ahead). WM = 3: 12 waves (three per SIMD), 384 A rows, fragments
+// single-buffered (the 168 registers a wave may hold at three waves per SIMD leave no room for a
+// second set; the other two waves of the SIMD cover the read latency).
+template <int kLateGroups, int kAKind = OP_DENSE, int kBKind = OP_GATHER, int WM = 2, bool kRagged = true>
 __device__ __forceinline__ void mma_mainloop(f32x16_t (&acc)[4][2], const Operand& A, const Operand& B, int K,
                                              char* smem) {
+  using G = Geo<WM>;
+  constexpr bool kAKM = kAKind == OP_KMAJOR, kBKM = kBKind == OP_KMAJOR;
   const int wave = threadIdx.x >> 6;
   const int wr = wave >> 2, wc = wave & 3;
   FragAddr<4> fa;
   FragAddr<2> fb;
-  frag_addr<kAKM>(fa, wr * 128);
-  frag_addr<kBKM>(fb, wc * 64);
+  frag_addr<kAKM, G::TM>(fa, wr * 128);
+  frag_addr<kBKM, 256>(fb, wc * 64);
   auto read_frags = [&](FragSet& f, const char* buf, int ks) {
-    read_operand<kAKM>(f.a, buf, fa, ks);
-    read_operand<kBKM>(f.b, buf + 32768, fb, ks);
+    read_operand<kAKM, G::TM>(f.a, buf, fa, ks);
+    read_operand<kBKM, 256>(f.b, buf + G::AREG, fb, ks);
   };
 
 #pragma unroll
@@ -355,82 +417,120 @@ __device__ __forceinline__ void mma_mainloop(f32x16_t (&acc)[4][2], const Operan
 
   const int S = (K + KSLICE - 1) / KSLICE;
   if (S <= 0) return;
-  const bool ragged = (K % KSLICE) != 0;
+  // kRagged = false: the caller guarantees K % 64 == 0
+  const bool ragged = kRagged && (K % KSLICE) != 0;
   // loads as inline asm where transposing reads are used (see dma16)
   constexpr bool kAsm = kAKM || kBKM;
+  const int lds0 = kAsm ? __builtin_amdgcn_readfirstlane((int)(uint32_t)(uintptr_t)smem) : 0;
   auto load = [&](int s) {
-    char* buf = smem + (s & 1) * SLICE_BYTES;
-    if (ragged && s == S - 1) load_slice<kAsm, kAKM, kBKM, true>(A, B, buf, s * KSLICE, K);
-    else load_slice<kAsm, kAKM, kBKM, false>(A, B, buf, s * KSLICE, K);
+    char* buf = smem + (s & 1) * G::SLICE;
+    const int bufoff = lds0 + (s & 1) * G::SLICE;
+    if (ragged && s == S - 1) load_slice<kAsm, kAKind, kBKind, WM, true>(A, B, buf, bufoff, s * KSLICE, K);
+    else load_slice<kAsm, kAKind, kBKind, WM, false>(A, B, buf, bufoff, s * KSLICE, K);
   };
 
+  // waves of a 12-wave workgroup past the eighth load only A: 4 loads per slice instead of 8
+  const bool a_only = WM == 3 && __builtin_amdgcn_readfirstlane(wave) >= 8;
   load(0);
   if (S > 1) {
     load(1);
-    LCE_WAIT_VM(8);
+    if (a_only) LCE_WAIT_VM(4);
+    else LCE_WAIT_VM(8);
   } else {
     LCE_WAIT_VM(0);
   }
   __builtin_amdgcn_s_barrier();
 
-  // The second wave of each SIMD (waves 4..7) issues its share of a slice's loads kLateGroups
-  // MFMA substeps after the barrier instead of right at it: half the load burst, and one wave
-  // per SIMD goes straight back to MFMA work.
-  const bool late = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6) >= 4;
+  // Waves 0..3 (the first wave of each SIMD) issue their share of a slice's loads at the barrier;
+  // the others kLateGroups MFMA substeps later: a smaller load burst, and the other waves of each
+  // SIMD go straight back to MFMA work.
+  const bool late = __builtin_amdgcn_readfirstlane(wave) >= 4;
   int pend = -1;
-  FragSet f0, f1;
-  read_frags(f0, smem, 0);
-  for (int j = 0; j < S; ++j) {
-    const char* cur = smem + (j & 1) * SLICE_BYTES;
-    const char* nxt = smem + ((j + 1) & 1) * SLICE_BYTES;
-    read_frags(f1, cur, 1);
-    mma_substep(acc, f0);
-    if (kLateGroups == 2 && pend >= 0) {
-      load(pend);
-      pend = -1;
-    }
-    read_frags(f0, cur, 2);
-    mma_substep(acc, f1);
-    read_frags(f1, cur, 3);
-    mma_substep(acc, f0);
-    if (j + 1 < S) {
-      // slice j+1 landed (own loads) and every wave is done with slice j's buffer
-      __builtin_amdgcn_s_waitcnt(0);
-      __builtin_amdgcn_s_barrier();
-      if (j + 2 < S) {
-        if (!late) load(j + 2);
-        else pend = j + 2;
+  if constexpr (WM == 2) {
+    FragSet f0, f1;
+    read_frags(f0, smem, 0);
+    for (int j = 0; j < S; ++j) {
+      const char* cur = smem + (j & 1) * G::SLICE;
+      const char* nxt = smem + ((j + 1) & 1) * G::SLICE;
+      read_frags(f1, cur, 1);
+      mma_substep(acc, f0);
+      if (kLateGroups == 2 && pend >= 0) {
+        load(pend);
+        pend = -1;
       }
-      read_frags(f0, nxt, 0);
+      read_frags(f0, cur, 2);
+      mma_substep(acc, f1);
+      read_frags(f1, cur, 3);
+      mma_substep(acc, f0);
+      if (j + 1 < S) {
+        // slice j+1 landed (own loads) and every wave is done with slice j's buffer
+        __builtin_amdgcn_s_waitcnt(0);
+        __builtin_amdgcn_s_barrier();
+        if (j + 2 < S) {
+          if (!late) load(j + 2);
+          else pend = j + 2;
+        }
+        read_frags(f0, nxt, 0);
+      }
+      mma_substep(acc, f1);
+      if (kLateGroups == 1 && pend >= 0) {
+        load(pend);
+        pend = -1;
+      }
     }
-    mma_substep(acc, f1);
-    if (kLateGroups == 1 && pend >= 0) {
-      load(pend);
-      pend = -1;
+  } else {
+    FragSet f;
+    for (int j = 0; j < S; ++j) {
+      const char* cur = smem + (j & 1) * G::SLICE;
+      read_frags(f, cur, 0);
+      mma_substep(acc, f);
+      if (kLateGroups == 2 && pend >= 0) {
+        load(pend);
+        pend = -1;
+      }
+      read_frags(f, cur, 1);
+      mma_substep(acc, f);
+      read_frags(f, cur, 2);
+      mma_substep(acc, f);
+      read_frags(f, cur, 3);
+      if (j + 1 < S) {
+        // slice j+1 landed (own loads) and every wave is done with slice j's buffer
+        __builtin_amdgcn_s_waitcnt(0);
+        __builtin_amdgcn_s_barrier();
+        if (j + 2 < S) {
+          if (!late) load(j + 2);
+          else pend = j + 2;
+        }
+      }
+      mma_substep(acc, f);
+      if (kLateGroups == 1 && pend >= 0) {
+        load(pend);
+        pend = -1;
+      }
     }
   }
   // every wave is done reading LDS before the caller reuses it
   __syncthreads();
 }
 
-// A row-major operand whose rows [row0, row0 + 256) are wanted (rsrc based at row0): the byte
-// offsets of the 4 rows this lane loads per slice; rows at or beyond `rows_left` are clamped.
+// A row-major operand of rows [row0, row0 + kW) (tile = row0's start) of a dense buffer with
+// rows_left rows from row0 on.
 __device__ __forceinline__ Operand dense_operand(const uint16_t* tile, int rows_left, int64_t ld) {
   Operand op;
   op.rsrc = make_rsrc(tile, (uint64_t)rows_left * ld * 2);
   op.rwords = make_rsrc_words(tile, (uint64_t)rows_left * ld * 2);
   const int j = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int ce = lane_chunk_even();
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    int r = w * 32 + q * 8 + (j >> 3);
-    r = r < rows_left ? r : rows_left - 1;
-    op.off[q] = (uint32_t)((int64_t)r * ld * 2 + (ce ^ (q & 1)) * 16);
-  }
+  const uint32_t row = (uint32_t)((int64_t)(w * 32 + (j >> 3)) * ld * 2);
+  op.off[0] = row + ce * 16;
+  op.off[1] = row + (ce ^ 1) * 16;
+  op.qstride = (uint32_t)(16 * ld);   // 8 rows
   return op;
 }
 
-// Same for rows gathered through the compacted valid-row list idx[0..nv) of a buffer of n rows.
+// kW rows n0.. of the compacted valid-row list idx[0..nv) of a buffer of n rows (rows past nv
+// repeat the last valid one).
+template <int kW = 256>
 __device__ __forceinline__ Operand gather_operand(const uint16_t* src, int64_t n, int64_t ld, const int* idx, int n0,
                                                   int nv) {
   Operand op;
@@ -440,25 +540,30 @@ __device__ __forceinline__ Operand gather_operand(const uint16_t* src, int64_t n
   const int ce = lane_chunk_even();
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
-    int r = n0 + w * 32 + q * 8 + (j >> 3);
+    int r = w * 32 + q * 8 + (j >> 3);
+    r = n0 + (r < kW ? r : kW - 1);
     r = r < nv ? r : nv - 1;
     op.off[q] = (uint32_t)((int64_t)idx[r] * ld * 2 + (ce ^ (q & 1)) * 16);
   }
   return op;
 }
 
-// A K-major operand: K-row 0 of the tile at `base` (its first column), rows `ld` elements apart,
-// `bytes` readable bytes from base on.
+// A kW-wide K-major operand: K-row 0 of the tile at `base` (its first column), rows `ld` elements
+// apart, `bytes` readable bytes from base on.
+template <int kW = 256>
 __device__ __forceinline__ Operand kmajor_operand(const uint16_t* base, int64_t ld, uint64_t bytes) {
   Operand op;
   op.base = base;
   op.ld = ld;
   op.bytes = bytes;
+  op.qstride = (uint32_t)(4 * ld);      // two K-rows (kW = 256)
   const int j = threadIdx.x & 63, w = threadIdx.x >> 6;
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const int k = w * 8 + 2 * q + (j >> 5);
-    op.off[q] = (uint32_t)((int64_t)k * ld * 2 + (((j & 31) ^ kswz(k)) << 4));
+  for (int q = 0; q < (kW == 256 ? 2 : 4); ++q) {
+    int p = w * 256 + q * 64 + j;                       // 16-byte unit of the region
+    p = p < kW * 8 ? p : kW * 8 - 1;                    // (waves that do not load this operand)
+    const int k = p / (kW / 8), pos = p % (kW / 8);
+    op.off[q] = (uint32_t)((int64_t)k * ld * 2 + (kchunk<kW>(k, pos) << 4));
   }
   return op;
 }
@@ -568,7 +673,7 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_fwd_stats(const uint16_t* __res
     const int v0 = vt * TILE;
     const int vleft = v - v0;
     const Operand opa = dense_operand(W + (int64_t)v0 * ldw, vleft, ldw);
-    mma_mainloop<2>(acc, opa, opb, d, smem);
+    mma_mainloop<2, OP_DENSE, OP_GATHER>(acc, opa, opb, d, smem);
 
     // rows (vocabulary ids) of this lane: v0 + wr*128 + 32 bi + 8 (r/4) + 4 (lane/32) + r%4
     const int vb = wr * 128 + (lane >> 5) * 4;
@@ -840,7 +945,7 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_bwd_g(const uint16_t* __restric
   const Operand opa = dense_operand(W + (v0 + vt0) * ldw, vleft, ldw);
   const Operand opb = gather_operand(H, n, ldh, idx, n0, nv);
   f32x16_t acc[4][2];
-  mma_mainloop<2>(acc, opa, opb, d, smem);
+  mma_mainloop<2, OP_DENSE, OP_GATHER>(acc, opa, opb, d, smem);
 
   const float c_all = grad_scale(grad, n_norm, reduction);
   int tok[2], tgt[2];
@@ -993,7 +1098,7 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_bwd_dw(const uint16_t* __restri
   const Operand opa = kmajor_operand(G + m0, vc, ((uint64_t)ldt * vc - m0) * 2);
   const Operand opb = dense_operand(Hvt + (int64_t)d0 * ldt, d - d0, ldt);
   f32x16_t acc[4][2];
-  mma_mainloop<1, true, false>(acc, opa, opb, kpad, smem);
+  mma_mainloop<1, OP_KMAJOR, OP_DENSE>(acc, opa, opb, kpad, smem);
   const int mb = m0 + wr * 128 + (lane >> 5) * 4;
   const int dc = d0 + wc * 64 + (lane & 31);
 #pragma unroll
@@ -1055,54 +1160,34 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_bwd_dw(const uint16_t* __restri
 
 // K6: dH32[m][dd] (+)= sum_k G[m][k] Ws[k][dd] over the slab's k < vs; rows m < Nv. Ws = W + v0 ldw
 // is the slab's first row, read K-major (transposing LDS reads); ws_rows = V - v0 rows follow.
-__global__ __launch_bounds__(NTHREADS, 2) void k_bwd_dh(const uint16_t* __restrict__ G, int vc, int vs,
+template <int WM>
+__global__ __launch_bounds__(Geo<WM>::NT, WM) void k_bwd_dh(const uint16_t* __restrict__ G, int vc, int vs,
                                                         const uint16_t* __restrict__ Ws, int64_t ldw,
                                                         int64_t ws_rows, int d,
                                                         const int* __restrict__ nv_ptr,
                                                         float* __restrict__ dH32, int accumulate) {
-  __shared__ __attribute__((aligned(16))) char smem[LDS_BYTES];
+  constexpr int TM = Geo<WM>::TM;
+  __shared__ __attribute__((aligned(16))) char smem[Geo<WM>::LDS];
   const int nv = *nv_ptr;
   int tm, tn;
-  if (!band_tile((nv + TILE - 1) / TILE, (d + TILE - 1) / TILE, tm, tn)) return;
-  const int m0 = tm * TILE, d0 = tn * TILE;
+  if (!band_tile((nv + TM - 1) / TM, (d + TILE - 1) / TILE, tm, tn)) return;
+  const int m0 = tm * TM, d0 = tn * TILE;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, wr = wave >> 2, wc = wave & 3;
   const Operand opa = dense_operand(G + (int64_t)m0 * vc, nv - m0, vc);
-  const Operand opb = kmajor_operand(Ws + d0, ldw, ((uint64_t)ws_rows * ldw - d0) * 2);
+  const Operand opb = kmajor_operand<TILE>(Ws + d0, ldw, ((uint64_t)ws_rows * ldw - d0) * 2);
   f32x16_t acc[4][2];
-  mma_mainloop<2, false, true>(acc, opa, opb, vs, smem);
-  // Read-modify-write of the fp32 accumulator, one 32-row block (32 values per lane) at a time
-  // so that its 32 loads are in flight together; interior tiles skip the bounds tests.
-  const int mb = m0 + wr * 128 + (lane >> 5) * 4;
+  // K = vs rounded up to 64: G holds zeros there and the W rows past V lie outside the buffer
+  // resource (zeros), so no slice needs masking
+  mma_mainloop<2, OP_DENSE, OP_KMAJOR, WM, false>(acc, opa, opb, (vs + KSLICE - 1) / KSLICE * KSLICE, smem);
+  // Read-modify-write of the fp32 accumulator through a buffer resource over this tile's valid
+  // rows (rows past Nv read 0 and drop their stores): one 32-bit per-lane offset and a
+  // wave-uniform row offset per element, so that only the accumulators occupy registers; one
+  // 32-row block (32 values per lane) at a time, its loads in flight together.
+  const int rows = nv - m0 < TM ? nv - m0 : TM;
+  const __amdgpu_buffer_rsrc_t rd = make_rsrc(dH32 + (int64_t)m0 * d, (uint64_t)rows * d * 4);
   const int dc = d0 + wc * 64 + (lane & 31);
-  const bool interior = (m0 + TILE <= nv) && (d0 + TILE <= d);
-  float* base = dH32 + (int64_t)mb * d + dc;
-  if (interior) {
-    if (accumulate) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        float old[2][16];
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
-#pragma unroll
-          for (int r = 0; r < 16; ++r)
-            old[j][r] = base[(int64_t)(i * 32 + (r >> 2) * 8 + (r & 3)) * d + j * 32];
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
-#pragma unroll
-          for (int r = 0; r < 16; ++r)
-            base[(int64_t)(i * 32 + (r >> 2) * 8 + (r & 3)) * d + j * 32] = old[j][r] + acc[i][j][r];
-      }
-    } else {
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
-#pragma unroll
-          for (int r = 0; r < 16; ++r)
-            base[(int64_t)(i * 32 + (r >> 2) * 8 + (r & 3)) * d + j * 32] = acc[i][j][r];
-    }
-    return;
-  }
+  const uint32_t voff = (uint32_t)(((wr * 128 + (lane >> 5) * 4) * d + dc) * 4);
+  const bool col_ok[2] = {dc < d, dc + 32 < d};
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     float old[2][16];
@@ -1110,17 +1195,21 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_bwd_dh(const uint16_t* __restri
     for (int j = 0; j < 2; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int m = mb + i * 32 + (r >> 2) * 8 + (r & 3);
-        const bool ok = accumulate && m < nv && dc + j * 32 < d;
-        old[j][r] = ok ? dH32[(int64_t)m * d + dc + j * 32] : 0.f;
+        const uint32_t so = (uint32_t)(((i * 32 + (r >> 2) * 8 + (r & 3)) * d + j * 32) * 4);
+        old[j][r] = (accumulate && col_ok[j])
+                        ? __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rd, (int)voff, (int)so, 0))
+                        : 0.f;
       }
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < 2; ++j) {
+      if (!col_ok[j]) continue;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int m = mb + i * 32 + (r >> 2) * 8 + (r & 3);
-        if (m < nv && dc + j * 32 < d) dH32[(int64_t)m * d + dc + j * 32] = old[j][r] + acc[i][j][r];
+        const uint32_t so = (uint32_t)(((i * 32 + (r >> 2) * 8 + (r & 3)) * d + j * 32) * 4);
+        __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, old[j][r] + acc[i][j][r]), rd, (int)voff,
+                                              (int)so, 0);
       }
+    }
   }
 }
 
@@ -1469,6 +1558,7 @@ lce_status_t backward_impl(const lce_problem_t* p, const ShardInfo* shard, const
   L(K_TRANSPOSE_H, k_transpose, dim3((unsigned)(npad / 64), (unsigned)((d + 63) / 64)), dim3(256), h, pl.ldh,
     (const int*)idx, (int64_t)0, (const int*)nv, 0, d, hvt, (int64_t)npad, npad);
   const int dt = (d + TILE - 1) / TILE;
+  const int dh_tiles = (int)((pl.npad + Geo<kDhWM>::TM - 1) / Geo<kDhWM>::TM);
   void (*dw_kernel)(const uint16_t*, int, int, int, const uint16_t*, int, const int*, int, uint16_t*, int64_t,
                     AdamWState, AdamWConst) =
       adamw ? k_bwd_dw<DW_ADAMW> : accumulate ? k_bwd_dw<DW_ACCUMULATE> : k_bwd_dw<DW_STORE>;
@@ -1501,7 +1591,7 @@ lce_status_t backward_impl(const lce_problem_t* p, const ShardInfo* shard, const
     }
     // dH reads the slab's W rows before the dW launch, whose AdamW epilogue (in-backward step)
     // may update them; later slabs read only their own rows
-    L(K_BWD_DH, k_bwd_dh, dim3((unsigned)(8 * ((pl.nt_max + 7) / 8) * dt)), dim3(NTHREADS), (const uint16_t*)g, vc, vs,
+    L(K_BWD_DH, k_bwd_dh<kDhWM>, dim3((unsigned)(8 * ((dh_tiles + 7) / 8) * dt)), dim3(Geo<kDhWM>::NT), (const uint16_t*)g, vc, vs,
       w + v0 * pl.ldw, pl.ldw, pl.v - v0, d, (const int*)nv, dh32, (int)(s > 0));
     L(K_BWD_DW, dw_kernel, dim3((unsigned)(8 * ((tm + 7) / 8) * dt)), dim3(NTHREADS), (const uint16_t*)g, vc, npad,
       vs, (const uint16_t*)hvt, d, (const int*)nv, tm, dW, v0, as, c);
