@@ -217,13 +217,15 @@ struct Geo {
 };
 constexpr int LDS_BYTES = Geo<2>::LDS;
 constexpr int kDhWM = 3;   // wave rows of the dH contraction
+constexpr int kDwWM = 3;   // wave rows of the dW contraction
 
 // One operand of the main loop, kW (256 or 384) tile rows (row-major) or tile columns (K-major)
 // wide. Waves w < kW / 32 load it, 4 KB of the operand's region per wave and slice; the load of
 // the q-th kilobyte reads at voffset off[.] + soffset.
-//  OP_DENSE:  rsrc covers the tile's rows (rows past the tile's end read as zeros); off[0] /
-//             off[1] are the byte offsets of row w*32 + lane/8 plus this lane's even / odd-q chunk;
-//             row 8q adds q * qstride (scalar) and the slice's K offset 2 k0 (scalar).
+//  OP_DENSE:  rsrc covers the tile's rows (rows past the tile's end read as zeros); off[0] is
+//             the byte offset of row w*32 + lane/8 plus this lane's even-q chunk (odd q: the
+//             neighbouring lane's); row 8q adds q * qstride (scalar) and the slice's K offset
+//             2 k0 (scalar).
 //  OP_GATHER: rsrc covers the source buffer; off[q] is the byte offset of the gathered row plus
 //             the chunk; the K offset is added as a scalar.
 //  OP_KMAJOR: base points at K-row 0, first column of the tile; rows are ld elements apart and
@@ -304,12 +306,13 @@ __device__ __forceinline__ bf16x8_t read_tr_pair(const char* p) {
 // Per-lane LDS read addresses of one operand.
 //  row-major: rk = row base | chunk of substep 0; substep ks reads at rk ^ 32 ks (the chunk index
 //             (2 ks + lane / 32) ^ swz is the substep-0 chunk ^ 2 ks), block b 4096 b further.
-//  K-major:   tr[b] for block b (+ 32 kW ks per substep); for kW = 256 the blocks of a wave's
-//             B columns differ by chunk ^ 4 in every K-row, so only tr[0] is kept.
+//  K-major:   tr for block 0 (+ 32 kW ks per substep); block b (32 columns further) reads at
+//             tr ^ (b << 6): within a wave's 128 or 64 columns the block index only changes bits
+//             2-3 of the chunk index, which both swizzles keep as an XOR.
 template <int kBlocks>
 struct FragAddr {
   uint32_t rk;
-  uint32_t tr[kBlocks];
+  uint32_t tr;
 };
 
 template <bool kKM, int kW, int kBlocks>
@@ -319,8 +322,7 @@ __device__ __forceinline__ void frag_addr(FragAddr<kBlocks>& fa, int row0) {
     const int swz = (lane & 7) ^ ((lane >> 3) & 1);
     fa.rk = (uint32_t)((row0 + (lane & 31)) * 128) | (uint32_t)(((lane >> 5) ^ swz) * 16);
   } else {
-#pragma unroll
-    for (int b = 0; b < kBlocks; ++b) fa.tr[b] = kmajor_frag_addr<kW>(row0 + 32 * b);
+    fa.tr = kmajor_frag_addr<kW>(row0);
   }
 }
 
@@ -333,10 +335,7 @@ __device__ __forceinline__ void read_operand(bf16x8_t (&f)[kBlocks], const char*
     for (int b = 0; b < kBlocks; ++b) f[b] = *reinterpret_cast<const bf16x8_t*>(p + b * 4096);
   } else {
 #pragma unroll
-    for (int b = 0; b < kBlocks; ++b) {
-      const uint32_t a = (kW == 256 && kBlocks == 2) ? (b == 0 ? fa.tr[0] : (fa.tr[0] ^ 64u)) : fa.tr[b];
-      f[b] = read_tr_pair<kW>(reg + a + ks * 32 * kW);
-    }
+    for (int b = 0; b < kBlocks; ++b) f[b] = read_tr_pair<kW>(reg + (fa.tr ^ (uint32_t)(b << 6)) + ks * 32 * kW);
   }
 }
 
@@ -354,10 +353,13 @@ template <bool kAsm, int kKind, int kW, bool kMasked>
 __device__ __forceinline__ void load_operand(const Operand& op, const char* dstp, int dst, int k0, int K) {
   if constexpr (kKind != OP_KMAJOR) {
     const int ce = lane_chunk_even();
+    // dense: the odd-q offset of lane L is the even-q offset of lane L ^ 1 (same row, the chunk
+    // with the other parity), fetched by a quad swap instead of held in a register
+    const uint32_t odd = kKind == OP_DENSE ? (uint32_t)__builtin_amdgcn_mov_dpp((int)op.off[0], 0xB1, 0xF, 0xF, false) : 0u;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const bool ok = !kMasked || k0 + (ce ^ (q & 1)) * 8 < K;
-      const uint32_t v = kKind == OP_DENSE ? op.off[q & 1] : op.off[q];
+      const uint32_t v = kKind == OP_DENSE ? ((q & 1) ? odd : op.off[0]) : op.off[q];
       const uint32_t so = (uint32_t)k0 * 2 + (kKind == OP_DENSE ? (uint32_t)q * op.qstride : 0u);
       dma16<kAsm>(op.rsrc, op.rwords, dstp + q * 1024, dst + q * 1024, ok ? v : kOobOffset, so);
     }
@@ -523,7 +525,6 @@ __device__ __forceinline__ Operand dense_operand(const uint16_t* tile, int rows_
   const int ce = lane_chunk_even();
   const uint32_t row = (uint32_t)((int64_t)(w * 32 + (j >> 3)) * ld * 2);
   op.off[0] = row + ce * 16;
-  op.off[1] = row + (ce ^ 1) * 16;
   op.qstride = (uint32_t)(16 * ld);   // 8 rows
   return op;
 }
@@ -1076,85 +1077,107 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_bwd_g(const uint16_t* __restric
 }
 
 // K5: dW[v0 + m][dd] = sum_k G[k][m] Hvt[dd][k] over k < round_up(Nv, 64), G [Npad][vc] read
-// K-major (transposing LDS reads), Hvt [D][Npad] row-major. The epilogue either
-// writes the block in bf16 (each element once), adds it to the bf16 values already there, or
-// hands each bf16-rounded element straight to the AdamW update of W (the in-backward step).
+// K-major (transposing LDS reads), Hvt [D][Npad] row-major; tiles of (128 WM) ids x 256 hidden
+// columns. The epilogue either writes the block in bf16 (each element once), adds it to the bf16
+// values already there, or hands each bf16-rounded element straight to the AdamW update of W (the
+// in-backward step). Its accesses go through buffer resources over the tile's rows below the slab
+// width (rows past it read 0 and drop their stores): a per-lane 32-bit offset and a wave-uniform
+// row offset per element, so that the accumulators are nearly the only registers it holds.
 enum DwMode { DW_STORE = 0, DW_ACCUMULATE = 1, DW_ADAMW = 2 };
 
-template <int kMode>
-__global__ __launch_bounds__(NTHREADS, 2) void k_bwd_dw(const uint16_t* __restrict__ G, int vc, int ldt, int vs,
-                                                        const uint16_t* __restrict__ Hvt, int d,
-                                                        const int* __restrict__ nv_ptr, int tm_count,
-                                                        uint16_t* __restrict__ dW, int64_t v0,
-                                                        AdamWState st, AdamWConst oc) {
-  __shared__ __attribute__((aligned(16))) char smem[LDS_BYTES];
+template <int kMode, int WM>
+__global__ __launch_bounds__(Geo<WM>::NT, WM) void k_bwd_dw(const uint16_t* __restrict__ G, int vc, int ldt, int vs,
+                                                           const uint16_t* __restrict__ Hvt, int d,
+                                                           const int* __restrict__ nv_ptr, int tm_count,
+                                                           uint16_t* __restrict__ dW, int64_t v0,
+                                                           AdamWState st, AdamWConst oc) {
+  constexpr int TM = Geo<WM>::TM;
+  __shared__ __attribute__((aligned(16))) char smem[Geo<WM>::LDS];
   int tm, tn;
   if (!band_tile(tm_count, (d + TILE - 1) / TILE, tm, tn)) return;
-  const int m0 = tm * TILE, d0 = tn * TILE;
+  const int m0 = tm * TM, d0 = tn * TILE;
   const int nv = *nv_ptr;
   const int kpad = ((nv + KPAD - 1) / KPAD) * KPAD;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, wr = wave >> 2, wc = wave & 3;
   // ldt = Npad: G has Npad rows of vc ids, Hvt D rows of Npad tokens
-  const Operand opa = kmajor_operand(G + m0, vc, ((uint64_t)ldt * vc - m0) * 2);
+  const Operand opa = kmajor_operand<TM>(G + m0, vc, ((uint64_t)ldt * vc - m0) * 2);
   const Operand opb = dense_operand(Hvt + (int64_t)d0 * ldt, d - d0, ldt);
   f32x16_t acc[4][2];
-  mma_mainloop<1, OP_KMAJOR, OP_DENSE>(acc, opa, opb, kpad, smem);
-  const int mb = m0 + wr * 128 + (lane >> 5) * 4;
+  mma_mainloop<1, OP_KMAJOR, OP_DENSE, WM, false>(acc, opa, opb, kpad, smem);
+
+  const int rows = vs - m0 < TM ? vs - m0 : TM;             // valid id rows of this tile
+  const int64_t r0 = v0 + m0;                               // its first row of W / dW
   const int dc = d0 + wc * 64 + (lane & 31);
+  const int lrow = wr * 128 + (lane >> 5) * 4;              // this lane's first tile row
+  const bool col_ok[2] = {dc < d, dc + 32 < d};
+  // row offset (in elements of a row of `stride`) of block i, register r
+  auto erow = [](int i, int r) { return i * 32 + (r >> 2) * 8 + (r & 3); };
+  if constexpr (kMode != DW_ADAMW) {
+    const __amdgpu_buffer_rsrc_t rw = make_rsrc(dW + r0 * d, (uint64_t)rows * d * 2);
+    const uint32_t voff = (uint32_t)((lrow * d + dc) * 2);
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    const int col = dc + j * 32;
-    if (col >= d) continue;
+    for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      if constexpr (kMode == DW_STORE) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int m = mb + i * 32 + (r >> 2) * 8 + (r & 3);
-          if (m < vs) dW[(v0 + m) * d + col] = to_bf16(acc[i][j][r]);
-        }
-      } else if constexpr (kMode == DW_ACCUMULATE) {
+      for (int j = 0; j < 2; ++j) {
+        if (!col_ok[j]) continue;
         float old[16];
+        if constexpr (kMode == DW_ACCUMULATE) {
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int m = mb + i * 32 + (r >> 2) * 8 + (r & 3);
-          old[r] = m < vs ? bf16_to_f32(dW[(v0 + m) * d + col]) : 0.f;
+          for (int r = 0; r < 16; ++r) {
+            const uint32_t so = (uint32_t)((erow(i, r) * d + j * 32) * 2);
+            old[r] = bf16_to_f32(__builtin_amdgcn_raw_buffer_load_b16(rw, (int)voff, (int)so, 0));
+          }
         }
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const int m = mb + i * 32 + (r >> 2) * 8 + (r & 3);
-          if (m < vs) dW[(v0 + m) * d + col] = to_bf16(old[r] + acc[i][j][r]);
+          const uint32_t so = (uint32_t)((erow(i, r) * d + j * 32) * 2);
+          const float x = kMode == DW_ACCUMULATE ? old[r] + acc[i][j][r] : acc[i][j][r];
+          __builtin_amdgcn_raw_buffer_store_b16(to_bf16(x), rw, (int)voff, (int)so, 0);
         }
-      } else {
+      }
+  } else {
+    // moments (and master) fp32 with row stride d, W bf16 with row stride ldw
+    const __amdgpu_buffer_rsrc_t rm = make_rsrc(st.m + r0 * d, (uint64_t)rows * d * 4);
+    const __amdgpu_buffer_rsrc_t rv = make_rsrc(st.v + r0 * d, (uint64_t)rows * d * 4);
+    const __amdgpu_buffer_rsrc_t rp = make_rsrc(st.master ? st.master + r0 * d : st.m, st.master ? (uint64_t)rows * d * 4 : 0);
+    const __amdgpu_buffer_rsrc_t rW = make_rsrc(st.W + r0 * st.ldw, (uint64_t)rows * st.ldw * 2);
+    const bool has_master = st.master != nullptr;
+    const uint32_t vo4 = (uint32_t)((lrow * d + dc) * 4);
+    const uint32_t voW = (uint32_t)((lrow * st.ldw + dc) * 2);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        if (!col_ok[j]) continue;
         // four consecutive rows at a time: all their loads first, then the updates and stores
 #pragma unroll
         for (int rq = 0; rq < 4; ++rq) {
-          const int mq = mb + i * 32 + rq * 8;
-          const int64_t base = (v0 + mq) * d + col;
-          const int64_t wbase = (v0 + mq) * st.ldw + col;
           float p[4], mo[4], vo[4];
 #pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            if (mq + r < vs) {
-              mo[r] = st.m[base + r * d];
-              vo[r] = st.v[base + r * d];
-              p[r] = st.master ? st.master[base + r * d] : bf16_to_f32(st.W[wbase + r * st.ldw]);
-            }
+          for (int e = 0; e < 4; ++e) {
+            const int row = erow(i, rq * 4 + e);
+            const uint32_t s4 = (uint32_t)((row * d + j * 32) * 4);
+            const uint32_t sW = (uint32_t)((row * st.ldw + j * 32) * 2);
+            mo[e] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rm, (int)vo4, (int)s4, 0));
+            vo[e] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rv, (int)vo4, (int)s4, 0));
+            p[e] = has_master ? __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rp, (int)vo4, (int)s4, 0))
+                              : bf16_to_f32(__builtin_amdgcn_raw_buffer_load_b16(rW, (int)voW, (int)sW, 0));
           }
 #pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            if (mq + r < vs) {
-              const float g = bf16_to_f32(to_bf16(acc[i][j][rq * 4 + r]));
-              adamw_update(p[r], mo[r], vo[r], g, oc);
-              st.m[base + r * d] = mo[r];
-              st.v[base + r * d] = vo[r];
-              if (st.master) st.master[base + r * d] = p[r];
-              st.W[wbase + r * st.ldw] = to_bf16(p[r]);
-            }
+          for (int e = 0; e < 4; ++e) {
+            const int row = erow(i, rq * 4 + e);
+            const uint32_t s4 = (uint32_t)((row * d + j * 32) * 4);
+            const uint32_t sW = (uint32_t)((row * st.ldw + j * 32) * 2);
+            const float g = bf16_to_f32(to_bf16(acc[i][j][rq * 4 + e]));
+            adamw_update(p[e], mo[e], vo[e], g, oc);
+            __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, mo[e]), rm, (int)vo4, (int)s4, 0);
+            __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, vo[e]), rv, (int)vo4, (int)s4, 0);
+            if (has_master)
+              __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, p[e]), rp, (int)vo4, (int)s4, 0);
+            __builtin_amdgcn_raw_buffer_store_b16(to_bf16(p[e]), rW, (int)voW, (int)sW, 0);
           }
         }
       }
-    }
   }
 }
 
@@ -1354,16 +1377,19 @@ lce_status_t make_plan(const lce_problem_t* p, Plan* pl) {
   // 32-bit limits: token / vocabulary indices, and byte offsets inside one buffer resource
   if (p->n >= (int64_t)1 << 30 || p->v >= (int64_t)1 << 30 || p->d >= (int64_t)1 << 20) return LCE_ERR_SHAPE;
   if ((uint64_t)p->n * ldh * 2 > 0x7FFFFFFFull) return LCE_ERR_SHAPE;
+  // byte offsets within one 384-row tile of W (bf16) and of the fp32 optimizer state
+  if ((uint64_t)384 * ldw * 2 > 0x7FFFFFFFull || (uint64_t)384 * p->d * 4 > 0x7FFFFFFFull) return LCE_ERR_SHAPE;
   pl->n = p->n; pl->d = p->d; pl->v = p->v; pl->ldh = ldh; pl->ldw = ldw;
   pl->npad = round_up(p->n > 0 ? p->n : 1, TILE);
   pl->nt_max = (int)(pl->npad / TILE);
   pl->vt_count = (int)((p->v + TILE - 1) / TILE);
   pl->nparts = pl->vt_count < MAX_PARTS ? pl->vt_count : MAX_PARTS;
-  // backward vocabulary slab: 4 D columns (at least 8192) keeps G at O(N D) while
-  // halving the dH accumulator passes of a 2 D slab
+  // backward vocabulary slab: about 4 D columns (at least 8192) keeps G at O(N D) while halving
+  // the dH accumulator passes of a 2 D slab; a multiple of 16 tiles of 384 ids, so that the dW
+  // launch of a 4096-wide head is whole rounds of workgroups on 256 CUs
   int64_t vc = 4 * p->d;
   if (vc < 8192) vc = 8192;
-  vc = round_up(vc, TILE);
+  vc = round_up(vc, 16 * 384);
   const int64_t vround = round_up(p->v, TILE);
   if (vc > vround) vc = vround;
   pl->vc = vc;
@@ -1561,7 +1587,7 @@ lce_status_t backward_impl(const lce_problem_t* p, const ShardInfo* shard, const
   const int dh_tiles = (int)((pl.npad + Geo<kDhWM>::TM - 1) / Geo<kDhWM>::TM);
   void (*dw_kernel)(const uint16_t*, int, int, int, const uint16_t*, int, const int*, int, uint16_t*, int64_t,
                     AdamWState, AdamWConst) =
-      adamw ? k_bwd_dw<DW_ADAMW> : accumulate ? k_bwd_dw<DW_ACCUMULATE> : k_bwd_dw<DW_STORE>;
+      adamw ? k_bwd_dw<DW_ADAMW, kDwWM> : accumulate ? k_bwd_dw<DW_ACCUMULATE, kDwWM> : k_bwd_dw<DW_STORE, kDwWM>;
   for (int64_t s = 0; s < pl.nslab; ++s) {
     const int64_t v0 = s * pl.vc;
     const int vs = (int)(pl.v - v0 < pl.vc ? pl.v - v0 : pl.vc);
@@ -1593,8 +1619,9 @@ lce_status_t backward_impl(const lce_problem_t* p, const ShardInfo* shard, const
     // may update them; later slabs read only their own rows
     L(K_BWD_DH, k_bwd_dh<kDhWM>, dim3((unsigned)(8 * ((dh_tiles + 7) / 8) * dt)), dim3(Geo<kDhWM>::NT), (const uint16_t*)g, vc, vs,
       w + v0 * pl.ldw, pl.ldw, pl.v - v0, d, (const int*)nv, dh32, (int)(s > 0));
-    L(K_BWD_DW, dw_kernel, dim3((unsigned)(8 * ((tm + 7) / 8) * dt)), dim3(NTHREADS), (const uint16_t*)g, vc, npad,
-      vs, (const uint16_t*)hvt, d, (const int*)nv, tm, dW, v0, as, c);
+    const int tmw = (vs + Geo<kDwWM>::TM - 1) / Geo<kDwWM>::TM;
+    L(K_BWD_DW, dw_kernel, dim3((unsigned)(8 * ((tmw + 7) / 8) * dt)), dim3(Geo<kDwWM>::NT), (const uint16_t*)g, vc,
+      npad, vs, (const uint16_t*)hvt, d, (const int*)nv, tmw, dW, v0, as, c);
   }
   const int64_t nthr = pl.n * pl.d / 8;
   L(K_DH_FINAL, k_dh_finalize, dim3((unsigned)((nthr + 255) / 256)), dim3(256), (const float*)dh32,
