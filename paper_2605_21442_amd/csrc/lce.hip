@@ -33,6 +33,7 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <algorithm>
 #include <mutex>
 #include <type_traits>
 #include <utility>
@@ -218,6 +219,7 @@ struct Geo {
 constexpr int LDS_BYTES = Geo<2>::LDS;
 constexpr int kDhWM = 3;   // wave rows of the dH contraction
 constexpr int kDwWM = 3;   // wave rows of the dW contraction
+constexpr int kGWM = 3;    // wave rows of the (one-hot) G kernel
 
 // One operand of the main loop, kW (256 or 384) tile rows (row-major) or tile columns (K-major)
 // wide. Waves w < kW / 32 load it, 4 KB of the operand's region per wave and slice; the load of
@@ -826,59 +828,23 @@ __global__ void k_fwd_empty(float* loss, int* nv_user, int* status) {
 }
 
 // ---------------------------------------------------------------------------------------------
-// Backward helpers
+// Hv[i][:] = H[idx[i]][:] for i < Nv (rows of d elements), zero rows up to round_up(Nv, 64): the
+// valid rows of H made contiguous. It is the B operand of the backward G tiles (row-major) and of
+// the dW contraction (K-major over tokens), so neither main loop gathers rows itself.
 // ---------------------------------------------------------------------------------------------
-
-// out[c][r] = src row (idx ? idx[r] : r0 + r) column c, for r < rows_ok; 0 for rows_ok <= r < rows_out.
-// 64x64 tiles through LDS. rows_ok comes from *cnt_ptr when given (device count), else cnt.
-__global__ __launch_bounds__(256) void k_transpose(const uint16_t* __restrict__ src, int64_t lds_, const int* __restrict__ idx,
-                                                   int64_t r0, const int* __restrict__ cnt_ptr, int cnt, int cols,
-                                                   uint16_t* __restrict__ out, int64_t ldo, int rows_out_pad64) {
-  __shared__ uint16_t tile[64][64 + 2];
-  const int rows_ok = cnt_ptr ? *cnt_ptr : cnt;
-  const int rt = blockIdx.x, ct = blockIdx.y;
-  const int rbeg = rt * 64, cbeg = ct * 64;
-  const int rlim = cnt_ptr ? ((rows_ok + 63) / 64) * 64 : rows_out_pad64;
-  if (rbeg >= rlim) return;
-  const int t = threadIdx.x;
-  {  // load: thread t -> row t/4, 16 columns starting at (t%4)*16
-    const int r = rbeg + t / 4;
-    const int c0 = cbeg + (t % 4) * 16;
-    uint16_t vals[16];
-#pragma unroll
-    for (int q = 0; q < 16; ++q) vals[q] = 0;
-    if (r < rows_ok) {
-      const int64_t srow = idx ? (int64_t)idx[r] : r0 + r;
-      const uint16_t* p = src + srow * lds_;
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        if (c0 + h * 8 < cols) {
-          const uint4 u = *reinterpret_cast<const uint4*>(p + c0 + h * 8);
-          const uint32_t w4[4] = {u.x, u.y, u.z, u.w};
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            vals[h * 8 + 2 * q] = (uint16_t)(w4[q] & 0xFFFF);
-            vals[h * 8 + 2 * q + 1] = (uint16_t)(w4[q] >> 16);
-          }
-        }
-      }
-    }
-#pragma unroll
-    for (int q = 0; q < 16; ++q) tile[t / 4][(t % 4) * 16 + q] = vals[q];
-  }
-  __syncthreads();
-  {  // store: thread t -> output row (column of src) t/4, 16 consecutive source rows
-    const int c = cbeg + t / 4;
-    const int rr = (t % 4) * 16;
-    if (c < cols) {
-      uint32_t w8[8];
-#pragma unroll
-      for (int q = 0; q < 8; ++q)
-        w8[q] = (uint32_t)tile[rr + 2 * q][t / 4] | ((uint32_t)tile[rr + 2 * q + 1][t / 4] << 16);
-      uint4* o = reinterpret_cast<uint4*>(out + (int64_t)c * ldo + rbeg + rr);
-      o[0] = make_uint4(w8[0], w8[1], w8[2], w8[3]);
-      o[1] = make_uint4(w8[4], w8[5], w8[6], w8[7]);
-    }
+__global__ __launch_bounds__(256) void k_gather_rows(const uint16_t* __restrict__ H, int64_t ldh,
+                                                     const int* __restrict__ idx, const int* __restrict__ nv_ptr,
+                                                     int d, uint16_t* __restrict__ Hv) {
+  const int nv = *nv_ptr;
+  const int64_t rows = (nv + 63) / 64 * 64;
+  const int cpr = d / 8;   // 16-byte chunks per row
+  const int64_t total = rows * cpr;
+  for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < total; e += (int64_t)gridDim.x * 256) {
+    const int64_t i = e / cpr;
+    const int c = (int)(e - i * cpr);
+    uint4 v = make_uint4(0, 0, 0, 0);
+    if (i < nv) v = *reinterpret_cast<const uint4*>(H + (int64_t)idx[i] * ldh + c * 8);
+    *reinterpret_cast<uint4*>(Hv + i * d + c * 8) = v;
   }
 }
 
@@ -924,8 +890,8 @@ __device__ __forceinline__ float grad_scale(const float* grad, const int* n_norm
 // scale2 = log2(e) / T (log2(e) for LCE), inv_t = 1 / T; lse is that of the scaled logits.
 enum GMode { G_ONEHOT = 0, G_SOFT = 1, Q_SOFT = 2, P_WRITE = 3, G_SOFT_Q = 4 };
 
-template <int kMode>
-__global__ __launch_bounds__(NTHREADS, 2) void k_bwd_g(const uint16_t* __restrict__ W, int64_t ldw, int64_t v0, int vs,
+template <int kMode, int WM>
+__global__ __launch_bounds__(Geo<WM>::NT, WM) void k_bwd_g(const uint16_t* __restrict__ W, int64_t ldw, int64_t v0, int vs,
                                                        const uint16_t* __restrict__ H, int64_t ldh, int64_t n,
                                                        const void* targets, int tbytes, int64_t id0,
                                                        const int* __restrict__ idx, const int* __restrict__ nv_ptr,
@@ -934,19 +900,29 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_bwd_g(const uint16_t* __restric
                                                        uint16_t* __restrict__ G, int vc, int ldt,
                                                        float scale2, float inv_t, float* __restrict__ P,
                                                        float* __restrict__ qpart, int64_t qrow) {
-  __shared__ __attribute__((aligned(16))) char smem[LDS_BYTES];
+  // 12 waves (WM = 3, 384 ids per tile) serve the one-hot LCE gradient when D % 64 == 0; the
+  // distillation modes and other widths keep 8 waves and the LDS-staged epilogue below
+  static_assert(WM == 2 || kMode == G_ONEHOT, "");
+  constexpr int TM = Geo<WM>::TM;
+  __shared__ __attribute__((aligned(16))) char smem[Geo<WM>::LDS];
   const int nv = *nv_ptr;
   const int tm = blockIdx.x % tm_count, tn = blockIdx.x / tm_count;
   const int n0 = tn * TILE;
   if (n0 >= nv) return;
-  const int vt0 = tm * TILE;                 // slab-relative
+  const int vt0 = tm * TM;                   // slab-relative
   const int vleft = vs - vt0;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, wr = wave >> 2, wc = wave & 3;
 
   const Operand opa = dense_operand(W + (v0 + vt0) * ldw, vleft, ldw);
-  const Operand opb = gather_operand(H, n, ldh, idx, n0, nv);
   f32x16_t acc[4][2];
-  mma_mainloop<2, OP_DENSE, OP_GATHER>(acc, opa, opb, d, smem);
+  if constexpr (WM == 3) {
+    // H is the gathered valid rows Hv (row stride ldh = d): a dense operand
+    const Operand opb = dense_operand(H + (int64_t)n0 * ldh, nv - n0, ldh);
+    mma_mainloop<2, OP_DENSE, OP_DENSE, WM, false>(acc, opa, opb, d, smem);   // d % 64 == 0 (host)
+  } else {
+    const Operand opb = gather_operand(H, n, ldh, idx, n0, nv);
+    mma_mainloop<2, OP_DENSE, OP_GATHER, WM>(acc, opa, opb, d, smem);
+  }
 
   const float c_all = grad_scale(grad, n_norm, reduction);
   int tok[2], tgt[2];
@@ -966,7 +942,40 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_bwd_g(const uint16_t* __restric
     }
   }
   const int vb = wr * 128 + (lane >> 5) * 4;  // tile-relative vocabulary row base of this lane
-  if constexpr (kMode == P_WRITE || kMode == Q_SOFT) {
+  if constexpr (WM == 3) {
+    // G straight from registers: per block and group of 4 ids, 8 bytes (4 ids of one token row)
+    // per lane; a wave's stores cover whole 128-byte lines of its rows, which L2 merges. Rows of
+    // tokens >= Nv and ids >= the slab width get zeros, so the whole 256 x 384 tile is written
+    // (the slab width vc is a multiple of 384).
+    const __amdgpu_buffer_rsrc_t rg = make_rsrc(G + (int64_t)n0 * vc, (uint64_t)TILE * vc * 2);
+    const uint32_t voff = (uint32_t)(((wc * 64 + (lane & 31)) * vc + vt0 + vb) * 2);
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const bool tok_ok = tok[j] < nv;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          float gq[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int vr = vb + i * 32 + q * 8 + e;
+            float g = 0.f;
+            if (tok_ok && vr < vleft) {
+              g = cj[j] * __builtin_amdgcn_exp2f(fmaf(acc[i][j][q * 4 + e], scale2, -l2[j]));
+              if (vr == tgt[j]) g -= cj[j];
+            }
+            gq[e] = g;
+          }
+          u32x2_t pk;
+          pk.x = pack_bf16x2(gq[0], gq[1]);
+          pk.y = pack_bf16x2(gq[2], gq[3]);
+          const uint32_t so = (uint32_t)((j * 32 * vc + i * 32 + q * 8) * 2);
+          __builtin_amdgcn_raw_buffer_store_b64(pk, rg, (int)voff, (int)so, 0);
+        }
+    }
+    return;
+  } else if constexpr (kMode == P_WRITE || kMode == Q_SOFT) {
     // P[v][token] rows of this tile: lanes of a half-wave hold 32 consecutive tokens of one row
     float q[2] = {0.f, 0.f};
 #pragma unroll
@@ -1076,8 +1085,8 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_bwd_g(const uint16_t* __restric
   }
 }
 
-// K5: dW[v0 + m][dd] = sum_k G[k][m] Hvt[dd][k] over k < round_up(Nv, 64), G [Npad][vc] read
-// K-major (transposing LDS reads), Hvt [D][Npad] row-major; tiles of (128 WM) ids x 256 hidden
+// K5: dW[v0 + m][dd] = sum_k G[k][m] Hv[k][dd] over k < round_up(Nv, 64), G [Npad][vc] and the
+// gathered valid rows Hv [Npad][D] both read K-major (transposing LDS reads); tiles of (128 WM) ids x 256 hidden
 // columns. The epilogue either writes the block in bf16 (each element once), adds it to the bf16
 // values already there, or hands each bf16-rounded element straight to the AdamW update of W (the
 // in-backward step). Its accesses go through buffer resources over the tile's rows below the slab
@@ -1087,7 +1096,7 @@ enum DwMode { DW_STORE = 0, DW_ACCUMULATE = 1, DW_ADAMW = 2 };
 
 template <int kMode, int WM>
 __global__ __launch_bounds__(Geo<WM>::NT, WM) void k_bwd_dw(const uint16_t* __restrict__ G, int vc, int ldt, int vs,
-                                                           const uint16_t* __restrict__ Hvt, int d,
+                                                           const uint16_t* __restrict__ Hv, int d,
                                                            const int* __restrict__ nv_ptr, int tm_count,
                                                            uint16_t* __restrict__ dW, int64_t v0,
                                                            AdamWState st, AdamWConst oc) {
@@ -1099,11 +1108,11 @@ __global__ __launch_bounds__(Geo<WM>::NT, WM) void k_bwd_dw(const uint16_t* __re
   const int nv = *nv_ptr;
   const int kpad = ((nv + KPAD - 1) / KPAD) * KPAD;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, wr = wave >> 2, wc = wave & 3;
-  // ldt = Npad: G has Npad rows of vc ids, Hvt D rows of Npad tokens
+  // ldt = Npad: G has Npad rows of vc ids, Hv Npad rows of d hidden columns
   const Operand opa = kmajor_operand<TM>(G + m0, vc, ((uint64_t)ldt * vc - m0) * 2);
-  const Operand opb = dense_operand(Hvt + (int64_t)d0 * ldt, d - d0, ldt);
+  const Operand opb = kmajor_operand<TILE>(Hv + d0, d, ((uint64_t)ldt * d - d0) * 2);
   f32x16_t acc[4][2];
-  mma_mainloop<1, OP_KMAJOR, OP_DENSE, WM, false>(acc, opa, opb, kpad, smem);
+  mma_mainloop<1, OP_KMAJOR, OP_KMAJOR, WM, false>(acc, opa, opb, kpad, smem);
 
   const int rows = vs - m0 < TM ? vs - m0 : TM;             // valid id rows of this tile
   const int64_t r0 = v0 + m0;                               // its first row of W / dW
@@ -1336,10 +1345,10 @@ __global__ __launch_bounds__(256) void k_kd_terms(const float* __restrict__ qpar
 // ---------------------------------------------------------------------------------------------
 // Host side: validation, plan, workspace carve-up, launches, optional timing.
 // ---------------------------------------------------------------------------------------------
-enum KernelId { K_COMPACT = 0, K_FWD_STATS, K_COMBINE, K_LOSS, K_TRANSPOSE_H, K_BWD_G,
+enum KernelId { K_COMPACT = 0, K_FWD_STATS, K_COMBINE, K_LOSS, K_GATHER_H, K_BWD_G,
                 K_BWD_DW, K_BWD_DH, K_DH_FINAL, K_ADAMW, K_SHARD_COMBINE, K_KD_P, K_KD_Q, K_KD_TERMS, K_MISC,
                 K_COUNT };
-const char* const kKernelNames[K_COUNT] = {"compact", "fwd_stats", "combine", "loss", "transpose_h",
+const char* const kKernelNames[K_COUNT] = {"compact", "fwd_stats", "combine", "loss", "gather_h",
                                            "bwd_g", "bwd_dw", "bwd_dh", "dh_finalize", "adamw", "shard_combine", "kd_teacher_p", "kd_q", "kd_terms", "misc"};
 
 struct Timing {
@@ -1358,7 +1367,7 @@ struct Plan {
   int64_t vc, nslab;
   // workspace offsets
   size_t o_idx, o_pos, o_nv, o_pm, o_ps, o_terms, fwd_bytes;
-  size_t o_hvt, o_g, o_dh32, bwd_bytes;
+  size_t o_hv, o_g, o_dh32, bwd_bytes;
 };
 
 inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
@@ -1390,11 +1399,12 @@ lce_status_t make_plan(const lce_problem_t* p, Plan* pl) {
   int64_t vc = 4 * p->d;
   if (vc < 8192) vc = 8192;
   vc = round_up(vc, 16 * 384);
-  const int64_t vround = round_up(p->v, TILE);
+  // a multiple of 768 in any case: both 256- and 384-wide G tiles end inside a G row
+  const int64_t vround = round_up(p->v, 768);
   if (vc > vround) vc = vround;
   pl->vc = vc;
   pl->nslab = (p->v + vc - 1) / vc;
-  if ((uint64_t)TILE * pl->npad * 2 > 0x7FFFFFFFull) return LCE_ERR_SHAPE;
+  if ((uint64_t)TILE * pl->npad * 2 > 0x7FFFFFFFull || (uint64_t)TILE * vc * 2 > 0x7FFFFFFFull) return LCE_ERR_SHAPE;
 
   auto take = [](size_t& cur, size_t bytes) { size_t o = cur; cur += (bytes + 255) / 256 * 256; return o; };
   size_t cur = 0;
@@ -1407,7 +1417,7 @@ lce_status_t make_plan(const lce_problem_t* p, Plan* pl) {
   pl->o_terms = take(cur, 4 * (size_t)pl->npad);
   pl->fwd_bytes = cur;
   cur = common;
-  pl->o_hvt = take(cur, 2 * (size_t)p->d * pl->npad);
+  pl->o_hv = take(cur, 2 * (size_t)p->d * pl->npad);
   pl->o_g = take(cur, 2 * (size_t)pl->npad * vc);
   pl->o_dh32 = take(cur, 4 * (size_t)pl->npad * p->d);
   pl->bwd_bytes = cur;
@@ -1571,7 +1581,7 @@ lce_status_t backward_impl(const lce_problem_t* p, const ShardInfo* shard, const
   int* idx = (int*)(ws + pl.o_idx);
   int* pos = (int*)(ws + pl.o_pos);
   int* nv = (int*)(ws + pl.o_nv);
-  uint16_t* hvt = (uint16_t*)(ws + pl.o_hvt);
+  uint16_t* hv = (uint16_t*)(ws + pl.o_hv);
   uint16_t* g = (uint16_t*)(ws + pl.o_g);
   float* dh32 = (float*)(ws + pl.o_dh32);
   const uint16_t* h = (const uint16_t*)H;
@@ -1580,9 +1590,9 @@ lce_status_t backward_impl(const lce_problem_t* p, const ShardInfo* shard, const
 
   L(K_COMPACT, k_compact, dim3(1), dim3(1024), targets, p->target_bytes, pl.n, si.v_total, p->ignore_index,
     idx, pos, nv, (int*)nullptr, (int*)nullptr, (float*)nullptr, (float*)nullptr);
-  // Hvt[d][i] = H[idx[i]][d] for i < Nv, zero up to round_up(Nv, 64)
-  L(K_TRANSPOSE_H, k_transpose, dim3((unsigned)(npad / 64), (unsigned)((d + 63) / 64)), dim3(256), h, pl.ldh,
-    (const int*)idx, (int64_t)0, (const int*)nv, 0, d, hvt, (int64_t)npad, npad);
+  // Hv[i] = H[idx[i]] for i < Nv, zero rows up to round_up(Nv, 64)
+  L(K_GATHER_H, k_gather_rows, dim3((unsigned)std::min<int64_t>((npad * (d / 8) + 255) / 256, 16384)), dim3(256), h,
+    pl.ldh, (const int*)idx, (const int*)nv, d, hv);
   const int dt = (d + TILE - 1) / TILE;
   const int dh_tiles = (int)((pl.npad + Geo<kDhWM>::TM - 1) / Geo<kDhWM>::TM);
   void (*dw_kernel)(const uint16_t*, int, int, int, const uint16_t*, int, const int*, int, uint16_t*, int64_t,
@@ -1595,25 +1605,33 @@ lce_status_t backward_impl(const lce_problem_t* p, const ShardInfo* shard, const
     if (kd) {
       // teacher probabilities of this slab, then G = c (softmax(zs / T) - P) / T
       float* P = (float*)(ws + pl.bwd_bytes);
-      L(K_KD_P, k_bwd_g<P_WRITE>, dim3((unsigned)(tm * pl.nt_max)), dim3(NTHREADS), kd->wt, kd->ldwt, v0, vs,
+      L(K_KD_P, k_bwd_g<P_WRITE, 2>, dim3((unsigned)(tm * pl.nt_max)), dim3(NTHREADS), kd->wt, kd->ldwt, v0, vs,
         kd->ht, kd->ldht, pl.n, targets, p->target_bytes, (int64_t)0, (const int*)idx, (const int*)nv, kd->lse_t,
         grad_loss, (const int*)n_valid, p->reduction, kd->dt, tm, (uint16_t*)nullptr, vc, npad,
         kd->scale2, kd->inv_t, P, (float*)nullptr, (int64_t)0);
       if (kd->qpart)
-        L(K_BWD_G, k_bwd_g<G_SOFT_Q>, dim3((unsigned)(tm * pl.nt_max)), dim3(NTHREADS), w, pl.ldw, v0, vs, h,
+        L(K_BWD_G, k_bwd_g<G_SOFT_Q, 2>, dim3((unsigned)(tm * pl.nt_max)), dim3(NTHREADS), w, pl.ldw, v0, vs, h,
           pl.ldh, pl.n, targets, p->target_bytes, (int64_t)0, (const int*)idx, (const int*)nv, lse, grad_loss,
           (const int*)n_valid, p->reduction, d, tm, g, vc, npad, kd->scale2, kd->inv_t, P, kd->qpart,
           (int64_t)(2 * (v0 / TILE)));
       else
-        L(K_BWD_G, k_bwd_g<G_SOFT>, dim3((unsigned)(tm * pl.nt_max)), dim3(NTHREADS), w, pl.ldw, v0, vs, h,
+        L(K_BWD_G, k_bwd_g<G_SOFT, 2>, dim3((unsigned)(tm * pl.nt_max)), dim3(NTHREADS), w, pl.ldw, v0, vs, h,
           pl.ldh, pl.n, targets, p->target_bytes, (int64_t)0, (const int*)idx, (const int*)nv, lse, grad_loss,
           (const int*)n_valid, p->reduction, d, tm, g, vc, npad, kd->scale2, kd->inv_t, P, (float*)nullptr,
           (int64_t)0);
     } else {
-      L(K_BWD_G, k_bwd_g<G_ONEHOT>, dim3((unsigned)(tm * pl.nt_max)), dim3(NTHREADS), w, pl.ldw, v0, vs, h, pl.ldh,
-        pl.n, targets, p->target_bytes, si.v_begin, (const int*)idx, (const int*)nv, lse, grad_loss,
-        (const int*)n_valid, p->reduction, d, tm, g, vc, npad, kLog2e, 1.f, (float*)nullptr, (float*)nullptr,
-        (int64_t)0);
+      if (d % KSLICE == 0) {
+        const int tmg = (vs + Geo<kGWM>::TM - 1) / Geo<kGWM>::TM;
+        L(K_BWD_G, k_bwd_g<G_ONEHOT, kGWM>, dim3((unsigned)(tmg * pl.nt_max)), dim3(Geo<kGWM>::NT), w, pl.ldw, v0, vs,
+          (const uint16_t*)hv, (int64_t)d, pl.n, targets, p->target_bytes, si.v_begin, (const int*)idx, (const int*)nv,
+          lse, grad_loss, (const int*)n_valid, p->reduction, d, tmg, g, vc, npad, kLog2e, 1.f, (float*)nullptr,
+          (float*)nullptr, (int64_t)0);
+      } else {
+        L(K_BWD_G, k_bwd_g<G_ONEHOT, 2>, dim3((unsigned)(tm * pl.nt_max)), dim3(NTHREADS), w, pl.ldw, v0, vs, h,
+          pl.ldh, pl.n, targets, p->target_bytes, si.v_begin, (const int*)idx, (const int*)nv, lse, grad_loss,
+          (const int*)n_valid, p->reduction, d, tm, g, vc, npad, kLog2e, 1.f, (float*)nullptr, (float*)nullptr,
+          (int64_t)0);
+      }
     }
     // dH reads the slab's W rows before the dW launch, whose AdamW epilogue (in-backward step)
     // may update them; later slabs read only their own rows
@@ -1621,7 +1639,7 @@ lce_status_t backward_impl(const lce_problem_t* p, const ShardInfo* shard, const
       w + v0 * pl.ldw, pl.ldw, pl.v - v0, d, (const int*)nv, dh32, (int)(s > 0));
     const int tmw = (vs + Geo<kDwWM>::TM - 1) / Geo<kDwWM>::TM;
     L(K_BWD_DW, dw_kernel, dim3((unsigned)(8 * ((tmw + 7) / 8) * dt)), dim3(Geo<kDwWM>::NT), (const uint16_t*)g, vc,
-      npad, vs, (const uint16_t*)hvt, d, (const int*)nv, tmw, dW, v0, as, c);
+      npad, vs, (const uint16_t*)hv, d, (const int*)nv, tmw, dW, v0, as, c);
   }
   const int64_t nthr = pl.n * pl.d / 8;
   L(K_DH_FINAL, k_dh_finalize, dim3((unsigned)((nthr + 255) / 256)), dim3(256), (const float*)dh32,
@@ -1797,11 +1815,11 @@ lce_status_t kd_forward_impl(const lce_kd_problem_t* p, const void* Hs, const vo
     const int64_t v0 = s * pl.vc;
     const int vs = (int)(pl.v - v0 < pl.vc ? pl.v - v0 : pl.vc);
     const int tm = (vs + TILE - 1) / TILE;
-    L(K_KD_P, k_bwd_g<P_WRITE>, dim3((unsigned)(tm * pl.nt_max)), dim3(NTHREADS), wt, tp.ldw, v0, vs, ht, tp.ldh,
+    L(K_KD_P, k_bwd_g<P_WRITE, 2>, dim3((unsigned)(tm * pl.nt_max)), dim3(NTHREADS), wt, tp.ldw, v0, vs, ht, tp.ldh,
       pl.n, targets, p->target_bytes, (int64_t)0, (const int*)idx, (const int*)nv, (const float*)lse_t,
       (const float*)nullptr, (const int*)nullptr, p->reduction, (int)tp.d, tm, (uint16_t*)nullptr, vc,
       npad, k.scale2, k.inv_t, P, (float*)nullptr, (int64_t)0);
-    L(K_KD_Q, k_bwd_g<Q_SOFT>, dim3((unsigned)(tm * pl.nt_max)), dim3(NTHREADS), wsm, pl.ldw, v0, vs, hs, pl.ldh,
+    L(K_KD_Q, k_bwd_g<Q_SOFT, 2>, dim3((unsigned)(tm * pl.nt_max)), dim3(NTHREADS), wsm, pl.ldw, v0, vs, hs, pl.ldh,
       pl.n, targets, p->target_bytes, (int64_t)0, (const int*)idx, (const int*)nv, (const float*)lse_s,
       (const float*)nullptr, (const int*)nullptr, p->reduction, (int)pl.d, tm, (uint16_t*)nullptr, vc,
       npad, k.scale2, k.inv_t, P, qpart, (int64_t)(2 * (v0 / TILE)));
