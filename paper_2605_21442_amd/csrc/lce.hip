@@ -627,20 +627,121 @@ __global__ __launch_bounds__(1024) void k_compact(const void* targets, int tbyte
 }
 
 // ---------------------------------------------------------------------------------------------
-// K2: forward statistics. Workgroup (token tile nt, vocabulary partition p) walks the partition's
-// 256-wide vocabulary tiles; per tile it computes S^T = W_tile H_valid^T (so a token's logits run
-// down a lane's registers) and folds them into a running (max, sum of exp) per token and lane.
-// At the end the two lane halves are merged and each wave row writes one partial pair per token
-// (in log2 units): part[(2 p + wave_row) * npad + token].
+// K2: forward statistics (paper section 3: the logits' log-sum-exp accumulated over vocabulary
+// tiles, never stored). Two forms, both writing per-token partial pairs (max, sum of exp) in log2
+// units, part[row * npad + token], merged by K3:
+//  - k_fwd_tile (12 waves, D % 64 == 0): one 384-id x 256-token tile per workgroup, H given as the
+//    gathered valid rows Hv; one partial row per vocabulary tile.
+//  - k_fwd_stats (8 waves, any D): workgroup (token tile nt, vocabulary partition p) walks the
+//    partition's 256-wide tiles with a running pair per token and lane, H's valid rows gathered
+//    through idx by the main loop; two partial rows (one per wave row) per partition.
+// In both, a tile's S^T = W_tile H^T runs a token's logits down a lane's registers.
 // ---------------------------------------------------------------------------------------------
-__global__ __launch_bounds__(NTHREADS, 2) void k_fwd_stats(const uint16_t* __restrict__ W, int64_t ldw, int v,
+// Tiles are taken in groups of gw vocabulary tiles (one backward slab's width) by all token
+// tiles, ids fastest: the group's W rows stay in the MALL while the token tiles pass, and the
+// workgroups resident on one XCD (consecutive blocks go to the 8 XCDs in turn) share their W and H
+// tiles through its L2 as in the backward's G launches.
+__global__ __launch_bounds__(Geo<3>::NT, 3) void k_fwd_tile(const uint16_t* __restrict__ W, int64_t ldw, int v,
+                                                            const uint16_t* __restrict__ Hv, int64_t ldh,
+                                                            const int* __restrict__ nv_ptr, int d, int vt_count,
+                                                            int gw, int nt_max, float* __restrict__ part_m,
+                                                            float* __restrict__ part_s, int npad, float scale2) {
+  constexpr int WM = 3, TM = Geo<WM>::TM;
+  __shared__ __attribute__((aligned(16))) char smem[Geo<WM>::LDS];
+  const int b = blockIdx.x;
+  const int full = vt_count / gw;
+  const int g = b / (gw * nt_max);
+  int tm, tn;
+  if (g < full) {
+    const int r = b - g * gw * nt_max;
+    tm = g * gw + r % gw;
+    tn = r / gw;
+  } else {
+    const int r = b - full * gw * nt_max, wl = vt_count - full * gw;
+    tm = full * gw + r % wl;
+    tn = r / wl;
+  }
+  const int nv = *nv_ptr;
+  const int n0 = tn * TILE;
+  if (n0 >= nv) return;
+  const int v0 = tm * TM, vleft = v - v0;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, wr = wave >> 2, wc = wave & 3;
+
+  const Operand opa = dense_operand(W + (int64_t)v0 * ldw, vleft, ldw);
+  const Operand opb = dense_operand(Hv + (int64_t)n0 * ldh, nv - n0, ldh);
+  f32x16_t acc[4][2];
+  mma_mainloop<2, OP_DENSE, OP_DENSE, WM, false>(acc, opa, opb, d, smem);   // d % 64 == 0 (host)
+  // the main loop ends with a barrier: its LDS is free for the wave rows' pairs [3][256] (m, s)
+  float* red_m = reinterpret_cast<float*>(smem);
+  float* red_s = red_m + WM * TILE;
+
+  // rows (vocabulary ids) of this lane: v0 + wr*128 + 32 bi + 8 (r/4) + 4 (lane/32) + r%4
+  const int vb = wr * 128 + (lane >> 5) * 4;
+  const bool ragged = vleft < TM;
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    float mx = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        if (ragged && (vb + i * 32 + (r >> 2) * 8 + (r & 3)) >= vleft) acc[i][j][r] = -INFINITY;
+        mx = fmaxf(mx, acc[i][j][r]);
+      }
+    const float nm = mx * scale2;
+    float st = 0.f;
+    if (nm != -INFINITY) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) st += __builtin_amdgcn_exp2f(fmaf(acc[i][j][r], scale2, -nm));
+    }
+    // merge the two lane halves (disjoint ids of the same tokens)
+    const float om = __shfl_xor(nm, 32), os = __shfl_xor(st, 32);
+    const float mm = fmaxf(nm, om);
+    float sm = 0.f;
+    if (mm != -INFINITY) {
+      sm = (nm == -INFINITY ? 0.f : st * __builtin_amdgcn_exp2f(nm - mm)) +
+           (om == -INFINITY ? 0.f : os * __builtin_amdgcn_exp2f(om - mm));
+    }
+    if (lane < 32) {
+      const int t = wr * TILE + wc * 64 + j * 32 + lane;
+      red_m[t] = mm;
+      red_s[t] = sm;
+    }
+  }
+  __syncthreads();
+  // merge the three wave rows in order; one thread per token of the tile
+  if (threadIdx.x < TILE) {
+    const int t = threadIdx.x, tok = n0 + t;
+    float m = red_m[t], s = red_s[t];
+#pragma unroll
+    for (int q = 1; q < WM; ++q) {
+      const float m2 = red_m[q * TILE + t], s2 = red_s[q * TILE + t];
+      const float mn = fmaxf(m, m2);
+      if (mn != -INFINITY)
+        s = (m == -INFINITY ? 0.f : s * __builtin_amdgcn_exp2f(m - mn)) +
+            (m2 == -INFINITY ? 0.f : s2 * __builtin_amdgcn_exp2f(m2 - mn));
+      m = mn;
+    }
+    if (tok < nv) {
+      part_m[(int64_t)tm * npad + tok] = m;
+      part_s[(int64_t)tm * npad + tok] = s;
+    }
+  }
+}
+
+template <int WM>
+__global__ __launch_bounds__(Geo<WM>::NT, WM) void k_fwd_stats(const uint16_t* __restrict__ W, int64_t ldw, int v,
                                                            const uint16_t* __restrict__ H, int64_t ldh, int64_t n,
                                                            const int* __restrict__ idx, const int* __restrict__ nv_ptr,
                                                            int d, int nparts, int nt_max, int vt_count,
                                                            float* __restrict__ part_m, float* __restrict__ part_s,
                                                            int npad, float scale2) {
-  // scale2 = log2(e) / T: partials are kept in base-2 units of the logits divided by T
-  __shared__ __attribute__((aligned(16))) char smem[LDS_BYTES];
+  // scale2 = log2(e) / T: partials are kept in base-2 units of the logits divided by T.
+  static_assert(WM == 2, "");
+  constexpr int TM = Geo<WM>::TM;
+  __shared__ __attribute__((aligned(16))) char smem[Geo<WM>::LDS];
   // Workgroups are dispatched round-robin over the 8 XCDs (block b runs on XCD b % 8). Each XCD
   // owns whole vocabulary partitions (p = xcd + 8 k, k < ppx) and runs its workgroups in rounds of
   // about 32 (one per CU): every round covers all ppx partitions for a group of 32 / ppx token
@@ -667,20 +768,20 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_fwd_stats(const uint16_t* __res
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, wr = wave >> 2, wc = wave & 3;
   const Operand opb = gather_operand(H, n, ldh, idx, n0, nv);
 
+  f32x16_t acc[4][2];
   float m2[2], ss[2];
 #pragma unroll
   for (int j = 0; j < 2; ++j) { m2[j] = -INFINITY; ss[j] = 0.f; }
 
-  f32x16_t acc[4][2];
   for (int vt = vt0; vt < vt1; ++vt) {
-    const int v0 = vt * TILE;
+    const int v0 = vt * TM;
     const int vleft = v - v0;
     const Operand opa = dense_operand(W + (int64_t)v0 * ldw, vleft, ldw);
-    mma_mainloop<2, OP_DENSE, OP_GATHER>(acc, opa, opb, d, smem);
+    mma_mainloop<2, OP_DENSE, OP_GATHER, WM>(acc, opa, opb, d, smem);
 
     // rows (vocabulary ids) of this lane: v0 + wr*128 + 32 bi + 8 (r/4) + 4 (lane/32) + r%4
     const int vb = wr * 128 + (lane >> 5) * 4;
-    const bool ragged = vleft < TILE;
+    const bool ragged = vleft < TM;
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
       float mx = -INFINITY;
@@ -714,7 +815,7 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_fwd_stats(const uint16_t* __res
     }
     const int tok = n0 + wc * 64 + j * 32 + (lane & 31);
     if (lane < 32 && tok < nv) {
-      const int64_t o = (int64_t)(2 * p + wr) * npad + tok;
+      const int64_t o = (int64_t)(WM * p + wr) * npad + tok;
       part_m[o] = nm;
       part_s[o] = s;
     }
@@ -724,52 +825,79 @@ __global__ __launch_bounds__(NTHREADS, 2) void k_fwd_stats(const uint16_t* __res
 // ---------------------------------------------------------------------------------------------
 // K3: per valid token: merge the vocabulary partials into lse, take the target logit
 // s[n, t_n] = H[n] . W[t_n] in fp32, and the per-row loss l_n = lse_n - s[n, t_n].
-// One wave per token; all reductions use a fixed butterfly order.
+// A workgroup of 16 waves serves 64 consecutive tokens. First each wave folds every 16th partial
+// row (rows w, w + 16, ...) for the 64 tokens, one token per lane (reads coalesced along the
+// tokens), and the 16 results are merged in wave order; then each wave takes the target logits of
+// 4 tokens, one wave-wide dot product each. All reductions run in a fixed order.
 // ---------------------------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void k_combine(const uint16_t* __restrict__ H, int64_t ldh,
-                                                 const uint16_t* __restrict__ W, int64_t ldw,
-                                                 const void* targets, int tbytes, int64_t id0, int64_t v_local,
-                                                 const int* __restrict__ idx, const int* __restrict__ nv_ptr,
-                                                 int d, int nparts2, const float* __restrict__ part_m,
-                                                 const float* __restrict__ part_s, int npad,
-                                                 float* __restrict__ lse_out, float* __restrict__ terms,
-                                                 float* __restrict__ per_token, float* __restrict__ tgt_part) {
-  const int lane = threadIdx.x & 63;
-  const int i = blockIdx.x * 4 + (threadIdx.x >> 6);
+constexpr int kCombTok = 64;
+
+__device__ __forceinline__ void merge_pair(float& m, float& s, float m2, float s2) {
+  const float mn = fmaxf(m, m2);
+  if (mn == -INFINITY) return;
+  s = (m == -INFINITY ? 0.f : s * exp2f(m - mn)) + (m2 == -INFINITY ? 0.f : s2 * exp2f(m2 - mn));
+  m = mn;
+}
+
+__global__ __launch_bounds__(1024) void k_combine(const uint16_t* __restrict__ H, int64_t ldh,
+                                                  const uint16_t* __restrict__ W, int64_t ldw,
+                                                  const void* targets, int tbytes, int64_t id0, int64_t v_local,
+                                                  const int* __restrict__ idx, const int* __restrict__ nv_ptr,
+                                                  int d, int nparts2, const float* __restrict__ part_m,
+                                                  const float* __restrict__ part_s, int npad,
+                                                  float* __restrict__ lse_out, float* __restrict__ terms,
+                                                  float* __restrict__ per_token, float* __restrict__ tgt_part) {
+  __shared__ float red_m[16][kCombTok], red_s[16][kCombTok], lse_t[kCombTok];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int i0 = blockIdx.x * kCombTok;
   const int nv = *nv_ptr;
-  if (i >= nv) return;
-  const int row = idx[i];
-  // target id relative to this W's first row (id0 > 0 only for a vocabulary shard, which may
-  // not hold the target: then its target logit is 0)
-  const int64_t tl = load_target(targets, tbytes, row) - id0;
-  float dot = 0.f;
-  if (tl >= 0 && tl < v_local) {
-    const uint4* hr = reinterpret_cast<const uint4*>(H + (int64_t)row * ldh);
-    const uint4* wt = reinterpret_cast<const uint4*>(W + tl * ldw);
-    for (int c = lane; c < d / 8; c += 64) {
-      const uint4 a = hr[c], b = wt[c];
-      const uint32_t av[4] = {a.x, a.y, a.z, a.w}, bv[4] = {b.x, b.y, b.z, b.w};
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        dot = fmaf(bf16_to_f32(av[q] & 0xFFFF), bf16_to_f32(bv[q] & 0xFFFF), dot);
-        dot = fmaf(bf16_to_f32(av[q] >> 16), bf16_to_f32(bv[q] >> 16), dot);
-      }
-    }
-    dot = wave_sum(dot);
+  if (i0 >= nv) return;
+  {
+    const int i = i0 + lane;
+    float m = -INFINITY, s = 0.f;
+    if (i < nv)
+      for (int q = wave; q < nparts2; q += 16) merge_pair(m, s, part_m[(int64_t)q * npad + i], part_s[(int64_t)q * npad + i]);
+    red_m[wave][lane] = m;
+    red_s[wave][lane] = s;
   }
-  const float m = lane < nparts2 ? part_m[(int64_t)lane * npad + i] : -INFINITY;
-  const float s = lane < nparts2 ? part_s[(int64_t)lane * npad + i] : 0.f;
-  const float mm = wave_max(m);
-  const float e = (m == -INFINITY) ? 0.f : s * exp2f(m - mm);
-  const float se = wave_sum(e);
-  const float lse = (mm + log2f(se)) * kLn2;
-  if (lane == 0) {
-    lse_out[row] = lse;
-    if (tgt_part) {
-      tgt_part[row] = dot;
-    } else {
-      terms[i] = lse - dot;
-      if (per_token) per_token[row] = lse - dot;
+  __syncthreads();
+  if (wave == 0) {
+    float m = red_m[0][lane], s = red_s[0][lane];
+    for (int q = 1; q < 16; ++q) merge_pair(m, s, red_m[q][lane], red_s[q][lane]);
+    lse_t[lane] = (m + log2f(s)) * kLn2;
+  }
+  __syncthreads();
+  for (int t = 0; t < kCombTok / 16; ++t) {
+    const int li = wave * (kCombTok / 16) + t, i = i0 + li;
+    if (i >= nv) break;
+    const int row = idx[i];
+    // target id relative to this W's first row (id0 > 0 only for a vocabulary shard, which may
+    // not hold the target: then its target logit is 0)
+    const int64_t tl = load_target(targets, tbytes, row) - id0;
+    float dot = 0.f;
+    if (tl >= 0 && tl < v_local) {
+      const uint4* hr = reinterpret_cast<const uint4*>(H + (int64_t)row * ldh);
+      const uint4* wt = reinterpret_cast<const uint4*>(W + tl * ldw);
+      for (int c = lane; c < d / 8; c += 64) {
+        const uint4 a = hr[c], b = wt[c];
+        const uint32_t av[4] = {a.x, a.y, a.z, a.w}, bv[4] = {b.x, b.y, b.z, b.w};
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          dot = fmaf(bf16_to_f32(av[q] & 0xFFFF), bf16_to_f32(bv[q] & 0xFFFF), dot);
+          dot = fmaf(bf16_to_f32(av[q] >> 16), bf16_to_f32(bv[q] >> 16), dot);
+        }
+      }
+      dot = wave_sum(dot);
+    }
+    if (lane == 0) {
+      const float lse = lse_t[li];
+      lse_out[row] = lse;
+      if (tgt_part) {
+        tgt_part[row] = dot;
+      } else {
+        terms[i] = lse - dot;
+        if (per_token) per_token[row] = lse - dot;
+      }
     }
   }
 }
@@ -1363,10 +1491,10 @@ Timing g_timing;
 
 struct Plan {
   int64_t n, d, v, ldh, ldw, npad;
-  int nt_max, vt_count, nparts;
+  int nt_max, vt_count, nparts, vt_count3;
   int64_t vc, nslab;
   // workspace offsets
-  size_t o_idx, o_pos, o_nv, o_pm, o_ps, o_terms, fwd_bytes;
+  size_t o_idx, o_pos, o_nv, o_pm, o_ps, o_terms, o_hvf, fwd_bytes;
   size_t o_hv, o_g, o_dh32, bwd_bytes;
 };
 
@@ -1393,6 +1521,8 @@ lce_status_t make_plan(const lce_problem_t* p, Plan* pl) {
   pl->nt_max = (int)(pl->npad / TILE);
   pl->vt_count = (int)((p->v + TILE - 1) / TILE);
   pl->nparts = pl->vt_count < MAX_PARTS ? pl->vt_count : MAX_PARTS;
+  // the 12-wave forward (D % 64 == 0): one workgroup and one partial row per 384-id tile
+  pl->vt_count3 = (int)((p->v + 383) / 384);
   // backward vocabulary slab: about 4 D columns (at least 8192) keeps G at O(N D) while halving
   // the dH accumulator passes of a 2 D slab; a multiple of 16 tiles of 384 ids, so that the dW
   // launch of a 4096-wide head is whole rounds of workgroups on 256 CUs
@@ -1412,9 +1542,11 @@ lce_status_t make_plan(const lce_problem_t* p, Plan* pl) {
   pl->o_pos = take(cur, 4 * (size_t)pl->npad);
   pl->o_nv = take(cur, 256);
   const size_t common = cur;
-  pl->o_pm = take(cur, 4 * (size_t)(2 * pl->nparts) * pl->npad);
-  pl->o_ps = take(cur, 4 * (size_t)(2 * pl->nparts) * pl->npad);
+  const int part_rows = 2 * pl->nparts > pl->vt_count3 ? 2 * pl->nparts : pl->vt_count3;
+  pl->o_pm = take(cur, 4 * (size_t)part_rows * pl->npad);
+  pl->o_ps = take(cur, 4 * (size_t)part_rows * pl->npad);
   pl->o_terms = take(cur, 4 * (size_t)pl->npad);
+  pl->o_hvf = take(cur, 2 * (size_t)p->d * pl->npad);   // valid rows of H, 12-wave forward
   pl->fwd_bytes = cur;
   cur = common;
   pl->o_hv = take(cur, 2 * (size_t)p->d * pl->npad);
@@ -1520,11 +1652,23 @@ lce_status_t forward_impl(const lce_problem_t* p, const ShardInfo* shard, const 
   // rows that are not valid get lse 0 and a zero per-token loss (or shard target logit)
   L(K_COMPACT, k_compact, dim3(1), dim3(1024), targets, p->target_bytes, pl.n, si.v_total, p->ignore_index,
     idx, pos, nv, n_valid, dev_status, lse, none ? loss : tgt_part);
-  L(K_FWD_STATS, k_fwd_stats, dim3(pl.nt_max * pl.nparts), dim3(NTHREADS), w, pl.ldw, (int)pl.v, h, pl.ldh,
-    pl.n, (const int*)idx, (const int*)nv, (int)pl.d, pl.nparts, pl.nt_max, pl.vt_count, pm, ps, (int)pl.npad,
-    kLog2e);
-  L(K_COMBINE, k_combine, dim3((unsigned)((pl.n + 3) / 4)), dim3(256), h, pl.ldh, w, pl.ldw, targets,
-    p->target_bytes, si.v_begin, pl.v, (const int*)idx, (const int*)nv, (int)pl.d, 2 * pl.nparts,
+  int parts2;   // partials per token
+  if (pl.d % KSLICE == 0 && (int64_t)pl.vt_count3 * pl.nt_max <= INT32_MAX) {
+    uint16_t* hv = (uint16_t*)(ws + pl.o_hvf);
+    L(K_GATHER_H, k_gather_rows, dim3((unsigned)std::min<int64_t>((pl.npad * (pl.d / 8) + 255) / 256, 16384)),
+      dim3(256), h, pl.ldh, (const int*)idx, (const int*)nv, (int)pl.d, hv);
+    L(K_FWD_STATS, k_fwd_tile, dim3((unsigned)(pl.vt_count3 * pl.nt_max)), dim3(Geo<3>::NT), w, pl.ldw, (int)pl.v,
+      (const uint16_t*)hv, pl.d, (const int*)nv, (int)pl.d, pl.vt_count3, (int)(pl.vc / Geo<3>::TM), pl.nt_max, pm,
+      ps, (int)pl.npad, kLog2e);
+    parts2 = pl.vt_count3;
+  } else {
+    L(K_FWD_STATS, k_fwd_stats<2>, dim3(pl.nt_max * pl.nparts), dim3(NTHREADS), w, pl.ldw, (int)pl.v, h, pl.ldh,
+      pl.n, (const int*)idx, (const int*)nv, (int)pl.d, pl.nparts, pl.nt_max, pl.vt_count, pm, ps, (int)pl.npad,
+      kLog2e);
+    parts2 = 2 * pl.nparts;
+  }
+  L(K_COMBINE, k_combine, dim3((unsigned)((pl.n + kCombTok - 1) / kCombTok)), dim3(1024), h, pl.ldh, w, pl.ldw, targets,
+    p->target_bytes, si.v_begin, pl.v, (const int*)idx, (const int*)nv, (int)pl.d, parts2,
     (const float*)pm, (const float*)ps, (int)pl.npad, lse, terms, none ? loss : (float*)nullptr, tgt_part);
   if (!none && !shard) L(K_LOSS, k_loss, dim3(1), dim3(1024), (const float*)terms, (const int*)nv, p->reduction, loss);
   return L.st;
@@ -1734,14 +1878,14 @@ lce_status_t kd_fused_impl(const lce_kd_problem_t* p, const void* Hs, const void
     Launcher L{(hipStream_t)stream};
     L(K_COMPACT, k_compact, dim3(1), dim3(1024), targets, p->target_bytes, pl.n, pl.v, p->ignore_index,
       idx, pos, nv, n_valid, dev_status, lse_s, lse_t);
-    L(K_FWD_STATS, k_fwd_stats, dim3(tp.nt_max * tp.nparts), dim3(NTHREADS), wt, tp.ldw, (int)tp.v, ht, tp.ldh,
+    L(K_FWD_STATS, k_fwd_stats<2>, dim3(tp.nt_max * tp.nparts), dim3(NTHREADS), wt, tp.ldw, (int)tp.v, ht, tp.ldh,
       tp.n, (const int*)idx, (const int*)nv, (int)tp.d, tp.nparts, tp.nt_max, tp.vt_count, pm, ps, npad, k.scale2);
-    L(K_COMBINE, k_combine, dim3((unsigned)((pl.n + 3) / 4)), dim3(256), ht, tp.ldh, wt, tp.ldw, targets,
+    L(K_COMBINE, k_combine, dim3((unsigned)((pl.n + kCombTok - 1) / kCombTok)), dim3(1024), ht, tp.ldh, wt, tp.ldw, targets,
       p->target_bytes, (int64_t)0, (int64_t)0, (const int*)idx, (const int*)nv, (int)tp.d, 2 * tp.nparts,
       (const float*)pm, (const float*)ps, npad, lse_t, (float*)nullptr, (float*)nullptr, tgt);
-    L(K_FWD_STATS, k_fwd_stats, dim3(pl.nt_max * pl.nparts), dim3(NTHREADS), wsm, pl.ldw, (int)pl.v, hs, pl.ldh,
+    L(K_FWD_STATS, k_fwd_stats<2>, dim3(pl.nt_max * pl.nparts), dim3(NTHREADS), wsm, pl.ldw, (int)pl.v, hs, pl.ldh,
       pl.n, (const int*)idx, (const int*)nv, (int)pl.d, pl.nparts, pl.nt_max, pl.vt_count, pm, ps, npad, k.scale2);
-    L(K_COMBINE, k_combine, dim3((unsigned)((pl.n + 3) / 4)), dim3(256), hs, pl.ldh, wsm, pl.ldw, targets,
+    L(K_COMBINE, k_combine, dim3((unsigned)((pl.n + kCombTok - 1) / kCombTok)), dim3(1024), hs, pl.ldh, wsm, pl.ldw, targets,
       p->target_bytes, (int64_t)0, (int64_t)0, (const int*)idx, (const int*)nv, (int)pl.d, 2 * pl.nparts,
       (const float*)pm, (const float*)ps, npad, lse_s, (float*)nullptr, (float*)nullptr, tgt);
     if (L.st != LCE_OK) return L.st;
@@ -1800,14 +1944,14 @@ lce_status_t kd_forward_impl(const lce_kd_problem_t* p, const void* Hs, const vo
     idx, pos, nv, n_valid, dev_status, lse_s, lse_t);
   // log-sum-exp of both heads' logits / T (no target logit: an empty id range)
   const Plan& tp = k.t;
-  L(K_FWD_STATS, k_fwd_stats, dim3(tp.nt_max * tp.nparts), dim3(NTHREADS), wt, tp.ldw, (int)tp.v, ht, tp.ldh,
+  L(K_FWD_STATS, k_fwd_stats<2>, dim3(tp.nt_max * tp.nparts), dim3(NTHREADS), wt, tp.ldw, (int)tp.v, ht, tp.ldh,
     tp.n, (const int*)idx, (const int*)nv, (int)tp.d, tp.nparts, tp.nt_max, tp.vt_count, pm, ps, npad, k.scale2);
-  L(K_COMBINE, k_combine, dim3((unsigned)((pl.n + 3) / 4)), dim3(256), ht, tp.ldh, wt, tp.ldw, targets,
+  L(K_COMBINE, k_combine, dim3((unsigned)((pl.n + kCombTok - 1) / kCombTok)), dim3(1024), ht, tp.ldh, wt, tp.ldw, targets,
     p->target_bytes, (int64_t)0, (int64_t)0, (const int*)idx, (const int*)nv, (int)tp.d, 2 * tp.nparts,
     (const float*)pm, (const float*)ps, npad, lse_t, terms, (float*)nullptr, tgt);
-  L(K_FWD_STATS, k_fwd_stats, dim3(pl.nt_max * pl.nparts), dim3(NTHREADS), wsm, pl.ldw, (int)pl.v, hs, pl.ldh,
+  L(K_FWD_STATS, k_fwd_stats<2>, dim3(pl.nt_max * pl.nparts), dim3(NTHREADS), wsm, pl.ldw, (int)pl.v, hs, pl.ldh,
     pl.n, (const int*)idx, (const int*)nv, (int)pl.d, pl.nparts, pl.nt_max, pl.vt_count, pm, ps, npad, k.scale2);
-  L(K_COMBINE, k_combine, dim3((unsigned)((pl.n + 3) / 4)), dim3(256), hs, pl.ldh, wsm, pl.ldw, targets,
+  L(K_COMBINE, k_combine, dim3((unsigned)((pl.n + kCombTok - 1) / kCombTok)), dim3(1024), hs, pl.ldh, wsm, pl.ldw, targets,
     p->target_bytes, (int64_t)0, (int64_t)0, (const int*)idx, (const int*)nv, (int)pl.d, 2 * pl.nparts,
     (const float*)pm, (const float*)ps, npad, lse_s, terms, (float*)nullptr, tgt);
   // per slab: teacher probabilities P, then the student's sum_v P zs / T per token and tile
