@@ -637,34 +637,66 @@ __global__ __launch_bounds__(1024) void k_compact(const void* targets, int tbyte
 //    through idx by the main loop; two partial rows (one per wave row) per partition.
 // In both, a tile's S^T = W_tile H^T runs a token's logits down a lane's registers.
 // ---------------------------------------------------------------------------------------------
-// Tiles are taken in groups of gw vocabulary tiles (one backward slab's width) by all token
-// tiles, ids fastest: the group's W rows stay in the MALL while the token tiles pass, and the
+// Tiles are taken in groups of gw consecutive vocabulary tiles (one backward slab's width) by all
+// token tiles, ids fastest: the group's W rows stay in the MALL while the token tiles pass, and the
 // workgroups resident on one XCD (consecutive blocks go to the 8 XCDs in turn) share their W and H
-// tiles through its L2 as in the backward's G launches.
+// tiles through its L2 as in the backward's G launches. One launch covers vt_launch tiles from tm0
+// on and writes one partial row per tile (row tm - tm0). When the rows of all tiles would take
+// more than 2 D bytes per token (one bf16 row of H), the host launches one group at a time
+// instead: group g writes to one of two row sets (by the parity of g), and in launch g >= 1 the
+// workgroup of the group's first tile of each token tile first folds the other set (group g - 1,
+// complete since launches on a stream run in order) into a running pair per token. The workspace
+// thus stays independent of V.
+__device__ __forceinline__ void merge_pair(float& m, float& s, float m2, float s2) {
+  const float mn = fmaxf(m, m2);
+  if (mn == -INFINITY) return;
+  s = (m == -INFINITY ? 0.f : s * exp2f(m - mn)) + (m2 == -INFINITY ? 0.f : s2 * exp2f(m2 - mn));
+  m = mn;
+}
+
 __global__ __launch_bounds__(Geo<3>::NT, 3) void k_fwd_tile(const uint16_t* __restrict__ W, int64_t ldw, int v,
                                                             const uint16_t* __restrict__ Hv, int64_t ldh,
-                                                            const int* __restrict__ nv_ptr, int d, int vt_count,
-                                                            int gw, int nt_max, float* __restrict__ part_m,
-                                                            float* __restrict__ part_s, int npad, float scale2) {
+                                                            const int* __restrict__ nv_ptr, int d, int tm0,
+                                                            int vt_launch, int gw, int nt_max,
+                                                            float* __restrict__ part_m, float* __restrict__ part_s,
+                                                            const float* __restrict__ prev_m,
+                                                            const float* __restrict__ prev_s, int wprev,
+                                                            float* __restrict__ run_m, float* __restrict__ run_s,
+                                                            int run_init, int npad, float scale2) {
   constexpr int WM = 3, TM = Geo<WM>::TM;
   __shared__ __attribute__((aligned(16))) char smem[Geo<WM>::LDS];
   const int b = blockIdx.x;
-  const int full = vt_count / gw;
+  const int full = vt_launch / gw;
   const int g = b / (gw * nt_max);
-  int tm, tn;
+  int tl, tn;   // launch-relative vocabulary tile, token tile
   if (g < full) {
     const int r = b - g * gw * nt_max;
-    tm = g * gw + r % gw;
+    tl = g * gw + r % gw;
     tn = r / gw;
   } else {
-    const int r = b - full * gw * nt_max, wl = vt_count - full * gw;
-    tm = full * gw + r % wl;
+    const int r = b - full * gw * nt_max, wl = vt_launch - full * gw;
+    tl = full * gw + r % wl;
     tn = r / wl;
   }
+  const int tm = tm0 + tl;
   const int nv = *nv_ptr;
   const int n0 = tn * TILE;
   if (n0 >= nv) return;
   const int v0 = tm * TM, vleft = v - v0;
+  if (prev_m && tl == 0 && threadIdx.x < TILE) {
+    const int tok = n0 + threadIdx.x;
+    if (tok < nv) {
+      float m = -INFINITY, s = 0.f;
+      if (!run_init) {
+        m = run_m[tok];
+        s = run_s[tok];
+      }
+#pragma unroll 8
+      for (int q = 0; q < wprev; ++q) merge_pair(m, s, prev_m[(int64_t)q * npad + tok], prev_s[(int64_t)q * npad + tok]);
+      run_m[tok] = m;
+      run_s[tok] = s;
+    }
+  }
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, wr = wave >> 2, wc = wave & 3;
 
   const Operand opa = dense_operand(W + (int64_t)v0 * ldw, vleft, ldw);
@@ -725,8 +757,8 @@ __global__ __launch_bounds__(Geo<3>::NT, 3) void k_fwd_tile(const uint16_t* __re
       m = mn;
     }
     if (tok < nv) {
-      part_m[(int64_t)tm * npad + tok] = m;
-      part_s[(int64_t)tm * npad + tok] = s;
+      part_m[(int64_t)tl * npad + tok] = m;
+      part_s[(int64_t)tl * npad + tok] = s;
     }
   }
 }
@@ -832,21 +864,16 @@ __global__ __launch_bounds__(Geo<WM>::NT, WM) void k_fwd_stats(const uint16_t* _
 // ---------------------------------------------------------------------------------------------
 constexpr int kCombTok = 64;
 
-__device__ __forceinline__ void merge_pair(float& m, float& s, float m2, float s2) {
-  const float mn = fmaxf(m, m2);
-  if (mn == -INFINITY) return;
-  s = (m == -INFINITY ? 0.f : s * exp2f(m - mn)) + (m2 == -INFINITY ? 0.f : s2 * exp2f(m2 - mn));
-  m = mn;
-}
-
 __global__ __launch_bounds__(1024) void k_combine(const uint16_t* __restrict__ H, int64_t ldh,
                                                   const uint16_t* __restrict__ W, int64_t ldw,
                                                   const void* targets, int tbytes, int64_t id0, int64_t v_local,
                                                   const int* __restrict__ idx, const int* __restrict__ nv_ptr,
                                                   int d, int nparts2, const float* __restrict__ part_m,
                                                   const float* __restrict__ part_s, int npad,
+                                                  const float* __restrict__ run_m, const float* __restrict__ run_s,
                                                   float* __restrict__ lse_out, float* __restrict__ terms,
                                                   float* __restrict__ per_token, float* __restrict__ tgt_part) {
+  // run_m / run_s (may be null): a running pair per token folded in before the partial rows
   __shared__ float red_m[16][kCombTok], red_s[16][kCombTok], lse_t[kCombTok];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int i0 = blockIdx.x * kCombTok;
@@ -855,6 +882,10 @@ __global__ __launch_bounds__(1024) void k_combine(const uint16_t* __restrict__ H
   {
     const int i = i0 + lane;
     float m = -INFINITY, s = 0.f;
+    if (i < nv && wave == 0 && run_m) {
+      m = run_m[i];
+      s = run_s[i];
+    }
     if (i < nv)
       for (int q = wave; q < nparts2; q += 16) merge_pair(m, s, part_m[(int64_t)q * npad + i], part_s[(int64_t)q * npad + i]);
     red_m[wave][lane] = m;
@@ -1491,12 +1522,18 @@ Timing g_timing;
 
 struct Plan {
   int64_t n, d, v, ldh, ldw, npad;
-  int nt_max, vt_count, nparts, vt_count3;
+  int nt_max, vt_count, nparts, vt_count3;   // vt_count3: 384-id tiles
   int64_t vc, nslab;
   // workspace offsets
   size_t o_idx, o_pos, o_nv, o_pm, o_ps, o_terms, o_hvf, fwd_bytes;
   size_t o_hv, o_g, o_dh32, bwd_bytes;
 };
+
+// the 12-wave forward in one launch: its partial rows (8 bytes per 384-id tile and token) take at
+// most 2 D bytes per token
+inline bool fwd_one_launch(const Plan& pl) {
+  return pl.vt_count3 <= pl.d / 4 && (int64_t)pl.vt_count3 * pl.nt_max <= INT32_MAX;
+}
 
 inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 
@@ -1521,7 +1558,6 @@ lce_status_t make_plan(const lce_problem_t* p, Plan* pl) {
   pl->nt_max = (int)(pl->npad / TILE);
   pl->vt_count = (int)((p->v + TILE - 1) / TILE);
   pl->nparts = pl->vt_count < MAX_PARTS ? pl->vt_count : MAX_PARTS;
-  // the 12-wave forward (D % 64 == 0): one workgroup and one partial row per 384-id tile
   pl->vt_count3 = (int)((p->v + 383) / 384);
   // backward vocabulary slab: about 4 D columns (at least 8192) keeps G at O(N D) while halving
   // the dH accumulator passes of a 2 D slab; a multiple of 16 tiles of 384 ids, so that the dW
@@ -1542,7 +1578,10 @@ lce_status_t make_plan(const lce_problem_t* p, Plan* pl) {
   pl->o_pos = take(cur, 4 * (size_t)pl->npad);
   pl->o_nv = take(cur, 256);
   const size_t common = cur;
-  const int part_rows = 2 * pl->nparts > pl->vt_count3 ? 2 * pl->nparts : pl->vt_count3;
+  // partial rows: 2 per partition (8-wave forward); one per 384-id tile while that is at most
+  // 2 D bytes per token, else two sets of vc / 384 rows and a running pair (12-wave forward)
+  const int64_t rows3 = fwd_one_launch(*pl) ? pl->vt_count3 : 2 * (vc / 384) + 1;
+  const int64_t part_rows = 2 * pl->nparts > rows3 ? 2 * pl->nparts : rows3;
   pl->o_pm = take(cur, 4 * (size_t)part_rows * pl->npad);
   pl->o_ps = take(cur, 4 * (size_t)part_rows * pl->npad);
   pl->o_terms = take(cur, 4 * (size_t)pl->npad);
@@ -1652,24 +1691,53 @@ lce_status_t forward_impl(const lce_problem_t* p, const ShardInfo* shard, const 
   // rows that are not valid get lse 0 and a zero per-token loss (or shard target logit)
   L(K_COMPACT, k_compact, dim3(1), dim3(1024), targets, p->target_bytes, pl.n, si.v_total, p->ignore_index,
     idx, pos, nv, n_valid, dev_status, lse, none ? loss : tgt_part);
-  int parts2;   // partials per token
-  if (pl.d % KSLICE == 0 && (int64_t)pl.vt_count3 * pl.nt_max <= INT32_MAX) {
+  if (pl.d % KSLICE == 0) {
     uint16_t* hv = (uint16_t*)(ws + pl.o_hvf);
     L(K_GATHER_H, k_gather_rows, dim3((unsigned)std::min<int64_t>((pl.npad * (pl.d / 8) + 255) / 256, 16384)),
       dim3(256), h, pl.ldh, (const int*)idx, (const int*)nv, (int)pl.d, hv);
-    L(K_FWD_STATS, k_fwd_tile, dim3((unsigned)(pl.vt_count3 * pl.nt_max)), dim3(Geo<3>::NT), w, pl.ldw, (int)pl.v,
-      (const uint16_t*)hv, pl.d, (const int*)nv, (int)pl.d, pl.vt_count3, (int)(pl.vc / Geo<3>::TM), pl.nt_max, pm,
-      ps, (int)pl.npad, kLog2e);
-    parts2 = pl.vt_count3;
+    const int gw = (int)(pl.vc / Geo<3>::TM);
+    const int ntl = pl.vt_count3;
+    if (fwd_one_launch(pl)) {
+      L(K_FWD_STATS, k_fwd_tile, dim3((unsigned)(ntl * pl.nt_max)), dim3(Geo<3>::NT), w, pl.ldw, (int)pl.v,
+        (const uint16_t*)hv, pl.d, (const int*)nv, (int)pl.d, 0, ntl, gw, pl.nt_max, pm, ps,
+        (const float*)nullptr, (const float*)nullptr, 0, (float*)nullptr, (float*)nullptr, 0, (int)pl.npad, kLog2e);
+      L(K_COMBINE, k_combine, dim3((unsigned)((pl.n + kCombTok - 1) / kCombTok)), dim3(1024), h, pl.ldh, w, pl.ldw,
+        targets, p->target_bytes, si.v_begin, pl.v, (const int*)idx, (const int*)nv, (int)pl.d, ntl,
+        (const float*)pm, (const float*)ps, (int)pl.npad, (const float*)nullptr, (const float*)nullptr, lse, terms,
+        none ? loss : (float*)nullptr, tgt_part);
+      if (!none && !shard) L(K_LOSS, k_loss, dim3(1), dim3(1024), (const float*)terms, (const int*)nv, p->reduction, loss);
+      return L.st;
+    }
+    // one group per launch; row sets: parity 0 at rows [0, gw), parity 1 at [gw, 2 gw), the
+    // running pair at row 2 gw
+    const int ng = (ntl + gw - 1) / gw;
+    const int64_t rs = (int64_t)gw * pl.npad;
+    float* run_m = pm + 2 * rs;
+    float* run_s = ps + 2 * rs;
+    for (int g = 0; g < ng; ++g) {
+      const int tm0 = g * gw, wl = std::min(gw, ntl - tm0);
+      const int64_t cur = (g & 1) * rs, prev = ((g + 1) & 1) * rs;
+      L(K_FWD_STATS, k_fwd_tile, dim3((unsigned)(wl * pl.nt_max)), dim3(Geo<3>::NT), w, pl.ldw, (int)pl.v,
+        (const uint16_t*)hv, pl.d, (const int*)nv, (int)pl.d, tm0, wl, gw, pl.nt_max, pm + cur, ps + cur,
+        g > 0 ? (const float*)(pm + prev) : (const float*)nullptr, (const float*)(ps + prev), gw, run_m, run_s,
+        g == 1 ? 1 : 0, (int)pl.npad, kLog2e);
+    }
+    const int wl_last = ntl - (ng - 1) * gw;
+    const int64_t last = ((ng - 1) & 1) * rs;
+    L(K_COMBINE, k_combine, dim3((unsigned)((pl.n + kCombTok - 1) / kCombTok)), dim3(1024), h, pl.ldh, w, pl.ldw,
+      targets, p->target_bytes, si.v_begin, pl.v, (const int*)idx, (const int*)nv, (int)pl.d, wl_last,
+      (const float*)(pm + last), (const float*)(ps + last), (int)pl.npad,
+      ng > 1 ? (const float*)run_m : (const float*)nullptr, (const float*)run_s, lse, terms,
+      none ? loss : (float*)nullptr, tgt_part);
   } else {
     L(K_FWD_STATS, k_fwd_stats<2>, dim3(pl.nt_max * pl.nparts), dim3(NTHREADS), w, pl.ldw, (int)pl.v, h, pl.ldh,
       pl.n, (const int*)idx, (const int*)nv, (int)pl.d, pl.nparts, pl.nt_max, pl.vt_count, pm, ps, (int)pl.npad,
       kLog2e);
-    parts2 = 2 * pl.nparts;
+    L(K_COMBINE, k_combine, dim3((unsigned)((pl.n + kCombTok - 1) / kCombTok)), dim3(1024), h, pl.ldh, w, pl.ldw,
+      targets, p->target_bytes, si.v_begin, pl.v, (const int*)idx, (const int*)nv, (int)pl.d, 2 * pl.nparts,
+      (const float*)pm, (const float*)ps, (int)pl.npad, (const float*)nullptr, (const float*)nullptr, lse, terms,
+      none ? loss : (float*)nullptr, tgt_part);
   }
-  L(K_COMBINE, k_combine, dim3((unsigned)((pl.n + kCombTok - 1) / kCombTok)), dim3(1024), h, pl.ldh, w, pl.ldw, targets,
-    p->target_bytes, si.v_begin, pl.v, (const int*)idx, (const int*)nv, (int)pl.d, parts2,
-    (const float*)pm, (const float*)ps, (int)pl.npad, lse, terms, none ? loss : (float*)nullptr, tgt_part);
   if (!none && !shard) L(K_LOSS, k_loss, dim3(1), dim3(1024), (const float*)terms, (const int*)nv, p->reduction, loss);
   return L.st;
 }
@@ -1882,12 +1950,12 @@ lce_status_t kd_fused_impl(const lce_kd_problem_t* p, const void* Hs, const void
       tp.n, (const int*)idx, (const int*)nv, (int)tp.d, tp.nparts, tp.nt_max, tp.vt_count, pm, ps, npad, k.scale2);
     L(K_COMBINE, k_combine, dim3((unsigned)((pl.n + kCombTok - 1) / kCombTok)), dim3(1024), ht, tp.ldh, wt, tp.ldw, targets,
       p->target_bytes, (int64_t)0, (int64_t)0, (const int*)idx, (const int*)nv, (int)tp.d, 2 * tp.nparts,
-      (const float*)pm, (const float*)ps, npad, lse_t, (float*)nullptr, (float*)nullptr, tgt);
+      (const float*)pm, (const float*)ps, npad, (const float*)nullptr, (const float*)nullptr, lse_t, (float*)nullptr, (float*)nullptr, tgt);
     L(K_FWD_STATS, k_fwd_stats<2>, dim3(pl.nt_max * pl.nparts), dim3(NTHREADS), wsm, pl.ldw, (int)pl.v, hs, pl.ldh,
       pl.n, (const int*)idx, (const int*)nv, (int)pl.d, pl.nparts, pl.nt_max, pl.vt_count, pm, ps, npad, k.scale2);
     L(K_COMBINE, k_combine, dim3((unsigned)((pl.n + kCombTok - 1) / kCombTok)), dim3(1024), hs, pl.ldh, wsm, pl.ldw, targets,
       p->target_bytes, (int64_t)0, (int64_t)0, (const int*)idx, (const int*)nv, (int)pl.d, 2 * pl.nparts,
-      (const float*)pm, (const float*)ps, npad, lse_s, (float*)nullptr, (float*)nullptr, tgt);
+      (const float*)pm, (const float*)ps, npad, (const float*)nullptr, (const float*)nullptr, lse_s, (float*)nullptr, (float*)nullptr, tgt);
     if (L.st != LCE_OK) return L.st;
   }
   const KdArgs kd{ht, tp.ldh, wt, tp.ldw, (int)tp.d, lse_t, k.scale2, k.inv_t, qpart};
@@ -1948,12 +2016,12 @@ lce_status_t kd_forward_impl(const lce_kd_problem_t* p, const void* Hs, const vo
     tp.n, (const int*)idx, (const int*)nv, (int)tp.d, tp.nparts, tp.nt_max, tp.vt_count, pm, ps, npad, k.scale2);
   L(K_COMBINE, k_combine, dim3((unsigned)((pl.n + kCombTok - 1) / kCombTok)), dim3(1024), ht, tp.ldh, wt, tp.ldw, targets,
     p->target_bytes, (int64_t)0, (int64_t)0, (const int*)idx, (const int*)nv, (int)tp.d, 2 * tp.nparts,
-    (const float*)pm, (const float*)ps, npad, lse_t, terms, (float*)nullptr, tgt);
+    (const float*)pm, (const float*)ps, npad, (const float*)nullptr, (const float*)nullptr, lse_t, terms, (float*)nullptr, tgt);
   L(K_FWD_STATS, k_fwd_stats<2>, dim3(pl.nt_max * pl.nparts), dim3(NTHREADS), wsm, pl.ldw, (int)pl.v, hs, pl.ldh,
     pl.n, (const int*)idx, (const int*)nv, (int)pl.d, pl.nparts, pl.nt_max, pl.vt_count, pm, ps, npad, k.scale2);
   L(K_COMBINE, k_combine, dim3((unsigned)((pl.n + kCombTok - 1) / kCombTok)), dim3(1024), hs, pl.ldh, wsm, pl.ldw, targets,
     p->target_bytes, (int64_t)0, (int64_t)0, (const int*)idx, (const int*)nv, (int)pl.d, 2 * pl.nparts,
-    (const float*)pm, (const float*)ps, npad, lse_s, terms, (float*)nullptr, tgt);
+    (const float*)pm, (const float*)ps, npad, (const float*)nullptr, (const float*)nullptr, lse_s, terms, (float*)nullptr, tgt);
   // per slab: teacher probabilities P, then the student's sum_v P zs / T per token and tile
   for (int64_t s = 0; s < pl.nslab; ++s) {
     const int64_t v0 = s * pl.vc;

@@ -42,9 +42,16 @@ def test_workspace_is_linear_in_tokens_and_never_tokens_times_vocab():
     slab = max(8192, 4 * d)
     bound = 4 * n * 4 + 2 * d * n + 2 * 2 * n * slab + 2 * d * slab + 4 * n * d + 4096
     assert b1 <= bound
-    # doubling the vocabulary leaves the workspace (almost) unchanged
-    f3, b3 = B.lce_workspace_size(B.problem(16384, 4096, 256512))
-    assert b3 == b1 and f3 <= f1 * 1.01
+    # the backward workspace does not depend on V; the forward's partial rows (8 bytes per token and
+    # 384-id tile) are capped at 2 D bytes per token, beyond which it switches to a fixed row count
+    fwd = {}
+    for vv in (128256, 256512, 393216, 393600, 1 << 20, 1 << 22):
+        fv, bv = B.lce_workspace_size(B.problem(n, d, vv))
+        assert bv == b1
+        fwd[vv] = fv
+    assert fwd[393216] - fwd[128256] == 8 * n * (1024 - 334)     # one row per tile up to D / 4 tiles
+    assert fwd[393600] < fwd[393216] and fwd[1 << 20] == fwd[1 << 22] == fwd[393600]
+    assert max(fwd.values()) <= f1 + 8 * n * (d // 4)
 
 
 @pytest.mark.parametrize("kw,code", [

@@ -42,6 +42,14 @@ def test_ragged_shapes(n, d, v):
     _case(WL.custom(n, d, v, seed=n + v, mask_frac=0.15, sigma_w=0.3))
 
 
+@pytest.mark.parametrize("n,d,v", [(300, 64, 20000), (270, 128, 30000), (520, 64, 40000)])
+def test_forward_vocabulary_groups(n, d, v):
+    # with D % 64 == 0 the forward runs one launch per group of 384-id tiles as wide as a backward
+    # slab (12288 ids at these widths): 2, 3 and 4 groups, a ragged last group, both partial row
+    # sets and the running pair
+    _case(WL.custom(n, d, v, seed=n + d, mask_frac=0.2, sigma_w=0.3))
+
+
 def test_sum_reduction_and_upstream_gradient():
     _case(WL.custom(300, 128, 2000, seed=2, mask_frac=0.3), reduction="sum", grad=0.37)
     _case(WL.custom(300, 128, 2000, seed=2, mask_frac=0.3), reduction="mean", grad=-2.5)
