@@ -332,7 +332,11 @@ template <bool kKM, int kW, int kBlocks>
 __device__ __forceinline__ void read_operand(bf16x8_t (&f)[kBlocks], const char* reg, const FragAddr<kBlocks>& fa,
                                              int ks) {
   if constexpr (!kKM) {
-    const char* p = reg + (fa.rk ^ (uint32_t)(32 * ks));
+    // the base address is made opaque at each read, so that its per-substep variants are formed
+    // next to the reads (one VALU op each) instead of being held in registers through the loop
+    uint32_t rk = fa.rk;
+    asm volatile("" : "+v"(rk));
+    const char* p = reg + (rk ^ (uint32_t)(32 * ks));
 #pragma unroll
     for (int b = 0; b < kBlocks; ++b) f[b] = *reinterpret_cast<const bf16x8_t*>(p + b * 4096);
   } else {
@@ -381,12 +385,12 @@ __device__ __forceinline__ void load_operand(const Operand& op, const char* dstp
   }
 }
 
+// w: this wave's index in the workgroup, a wave-uniform (scalar) value
 template <bool kAsm, int kAKind, int kBKind, int WM, bool kMasked>
 __device__ __forceinline__ void load_slice(const Operand& A, const Operand& B, const char* buf, int bufoff, int k0,
-                                           int K) {
-  const int w = threadIdx.x >> 6;
+                                           int K, int w) {
   const char* dstp = buf + w * 4096;
-  const int dst = bufoff + __builtin_amdgcn_readfirstlane(w) * 4096;   // LDS byte address (asm loads)
+  const int dst = bufoff + w * 4096;   // LDS byte address (asm loads)
   load_operand<kAsm, kAKind, Geo<WM>::TM, kMasked>(A, dstp, dst, k0, K);
   if (WM == 2 || w < 8) load_operand<kAsm, kBKind, 256, kMasked>(B, dstp + Geo<WM>::AREG, dst + Geo<WM>::AREG, k0, K);
 }
@@ -426,15 +430,20 @@ __device__ __forceinline__ void mma_mainloop(f32x16_t (&acc)[4][2], const Operan
   // loads as inline asm where transposing reads are used (see dma16)
   constexpr bool kAsm = kAKM || kBKM;
   const int lds0 = kAsm ? __builtin_amdgcn_readfirstlane((int)(uint32_t)(uintptr_t)smem) : 0;
+  // One scalar copy of the wave index for the whole loop. Opaque to the compiler, so that it is
+  // not recomputed from the work-item id register inside the loop: under register pressure that
+  // register is spilled, and its reload would wait for every load in flight.
+  int wsc = __builtin_amdgcn_readfirstlane(wave);
+  asm volatile("" : "+s"(wsc));
   auto load = [&](int s) {
     char* buf = smem + (s & 1) * G::SLICE;
     const int bufoff = lds0 + (s & 1) * G::SLICE;
-    if (ragged && s == S - 1) load_slice<kAsm, kAKind, kBKind, WM, true>(A, B, buf, bufoff, s * KSLICE, K);
-    else load_slice<kAsm, kAKind, kBKind, WM, false>(A, B, buf, bufoff, s * KSLICE, K);
+    if (ragged && s == S - 1) load_slice<kAsm, kAKind, kBKind, WM, true>(A, B, buf, bufoff, s * KSLICE, K, wsc);
+    else load_slice<kAsm, kAKind, kBKind, WM, false>(A, B, buf, bufoff, s * KSLICE, K, wsc);
   };
 
   // waves of a 12-wave workgroup past the eighth load only A: 4 loads per slice instead of 8
-  const bool a_only = WM == 3 && __builtin_amdgcn_readfirstlane(wave) >= 8;
+  const bool a_only = WM == 3 && wsc >= 8;
   load(0);
   if (S > 1) {
     load(1);
@@ -448,7 +457,7 @@ __device__ __forceinline__ void mma_mainloop(f32x16_t (&acc)[4][2], const Operan
   // Waves 0..3 (the first wave of each SIMD) issue their share of a slice's loads at the barrier;
   // the others kLateGroups MFMA substeps later: a smaller load burst, and the other waves of each
   // SIMD go straight back to MFMA work.
-  const bool late = __builtin_amdgcn_readfirstlane(wave) >= 4;
+  const bool late = wsc >= 4;
   int pend = -1;
   if constexpr (WM == 2) {
     FragSet f0, f1;
