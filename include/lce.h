@@ -107,8 +107,10 @@ typedef struct lce_adamw {
 
 /*
  * Workspace sizes, in bytes, for lce_forward (*fwd_bytes) and lce_backward
- * (*bwd_bytes). They grow as O(N*D + D*V_slab) with V_slab <= max(8192, 4*D)
- * rounded to 256: never O(N*V). Either output pointer may be NULL.
+ * (*bwd_bytes). They grow as O(N*D + N*V_slab) with V_slab = max(8192, 4*D)
+ * rounded up to a multiple of 6144 (at most V rounded up to 768): never O(N*V).
+ * The backward's size does not depend on V; the forward's vocabulary partials
+ * take at most 2*D bytes per token. Either output pointer may be NULL.
  */
 lce_status_t lce_workspace_size(const lce_problem_t* p, size_t* fwd_bytes, size_t* bwd_bytes);
 

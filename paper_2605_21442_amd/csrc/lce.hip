@@ -8,24 +8,26 @@
 // documented in include/lce.h.
 //
 // Path (all kernels enqueue on the caller's stream, no host synchronisation):
-//   forward : compact -> fwd_stats (bf16 MFMA tiles of S^T = W H_valid^T with an
-//             online max / sum-exp epilogue) -> combine (merge partials, target
-//             logit, per-row loss) -> loss (fixed-order reduction)
-//   backward: compact -> gather/transpose H_valid -> per vocabulary slab:
-//             G tile (recompute S^T, G = c (softmax - onehot)), dH32 (+)= G W_slab,
-//             dW slab = G^T H_valid -> finalise dH
+//   forward : compact -> gather the valid rows Hv -> fwd_tile (bf16 MFMA tiles of
+//             S^T = W Hv^T, each reduced to a (max, sum-exp) partial per token) ->
+//             combine (merge partials, target logit, per-row loss) -> loss (fixed-order
+//             reduction)
+//   backward: compact -> gather Hv -> per vocabulary slab: G tile (recompute S^T,
+//             G = c (softmax - onehot)), dH32 (+)= G W_slab, dW slab = G^T Hv ->
+//             finalise dH
 // Built on the same kernels: the backward with an AdamW step on each finished dW block
 // (paper Sec. 4.1), a vocabulary-shard (loss-parallel) forward / combine / backward, and a
 // fused linear knowledge-distillation loss whose G kernel takes the teacher's probabilities
 // as soft targets.
 //
-// Every contraction C = A B^T (C [M, N], sum over K) runs one MFMA main loop:
-// 256x256 output tiles, 8 waves of 128x64, bf16 v_mfma_f32_32x32x16 with fp32
-// accumulation, K streamed through two 64-wide LDS slices filled by direct-to-LDS
-// buffer loads (XOR-swizzled 16-byte chunks). Each operand is either K-contiguous
-// (H, W in the forward and G kernels; G in dH) or K-major (G in dW, the W slab in
-// dH: the MFMA fragments then come from transposing LDS reads), so G is written
-// once, token-major, and W is never copied.
+// Every contraction C = A B^T (C [M, N], sum over K) runs one MFMA main loop: bf16
+// v_mfma_f32_32x32x16 with fp32 accumulation, waves of 128x64 outputs, K streamed through
+// two 64-wide LDS slices filled by direct-to-LDS buffer loads (XOR-swizzled 16-byte
+// chunks). Tiles are 384x256 with 12 waves (three per SIMD) for the LCE contractions when
+// D % 64 == 0, else 256x256 with 8 waves. Each operand is either K-contiguous (W and Hv in
+// the forward and G kernels; G in dH) or K-major (G and Hv in dW, the W slab in dH: the
+// MFMA fragments then come from transposing LDS reads), so G is written once, token-major,
+// and W is never copied.
 
 #include <hip/hip_runtime.h>
 
@@ -1044,7 +1046,7 @@ __device__ __forceinline__ float grad_scale(const float* grad, const int* n_norm
 
 // ---------------------------------------------------------------------------------------------
 // K4: softmax-gradient tile for one vocabulary slab. Tile (vocabulary tile tm, token tile tn) of
-// S^T = W_slab H_valid^T is recomputed and turned into G = c (exp(s - lse) - onehot), rounded to
+// S^T = W_slab Hv^T is recomputed and turned into G = c (exp(s - lse) - onehot), rounded to
 // bf16 and written as G[token][v] (row stride vc). Every tile is written whole: entries of tokens
 // at or beyond Nv and of ids at or beyond the slab width are zeros, so the two contractions that
 // read G (dH with K = ids, dW with K = tokens, G read K-major) need no masking of G.
