@@ -1671,6 +1671,57 @@ lce_status_t shard_info(const lce_problem_t* p, const lce_shard_t* sh, ShardInfo
   return LCE_OK;
 }
 
+// Partial rows that k_combine folds for one head: `count` rows of Npad from (m, s), after an
+// optional running pair (run_m, run_s).
+struct PartRows {
+  const float* m;
+  const float* s;
+  int count;
+  const float* run_m;
+  const float* run_s;
+};
+
+// Vocabulary statistics of one head, in log2 units of the logits times scale2 / log2(e). With
+// D % 64 == 0 and a gather buffer hv (Npad x D bf16), the valid rows of H are gathered and the
+// 12-wave tiles run, in one launch or one per group of tiles as `layout` (the plan that sized the
+// partial rows pm / ps) decides; otherwise the 8-wave partitions gather rows in their loop.
+PartRows launch_fwd_stats(Launcher& L, const Plan& layout, const uint16_t* W, int64_t ldw, const uint16_t* H,
+                          int64_t ldh, int d, const int* idx, const int* nv, uint16_t* hv, float* pm, float* ps,
+                          float scale2) {
+  const int v = (int)layout.v, npad = (int)layout.npad, nt_max = layout.nt_max;
+  if (!(hv && d % KSLICE == 0 && (int64_t)layout.vt_count3 * nt_max <= INT32_MAX)) {
+    L(K_FWD_STATS, k_fwd_stats<2>, dim3(nt_max * layout.nparts), dim3(NTHREADS), W, ldw, v, H, ldh, layout.n, idx,
+      nv, d, layout.nparts, nt_max, layout.vt_count, pm, ps, npad, scale2);
+    return PartRows{pm, ps, 2 * layout.nparts, nullptr, nullptr};
+  }
+  L(K_GATHER_H, k_gather_rows, dim3((unsigned)std::min<int64_t>(((int64_t)npad * (d / 8) + 255) / 256, 16384)),
+    dim3(256), H, ldh, idx, nv, d, hv);
+  const int gw = (int)(layout.vc / Geo<3>::TM);
+  const int ntl = layout.vt_count3;
+  if (fwd_one_launch(layout)) {
+    L(K_FWD_STATS, k_fwd_tile, dim3((unsigned)(ntl * nt_max)), dim3(Geo<3>::NT), W, ldw, v, (const uint16_t*)hv,
+      (int64_t)d, nv, d, 0, ntl, gw, nt_max, pm, ps, (const float*)nullptr, (const float*)nullptr, 0,
+      (float*)nullptr, (float*)nullptr, 0, npad, scale2);
+    return PartRows{pm, ps, ntl, nullptr, nullptr};
+  }
+  // one group per launch; row sets: parity 0 at rows [0, gw), parity 1 at [gw, 2 gw), the
+  // running pair at row 2 gw
+  const int ng = (ntl + gw - 1) / gw;
+  const int64_t rs = (int64_t)gw * npad;
+  float* run_m = pm + 2 * rs;
+  float* run_s = ps + 2 * rs;
+  for (int g = 0; g < ng; ++g) {
+    const int tm0 = g * gw, wl = std::min(gw, ntl - tm0);
+    const int64_t cur = (g & 1) * rs, prev = ((g + 1) & 1) * rs;
+    L(K_FWD_STATS, k_fwd_tile, dim3((unsigned)(wl * nt_max)), dim3(Geo<3>::NT), W, ldw, v, (const uint16_t*)hv,
+      (int64_t)d, nv, d, tm0, wl, gw, nt_max, pm + cur, ps + cur,
+      g > 0 ? (const float*)(pm + prev) : (const float*)nullptr, (const float*)(ps + prev), gw, run_m, run_s,
+      g == 1 ? 1 : 0, npad, scale2);
+  }
+  const int64_t last = ((ng - 1) & 1) * rs;
+  return PartRows{pm + last, ps + last, ntl - (ng - 1) * gw, ng > 1 ? run_m : nullptr, run_s};
+}
+
 // The forward pass behind lce_forward and (tgt_part != null) lce_forward_shard.
 lce_status_t forward_impl(const lce_problem_t* p, const ShardInfo* shard, const void* H, const void* W,
                           const void* targets, float* loss, float* lse, float* tgt_part, int32_t* n_valid,
@@ -1702,53 +1753,11 @@ lce_status_t forward_impl(const lce_problem_t* p, const ShardInfo* shard, const 
   // rows that are not valid get lse 0 and a zero per-token loss (or shard target logit)
   L(K_COMPACT, k_compact, dim3(1), dim3(1024), targets, p->target_bytes, pl.n, si.v_total, p->ignore_index,
     idx, pos, nv, n_valid, dev_status, lse, none ? loss : tgt_part);
-  if (pl.d % KSLICE == 0) {
-    uint16_t* hv = (uint16_t*)(ws + pl.o_hvf);
-    L(K_GATHER_H, k_gather_rows, dim3((unsigned)std::min<int64_t>((pl.npad * (pl.d / 8) + 255) / 256, 16384)),
-      dim3(256), h, pl.ldh, (const int*)idx, (const int*)nv, (int)pl.d, hv);
-    const int gw = (int)(pl.vc / Geo<3>::TM);
-    const int ntl = pl.vt_count3;
-    if (fwd_one_launch(pl)) {
-      L(K_FWD_STATS, k_fwd_tile, dim3((unsigned)(ntl * pl.nt_max)), dim3(Geo<3>::NT), w, pl.ldw, (int)pl.v,
-        (const uint16_t*)hv, pl.d, (const int*)nv, (int)pl.d, 0, ntl, gw, pl.nt_max, pm, ps,
-        (const float*)nullptr, (const float*)nullptr, 0, (float*)nullptr, (float*)nullptr, 0, (int)pl.npad, kLog2e);
-      L(K_COMBINE, k_combine, dim3((unsigned)((pl.n + kCombTok - 1) / kCombTok)), dim3(1024), h, pl.ldh, w, pl.ldw,
-        targets, p->target_bytes, si.v_begin, pl.v, (const int*)idx, (const int*)nv, (int)pl.d, ntl,
-        (const float*)pm, (const float*)ps, (int)pl.npad, (const float*)nullptr, (const float*)nullptr, lse, terms,
-        none ? loss : (float*)nullptr, tgt_part);
-      if (!none && !shard) L(K_LOSS, k_loss, dim3(1), dim3(1024), (const float*)terms, (const int*)nv, p->reduction, loss);
-      return L.st;
-    }
-    // one group per launch; row sets: parity 0 at rows [0, gw), parity 1 at [gw, 2 gw), the
-    // running pair at row 2 gw
-    const int ng = (ntl + gw - 1) / gw;
-    const int64_t rs = (int64_t)gw * pl.npad;
-    float* run_m = pm + 2 * rs;
-    float* run_s = ps + 2 * rs;
-    for (int g = 0; g < ng; ++g) {
-      const int tm0 = g * gw, wl = std::min(gw, ntl - tm0);
-      const int64_t cur = (g & 1) * rs, prev = ((g + 1) & 1) * rs;
-      L(K_FWD_STATS, k_fwd_tile, dim3((unsigned)(wl * pl.nt_max)), dim3(Geo<3>::NT), w, pl.ldw, (int)pl.v,
-        (const uint16_t*)hv, pl.d, (const int*)nv, (int)pl.d, tm0, wl, gw, pl.nt_max, pm + cur, ps + cur,
-        g > 0 ? (const float*)(pm + prev) : (const float*)nullptr, (const float*)(ps + prev), gw, run_m, run_s,
-        g == 1 ? 1 : 0, (int)pl.npad, kLog2e);
-    }
-    const int wl_last = ntl - (ng - 1) * gw;
-    const int64_t last = ((ng - 1) & 1) * rs;
-    L(K_COMBINE, k_combine, dim3((unsigned)((pl.n + kCombTok - 1) / kCombTok)), dim3(1024), h, pl.ldh, w, pl.ldw,
-      targets, p->target_bytes, si.v_begin, pl.v, (const int*)idx, (const int*)nv, (int)pl.d, wl_last,
-      (const float*)(pm + last), (const float*)(ps + last), (int)pl.npad,
-      ng > 1 ? (const float*)run_m : (const float*)nullptr, (const float*)run_s, lse, terms,
-      none ? loss : (float*)nullptr, tgt_part);
-  } else {
-    L(K_FWD_STATS, k_fwd_stats<2>, dim3(pl.nt_max * pl.nparts), dim3(NTHREADS), w, pl.ldw, (int)pl.v, h, pl.ldh,
-      pl.n, (const int*)idx, (const int*)nv, (int)pl.d, pl.nparts, pl.nt_max, pl.vt_count, pm, ps, (int)pl.npad,
-      kLog2e);
-    L(K_COMBINE, k_combine, dim3((unsigned)((pl.n + kCombTok - 1) / kCombTok)), dim3(1024), h, pl.ldh, w, pl.ldw,
-      targets, p->target_bytes, si.v_begin, pl.v, (const int*)idx, (const int*)nv, (int)pl.d, 2 * pl.nparts,
-      (const float*)pm, (const float*)ps, (int)pl.npad, (const float*)nullptr, (const float*)nullptr, lse, terms,
-      none ? loss : (float*)nullptr, tgt_part);
-  }
+  const PartRows pr = launch_fwd_stats(L, pl, w, pl.ldw, h, pl.ldh, (int)pl.d, (const int*)idx, (const int*)nv,
+                                       (uint16_t*)(ws + pl.o_hvf), pm, ps, kLog2e);
+  L(K_COMBINE, k_combine, dim3((unsigned)((pl.n + kCombTok - 1) / kCombTok)), dim3(1024), h, pl.ldh, w, pl.ldw,
+    targets, p->target_bytes, si.v_begin, pl.v, (const int*)idx, (const int*)nv, (int)pl.d, pr.count, pr.m, pr.s,
+    (int)pl.npad, pr.run_m, pr.run_s, lse, terms, none ? loss : (float*)nullptr, tgt_part);
   if (!none && !shard) L(K_LOSS, k_loss, dim3(1), dim3(1024), (const float*)terms, (const int*)nv, p->reduction, loss);
   return L.st;
 }
@@ -1768,6 +1777,14 @@ struct KdArgs {
 };
 
 inline size_t kd_p_bytes(const Plan& pl) { return (size_t)4 * pl.vc * pl.npad; }
+
+// Gather buffer for the 12-wave statistics of both distillation heads (Npad x max(Ds, Dt) bf16),
+// placed in the teacher-probability buffer P (free before the slab loop), or null when P is
+// too small (the 8-wave statistics then need none).
+inline uint16_t* kd_stats_gather(const Plan& s, const Plan& t, char* p_buf) {
+  const int64_t dmax = s.d > t.d ? s.d : t.d;
+  return (size_t)2 * dmax * s.npad <= kd_p_bytes(s) ? (uint16_t*)p_buf : nullptr;
+}
 
 // The backward pass behind lce_backward (dW != null), lce_backward_adamw (adamw != null),
 // lce_backward_shard (shard != null, fp32 dH term in dHf) and lce_kd_backward (kd != null).
@@ -1957,16 +1974,18 @@ lce_status_t kd_fused_impl(const lce_kd_problem_t* p, const void* Hs, const void
     Launcher L{(hipStream_t)stream};
     L(K_COMPACT, k_compact, dim3(1), dim3(1024), targets, p->target_bytes, pl.n, pl.v, p->ignore_index,
       idx, pos, nv, n_valid, dev_status, lse_s, lse_t);
-    L(K_FWD_STATS, k_fwd_stats<2>, dim3(tp.nt_max * tp.nparts), dim3(NTHREADS), wt, tp.ldw, (int)tp.v, ht, tp.ldh,
-      tp.n, (const int*)idx, (const int*)nv, (int)tp.d, tp.nparts, tp.nt_max, tp.vt_count, pm, ps, npad, k.scale2);
+    // the statistics' row gathers use the P buffer, free until the slab loop
+    uint16_t* hvk = kd_stats_gather(pl, tp, ws + pl.bwd_bytes);
+    const PartRows pt = launch_fwd_stats(L, pl, wt, tp.ldw, ht, tp.ldh, (int)tp.d, (const int*)idx, (const int*)nv, hvk,
+                                         pm, ps, k.scale2);
     L(K_COMBINE, k_combine, dim3((unsigned)((pl.n + kCombTok - 1) / kCombTok)), dim3(1024), ht, tp.ldh, wt, tp.ldw, targets,
-      p->target_bytes, (int64_t)0, (int64_t)0, (const int*)idx, (const int*)nv, (int)tp.d, 2 * tp.nparts,
-      (const float*)pm, (const float*)ps, npad, (const float*)nullptr, (const float*)nullptr, lse_t, (float*)nullptr, (float*)nullptr, tgt);
-    L(K_FWD_STATS, k_fwd_stats<2>, dim3(pl.nt_max * pl.nparts), dim3(NTHREADS), wsm, pl.ldw, (int)pl.v, hs, pl.ldh,
-      pl.n, (const int*)idx, (const int*)nv, (int)pl.d, pl.nparts, pl.nt_max, pl.vt_count, pm, ps, npad, k.scale2);
+      p->target_bytes, (int64_t)0, (int64_t)0, (const int*)idx, (const int*)nv, (int)tp.d, pt.count, pt.m, pt.s, npad,
+      pt.run_m, pt.run_s, lse_t, (float*)nullptr, (float*)nullptr, tgt);
+    const PartRows pq = launch_fwd_stats(L, pl, wsm, pl.ldw, hs, pl.ldh, (int)pl.d, (const int*)idx, (const int*)nv, hvk,
+                                         pm, ps, k.scale2);
     L(K_COMBINE, k_combine, dim3((unsigned)((pl.n + kCombTok - 1) / kCombTok)), dim3(1024), hs, pl.ldh, wsm, pl.ldw, targets,
-      p->target_bytes, (int64_t)0, (int64_t)0, (const int*)idx, (const int*)nv, (int)pl.d, 2 * pl.nparts,
-      (const float*)pm, (const float*)ps, npad, (const float*)nullptr, (const float*)nullptr, lse_s, (float*)nullptr, (float*)nullptr, tgt);
+      p->target_bytes, (int64_t)0, (int64_t)0, (const int*)idx, (const int*)nv, (int)pl.d, pq.count, pq.m, pq.s, npad,
+      pq.run_m, pq.run_s, lse_s, (float*)nullptr, (float*)nullptr, tgt);
     if (L.st != LCE_OK) return L.st;
   }
   const KdArgs kd{ht, tp.ldh, wt, tp.ldw, (int)tp.d, lse_t, k.scale2, k.inv_t, qpart};
@@ -2023,16 +2042,18 @@ lce_status_t kd_forward_impl(const lce_kd_problem_t* p, const void* Hs, const vo
     idx, pos, nv, n_valid, dev_status, lse_s, lse_t);
   // log-sum-exp of both heads' logits / T (no target logit: an empty id range)
   const Plan& tp = k.t;
-  L(K_FWD_STATS, k_fwd_stats<2>, dim3(tp.nt_max * tp.nparts), dim3(NTHREADS), wt, tp.ldw, (int)tp.v, ht, tp.ldh,
-    tp.n, (const int*)idx, (const int*)nv, (int)tp.d, tp.nparts, tp.nt_max, tp.vt_count, pm, ps, npad, k.scale2);
+  // the statistics' row gathers use the P buffer, free until the slab loop
+  uint16_t* hvk = kd_stats_gather(pl, tp, (char*)P);
+  const PartRows pt = launch_fwd_stats(L, pl, wt, tp.ldw, ht, tp.ldh, (int)tp.d, (const int*)idx, (const int*)nv, hvk,
+                                       pm, ps, k.scale2);
   L(K_COMBINE, k_combine, dim3((unsigned)((pl.n + kCombTok - 1) / kCombTok)), dim3(1024), ht, tp.ldh, wt, tp.ldw, targets,
-    p->target_bytes, (int64_t)0, (int64_t)0, (const int*)idx, (const int*)nv, (int)tp.d, 2 * tp.nparts,
-    (const float*)pm, (const float*)ps, npad, (const float*)nullptr, (const float*)nullptr, lse_t, terms, (float*)nullptr, tgt);
-  L(K_FWD_STATS, k_fwd_stats<2>, dim3(pl.nt_max * pl.nparts), dim3(NTHREADS), wsm, pl.ldw, (int)pl.v, hs, pl.ldh,
-    pl.n, (const int*)idx, (const int*)nv, (int)pl.d, pl.nparts, pl.nt_max, pl.vt_count, pm, ps, npad, k.scale2);
+    p->target_bytes, (int64_t)0, (int64_t)0, (const int*)idx, (const int*)nv, (int)tp.d, pt.count, pt.m, pt.s, npad,
+    pt.run_m, pt.run_s, lse_t, terms, (float*)nullptr, tgt);
+  const PartRows pq = launch_fwd_stats(L, pl, wsm, pl.ldw, hs, pl.ldh, (int)pl.d, (const int*)idx, (const int*)nv, hvk,
+                                       pm, ps, k.scale2);
   L(K_COMBINE, k_combine, dim3((unsigned)((pl.n + kCombTok - 1) / kCombTok)), dim3(1024), hs, pl.ldh, wsm, pl.ldw, targets,
-    p->target_bytes, (int64_t)0, (int64_t)0, (const int*)idx, (const int*)nv, (int)pl.d, 2 * pl.nparts,
-    (const float*)pm, (const float*)ps, npad, (const float*)nullptr, (const float*)nullptr, lse_s, terms, (float*)nullptr, tgt);
+    p->target_bytes, (int64_t)0, (int64_t)0, (const int*)idx, (const int*)nv, (int)pl.d, pq.count, pq.m, pq.s, npad,
+    pq.run_m, pq.run_s, lse_s, terms, (float*)nullptr, tgt);
   // per slab: teacher probabilities P, then the student's sum_v P zs / T per token and tile
   for (int64_t s = 0; s < pl.nslab; ++s) {
     const int64_t v0 = s * pl.vc;
