@@ -1,7 +1,9 @@
 """Fused linear knowledge-distillation loss on the GPU against the CPU oracle.
 
 Student and teacher heads of different hidden sizes over one vocabulary, ragged tiles, several
-vocabulary slabs, temperatures 1 and 2, every reduction, empty and fully masked batches.
+vocabulary slabs, temperatures 1 and 2, every reduction, empty and fully masked batches. The
+heads' statistics run on 12-wave tiles (D % 64 == 0), 8-wave tiles, or one of each, and with
+D = 64 and 9000 ids in one launch per group of tiles (the student's layout serves both heads).
 Tolerances as for LCE: loss 1e-3 absolute (per token for "none"), lse 1e-3, relative Frobenius
 1e-2 on dHs and dWs.
 """
@@ -57,7 +59,7 @@ def _check(gpu, ref):
 
 
 @pytest.mark.parametrize("n,ds,dt,v", [(300, 264, 136, 1000), (600, 128, 256, 9000), (1, 8, 16, 5),
-                                       (257, 64, 72, 300), (513, 96, 520, 4097)])
+                                       (257, 64, 72, 300), (513, 96, 520, 4097), (300, 64, 128, 9000)])
 @pytest.mark.parametrize("temperature", [1.0, 2.0])
 def test_kd_matches_oracle(n, ds, dt, v, temperature):
     print(f"kd n={n} ds={ds} dt={dt} v={v} T={temperature}", flush=True)
@@ -123,7 +125,8 @@ def test_kd_autograd_function():
 
 
 @pytest.mark.parametrize("n,ds,dt,v,reduction", [(600, 128, 256, 9000, "mean"), (300, 264, 136, 1000, "none"),
-                                                 (1, 8, 16, 5, "sum"), (40, 16, 32, 300, "mean")])
+                                                 (1, 8, 16, 5, "sum"), (40, 16, 32, 300, "mean"),
+                                                 (300, 64, 128, 9000, "mean")])
 def test_fused_forward_backward_is_bitwise_the_two_calls(n, ds, dt, v, reduction):
     import torch
     from paper_2605_21442_amd import autograd as AG
