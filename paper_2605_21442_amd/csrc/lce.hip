@@ -1024,8 +1024,8 @@ __global__ __launch_bounds__(256) void k_gather_rows(const uint16_t* __restrict_
 // workgroups resident on one XCD share the band's A tiles and a few B tiles in its L2, and each
 // large A operand is fetched by one XCD only. The grid is 8 * ceil(T_max / 8) * tn_count blocks;
 // blocks past the live tiles return false.
-__device__ __forceinline__ bool band_tile(int tm_live, int tn_count, int& tm, int& tn) {
-  const int x = blockIdx.x & 7, k = blockIdx.x >> 3;
+__device__ __forceinline__ bool band_tile(int blk, int tm_live, int tn_count, int& tm, int& tn) {
+  const int x = blk & 7, k = blk >> 3;
   const int r0 = (x * tm_live) >> 3, r1 = ((x + 1) * tm_live) >> 3;
   const int rows = r1 - r0;
   if (rows <= 0 || k >= rows * tn_count) return false;
@@ -1273,7 +1273,7 @@ __global__ __launch_bounds__(Geo<WM>::NT, WM) void k_bwd_dw(const uint16_t* __re
   constexpr int TM = Geo<WM>::TM;
   __shared__ __attribute__((aligned(16))) char smem[Geo<WM>::LDS];
   int tm, tn;
-  if (!band_tile(tm_count, (d + TILE - 1) / TILE, tm, tn)) return;
+  if (!band_tile(blockIdx.x, tm_count, (d + TILE - 1) / TILE, tm, tn)) return;
   const int m0 = tm * TM, d0 = tn * TILE;
   const int nv = *nv_ptr;
   const int kpad = ((nv + KPAD - 1) / KPAD) * KPAD;
@@ -1362,25 +1362,43 @@ __global__ __launch_bounds__(Geo<WM>::NT, WM) void k_bwd_dw(const uint16_t* __re
 
 // K6: dH32[m][dd] (+)= sum_k G[m][k] Ws[k][dd] over the slab's k < vs; rows m < Nv. Ws = W + v0 ldw
 // is the slab's first row, read K-major (transposing LDS reads); ws_rows = V - v0 rows follow.
+// kz = 2 splits K in two halves for launches with fewer output tiles than CUs: blocks of the
+// second half (the upper half of the grid) accumulate into a second buffer dH32b, which the
+// finalise adds in a fixed order.
 template <int WM>
 __global__ __launch_bounds__(Geo<WM>::NT, WM) void k_bwd_dh(const uint16_t* __restrict__ G, int vc, int vs,
                                                         const uint16_t* __restrict__ Ws, int64_t ldw,
                                                         int64_t ws_rows, int d,
                                                         const int* __restrict__ nv_ptr,
-                                                        float* __restrict__ dH32, int accumulate) {
+                                                        float* __restrict__ dH32, int accumulate, int kz,
+                                                        float* __restrict__ dH32b) {
   constexpr int TM = Geo<WM>::TM;
   __shared__ __attribute__((aligned(16))) char smem[Geo<WM>::LDS];
   const int nv = *nv_ptr;
+  const int g1 = (int)gridDim.x / kz;
+  const int z = (int)blockIdx.x / g1;
   int tm, tn;
-  if (!band_tile((nv + TM - 1) / TM, (d + TILE - 1) / TILE, tm, tn)) return;
+  if (!band_tile((int)blockIdx.x - z * g1, (nv + TM - 1) / TM, (d + TILE - 1) / TILE, tm, tn)) return;
   const int m0 = tm * TM, d0 = tn * TILE;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, wr = wave >> 2, wc = wave & 3;
-  const Operand opa = dense_operand(G + (int64_t)m0 * vc, nv - m0, vc);
-  const Operand opb = kmajor_operand<TILE>(Ws + d0, ldw, ((uint64_t)ws_rows * ldw - d0) * 2);
-  f32x16_t acc[4][2];
   // K = vs rounded up to 64: G holds zeros there and the W rows past V lie outside the buffer
-  // resource (zeros), so no slice needs masking
-  mma_mainloop<2, OP_DENSE, OP_KMAJOR, WM, false>(acc, opa, opb, (vs + KSLICE - 1) / KSLICE * KSLICE, smem);
+  // resource (zeros), so no slice needs masking. Half z covers [k0, k0 + kzn).
+  const int kt = (vs + KSLICE - 1) / KSLICE * KSLICE;
+  const int kh = ((kt + kz - 1) / kz + KSLICE - 1) / KSLICE * KSLICE;
+  const int k0 = z * kh;
+  const int kzn = kt - k0 < kh ? kt - k0 : kh;
+  f32x16_t acc[4][2];
+  if (kzn > 0) {
+    const Operand opa = dense_operand(G + (int64_t)m0 * vc + k0, nv - m0, vc);
+    const Operand opb = kmajor_operand<TILE>(Ws + (int64_t)k0 * ldw + d0, ldw, ((uint64_t)(ws_rows - k0) * ldw - d0) * 2);
+    mma_mainloop<2, OP_DENSE, OP_KMAJOR, WM, false>(acc, opa, opb, kzn, smem);
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) acc[i][j] = (f32x16_t){};
+  }
+  if (z) dH32 = dH32b;
   // Read-modify-write of the fp32 accumulator through a buffer resource over this tile's valid
   // rows (rows past Nv read 0 and drop their stores): one 32-bit per-lane offset and a
   // wave-uniform row offset per element, so that only the accumulators occupy registers; one
@@ -1416,9 +1434,11 @@ __global__ __launch_bounds__(Geo<WM>::NT, WM) void k_bwd_dh(const uint16_t* __re
 }
 
 // K7: dH[row] = bf16(dH32[pos[row]]) for valid rows, +0.0 for the others. 8 elements per thread.
-__global__ __launch_bounds__(256) void k_dh_finalize(const float* __restrict__ dH32, const int* __restrict__ pos,
+__global__ __launch_bounds__(256) void k_dh_finalize(const float* __restrict__ dH32,
+                                                     const float* __restrict__ dH32b, const int* __restrict__ pos,
                                                      int64_t n, int d, uint16_t* __restrict__ dH,
                                                      float* __restrict__ dHf, int has_slabs) {
+  // dH32b (may be null): the second K half of split dH launches, added after dH32
   const int64_t e = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 8;
   if (e >= n * d) return;
   const int64_t row = e / d;
@@ -1428,6 +1448,12 @@ __global__ __launch_bounds__(256) void k_dh_finalize(const float* __restrict__ d
   if (p >= 0 && has_slabs) {
     a = *reinterpret_cast<const float4*>(dH32 + (int64_t)p * d + col);
     b = *reinterpret_cast<const float4*>(dH32 + (int64_t)p * d + col + 4);
+    if (dH32b) {
+      const float4 a2 = *reinterpret_cast<const float4*>(dH32b + (int64_t)p * d + col);
+      const float4 b2 = *reinterpret_cast<const float4*>(dH32b + (int64_t)p * d + col + 4);
+      a = make_float4(a.x + a2.x, a.y + a2.y, a.z + a2.z, a.w + a2.w);
+      b = make_float4(b.x + b2.x, b.y + b2.y, b.z + b2.z, b.w + b2.w);
+    }
   }
   if (dHf) {   // fp32 rows (a vocabulary shard's term of dH, to be summed over shards)
     *reinterpret_cast<float4*>(dHf + e) = a;
@@ -1537,7 +1563,8 @@ struct Plan {
   int64_t vc, nslab;
   // workspace offsets
   size_t o_idx, o_pos, o_nv, o_pm, o_ps, o_terms, o_hvf, fwd_bytes;
-  size_t o_hv, o_g, o_dh32, bwd_bytes;
+  size_t o_hv, o_g, o_dh32, o_dh32b, bwd_bytes;   // o_dh32b: second K half of split dH (or 0)
+  int dh_kz;                                    // K halves of the dH launches (1 or 2)
 };
 
 // the 12-wave forward in one launch: its partial rows (8 bytes per 384-id tile and token) take at
@@ -1602,6 +1629,11 @@ lce_status_t make_plan(const lce_problem_t* p, Plan* pl) {
   pl->o_hv = take(cur, 2 * (size_t)p->d * pl->npad);
   pl->o_g = take(cur, 2 * (size_t)pl->npad * vc);
   pl->o_dh32 = take(cur, 4 * (size_t)pl->npad * p->d);
+  // dH launches with fewer 384 x 256 output tiles than the 256 CUs split K in two halves, the
+  // second accumulated in a buffer of its own
+  const int64_t dh_tiles = (pl->npad + 383) / 384 * ((p->d + TILE - 1) / TILE);
+  pl->dh_kz = dh_tiles < 256 ? 2 : 1;
+  pl->o_dh32b = pl->dh_kz > 1 ? take(cur, 4 * (size_t)pl->npad * p->d) : 0;
   pl->bwd_bytes = cur;
   return LCE_OK;
 }
@@ -1824,6 +1856,7 @@ lce_status_t backward_impl(const lce_problem_t* p, const ShardInfo* shard, const
   uint16_t* hv = (uint16_t*)(ws + pl.o_hv);
   uint16_t* g = (uint16_t*)(ws + pl.o_g);
   float* dh32 = (float*)(ws + pl.o_dh32);
+  float* dh32b = pl.dh_kz > 1 ? (float*)(ws + pl.o_dh32b) : nullptr;
   const uint16_t* h = (const uint16_t*)H;
   const uint16_t* w = (const uint16_t*)W;
   const int d = (int)pl.d, npad = (int)pl.npad, vc = (int)pl.vc;
@@ -1875,15 +1908,16 @@ lce_status_t backward_impl(const lce_problem_t* p, const ShardInfo* shard, const
     }
     // dH reads the slab's W rows before the dW launch, whose AdamW epilogue (in-backward step)
     // may update them; later slabs read only their own rows
-    L(K_BWD_DH, k_bwd_dh<kDhWM>, dim3((unsigned)(8 * ((dh_tiles + 7) / 8) * dt)), dim3(Geo<kDhWM>::NT), (const uint16_t*)g, vc, vs,
-      w + v0 * pl.ldw, pl.ldw, pl.v - v0, d, (const int*)nv, dh32, (int)(s > 0));
+    L(K_BWD_DH, k_bwd_dh<kDhWM>, dim3((unsigned)(pl.dh_kz * 8 * ((dh_tiles + 7) / 8) * dt)), dim3(Geo<kDhWM>::NT),
+      (const uint16_t*)g, vc, vs, w + v0 * pl.ldw, pl.ldw, pl.v - v0, d, (const int*)nv, dh32, (int)(s > 0), pl.dh_kz,
+      dh32b);
     const int tmw = (vs + Geo<kDwWM>::TM - 1) / Geo<kDwWM>::TM;
     L(K_BWD_DW, dw_kernel, dim3((unsigned)(8 * ((tmw + 7) / 8) * dt)), dim3(Geo<kDwWM>::NT), (const uint16_t*)g, vc,
       npad, vs, (const uint16_t*)hv, d, (const int*)nv, tmw, dW, v0, as, c);
   }
   const int64_t nthr = pl.n * pl.d / 8;
   L(K_DH_FINAL, k_dh_finalize, dim3((unsigned)((nthr + 255) / 256)), dim3(256), (const float*)dh32,
-    (const int*)pos, pl.n, d, (uint16_t*)dH, dHf, 1);
+    (const float*)dh32b, (const int*)pos, pl.n, d, (uint16_t*)dH, dHf, 1);
   return L.st;
 }
 
