@@ -100,10 +100,11 @@ __device__ __forceinline__ void dma16(const __amdgpu_buffer_rsrc_t& rs, const i3
   if constexpr (!kAsm) {
     __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void_t*)lds, 16, (int)voffset, (int)soffset, 0, 0);
   } else {
-    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+    // m0 is an input operand: the compiler sets it (and knows the value it holds afterwards)
+    asm volatile("s_nop 0\n\tbuffer_load_dwordx4 %0, %1, %2 offen lds"
                  :
-                 : "s"(m0), "v"(voffset), "s"(rw), "s"(soffset)
-                 : "memory", "m0");
+                 : "v"(voffset), "s"(rw), "s"(soffset), "{m0}"(m0)
+                 : "memory");
   }
 }
 
