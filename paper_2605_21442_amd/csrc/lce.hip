@@ -1114,35 +1114,46 @@ __global__ __launch_bounds__(Geo<WM>::NT, WM) void k_bwd_g(const uint16_t* __res
   }
   const int vb = wr * 128 + (lane >> 5) * 4;  // tile-relative vocabulary row base of this lane
   if constexpr (WM == 3) {
-    // G straight from registers: per block and group of 4 ids, 8 bytes (4 ids of one token row)
-    // per lane; a wave's stores cover whole 128-byte lines of its rows, which L2 merges. Rows of
-    // tokens >= Nv and ids >= the slab width get zeros, so the whole 256 x 384 tile is written
-    // (the slab width vc is a multiple of 384).
+    // G straight from registers. A lane holds 4 consecutive ids of a token row per (block, group
+    // of 8 ids), the other 4 sit in lane L ^ 32; one lane swap across the wave halves
+    // (permlane32 swap) per pair of groups gives each lane 8 consecutive ids (lanes < 32 the even
+    // group, the others the odd one), stored as 16 bytes. Rows of tokens >= Nv and ids >= the
+    // slab width get zeros, so the whole 256 x 384 tile is written (the slab width vc is a
+    // multiple of 384).
     const __amdgpu_buffer_rsrc_t rg = make_rsrc(G + (int64_t)n0 * vc, (uint64_t)TILE * vc * 2);
-    const uint32_t voff = (uint32_t)(((wc * 64 + (lane & 31)) * vc + vt0 + vb) * 2);
+    const uint32_t voff = (uint32_t)(((wc * 64 + (lane & 31)) * vc + vt0 + wr * 128 + (lane >> 5) * 8) * 2);
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
       const bool tok_ok = tok[j] < nv;
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          float gq[4];
+        for (int p = 0; p < 2; ++p) {
+          u32x2_t pk[2];
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const int vr = vb + i * 32 + q * 8 + e;
-            float g = 0.f;
-            if (tok_ok && vr < vleft) {
-              g = cj[j] * __builtin_amdgcn_exp2f(fmaf(acc[i][j][q * 4 + e], scale2, -l2[j]));
-              if (vr == tgt[j]) g -= cj[j];
+          for (int h = 0; h < 2; ++h) {
+            const int q = 2 * p + h;
+            float gq[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const int vr = vb + i * 32 + q * 8 + e;
+              float g = 0.f;
+              if (tok_ok && vr < vleft) {
+                g = cj[j] * __builtin_amdgcn_exp2f(fmaf(acc[i][j][q * 4 + e], scale2, -l2[j]));
+                if (vr == tgt[j]) g -= cj[j];
+              }
+              gq[e] = g;
             }
-            gq[e] = g;
+            pk[h].x = pack_bf16x2(gq[0], gq[1]);
+            pk[h].y = pack_bf16x2(gq[2], gq[3]);
           }
-          u32x2_t pk;
-          pk.x = pack_bf16x2(gq[0], gq[1]);
-          pk.y = pack_bf16x2(gq[2], gq[3]);
-          const uint32_t so = (uint32_t)((j * 32 * vc + i * 32 + q * 8) * 2);
-          __builtin_amdgcn_raw_buffer_store_b64(pk, rg, (int)voff, (int)so, 0);
+          // lane L < 32: (its group 2p ids 0-3, lane L + 32's ids 4-7); lane L + 32: (lane L's
+          // group 2p + 1 ids 0-3, its own ids 4-7)
+          const auto sx = __builtin_amdgcn_permlane32_swap(pk[0].x, pk[1].x, false, false);
+          const auto sy = __builtin_amdgcn_permlane32_swap(pk[0].y, pk[1].y, false, false);
+          const i32x4_t v16 = {(int)sx[0], (int)sy[0], (int)sx[1], (int)sy[1]};
+          const uint32_t so = (uint32_t)((j * 32 * vc + i * 32 + p * 16) * 2);
+          __builtin_amdgcn_raw_buffer_store_b128(v16, rg, (int)voff, (int)so, 0);
         }
     }
     return;
