@@ -468,7 +468,13 @@ __device__ __forceinline__ void mma_mainloop(f32x16_t (&acc)[4][2], const Operan
   // Waves 0..3 (the first wave of each SIMD) issue their share of a slice's loads at the barrier;
   // the others kLateGroups MFMA substeps later: a smaller load burst, and the other waves of each
   // SIMD go straight back to MFMA work.
-  const bool late = wsc >= 4;
+  // slot of this wave's loads: 0 at the barrier, 1 after the slice's last substep, 2 after the
+  // next slice's first substep. kLateGroups = 1 or 2: waves 4.. use that slot; 1xy (WM = 3):
+  // waves 4..7 use slot x, waves 8..11 slot y.
+  constexpr int kMid = kLateGroups >= 100 ? (kLateGroups / 10) % 10 : kLateGroups;
+  constexpr int kLast = kLateGroups >= 100 ? kLateGroups % 10 : kLateGroups;
+  const int slot = wsc < 4 ? 0 : (WM == 3 && wsc >= 8 ? kLast : kMid);
+  const bool late = slot != 0;
   int pend = -1;
   if constexpr (WM == 2) {
     FragSet f0, f1;
@@ -478,7 +484,7 @@ __device__ __forceinline__ void mma_mainloop(f32x16_t (&acc)[4][2], const Operan
       const char* nxt = smem + ((j + 1) & 1) * G::SLICE;
       read_frags(f1, cur, 1);
       mma_substep(acc, f0);
-      if (kLateGroups == 2 && pend >= 0) {
+      if (slot == 2 && pend >= 0) {
         load(pend);
         pend = -1;
       }
@@ -497,7 +503,7 @@ __device__ __forceinline__ void mma_mainloop(f32x16_t (&acc)[4][2], const Operan
         read_frags(f0, nxt, 0);
       }
       mma_substep(acc, f1);
-      if (kLateGroups == 1 && pend >= 0) {
+      if (slot == 1 && pend >= 0) {
         load(pend);
         pend = -1;
       }
@@ -508,7 +514,7 @@ __device__ __forceinline__ void mma_mainloop(f32x16_t (&acc)[4][2], const Operan
       const char* cur = smem + (j & 1) * G::SLICE;
       read_frags(f, cur, 0);
       mma_substep(acc, f);
-      if (kLateGroups == 2 && pend >= 0) {
+      if (slot == 2 && pend >= 0) {
         load(pend);
         pend = -1;
       }
@@ -527,7 +533,7 @@ __device__ __forceinline__ void mma_mainloop(f32x16_t (&acc)[4][2], const Operan
         }
       }
       mma_substep(acc, f);
-      if (kLateGroups == 1 && pend >= 0) {
+      if (slot == 1 && pend >= 0) {
         load(pend);
         pend = -1;
       }
@@ -722,7 +728,7 @@ __global__ __launch_bounds__(Geo<3>::NT, 3) void k_fwd_tile(const uint16_t* __re
   const Operand opa = dense_operand(W + (int64_t)v0 * ldw, vleft, ldw);
   const Operand opb = dense_operand(Hv + (int64_t)n0 * ldh, nv - n0, ldh);
   f32x16_t acc[4][2];
-  mma_mainloop<2, OP_DENSE, OP_DENSE, WM, false>(acc, opa, opb, d, smem);   // d % 64 == 0 (host)
+  mma_mainloop<1, OP_DENSE, OP_DENSE, WM, false>(acc, opa, opb, d, smem);   // d % 64 == 0 (host)
   // the main loop ends with a barrier: its LDS is free for the wave rows' pairs [3][256] (m, s)
   float* red_m = reinterpret_cast<float*>(smem);
   float* red_s = red_m + WM * TILE;
@@ -1097,7 +1103,7 @@ __global__ __launch_bounds__(Geo<WM>::NT, WM) void k_bwd_g(const uint16_t* __res
   if constexpr (WM == 3) {
     // H is the gathered valid rows Hv (row stride ldh = d): a dense operand
     const Operand opb = dense_operand(H + (int64_t)n0 * ldh, nv - n0, ldh);
-    mma_mainloop<2, OP_DENSE, OP_DENSE, WM, false>(acc, opa, opb, d, smem);   // d % 64 == 0 (host)
+    mma_mainloop<1, OP_DENSE, OP_DENSE, WM, false>(acc, opa, opb, d, smem);   // d % 64 == 0 (host)
   } else {
     const Operand opb = gather_operand(H, n, ldh, idx, n0, nv);
     mma_mainloop<2, OP_DENSE, OP_GATHER, WM>(acc, opa, opb, d, smem);
