@@ -1087,7 +1087,7 @@ __global__ __launch_bounds__(Geo<WM>::NT, WM) void k_bwd_g(const uint16_t* __res
                                                        float* __restrict__ qpart, int64_t qrow) {
   // 12 waves (WM = 3, 384 ids per tile) serve the one-hot LCE gradient when D % 64 == 0; the
   // distillation modes and other widths keep 8 waves and the LDS-staged epilogue below
-  static_assert(WM == 2 || kMode == G_ONEHOT, "");
+  static_assert(WM == 2 || kMode == G_ONEHOT || kMode == P_WRITE, "");
   constexpr int TM = Geo<WM>::TM;
   __shared__ __attribute__((aligned(16))) char smem[Geo<WM>::LDS];
   const int nv = *nv_ptr;
@@ -1109,7 +1109,10 @@ __global__ __launch_bounds__(Geo<WM>::NT, WM) void k_bwd_g(const uint16_t* __res
     mma_mainloop<2, OP_DENSE, OP_GATHER, WM>(acc, opa, opb, d, smem);
   }
 
-  const float c_all = grad_scale(grad, n_norm, reduction);
+  // the gradient scale exists only for the modes that write G (the probability and Q passes get
+  // no upstream gradient: grad and n_norm may be null there)
+  constexpr bool kWritesG = kMode == G_ONEHOT || kMode == G_SOFT || kMode == G_SOFT_Q;
+  const float c_all = kWritesG ? grad_scale(grad, n_norm, reduction) : 0.f;
   int tok[2], tgt[2];
   float l2[2], cj[2];
 #pragma unroll
@@ -1119,7 +1122,7 @@ __global__ __launch_bounds__(Geo<WM>::NT, WM) void k_bwd_g(const uint16_t* __res
       const int row = idx[tok[j]];
       l2[j] = lse[row] * kLog2e;
       tgt[j] = kMode == G_ONEHOT ? (int)(load_target(targets, tbytes, row) - id0 - v0) - vt0 : -1;
-      cj[j] = reduction == LCE_REDUCE_NONE ? grad[row] : c_all;
+      cj[j] = kWritesG && reduction == LCE_REDUCE_NONE ? grad[row] : c_all;
     } else {
       l2[j] = 0.f;
       tgt[j] = -1;
@@ -1127,7 +1130,7 @@ __global__ __launch_bounds__(Geo<WM>::NT, WM) void k_bwd_g(const uint16_t* __res
     }
   }
   const int vb = wr * 128 + (lane >> 5) * 4;  // tile-relative vocabulary row base of this lane
-  if constexpr (WM == 3) {
+  if constexpr (WM == 3 && kMode == G_ONEHOT) {
     // G straight from registers. A lane holds 4 consecutive ids of a token row per (block, group
     // of 8 ids), the other 4 sit in lane L ^ 32; one lane swap across the wave halves
     // (permlane32 swap) per pair of groups gives each lane 8 consecutive ids (lanes < 32 the even
@@ -1836,6 +1839,12 @@ struct KdArgs {
 
 inline size_t kd_p_bytes(const Plan& pl) { return (size_t)4 * pl.vc * pl.npad; }
 
+// The teacher's valid rows gathered for its 12-wave probability pass (Npad x Dt bf16), when
+// Dt % 64 == 0; placed after P.
+inline size_t kd_hvt_bytes(const Plan& pl, int64_t dt) {
+  return dt % KSLICE == 0 ? ((size_t)2 * dt * pl.npad + 255) / 256 * 256 : 0;
+}
+
 // Gather buffer for the 12-wave statistics of both distillation heads (Npad x max(Ds, Dt) bf16),
 // placed in the teacher-probability buffer P (free before the slab loop), or null when P is
 // too small (the 8-wave statistics then need none).
@@ -1859,7 +1868,7 @@ lce_status_t backward_impl(const lce_problem_t* p, const ShardInfo* shard, const
   if (pl.n > 0 && (!H || !targets || !lse || !dH_any || !workspace)) return LCE_ERR_NULL;
   if (!aligned16(W)) return LCE_ERR_ALIGN;
   if (pl.n > 0 && (!aligned16(H) || !aligned16(dH_any) || ((uintptr_t)workspace & 255) != 0)) return LCE_ERR_ALIGN;
-  const size_t need = pl.bwd_bytes + (kd ? kd_p_bytes(pl) : 0);
+  const size_t need = pl.bwd_bytes + (kd ? kd_p_bytes(pl) + kd_hvt_bytes(pl, kd->dt) : 0);
   if (pl.n > 0 && workspace_bytes < need) return LCE_ERR_WORKSPACE;
   const bool accumulate = (p->flags & LCE_FLAG_ACCUMULATE_DW) != 0;
   const AdamWState as = adamw ? *adamw : AdamWState{nullptr, 0, nullptr, nullptr, nullptr};
@@ -1892,6 +1901,11 @@ lce_status_t backward_impl(const lce_problem_t* p, const ShardInfo* shard, const
   // Hv[i] = H[idx[i]] for i < Nv, zero rows up to round_up(Nv, 64)
   L(K_GATHER_H, k_gather_rows, dim3((unsigned)std::min<int64_t>((npad * (d / 8) + 255) / 256, 16384)), dim3(256), h,
     pl.ldh, (const int*)idx, (const int*)nv, d, hv);
+  // KD: the teacher's valid rows for its 12-wave probability pass
+  uint16_t* hvt = (kd && kd_hvt_bytes(pl, kd->dt) > 0) ? (uint16_t*)(ws + pl.bwd_bytes + kd_p_bytes(pl)) : nullptr;
+  if (hvt)
+    L(K_GATHER_H, k_gather_rows, dim3((unsigned)std::min<int64_t>(((int64_t)npad * (kd->dt / 8) + 255) / 256, 16384)),
+      dim3(256), kd->ht, kd->ldht, (const int*)idx, (const int*)nv, kd->dt, hvt);
   const int dt = (d + TILE - 1) / TILE;
   const int dh_tiles = (int)((pl.npad + Geo<kDhWM>::TM - 1) / Geo<kDhWM>::TM);
   void (*dw_kernel)(const uint16_t*, int, int, int, const uint16_t*, int, const int*, int, uint16_t*, int64_t,
@@ -1904,10 +1918,18 @@ lce_status_t backward_impl(const lce_problem_t* p, const ShardInfo* shard, const
     if (kd) {
       // teacher probabilities of this slab, then G = c (softmax(zs / T) - P) / T
       float* P = (float*)(ws + pl.bwd_bytes);
-      L(K_KD_P, k_bwd_g<P_WRITE, 2>, dim3((unsigned)(tm * pl.nt_max)), dim3(NTHREADS), kd->wt, kd->ldwt, v0, vs,
-        kd->ht, kd->ldht, pl.n, targets, p->target_bytes, (int64_t)0, (const int*)idx, (const int*)nv, kd->lse_t,
-        grad_loss, (const int*)n_valid, p->reduction, kd->dt, tm, (uint16_t*)nullptr, vc, npad,
-        kd->scale2, kd->inv_t, P, (float*)nullptr, (int64_t)0);
+      if (hvt) {
+        const int tmg = (vs + Geo<3>::TM - 1) / Geo<3>::TM;
+        L(K_KD_P, k_bwd_g<P_WRITE, 3>, dim3((unsigned)(tmg * pl.nt_max)), dim3(Geo<3>::NT), kd->wt, kd->ldwt, v0, vs,
+          (const uint16_t*)hvt, (int64_t)kd->dt, pl.n, targets, p->target_bytes, (int64_t)0, (const int*)idx,
+          (const int*)nv, kd->lse_t, grad_loss, (const int*)n_valid, p->reduction, kd->dt, tmg, (uint16_t*)nullptr, vc,
+          npad, kd->scale2, kd->inv_t, P, (float*)nullptr, (int64_t)0);
+      } else {
+        L(K_KD_P, k_bwd_g<P_WRITE, 2>, dim3((unsigned)(tm * pl.nt_max)), dim3(NTHREADS), kd->wt, kd->ldwt, v0, vs,
+          kd->ht, kd->ldht, pl.n, targets, p->target_bytes, (int64_t)0, (const int*)idx, (const int*)nv, kd->lse_t,
+          grad_loss, (const int*)n_valid, p->reduction, kd->dt, tm, (uint16_t*)nullptr, vc, npad,
+          kd->scale2, kd->inv_t, P, (float*)nullptr, (int64_t)0);
+      }
       if (kd->qpart)
         L(K_BWD_G, k_bwd_g<G_SOFT_Q, 2>, dim3((unsigned)(tm * pl.nt_max)), dim3(NTHREADS), w, pl.ldw, v0, vs, h,
           pl.ldh, pl.n, targets, p->target_bytes, (int64_t)0, (const int*)idx, (const int*)nv, lse, grad_loss,
@@ -1952,7 +1974,7 @@ struct KdPlan {
   lce_problem_t ps, pt;   // student and teacher heads as LCE problems
   Plan s, t;
   float scale2, inv_t;
-  size_t o_tgt, o_q, o_p, fwd_bytes, bwd_bytes;
+  size_t o_tgt, o_q, o_p, o_hvt, fwd_bytes, bwd_bytes;
   size_t f_q, f_tgt, fused_bytes;   // fused call: backward regions, P, then Q partials and scratch
 };
 
@@ -1978,8 +2000,10 @@ lce_status_t make_kd_plan(const lce_kd_problem_t* p, KdPlan* k) {
   cur += up((size_t)4 * 2 * k->s.vt_count * k->s.npad);
   k->o_p = cur;
   cur += up(kd_p_bytes(k->s));
+  k->o_hvt = cur;
+  cur += kd_hvt_bytes(k->s, k->t.d);
   k->fwd_bytes = cur;
-  k->bwd_bytes = k->s.bwd_bytes + kd_p_bytes(k->s);
+  k->bwd_bytes = k->s.bwd_bytes + kd_p_bytes(k->s) + kd_hvt_bytes(k->s, k->t.d);
   cur = up(k->bwd_bytes);
   k->f_q = cur;
   cur += up((size_t)4 * 2 * k->s.vt_count * k->s.npad);
@@ -2115,14 +2139,26 @@ lce_status_t kd_forward_impl(const lce_kd_problem_t* p, const void* Hs, const vo
     p->target_bytes, (int64_t)0, (int64_t)0, (const int*)idx, (const int*)nv, (int)pl.d, pq.count, pq.m, pq.s, npad,
     pq.run_m, pq.run_s, lse_s, terms, (float*)nullptr, tgt);
   // per slab: teacher probabilities P, then the student's sum_v P zs / T per token and tile
+  uint16_t* hvt = kd_hvt_bytes(pl, tp.d) > 0 ? (uint16_t*)(ws + k.o_hvt) : nullptr;
+  if (hvt)
+    L(K_GATHER_H, k_gather_rows, dim3((unsigned)std::min<int64_t>(((int64_t)npad * (tp.d / 8) + 255) / 256, 16384)),
+      dim3(256), ht, tp.ldh, (const int*)idx, (const int*)nv, (int)tp.d, hvt);
   for (int64_t s = 0; s < pl.nslab; ++s) {
     const int64_t v0 = s * pl.vc;
     const int vs = (int)(pl.v - v0 < pl.vc ? pl.v - v0 : pl.vc);
     const int tm = (vs + TILE - 1) / TILE;
-    L(K_KD_P, k_bwd_g<P_WRITE, 2>, dim3((unsigned)(tm * pl.nt_max)), dim3(NTHREADS), wt, tp.ldw, v0, vs, ht, tp.ldh,
-      pl.n, targets, p->target_bytes, (int64_t)0, (const int*)idx, (const int*)nv, (const float*)lse_t,
-      (const float*)nullptr, (const int*)nullptr, p->reduction, (int)tp.d, tm, (uint16_t*)nullptr, vc,
-      npad, k.scale2, k.inv_t, P, (float*)nullptr, (int64_t)0);
+    if (hvt) {
+      const int tmg = (vs + Geo<3>::TM - 1) / Geo<3>::TM;
+      L(K_KD_P, k_bwd_g<P_WRITE, 3>, dim3((unsigned)(tmg * pl.nt_max)), dim3(Geo<3>::NT), wt, tp.ldw, v0, vs,
+        (const uint16_t*)hvt, tp.d, pl.n, targets, p->target_bytes, (int64_t)0, (const int*)idx, (const int*)nv,
+        (const float*)lse_t, (const float*)nullptr, (const int*)nullptr, p->reduction, (int)tp.d, tmg,
+        (uint16_t*)nullptr, vc, npad, k.scale2, k.inv_t, P, (float*)nullptr, (int64_t)0);
+    } else {
+      L(K_KD_P, k_bwd_g<P_WRITE, 2>, dim3((unsigned)(tm * pl.nt_max)), dim3(NTHREADS), wt, tp.ldw, v0, vs, ht, tp.ldh,
+        pl.n, targets, p->target_bytes, (int64_t)0, (const int*)idx, (const int*)nv, (const float*)lse_t,
+        (const float*)nullptr, (const int*)nullptr, p->reduction, (int)tp.d, tm, (uint16_t*)nullptr, vc,
+        npad, k.scale2, k.inv_t, P, (float*)nullptr, (int64_t)0);
+    }
     L(K_KD_Q, k_bwd_g<Q_SOFT, 2>, dim3((unsigned)(tm * pl.nt_max)), dim3(NTHREADS), wsm, pl.ldw, v0, vs, hs, pl.ldh,
       pl.n, targets, p->target_bytes, (int64_t)0, (const int*)idx, (const int*)nv, (const float*)lse_s,
       (const float*)nullptr, (const int*)nullptr, p->reduction, (int)pl.d, tm, (uint16_t*)nullptr, vc,
