@@ -600,56 +600,68 @@ __device__ __forceinline__ Operand kmajor_operand(const uint16_t* base, int64_t 
 // ---------------------------------------------------------------------------------------------
 // K1: valid-row compaction ("masks ignored tokens before projection", Sec. 4.2).
 // idx[0..Nv) = ascending rows whose target is in [0, V); pos[n] = its index there or -1.
-// One workgroup; thread t owns a contiguous run of rows, so idx comes out sorted.
+// One workgroup of 16 waves walks the rows in rounds of 1024 consecutive rows (coalesced target
+// loads, up to 16 rounds loaded ahead): a row's index is the valid rows of earlier rounds, of
+// earlier waves of its round (wave ballots summed through LDS) and of lower lanes of its wave
+// (popcount of its ballot), so idx comes out sorted.
 // ---------------------------------------------------------------------------------------------
 __global__ __launch_bounds__(1024) void k_compact(const void* targets, int tbytes, int64_t n, int64_t v,
                                                   int ignore, int* idx, int* pos, int* nv_ws,
                                                   int* nv_user, int* status, float* lse_zero,
                                                   float* loss_zero) {
-  __shared__ int scan[1024];
+  constexpr int kAhead = 16;
+  __shared__ int wsum[2][16];
   __shared__ int bad_any;
-  const int t = threadIdx.x;
-  const int64_t per = (n + 1023) / 1024;
-  const int64_t beg = t * per < n ? t * per : n;
-  const int64_t end = beg + per < n ? beg + per : n;
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
   if (t == 0) bad_any = 0;
-  int cnt = 0, bad = 0;
-  for (int64_t i = beg; i < end; ++i) {
-    const int64_t tg = load_target(targets, tbytes, i);
-    const bool ign = tg == (int64_t)ignore;
-    const bool ok = !ign && tg >= 0 && tg < v;
-    cnt += ok;
-    bad |= (!ign && !ok);
-  }
-  scan[t] = cnt;
   __syncthreads();
-  if (bad) bad_any = 1;  // benign same-value race
-  for (int off = 1; off < 1024; off <<= 1) {
-    const int x = t >= off ? scan[t - off] : 0;
-    __syncthreads();
-    scan[t] += x;
-    __syncthreads();
-  }
-  int o = scan[t] - cnt;
-  for (int64_t i = beg; i < end; ++i) {
-    const int64_t tg = load_target(targets, tbytes, i);
-    const bool ok = tg != (int64_t)ignore && tg >= 0 && tg < v;
-    if (ok) {
-      idx[o] = (int)i;
-      pos[i] = o;
-      ++o;
-    } else {
-      pos[i] = -1;
-      if (lse_zero) lse_zero[i] = 0.0f;
-      if (loss_zero) loss_zero[i] = 0.0f;
+  int base = 0, bad = 0;
+  for (int64_t g0 = 0; g0 < n; g0 += (int64_t)1024 * kAhead) {
+    int64_t tg[kAhead];
+#pragma unroll
+    for (int r = 0; r < kAhead; ++r) {
+      const int64_t i = g0 + (int64_t)r * 1024 + t;
+      tg[r] = i < n ? load_target(targets, tbytes, i) : (int64_t)ignore;
+    }
+#pragma unroll
+    for (int r = 0; r < kAhead; ++r) {
+      const int64_t i = g0 + (int64_t)r * 1024 + t;
+      if (g0 + (int64_t)r * 1024 >= n) break;   // uniform
+      const bool ign = tg[r] == (int64_t)ignore;
+      const bool ok = i < n && !ign && tg[r] >= 0 && tg[r] < v;
+      bad |= (i < n && !ign && !ok);
+      const unsigned long long m = __ballot(ok);
+      const int below = __popcll(m & ((1ull << lane) - 1ull));
+      if (lane == 0) wsum[r & 1][w] = __popcll(m);
+      __syncthreads();   // (the buffer written here was last read two rounds ago, before a barrier)
+      int before = base, total = 0;
+#pragma unroll
+      for (int k = 0; k < 16; ++k) {
+        const int c = wsum[r & 1][k];
+        before += k < w ? c : 0;
+        total += c;
+      }
+      if (i < n) {
+        if (ok) {
+          const int o = before + below;
+          idx[o] = (int)i;
+          pos[i] = o;
+        } else {
+          pos[i] = -1;
+          if (lse_zero) lse_zero[i] = 0.0f;
+          if (loss_zero) loss_zero[i] = 0.0f;
+        }
+      }
+      base += total;
     }
   }
-  if (t == 1023) {
-    *nv_ws = scan[1023];
-    if (nv_user) *nv_user = scan[1023];
-  }
+  if (bad) bad_any = 1;  // benign same-value race
   __syncthreads();
-  if (t == 0 && status) *status = bad_any ? LCE_STATUS_TARGET_OUT_OF_RANGE : 0;
+  if (t == 0) {
+    *nv_ws = base;
+    if (nv_user) *nv_user = base;
+    if (status) *status = bad_any ? LCE_STATUS_TARGET_OUT_OF_RANGE : 0;
+  }
 }
 
 // ---------------------------------------------------------------------------------------------
