@@ -1432,7 +1432,7 @@ __global__ __launch_bounds__(Geo<WM>::NT, WM) void k_bwd_dh(const uint16_t* __re
   if (kzn > 0) {
     const Operand opa = dense_operand(G + (int64_t)m0 * vc + k0, nv - m0, vc);
     const Operand opb = kmajor_operand<TILE>(Ws + (int64_t)k0 * ldw + d0, ldw, ((uint64_t)(ws_rows - k0) * ldw - d0) * 2);
-    mma_mainloop<2, OP_DENSE, OP_KMAJOR, WM, false>(acc, opa, opb, kzn, smem);
+    mma_mainloop<121, OP_DENSE, OP_KMAJOR, WM, false>(acc, opa, opb, kzn, smem);
   } else {
 #pragma unroll
     for (int i = 0; i < 4; ++i)
