@@ -42,6 +42,14 @@ def test_ragged_shapes(n, d, v):
     _case(WL.custom(n, d, v, seed=n + v, mask_frac=0.15, sigma_w=0.3))
 
 
+@pytest.mark.parametrize("n,d,v", [(300, 64, 12300), (200, 128, 12289)])
+def test_last_slab_shorter_than_one_k_slice(n, d, v):
+    # 12288-id slabs at these widths: the last slab holds 12 ids (1 id), less than one 64-wide K
+    # slice, so in the split dH launches (fewer output tiles than CUs) the second K half is empty
+    # and only writes zeros into its accumulator
+    _case(WL.custom(n, d, v, seed=n + v, mask_frac=0.2, sigma_w=0.3))
+
+
 @pytest.mark.parametrize("n,d,v", [(300, 64, 20000), (270, 128, 30000), (520, 64, 40000)])
 def test_forward_vocabulary_groups(n, d, v):
     # with D % 64 == 0 the forward runs one launch per group of 384-id tiles as wide as a backward
