@@ -42,6 +42,13 @@ def test_ragged_shapes(n, d, v):
     _case(WL.custom(n, d, v, seed=n + v, mask_frac=0.15, sigma_w=0.3))
 
 
+@pytest.mark.parametrize("n,d,v", [(768, 128, 1536), (512, 256, 768), (1152, 64, 3072)])
+def test_tile_exact_shapes(n, d, v):
+    # every count a whole number of tiles (no ragged tile anywhere): N and V multiples of 384 and
+    # 256, no masked token, so Nv = N
+    _case(WL.custom(n, d, v, seed=n + d, mask_frac=0.0, sigma_w=0.3))
+
+
 @pytest.mark.parametrize("n,d,v", [(300, 64, 12300), (200, 128, 12289)])
 def test_last_slab_shorter_than_one_k_slice(n, d, v):
     # 12288-id slabs at these widths: the last slab holds 12 ids (1 id), less than one 64-wide K
