@@ -14,13 +14,24 @@ import torch
 from . import binding as B
 
 
+def _rows_usable(shape, strides, data_ptr: int) -> bool:
+    """Whether a 2-D bf16 view can be handed to the library as it is: unit column stride, 16-byte
+    aligned start, a row stride that is a multiple of 8 and rows that do not overlap. A row stride
+    below the row length (0 for an expand()ed tensor) would be read by the library as rows the
+    allocation does not hold."""
+    rows, cols = shape
+    if rows > 1 and strides[0] < cols:
+        return False
+    return strides[1] == 1 and data_ptr % 16 == 0 and strides[0] % 8 == 0
+
+
 def _as_rows(x: torch.Tensor, name: str) -> tuple[torch.Tensor, int]:
     if x.dtype != torch.bfloat16:
         raise TypeError(f"{name} must be bfloat16, got {x.dtype}")
     if not x.is_cuda:
         raise ValueError(f"{name} must be a GPU tensor")
     x2 = x.reshape(-1, x.shape[-1]) if x.dim() != 2 else x
-    if x2.stride(-1) != 1 or x2.data_ptr() % 16 or x2.stride(0) % 8:
+    if not _rows_usable(tuple(x2.shape), x2.stride(), x2.data_ptr()):
         x2 = x2.contiguous()
     return x2, (x2.stride(0) if x2.shape[0] > 1 else x2.shape[1])
 
@@ -113,9 +124,10 @@ class AdamWState:
                  weight_decay: float = 0.01, master_weights: bool = False):
         if weight.dtype != torch.bfloat16 or weight.dim() != 2 or not weight.is_cuda:
             raise ValueError("weight must be a 2-D bf16 GPU tensor")
-        if weight.stride(-1) != 1 or weight.stride(0) % 8 or weight.data_ptr() % 16:
-            raise ValueError("weight must have unit column stride, a row stride divisible by 8 and "
-                             "16-byte alignment, since it is updated in place")
+        if (weight.stride(-1) != 1 or weight.stride(0) % 8 or weight.data_ptr() % 16
+                or (weight.shape[0] > 1 and weight.stride(0) < weight.shape[1])):
+            raise ValueError("weight must have unit column stride, rows that do not overlap, a row "
+                             "stride divisible by 8 and 16-byte alignment, since it is updated in place")
         self.weight = weight
         self.lr, self.betas, self.eps, self.weight_decay = lr, tuple(betas), eps, weight_decay
         self.exp_avg = torch.zeros(weight.shape, dtype=torch.float32, device=weight.device)

@@ -246,3 +246,16 @@ def test_kd_argument_checks_run_before_any_launch():
         with pytest.raises(B.LceError) as e:
             B.lce_kd_backward(p, **dict(bok, **change))
         assert e.value.code == code, change
+
+
+def test_overlapping_rows_are_copied_before_the_call():
+    # an expand()ed tensor has row stride 0, which the library would read as "dense" rows
+    from paper_2605_21442_amd.autograd import _rows_usable
+    assert not _rows_usable((4, 64), (0, 1), 0)          # expand() of one row
+    assert not _rows_usable((4, 64), (32, 1), 0)         # rows overlapping by half
+    assert not _rows_usable((4, 64), (64, 2), 0)         # non-unit column stride
+    assert not _rows_usable((4, 64), (72, 1), 8)         # misaligned start
+    assert not _rows_usable((4, 64), (68, 1), 0)         # row stride not a multiple of 8
+    assert _rows_usable((4, 64), (64, 1), 0)             # dense
+    assert _rows_usable((4, 64), (160, 1), 64)           # strided view of wider rows
+    assert _rows_usable((1, 64), (0, 1), 0)              # one row: its stride is never used

@@ -131,6 +131,21 @@ def test_strided_hidden_view():
     U.assert_parity(gpu, ref)
 
 
+def test_expanded_hidden_matches_its_contiguous_copy():
+    # an expand()ed hidden (row stride 0) must be made dense before the call, not passed as ld 0
+    import torch
+    inp = WL.custom(300, 128, 1000, seed=15, mask_frac=0.2)
+    h, w, t = U.to_device(inp)
+    he = h[:1].expand(300, 128)
+    assert he.stride(0) == 0
+    a = U.run_gpu(he, w, t)
+    b = U.run_gpu(he.contiguous(), w, t)
+    assert a["loss"] == b["loss"]
+    assert torch.equal(a["dH_t"], b["dH_t"]) and torch.equal(a["dW_t"], b["dW_t"])
+    rows = np.repeat(inp.h_bits[:1], 300, axis=0)
+    U.assert_parity(a, O.lce(rows, inp.w_bits, inp.targets))
+
+
 def test_softmax_grad_rows_sum_to_zero_on_gpu():
     inp = WL.custom(600, 256, 5000, seed=12, mask_frac=0.2, sigma_w=0.1)
     h, w, t = U.to_device(inp)
