@@ -20,8 +20,9 @@
  *
  * Conventions shared by every entry point
  *  - All tensors are caller-owned device memory; the library never allocates
- *    device memory and keeps no state between calls except the optional
- *    kernel-timing records below.
+ *    device memory and keeps no state between calls. The one exception is the
+ *    optional kernel-timing facility below, the library's only mutable global
+ *    state: a process-wide pool of HIP events behind a mutex, used for profiling.
  *  - H, W, dH and dW are bf16 (stored as 16-bit words), row-major. H and W may
  *    have a row stride (ld_h, ld_w, in elements, >= d, multiple of 8); dH and dW
  *    are dense [N, D] and [V, D]. Every pointer must be 16-byte aligned; the
@@ -88,6 +89,16 @@ typedef struct lce_problem {
  * lce_backward_adamw rejects it (one update per backward pass). */
 #define LCE_FLAG_ACCUMULATE_DW 1
 
+/* For lce_backward, lce_backward_adamw and lce_backward_shard: the workspace still holds what the
+ * immediately preceding lce_forward (or lce_forward_shard, then lce_combine_shards) of the same
+ * problem, H and targets left in it, on the same stream and with nothing else written to the
+ * workspace in between. The backward then reuses that call's valid-row list (and, where the
+ * forward gathered them, the valid rows of H) instead of forming them again: two fewer kernels
+ * per step. Without the flag the backward depends on no earlier call. The forward and the
+ * combine ignore the flag; the KD calls reject it (LCE_ERR_ARG). The workspace must be at
+ * least max(fwd_bytes, bwd_bytes). */
+#define LCE_FLAG_REUSE_FORWARD 2
+
 /*
  * Hyper-parameters of one AdamW step (decoupled weight decay, bias-corrected moments), the
  * optimizer that paper Sec. 4.1 fuses into the backward pass. With t = step:
@@ -115,6 +126,31 @@ typedef struct lce_adamw {
 lce_status_t lce_workspace_size(const lce_problem_t* p, size_t* fwd_bytes, size_t* bwd_bytes);
 
 /*
+ * Layout of the workspace that lce_forward and lce_backward carve for problem p, for tests and
+ * tools that check it (host only; nothing is launched). Offsets and sizes are in bytes from the
+ * workspace start; rows in elements. A prefix is shared by both passes: the valid-row list idx
+ * and inverse map pos ([npad] int32 each), the count Nv, and the gathered valid rows of H
+ * ([npad][d] bf16). The forward then holds its vocabulary partial pairs (two [part_rows][npad]
+ * fp32 arrays) and per-row terms ([npad] fp32); the backward holds G ([rows_g][vc] bf16, one
+ * vocabulary slab of vc ids, nslab slabs) and the fp32 dH accumulator ([rows_g][d]), plus a
+ * second one when the dH launches split K in two halves (dh_kz = 2; else o_dh32b = 0).
+ */
+typedef struct lce_plan_info {
+  int64_t npad;             /* N rounded up to 256 */
+  int64_t rows_g;           /* npad rounded up to 384: rows of G and of the dH accumulators */
+  int64_t vc, nslab;        /* backward slab width (ids) and slab count */
+  int64_t dh_kz;            /* 1, or 2 when the dH launches split K in two halves */
+  int64_t part_rows;        /* partial rows of the forward statistics */
+  int64_t fwd_gathers;      /* 1 if the forward leaves the gathered rows of H in the prefix */
+  int64_t fwd_one_launch;   /* 1 if the forward statistics run as one launch */
+  int64_t o_idx, o_pos, o_nv, o_hv;
+  int64_t o_pm, o_ps, o_terms, fwd_bytes;
+  int64_t o_g, o_dh32, o_dh32b, bwd_bytes;
+} lce_plan_info_t;
+
+lce_status_t lce_plan_info(const lce_problem_t* p, lce_plan_info_t* out);
+
+/*
  * Forward pass (paper Sec. 4.2): computes the loss without materialising the
  * logits. Outputs, all device memory:
  *   loss        fp32: [1] L for mean / sum (0 when Nv = 0); [N] per-token losses
@@ -131,8 +167,10 @@ lce_status_t lce_forward(const lce_problem_t* p,
                          void* workspace, size_t workspace_bytes, void* stream);
 
 /*
- * Backward pass: recomputes the logits tile by tile, forms
- * G = c (softmax - onehot) and writes both gradients.
+ * Backward pass of the same objective (paper Sec. 4.2; the gradients of the standard
+ * cross-entropy it replaces, Sec. 3.3): recomputes the logits tile by tile (they were never
+ * stored), forms G = c (softmax - onehot) one vocabulary slab at a time and writes both
+ * gradients, dH = G W and dW = G^T H.
  *   lse         [N] fp32 from lce_forward on the same inputs
  *   n_valid     [1] int32: the count that "mean" divides by (lce_forward's
  *               n_valid on one device; a global count when the tokens of one
@@ -315,8 +353,12 @@ const char* lce_status_string(lce_status_t s);
  * the caller's stream (up to a fixed pool of pairs per enable; later launches
  * are not recorded). lce_timing_read waits for the recorded events and
  * returns the summed milliseconds and the number of launches of kernel `k`
- * (0 <= k < lce_timing_kernel_count()). Enabling resets the records. These
- * calls create and destroy HIP events, so they are not for graph capture.
+ * (0 <= k < lce_timing_kernel_count()). Enabling resets the records. The pool
+ * (8192 event pairs, created on the first enable on the current device and kept
+ * until the process ends) and the on/off switch are global to the process and
+ * guarded by a mutex; they are the library's only mutable global state, and the
+ * compute entry points touch them only while timing is on. Enabling creates HIP
+ * events, so these calls are not for graph capture.
  */
 lce_status_t lce_timing_enable(int on);
 int lce_timing_kernel_count(void);

@@ -52,9 +52,12 @@ def _stream(dev: torch.device) -> int:
 
 
 def forward(hidden: torch.Tensor, weight: torch.Tensor, targets: torch.Tensor,
-            ignore_index: int = -100, reduction: str = "mean"):
+            ignore_index: int = -100, reduction: str = "mean", keep_workspace: bool = False):
     """(loss, lse fp32 [N], n_valid int32 [1], status int32 [1]) computed by lce_forward; loss is
-    a fp32 scalar for "mean" / "sum" and the fp32 per-token losses [N] for "none"."""
+    a fp32 scalar for "mean" / "sum" and the fp32 per-token losses [N] for "none". With
+    ``keep_workspace`` a fifth element is the workspace, sized for the backward too, which a
+    following ``backward(..., workspace=...)`` reuses (the valid-row list and gathered rows the
+    forward left in it)."""
     h, ldh = _as_rows(hidden, "hidden")
     w, ldw = _as_rows(weight, "weight")
     n, d = h.shape
@@ -64,15 +67,17 @@ def forward(hidden: torch.Tensor, weight: torch.Tensor, targets: torch.Tensor,
     t, tb = _targets(targets, n)
     p = B.problem(n, d, v, ld_h=ldh, ld_w=ldw, ignore_index=ignore_index, reduction=reduction,
                   target_bytes=tb)
-    fwd_bytes, _ = B.lce_workspace_size(p)
+    fwd_bytes, bwd_bytes = B.lce_workspace_size(p)
     dev = h.device
     loss = torch.empty((n,) if reduction == "none" else (), dtype=torch.float32, device=dev)
     lse = torch.empty(n, dtype=torch.float32, device=dev)
     nv = torch.empty(1, dtype=torch.int32, device=dev)
     status = torch.empty(1, dtype=torch.int32, device=dev)
-    ws = torch.empty(max(fwd_bytes, 1), dtype=torch.uint8, device=dev)
+    ws = torch.empty(max(fwd_bytes, bwd_bytes if keep_workspace else 0, 1), dtype=torch.uint8, device=dev)
     B.lce_forward(p, h.data_ptr(), w.data_ptr(), t.data_ptr(), loss.data_ptr(), lse.data_ptr(),
                   nv.data_ptr(), status.data_ptr(), ws.data_ptr(), fwd_bytes, _stream(dev))
+    if keep_workspace:
+        return loss, lse, nv, status, ws
     return loss, lse, nv, status
 
 
@@ -92,12 +97,26 @@ def _backward_args(hidden, weight, targets, lse, grad_loss, ignore_index, reduct
     return p, h, w, t, grad_loss.contiguous()
 
 
+def _workspace(workspace, nbytes, dev):
+    """The caller's workspace (from ``forward(..., keep_workspace=True)``) or a new one."""
+    if workspace is None:
+        return torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
+    if workspace.dtype != torch.uint8 or workspace.numel() < nbytes or not workspace.is_contiguous():
+        raise ValueError("workspace is not the one forward(..., keep_workspace=True) returned for this problem")
+    return workspace
+
+
 def backward(hidden: torch.Tensor, weight: torch.Tensor, targets: torch.Tensor, lse: torch.Tensor,
              n_valid: torch.Tensor, grad_loss: torch.Tensor, ignore_index: int = -100,
-             reduction: str = "mean", accumulate_into: torch.Tensor | None = None):
+             reduction: str = "mean", accumulate_into: torch.Tensor | None = None,
+             workspace: torch.Tensor | None = None):
     """(dH bf16 [N, D], dW bf16 [V, D]) computed by lce_backward. With ``accumulate_into`` (a
-    dense bf16 [V, D] tensor) this call's dW is added to it in place and it is returned as dW."""
+    dense bf16 [V, D] tensor) this call's dW is added to it in place and it is returned as dW.
+    ``workspace`` is the one the forward of the same inputs kept (``keep_workspace=True``), untouched
+    since: the backward then reuses what that forward left in it (LCE_FLAG_REUSE_FORWARD)."""
     flags = B.LCE_FLAG_ACCUMULATE_DW if accumulate_into is not None else 0
+    if workspace is not None:
+        flags |= B.LCE_FLAG_REUSE_FORWARD
     p, h, w, t, g = _backward_args(hidden, weight, targets, lse, grad_loss, ignore_index, reduction, flags)
     _, bwd_bytes = B.lce_workspace_size(p)
     dev = h.device
@@ -108,7 +127,7 @@ def backward(hidden: torch.Tensor, weight: torch.Tensor, targets: torch.Tensor, 
         dw = accumulate_into
         if dw.dtype != torch.bfloat16 or tuple(dw.shape) != (p.v, p.d) or not dw.is_contiguous():
             raise ValueError("accumulate_into must be a contiguous bf16 [V, D] tensor")
-    ws = torch.empty(max(bwd_bytes, 1), dtype=torch.uint8, device=dev)
+    ws = _workspace(workspace, bwd_bytes, dev)
     B.lce_backward(p, h.data_ptr(), w.data_ptr(), t.data_ptr(), lse.data_ptr(), n_valid.data_ptr(),
                    g.data_ptr(), dh.data_ptr(), dw.data_ptr(), ws.data_ptr(), bwd_bytes, _stream(dev))
     return dh, dw
@@ -174,16 +193,17 @@ class AdamWState:
 
 def backward_adamw(hidden: torch.Tensor, targets: torch.Tensor, lse: torch.Tensor, n_valid: torch.Tensor,
                    grad_loss: torch.Tensor, state: AdamWState, ignore_index: int = -100,
-                   reduction: str = "mean") -> torch.Tensor:
+                   reduction: str = "mean", workspace: torch.Tensor | None = None) -> torch.Tensor:
     """dH bf16 [N, D] from lce_backward_adamw; the weight of ``state`` takes one AdamW step
-    with its gradient inside the call."""
-    p, h, w, t, g = _backward_args(hidden, state.weight, targets, lse, grad_loss, ignore_index, reduction)
+    with its gradient inside the call. ``workspace`` as for ``backward``."""
+    flags = B.LCE_FLAG_REUSE_FORWARD if workspace is not None else 0
+    p, h, w, t, g = _backward_args(hidden, state.weight, targets, lse, grad_loss, ignore_index, reduction, flags)
     if w.data_ptr() != state.weight.data_ptr():
         raise ValueError("the weight must be usable in place")
     _, bwd_bytes = B.lce_workspace_size(p)
     dev = h.device
     dh = torch.empty((p.n, p.d), dtype=torch.bfloat16, device=dev)
-    ws = torch.empty(max(bwd_bytes, 1), dtype=torch.uint8, device=dev)
+    ws = _workspace(workspace, bwd_bytes, dev)
     B.lce_backward_adamw(p, h.data_ptr(), w.data_ptr(), t.data_ptr(), lse.data_ptr(), n_valid.data_ptr(),
                          g.data_ptr(), dh.data_ptr(), *state._ptrs(), state.next_opt(), ws.data_ptr(),
                          bwd_bytes, _stream(dev))
@@ -258,8 +278,12 @@ class LinearCrossEntropy(torch.autograd.Function):
 
     @staticmethod
     def forward(ctx, hidden, weight, targets, ignore_index=-100, reduction="mean"):
-        loss, lse, nv, _ = forward(hidden, weight, targets, ignore_index, reduction)
+        # when a gradient will be taken, the workspace (sized for both passes) is kept for the
+        # backward, which then skips the compaction and row gather the forward already did
+        keep = any(ctx.needs_input_grad[:2])
+        loss, lse, nv, _, *ws = forward(hidden, weight, targets, ignore_index, reduction, keep_workspace=keep)
         ctx.save_for_backward(hidden, weight, targets, lse, nv)
+        ctx.ws = ws[0] if keep else None
         ctx.ignore_index = ignore_index
         ctx.reduction = reduction
         return loss.view(targets.shape) if reduction == "none" else loss
@@ -270,7 +294,8 @@ class LinearCrossEntropy(torch.autograd.Function):
         g = grad.reshape(-1)
         if g.dtype != torch.float32:
             g = g.float()
-        dh, dw = backward(hidden, weight, targets, lse, nv, g, ctx.ignore_index, ctx.reduction)
+        ws, ctx.ws = ctx.ws, None     # used once: a second backward through the graph forms its own
+        dh, dw = backward(hidden, weight, targets, lse, nv, g, ctx.ignore_index, ctx.reduction, workspace=ws)
         return dh.view(hidden.shape), dw, None, None, None
 
 
@@ -280,8 +305,9 @@ class LinearCrossEntropyAdamW(torch.autograd.Function):
 
     @staticmethod
     def forward(ctx, hidden, weight, targets, state, ignore_index=-100, reduction="mean"):
-        loss, lse, nv, _ = forward(hidden, weight, targets, ignore_index, reduction)
+        loss, lse, nv, _, ws = forward(hidden, weight, targets, ignore_index, reduction, keep_workspace=True)
         ctx.save_for_backward(hidden, targets, lse, nv)
+        ctx.ws = ws
         ctx.state = state
         ctx.ignore_index = ignore_index
         ctx.reduction = reduction
@@ -293,7 +319,8 @@ class LinearCrossEntropyAdamW(torch.autograd.Function):
         g = grad.reshape(-1)
         if g.dtype != torch.float32:
             g = g.float()
-        dh = backward_adamw(hidden, targets, lse, nv, g, ctx.state, ctx.ignore_index, ctx.reduction)
+        ws, ctx.ws = ctx.ws, None
+        dh = backward_adamw(hidden, targets, lse, nv, g, ctx.state, ctx.ignore_index, ctx.reduction, workspace=ws)
         return dh.view(hidden.shape), None, None, None, None, None
 
 

@@ -29,6 +29,7 @@ LCE_REDUCE_SUM = 1
 LCE_REDUCE_NONE = 2
 LCE_STATUS_TARGET_OUT_OF_RANGE = 1
 LCE_FLAG_ACCUMULATE_DW = 1
+LCE_FLAG_REUSE_FORWARD = 2
 
 REDUCTIONS = {"mean": LCE_REDUCE_MEAN, "sum": LCE_REDUCE_SUM, "none": LCE_REDUCE_NONE}
 
@@ -37,7 +38,7 @@ EXPORTED = ("lce_workspace_size", "lce_forward", "lce_backward", "lce_status_str
             "lce_timing_enable", "lce_timing_kernel_count", "lce_timing_kernel_name",
             "lce_timing_read", "lce_adamw_step", "lce_backward_adamw", "lce_forward_shard",
             "lce_combine_shards", "lce_backward_shard", "lce_kd_workspace_size", "lce_kd_forward",
-            "lce_kd_backward", "lce_kd_workspace_size_fused", "lce_kd_forward_backward")
+            "lce_kd_backward", "lce_kd_workspace_size_fused", "lce_kd_forward_backward", "lce_plan_info")
 
 
 class LceError(RuntimeError):
@@ -73,6 +74,13 @@ def kd_problem(n: int, ds: int, dt: int, v: int, *, ld_hs: int = 0, ld_ws: int =
     red = REDUCTIONS[reduction] if isinstance(reduction, str) else int(reduction)
     return LceKdProblem(n, ds, dt, v, ld_hs, ld_ws, ld_ht, ld_wt, temperature, ignore_index, red, target_bytes,
                         flags, 0)
+
+
+class LcePlanInfo(ctypes.Structure):
+    _fields_ = [(k, ctypes.c_int64) for k in (
+        "npad", "rows_g", "vc", "nslab", "dh_kz", "part_rows", "fwd_gathers", "fwd_one_launch",
+        "o_idx", "o_pos", "o_nv", "o_hv", "o_pm", "o_ps", "o_terms", "fwd_bytes",
+        "o_g", "o_dh32", "o_dh32b", "bwd_bytes")]
 
 
 class LceShard(ctypes.Structure):
@@ -121,6 +129,7 @@ def load() -> ctypes.CDLL:
         lib.lce_kd_backward.argtypes = [KP, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
         lib.lce_kd_workspace_size_fused.argtypes = [KP, ctypes.POINTER(sz)]
         lib.lce_kd_forward_backward.argtypes = [KP, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+        lib.lce_plan_info.argtypes = [P, ctypes.POINTER(LcePlanInfo)]
         lib.lce_status_string.argtypes = [ctypes.c_int]
         lib.lce_status_string.restype = ctypes.c_char_p
         lib.lce_timing_enable.argtypes = [ctypes.c_int]
@@ -132,7 +141,8 @@ def load() -> ctypes.CDLL:
         for name in ("lce_workspace_size", "lce_forward", "lce_backward", "lce_timing_enable",
                      "lce_timing_read", "lce_timing_kernel_count", "lce_adamw_step", "lce_backward_adamw",
                      "lce_forward_shard", "lce_combine_shards", "lce_backward_shard", "lce_kd_workspace_size",
-                     "lce_kd_forward", "lce_kd_backward", "lce_kd_workspace_size_fused", "lce_kd_forward_backward"):
+                     "lce_kd_forward", "lce_kd_backward", "lce_kd_workspace_size_fused", "lce_kd_forward_backward",
+                     "lce_plan_info"):
             getattr(lib, name).restype = ctypes.c_int
         _lib = lib
         return lib
@@ -152,6 +162,13 @@ def lce_workspace_size(p: LceProblem) -> tuple[int, int]:
     _check(load().lce_workspace_size(ctypes.byref(p), ctypes.byref(f), ctypes.byref(b)),
            "lce_workspace_size")
     return f.value, b.value
+
+
+def lce_plan_info(p: LceProblem) -> dict:
+    """The workspace layout the library carves for problem p (host only)."""
+    out = LcePlanInfo()
+    _check(load().lce_plan_info(ctypes.byref(p), ctypes.byref(out)), "lce_plan_info")
+    return {k: getattr(out, k) for k, _ in LcePlanInfo._fields_}
 
 
 def lce_forward(p: LceProblem, H: int, W: int, targets: int, loss: int, lse: int, n_valid: int,

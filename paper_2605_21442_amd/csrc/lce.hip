@@ -577,10 +577,32 @@ __device__ __forceinline__ Operand gather_operand(const uint16_t* src, int64_t n
   return op;
 }
 
+// The kW rows of a row-major tile (tile = its first row) of which only the first rows_left exist,
+// e.g. the last vocabulary tile of W: per-row offsets as for a gathered operand (kind OP_GATHER),
+// with the rows at or past rows_left pointed at kOobOffset. No address past the existing rows is
+// formed, and the loads of the missing rows return zeros.
+template <int kW>
+__device__ __forceinline__ Operand masked_dense_operand(const uint16_t* tile, int rows_left, int64_t ld) {
+  Operand op;
+  op.rsrc = make_rsrc(tile, (uint64_t)rows_left * ld * 2);
+  op.rwords = make_rsrc_words(tile, (uint64_t)rows_left * ld * 2);
+  const int j = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int ce = lane_chunk_even();
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    int r = w * 32 + q * 8 + (j >> 3);
+    r = r < kW ? r : kW - 1;   // (waves that do not load this operand)
+    op.off[q] = r < rows_left ? (uint32_t)((int64_t)r * ld * 2 + (ce ^ (q & 1)) * 16) : kOobOffset;
+  }
+  return op;
+}
+
 // A kW-wide K-major operand: K-row 0 of the tile at `base` (its first column), rows `ld` elements
-// apart, `bytes` readable bytes from base on.
+// apart, `bytes` readable bytes from base on, and `cols` columns from base on that exist (the
+// lanes whose chunk lies at or past them load from kOobOffset: zeros, and no address past a
+// row's existing columns).
 template <int kW = 256>
-__device__ __forceinline__ Operand kmajor_operand(const uint16_t* base, int64_t ld, uint64_t bytes) {
+__device__ __forceinline__ Operand kmajor_operand(const uint16_t* base, int64_t ld, uint64_t bytes, int cols) {
   Operand op;
   op.base = base;
   op.ld = ld;
@@ -592,13 +614,16 @@ __device__ __forceinline__ Operand kmajor_operand(const uint16_t* base, int64_t 
     int p = w * 256 + q * 64 + j;                       // 16-byte unit of the region
     p = p < kW * 8 ? p : kW * 8 - 1;                    // (waves that do not load this operand)
     const int k = p / (kW / 8), pos = p % (kW / 8);
-    op.off[q] = (uint32_t)((int64_t)k * ld * 2 + (kchunk<kW>(k, pos) << 4));
+    const int c = kchunk<kW>(k, pos);
+    // kW = 256: the K-rows 4 further (q = 2, 3) have the same chunk (same bits 0-1 and 3 of k)
+    op.off[q] = c * 8 < cols ? (uint32_t)((int64_t)k * ld * 2 + (c << 4)) : kOobOffset;
   }
   return op;
 }
 
 // ---------------------------------------------------------------------------------------------
-// K1: valid-row compaction ("masks ignored tokens before projection", Sec. 4.2).
+// K1: valid-row compaction: the LCE objective drops ignored targets before the projection
+// (Sec. 4.2), so no MFMA work is spent on their rows.
 // idx[0..Nv) = ascending rows whose target is in [0, V); pos[n] = its index there or -1.
 // One workgroup of 16 waves walks the rows in rounds of 1024 consecutive rows (coalesced target
 // loads, up to 16 rounds loaded ahead): a row's index is the valid rows of earlier rounds, of
@@ -665,9 +690,11 @@ __global__ __launch_bounds__(1024) void k_compact(const void* targets, int tbyte
 }
 
 // ---------------------------------------------------------------------------------------------
-// K2: forward statistics (paper section 3: the logits' log-sum-exp accumulated over vocabulary
-// tiles, never stored). Two forms, both writing per-token partial pairs (max, sum of exp) in log2
-// units, part[row * npad + token], merged by K3:
+// K2: forward statistics. The objective (Sec. 4.2) needs each valid row's log-sum-exp over the
+// whole vocabulary; here it is accumulated tile by tile from logits that are never stored (this
+// library's design: the paper states the objective, not an algorithm for it). Two forms, both
+// writing per-token partial pairs (max, sum of exp) in log2 units, part[row * npad + token],
+// merged by K3:
 //  - k_fwd_tile (12 waves, D % 64 == 0): one 384-id x 256-token tile per workgroup, H given as the
 //    gathered valid rows Hv; one partial row per vocabulary tile.
 //  - k_fwd_stats (8 waves, any D): workgroup (token tile nt, vocabulary partition p) walks the
@@ -737,10 +764,15 @@ __global__ __launch_bounds__(Geo<3>::NT, 3) void k_fwd_tile(const uint16_t* __re
   }
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, wr = wave >> 2, wc = wave & 3;
 
-  const Operand opa = dense_operand(W + (int64_t)v0 * ldw, vleft, ldw);
   const Operand opb = dense_operand(Hv + (int64_t)n0 * ldh, nv - n0, ldh);
   f32x16_t acc[4][2];
-  mma_mainloop<1, OP_DENSE, OP_DENSE, WM, false>(acc, opa, opb, d, smem);   // d % 64 == 0 (host)
+  // d % 64 == 0 (host); the last vocabulary tile may hold fewer than TM rows of W
+  if (vleft >= TM)
+    mma_mainloop<1, OP_DENSE, OP_DENSE, WM, false>(acc, dense_operand(W + (int64_t)v0 * ldw, vleft, ldw), opb, d,
+                                                   smem);
+  else
+    mma_mainloop<1, OP_GATHER, OP_DENSE, WM, false>(acc, masked_dense_operand<TM>(W + (int64_t)v0 * ldw, vleft, ldw),
+                                                    opb, d, smem);
   // the main loop ends with a barrier: its LDS is free for the wave rows' pairs [3][256] (m, s)
   float* red_m = reinterpret_cast<float*>(smem);
   float* red_s = red_m + WM * TILE;
@@ -846,8 +878,11 @@ __global__ __launch_bounds__(Geo<WM>::NT, WM) void k_fwd_stats(const uint16_t* _
   for (int vt = vt0; vt < vt1; ++vt) {
     const int v0 = vt * TM;
     const int vleft = v - v0;
-    const Operand opa = dense_operand(W + (int64_t)v0 * ldw, vleft, ldw);
-    mma_mainloop<2, OP_DENSE, OP_GATHER, WM>(acc, opa, opb, d, smem);
+    if (vleft >= TM)
+      mma_mainloop<2, OP_DENSE, OP_GATHER, WM>(acc, dense_operand(W + (int64_t)v0 * ldw, vleft, ldw), opb, d, smem);
+    else
+      mma_mainloop<2, OP_GATHER, OP_GATHER, WM>(acc, masked_dense_operand<TM>(W + (int64_t)v0 * ldw, vleft, ldw), opb,
+                                                d, smem);
 
     // rows (vocabulary ids) of this lane: v0 + wr*128 + 32 bi + 8 (r/4) + 4 (lane/32) + r%4
     const int vb = wr * 128 + (lane >> 5) * 4;
@@ -1110,15 +1145,22 @@ __global__ __launch_bounds__(Geo<WM>::NT, WM) void k_bwd_g(const uint16_t* __res
   const int vleft = vs - vt0;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, wr = wave >> 2, wc = wave & 3;
 
-  const Operand opa = dense_operand(W + (v0 + vt0) * ldw, vleft, ldw);
+  const uint16_t* wt = W + (v0 + vt0) * ldw;
   f32x16_t acc[4][2];
+  // the last tile of the vocabulary may hold fewer than TM rows of W
   if constexpr (WM == 3) {
-    // H is the gathered valid rows Hv (row stride ldh = d): a dense operand
+    // H is the gathered valid rows Hv (row stride ldh = d): a dense operand; d % 64 == 0 (host)
     const Operand opb = dense_operand(H + (int64_t)n0 * ldh, nv - n0, ldh);
-    mma_mainloop<1, OP_DENSE, OP_DENSE, WM, false>(acc, opa, opb, d, smem);   // d % 64 == 0 (host)
+    if (vleft >= TM)
+      mma_mainloop<1, OP_DENSE, OP_DENSE, WM, false>(acc, dense_operand(wt, vleft, ldw), opb, d, smem);
+    else
+      mma_mainloop<1, OP_GATHER, OP_DENSE, WM, false>(acc, masked_dense_operand<TM>(wt, vleft, ldw), opb, d, smem);
   } else {
     const Operand opb = gather_operand(H, n, ldh, idx, n0, nv);
-    mma_mainloop<2, OP_DENSE, OP_GATHER, WM>(acc, opa, opb, d, smem);
+    if (vleft >= TM)
+      mma_mainloop<2, OP_DENSE, OP_GATHER, WM>(acc, dense_operand(wt, vleft, ldw), opb, d, smem);
+    else
+      mma_mainloop<2, OP_GATHER, OP_GATHER, WM>(acc, masked_dense_operand<TM>(wt, vleft, ldw), opb, d, smem);
   }
 
   // the gradient scale exists only for the modes that write G (the probability and Q passes get
@@ -1320,8 +1362,8 @@ __global__ __launch_bounds__(Geo<WM>::NT, WM) void k_bwd_dw(const uint16_t* __re
   const int kpad = ((nv + KPAD - 1) / KPAD) * KPAD;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, wr = wave >> 2, wc = wave & 3;
   // ldt = Npad: G has Npad rows of vc ids, Hv Npad rows of d hidden columns
-  const Operand opa = kmajor_operand<TM>(G + m0, vc, ((uint64_t)ldt * vc - m0) * 2);
-  const Operand opb = kmajor_operand<TILE>(Hv + d0, d, ((uint64_t)ldt * d - d0) * 2);
+  const Operand opa = kmajor_operand<TM>(G + m0, vc, ((uint64_t)ldt * vc - m0) * 2, vc - m0);
+  const Operand opb = kmajor_operand<TILE>(Hv + d0, d, ((uint64_t)ldt * d - d0) * 2, d - d0);
   f32x16_t acc[4][2];
   mma_mainloop<1, OP_KMAJOR, OP_KMAJOR, WM, false>(acc, opa, opb, kpad, smem);
 
@@ -1332,6 +1374,10 @@ __global__ __launch_bounds__(Geo<WM>::NT, WM) void k_bwd_dw(const uint16_t* __re
   const bool col_ok[2] = {dc < d, dc + 32 < d};
   // row offset (in elements of a row of `stride`) of block i, register r
   auto erow = [](int i, int r) { return i * 32 + (r >> 2) * 8 + (r & 3); };
+  // on the last tile of the vocabulary, the rows past it are not accessed at all (dW and the
+  // optimizer state end there)
+  const bool partial = rows < TM;
+  auto row_ok = [&](int i, int r) { return !partial || lrow + erow(i, r) < rows; };
   if constexpr (kMode != DW_ADAMW) {
     const __amdgpu_buffer_rsrc_t rw = make_rsrc(dW + r0 * d, (uint64_t)rows * d * 2);
     const uint32_t voff = (uint32_t)((lrow * d + dc) * 2);
@@ -1345,14 +1391,14 @@ __global__ __launch_bounds__(Geo<WM>::NT, WM) void k_bwd_dw(const uint16_t* __re
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
             const uint32_t so = (uint32_t)((erow(i, r) * d + j * 32) * 2);
-            old[r] = bf16_to_f32(__builtin_amdgcn_raw_buffer_load_b16(rw, (int)voff, (int)so, 0));
+            old[r] = row_ok(i, r) ? bf16_to_f32(__builtin_amdgcn_raw_buffer_load_b16(rw, (int)voff, (int)so, 0)) : 0.f;
           }
         }
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const uint32_t so = (uint32_t)((erow(i, r) * d + j * 32) * 2);
           const float x = kMode == DW_ACCUMULATE ? old[r] + acc[i][j][r] : acc[i][j][r];
-          __builtin_amdgcn_raw_buffer_store_b16(to_bf16(x), rw, (int)voff, (int)so, 0);
+          if (row_ok(i, r)) __builtin_amdgcn_raw_buffer_store_b16(to_bf16(x), rw, (int)voff, (int)so, 0);
         }
       }
   } else {
@@ -1378,16 +1424,20 @@ __global__ __launch_bounds__(Geo<WM>::NT, WM) void k_bwd_dw(const uint16_t* __re
             const int row = erow(i, rq * 4 + e);
             const uint32_t s4 = (uint32_t)((row * d + j * 32) * 4);
             const uint32_t sW = (uint32_t)((row * st.ldw + j * 32) * 2);
-            mo[e] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rm, (int)vo4, (int)s4, 0));
-            vo[e] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rv, (int)vo4, (int)s4, 0));
-            p[e] = has_master ? __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rp, (int)vo4, (int)s4, 0))
-                              : bf16_to_f32(__builtin_amdgcn_raw_buffer_load_b16(rW, (int)voW, (int)sW, 0));
+            mo[e] = vo[e] = p[e] = 0.f;
+            if (row_ok(i, rq * 4 + e)) {
+              mo[e] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rm, (int)vo4, (int)s4, 0));
+              vo[e] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rv, (int)vo4, (int)s4, 0));
+              p[e] = has_master ? __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rp, (int)vo4, (int)s4, 0))
+                                : bf16_to_f32(__builtin_amdgcn_raw_buffer_load_b16(rW, (int)voW, (int)sW, 0));
+            }
           }
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
             const int row = erow(i, rq * 4 + e);
             const uint32_t s4 = (uint32_t)((row * d + j * 32) * 4);
             const uint32_t sW = (uint32_t)((row * st.ldw + j * 32) * 2);
+            if (!row_ok(i, rq * 4 + e)) continue;
             const float g = bf16_to_f32(to_bf16(acc[i][j][rq * 4 + e]));
             adamw_update(p[e], mo[e], vo[e], g, oc);
             __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, mo[e]), rm, (int)vo4, (int)s4, 0);
@@ -1422,17 +1472,22 @@ __global__ __launch_bounds__(Geo<WM>::NT, WM) void k_bwd_dh(const uint16_t* __re
   if (!band_tile((int)blockIdx.x - z * g1, (nv + TM - 1) / TM, (d + TILE - 1) / TILE, tm, tn)) return;
   const int m0 = tm * TM, d0 = tn * TILE;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, wr = wave >> 2, wc = wave & 3;
-  // K = vs rounded up to 64: G holds zeros there and the W rows past V lie outside the buffer
-  // resource (zeros), so no slice needs masking. Half z covers [k0, k0 + kzn).
+  // K = the slab's vs ids; the last slice of a slab whose width is not a multiple of 64 is masked
+  // (lanes past K load zeros), so no W row past the vocabulary is addressed. Half z covers
+  // [k0, k0 + kzn), the first half a whole number of 64-wide slices.
   const int kt = (vs + KSLICE - 1) / KSLICE * KSLICE;
   const int kh = ((kt + kz - 1) / kz + KSLICE - 1) / KSLICE * KSLICE;
   const int k0 = z * kh;
-  const int kzn = kt - k0 < kh ? kt - k0 : kh;
+  const int kzn = vs - k0 < kh ? vs - k0 : kh;
   f32x16_t acc[4][2];
   if (kzn > 0) {
     const Operand opa = dense_operand(G + (int64_t)m0 * vc + k0, nv - m0, vc);
-    const Operand opb = kmajor_operand<TILE>(Ws + (int64_t)k0 * ldw + d0, ldw, ((uint64_t)(ws_rows - k0) * ldw - d0) * 2);
-    mma_mainloop<121, OP_DENSE, OP_KMAJOR, WM, false>(acc, opa, opb, kzn, smem);
+    const Operand opb = kmajor_operand<TILE>(Ws + (int64_t)k0 * ldw + d0, ldw, ((uint64_t)(ws_rows - k0) * ldw - d0) * 2,
+                                             d - d0);
+    if (kzn % KSLICE == 0)
+      mma_mainloop<121, OP_DENSE, OP_KMAJOR, WM, false>(acc, opa, opb, kzn, smem);
+    else
+      mma_mainloop<121, OP_DENSE, OP_KMAJOR, WM, true>(acc, opa, opb, kzn, smem);
   } else {
 #pragma unroll
     for (int i = 0; i < 4; ++i)
@@ -1602,10 +1657,12 @@ struct Plan {
   int64_t n, d, v, ldh, ldw, npad;
   int nt_max, vt_count, nparts, vt_count3;   // vt_count3: 384-id tiles
   int64_t vc, nslab;
-  // workspace offsets
-  size_t o_idx, o_pos, o_nv, o_pm, o_ps, o_terms, o_hvf, fwd_bytes;
-  size_t o_hv, o_g, o_dh32, o_dh32b, bwd_bytes;   // o_dh32b: second K half of split dH (or 0)
-  int dh_kz;                                    // K halves of the dH launches (1 or 2)
+  int64_t rows_g;                            // rows of G and dH32: Npad rounded up to a 384-row tile
+  // workspace offsets; idx, pos, Nv and the gathered rows Hv form a prefix both passes share
+  size_t o_idx, o_pos, o_nv, o_hv, o_pm, o_ps, o_terms, fwd_bytes;
+  size_t o_g, o_dh32, o_dh32b, bwd_bytes;    // o_dh32b: second K half of split dH (or 0)
+  int dh_kz;                                 // K halves of the dH launches (1 or 2)
+  int part_rows;                             // partial rows of the forward statistics
 };
 
 // the 12-wave forward in one launch: its partial rows (8 bytes per 384-id tile and token) take at
@@ -1614,11 +1671,16 @@ inline bool fwd_one_launch(const Plan& pl) {
   return pl.vt_count3 <= pl.d / 4 && (int64_t)pl.vt_count3 * pl.nt_max <= INT32_MAX;
 }
 
+// the forward statistics run on 12-wave tiles over the gathered rows Hv (left in the workspace)
+inline bool fwd_gathers(const Plan& pl) {
+  return pl.d % KSLICE == 0 && (int64_t)pl.vt_count3 * pl.nt_max <= INT32_MAX;
+}
+
 inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
 
 lce_status_t make_plan(const lce_problem_t* p, Plan* pl) {
   if (!p) return LCE_ERR_NULL;
-  if ((p->flags & ~LCE_FLAG_ACCUMULATE_DW) != 0) return LCE_ERR_ARG;
+  if ((p->flags & ~(LCE_FLAG_ACCUMULATE_DW | LCE_FLAG_REUSE_FORWARD)) != 0) return LCE_ERR_ARG;
   if (p->n < 0 || p->d < 1 || p->v < 1) return LCE_ERR_SHAPE;
   if (p->d % 8 != 0) return LCE_ERR_UNSUPPORTED;
   if (p->reduction != LCE_REDUCE_MEAN && p->reduction != LCE_REDUCE_SUM && p->reduction != LCE_REDUCE_NONE)
@@ -1656,25 +1718,30 @@ lce_status_t make_plan(const lce_problem_t* p, Plan* pl) {
   pl->o_idx = take(cur, 4 * (size_t)pl->npad);
   pl->o_pos = take(cur, 4 * (size_t)pl->npad);
   pl->o_nv = take(cur, 256);
+  // valid rows of H, gathered by the forward (12-wave statistics) and by the backward; a backward
+  // with LCE_FLAG_REUSE_FORWARD finds the forward's here
+  pl->o_hv = take(cur, 2 * (size_t)p->d * pl->npad);
   const size_t common = cur;
   // partial rows: 2 per partition (8-wave forward); one per 384-id tile while that is at most
   // 2 D bytes per token, else two sets of vc / 384 rows and a running pair (12-wave forward)
   const int64_t rows3 = fwd_one_launch(*pl) ? pl->vt_count3 : 2 * (vc / 384) + 1;
   const int64_t part_rows = 2 * pl->nparts > rows3 ? 2 * pl->nparts : rows3;
+  pl->part_rows = (int)part_rows;
   pl->o_pm = take(cur, 4 * (size_t)part_rows * pl->npad);
   pl->o_ps = take(cur, 4 * (size_t)part_rows * pl->npad);
   pl->o_terms = take(cur, 4 * (size_t)pl->npad);
-  pl->o_hvf = take(cur, 2 * (size_t)p->d * pl->npad);   // valid rows of H, 12-wave forward
   pl->fwd_bytes = cur;
   cur = common;
-  pl->o_hv = take(cur, 2 * (size_t)p->d * pl->npad);
-  pl->o_g = take(cur, 2 * (size_t)pl->npad * vc);
-  pl->o_dh32 = take(cur, 4 * (size_t)pl->npad * p->d);
+  // G and the fp32 dH accumulators hold every row a 384-row dH tile can address (the tiles of
+  // the last token rows reach past Npad), so that no access leaves its region
+  pl->rows_g = round_up(pl->npad, 384);
+  pl->o_g = take(cur, 2 * (size_t)pl->rows_g * vc);
+  pl->o_dh32 = take(cur, 4 * (size_t)pl->rows_g * p->d);
   // dH launches with fewer 384 x 256 output tiles than the 256 CUs split K in two halves, the
   // second accumulated in a buffer of its own
   const int64_t dh_tiles = (pl->npad + 383) / 384 * ((p->d + TILE - 1) / TILE);
   pl->dh_kz = dh_tiles < 256 ? 2 : 1;
-  pl->o_dh32b = pl->dh_kz > 1 ? take(cur, 4 * (size_t)pl->npad * p->d) : 0;
+  pl->o_dh32b = pl->dh_kz > 1 ? take(cur, 4 * (size_t)pl->rows_g * p->d) : 0;
   pl->bwd_bytes = cur;
   return LCE_OK;
 }
@@ -1762,6 +1829,7 @@ PartRows launch_fwd_stats(Launcher& L, const Plan& layout, const uint16_t* W, in
                           int64_t ldh, int d, const int* idx, const int* nv, uint16_t* hv, float* pm, float* ps,
                           float scale2) {
   const int v = (int)layout.v, npad = (int)layout.npad, nt_max = layout.nt_max;
+  // (the same condition as fwd_gathers(layout) when d is the plan's own width)
   if (!(hv && d % KSLICE == 0 && (int64_t)layout.vt_count3 * nt_max <= INT32_MAX)) {
     L(K_FWD_STATS, k_fwd_stats<2>, dim3(nt_max * layout.nparts), dim3(NTHREADS), W, ldw, v, H, ldh, layout.n, idx,
       nv, d, layout.nparts, nt_max, layout.vt_count, pm, ps, npad, scale2);
@@ -1827,7 +1895,7 @@ lce_status_t forward_impl(const lce_problem_t* p, const ShardInfo* shard, const 
   L(K_COMPACT, k_compact, dim3(1), dim3(1024), targets, p->target_bytes, pl.n, si.v_total, p->ignore_index,
     idx, pos, nv, n_valid, dev_status, lse, none ? loss : tgt_part);
   const PartRows pr = launch_fwd_stats(L, pl, w, pl.ldw, h, pl.ldh, (int)pl.d, (const int*)idx, (const int*)nv,
-                                       (uint16_t*)(ws + pl.o_hvf), pm, ps, kLog2e);
+                                       (uint16_t*)(ws + pl.o_hv), pm, ps, kLog2e);
   L(K_COMBINE, k_combine, dim3((unsigned)((pl.n + kCombTok - 1) / kCombTok)), dim3(1024), h, pl.ldh, w, pl.ldw,
     targets, p->target_bytes, si.v_begin, pl.v, (const int*)idx, (const int*)nv, (int)pl.d, pr.count, pr.m, pr.s,
     (int)pl.npad, pr.run_m, pr.run_s, lse, terms, none ? loss : (float*)nullptr, tgt_part);
@@ -1908,11 +1976,16 @@ lce_status_t backward_impl(const lce_problem_t* p, const ShardInfo* shard, const
   const uint16_t* w = (const uint16_t*)W;
   const int d = (int)pl.d, npad = (int)pl.npad, vc = (int)pl.vc;
 
-  L(K_COMPACT, k_compact, dim3(1), dim3(1024), targets, p->target_bytes, pl.n, si.v_total, p->ignore_index,
-    idx, pos, nv, (int*)nullptr, (int*)nullptr, (float*)nullptr, (float*)nullptr);
+  // with LCE_FLAG_REUSE_FORWARD the workspace holds the forward's valid-row list (and, when the
+  // forward gathered them, the rows Hv); otherwise both are formed again
+  const bool reuse = !kd && (p->flags & LCE_FLAG_REUSE_FORWARD) != 0;
+  if (!reuse)
+    L(K_COMPACT, k_compact, dim3(1), dim3(1024), targets, p->target_bytes, pl.n, si.v_total, p->ignore_index,
+      idx, pos, nv, (int*)nullptr, (int*)nullptr, (float*)nullptr, (float*)nullptr);
   // Hv[i] = H[idx[i]] for i < Nv, zero rows up to round_up(Nv, 64)
-  L(K_GATHER_H, k_gather_rows, dim3((unsigned)std::min<int64_t>((npad * (d / 8) + 255) / 256, 16384)), dim3(256), h,
-    pl.ldh, (const int*)idx, (const int*)nv, d, hv);
+  if (!(reuse && fwd_gathers(pl)))
+    L(K_GATHER_H, k_gather_rows, dim3((unsigned)std::min<int64_t>((npad * (d / 8) + 255) / 256, 16384)), dim3(256),
+      h, pl.ldh, (const int*)idx, (const int*)nv, d, hv);
   // KD: the teacher's valid rows for its 12-wave probability pass
   uint16_t* hvt = (kd && kd_hvt_bytes(pl, kd->dt) > 0) ? (uint16_t*)(ws + pl.bwd_bytes + kd_p_bytes(pl)) : nullptr;
   if (hvt)
@@ -1994,6 +2067,7 @@ lce_status_t make_kd_plan(const lce_kd_problem_t* p, KdPlan* k) {
   if (!p) return LCE_ERR_NULL;
   if (p->reserved != 0) return LCE_ERR_ARG;
   if (!(p->temperature > 0.f && p->temperature < INFINITY)) return LCE_ERR_ARG;
+  if (p->flags & LCE_FLAG_REUSE_FORWARD) return LCE_ERR_ARG;   // the KD calls lay out their own workspace
   k->ps = lce_problem_t{p->n, p->ds, p->v, p->ld_hs, p->ld_ws, p->ignore_index, p->reduction, p->target_bytes, p->flags};
   k->pt = lce_problem_t{p->n, p->dt, p->v, p->ld_ht, p->ld_wt, p->ignore_index, p->reduction, p->target_bytes, 0};
   lce_status_t st = make_plan(&k->ps, &k->s);
@@ -2198,6 +2272,34 @@ const char* lce_status_string(lce_status_t s) {
     case LCE_ERR_ARG: return "invalid argument";
   }
   return "unknown status";
+}
+
+lce_status_t lce_plan_info(const lce_problem_t* p, lce_plan_info_t* out) {
+  Plan pl;
+  lce_status_t st = make_plan(p, &pl);
+  if (st != LCE_OK) return st;
+  if (!out) return LCE_ERR_NULL;
+  out->npad = pl.npad;
+  out->rows_g = pl.rows_g;
+  out->vc = pl.vc;
+  out->nslab = pl.nslab;
+  out->dh_kz = pl.dh_kz;
+  out->part_rows = pl.part_rows;
+  out->fwd_gathers = fwd_gathers(pl) ? 1 : 0;
+  out->fwd_one_launch = fwd_one_launch(pl) ? 1 : 0;
+  out->o_idx = (int64_t)pl.o_idx;
+  out->o_pos = (int64_t)pl.o_pos;
+  out->o_nv = (int64_t)pl.o_nv;
+  out->o_hv = (int64_t)pl.o_hv;
+  out->o_pm = (int64_t)pl.o_pm;
+  out->o_ps = (int64_t)pl.o_ps;
+  out->o_terms = (int64_t)pl.o_terms;
+  out->fwd_bytes = (int64_t)pl.fwd_bytes;
+  out->o_g = (int64_t)pl.o_g;
+  out->o_dh32 = (int64_t)pl.o_dh32;
+  out->o_dh32b = (int64_t)pl.o_dh32b;
+  out->bwd_bytes = (int64_t)pl.bwd_bytes;
+  return LCE_OK;
 }
 
 lce_status_t lce_workspace_size(const lce_problem_t* p, size_t* fwd_bytes, size_t* bwd_bytes) {

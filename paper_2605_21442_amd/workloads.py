@@ -9,7 +9,7 @@ The five named workloads are vocabulary-head shapes of the models the paper
 fine-tunes (Sec. 3.2 model zoo, Tab. 1-2 and App. D): a tiny case that the
 oracle finishes in seconds, and Llama-3.2-1B, Llama-3.1-8B, Qwen2.5-7B
 (long sequence) and Llama-3.1-70B heads. The paper measures on Alpaca-style
-SFT data with real checkpoints (Sec. 4.3); neither is available here, and the
+SFT data with real checkpoints (Sec. 5.1); neither is available here, and the
 LCE kernels only see shapes and value statistics, so seeded synthetic tensors
 with the same shapes stand in for them:
 

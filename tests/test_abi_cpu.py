@@ -72,13 +72,34 @@ def test_bad_problems_are_rejected(kw, code):
     assert e.value.code == code
 
 
-@pytest.mark.parametrize("flags", [2, 4, 1 << 30, -1])
+@pytest.mark.parametrize("flags", [4, 8, 1 << 30, -1])
 def test_unknown_flag_bits_are_rejected(flags):
     p = B.problem(4, 64, 10, flags=flags)
     with pytest.raises(B.LceError) as e:
         B.lce_workspace_size(p)
     assert e.value.code == B.LCE_ERR_ARG
     B.lce_workspace_size(B.problem(4, 64, 10, flags=B.LCE_FLAG_ACCUMULATE_DW))
+    B.lce_workspace_size(B.problem(4, 64, 10, flags=B.LCE_FLAG_REUSE_FORWARD))
+    B.lce_workspace_size(B.problem(4, 64, 10, flags=B.LCE_FLAG_REUSE_FORWARD | B.LCE_FLAG_ACCUMULATE_DW))
+
+
+def test_reuse_flag_is_rejected_by_the_distillation_calls():
+    # the KD calls lay out their workspace differently from lce_forward
+    with pytest.raises(B.LceError) as e:
+        B.lce_kd_workspace_size(B.kd_problem(8, 64, 64, 100, flags=B.LCE_FLAG_REUSE_FORWARD))
+    assert e.value.code == B.LCE_ERR_ARG
+
+
+@pytest.mark.parametrize("n,d,v", [(16384, 4096, 128256), (300, 264, 1000), (1, 8, 5), (8192, 2048, 128256)])
+def test_the_forward_and_backward_share_the_prefix_the_reuse_flag_relies_on(n, d, v):
+    # idx, pos, Nv and the gathered rows sit at the same offsets in both passes' layouts, and the
+    # forward's own regions (partials, terms) start after them, so a backward reusing the
+    # forward's workspace finds its list and rows untouched
+    info = B.lce_plan_info(B.problem(n, d, v))
+    assert info["o_idx"] < info["o_pos"] < info["o_nv"] < info["o_hv"]
+    prefix_end = info["o_hv"] + 2 * d * info["npad"]
+    assert info["o_pm"] >= prefix_end and info["o_g"] >= prefix_end
+    assert info["fwd_gathers"] == (1 if d % 64 == 0 else 0)
 
 
 def _fake(addr=0x100000):

@@ -15,7 +15,8 @@ def _bits(x):
     return x.contiguous().view(torch.uint8).cpu().numpy().copy()
 
 
-def test_lce_forward_backward_graph_replays_match_eager():
+@pytest.mark.parametrize("reuse", [False, True])
+def test_lce_forward_backward_graph_replays_match_eager(reuse):
     import torch
     from paper_2605_21442_amd import binding as B
     inp = WL.custom(600, 128, 9000, seed=12, mask_frac=0.2, sigma_w=0.3)
@@ -23,6 +24,8 @@ def test_lce_forward_backward_graph_replays_match_eager():
     n, d = h.shape
     v = w.shape[0]
     p = B.problem(n, d, v)
+    # the backward may take the forward's valid-row list and gathered rows from the workspace
+    pb = B.problem(n, d, v, flags=B.LCE_FLAG_REUSE_FORWARD if reuse else 0)
     fwd_bytes, bwd_bytes = B.lce_workspace_size(p)
     dev = h.device
     loss = torch.empty(1, dtype=torch.float32, device=dev)
@@ -39,7 +42,7 @@ def test_lce_forward_backward_graph_replays_match_eager():
         s = torch.cuda.current_stream().cuda_stream
         B.lce_forward(p, h.data_ptr(), w.data_ptr(), t.data_ptr(), loss.data_ptr(), lse.data_ptr(), nv.data_ptr(),
                       status.data_ptr(), ws.data_ptr(), fwd_bytes, s)
-        B.lce_backward(p, h.data_ptr(), w.data_ptr(), t.data_ptr(), lse.data_ptr(), nv.data_ptr(), grad.data_ptr(),
+        B.lce_backward(pb, h.data_ptr(), w.data_ptr(), t.data_ptr(), lse.data_ptr(), nv.data_ptr(), grad.data_ptr(),
                        dh.data_ptr(), dw.data_ptr(), ws.data_ptr(), bwd_bytes, s)
 
     step()

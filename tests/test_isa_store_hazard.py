@@ -64,8 +64,8 @@ def violations(lines):
         n = 0
         for k in range(i + 1, len(lines)):
             y = lines[k]
-            if y.endswith(">:"):
-                break
+            if y.endswith(">:") or y.startswith("s_endpgm"):
+                break   # (after s_endpgm the wave runs nothing more; what follows is another block)
             if not y:
                 continue
             nop = re.match(r"s_nop\s+(0x[0-9a-fA-F]+|\d+)", y)
@@ -88,7 +88,8 @@ def test_scanner_flags_short_gaps_only():
     lines = ["<k>:", "buffer_store_dwordx4 v[4:7], v0, s[0:3], 0 offen", "v_mov_b32_e32 v1, v2",
              "v_mul_f32_e32 v5, v6, v7",                                   # rewrites v5: 2 after
              "global_store_dwordx4 v[8:9], v[10:13], off", "s_nop 7", "v_mov_b32_e32 v10, 0",   # 9 after
-             "global_store_dwordx2 v[8:9], v[20:21], off", "v_mov_b32_e32 v20, 0"]              # 8 bytes
+             "global_store_dwordx2 v[8:9], v[20:21], off", "v_mov_b32_e32 v20, 0",              # 8 bytes
+             "buffer_store_dwordx4 v[4:7], v0, s[0:3], 0 offen", "s_endpgm", "v_mov_b32_e32 v5, 0"]  # wave ended
     bad = violations(lines)
     assert [(b[1].split()[0], b[3]) for b in bad] == [("buffer_store_dwordx4", 2)]
 
