@@ -1,0 +1,200 @@
+"""Every address the kernels form stays inside its buffer, whatever the hardware's range checks do.
+
+For each launch of the plan (the five heads and small edge shapes, at several valid-token counts
+Nv), this test recomputes, from the layout lce_plan_info reports, the largest byte offset that
+each kernel's loads, stores and read-modify-writes can form and checks it against the size of
+the region (workspace) or of the caller's tensor it addresses. The arithmetic follows the
+kernels' index expressions:
+
+* tiles are 384 x 256 (D % 64 == 0: 12 waves) or 256 x 256 (other widths: 8 waves); the rows of
+  the last vocabulary tile past V are loaded through the out-of-range offset (zeros, no address),
+  so the W rows addressed are those below V;
+* K-major operands send the lanes whose columns lie past D (the hidden width) to the same offset;
+* dH runs K over the slab's vs ids (a ragged last slice masks the rest), in one or two halves;
+* G and the dH accumulators hold rows_g rows, the 384-row tiles of the last token rows included;
+* the dW / AdamW epilogues touch only the rows of the slab that exist.
+
+Accesses sent to the out-of-range offset form no address and are not counted. No GPU is needed.
+"""
+import pytest
+
+from paper_2605_21442_amd import binding as B
+
+HEADS = [(256, 512, 4096), (8192, 2048, 128256), (16384, 4096, 128256), (32768, 3584, 152064),
+         (16384, 8192, 128256)]
+EDGES = [(1, 8, 5), (300, 264, 1000), (257, 64, 9000), (513, 520, 300), (300, 64, 12300), (200, 128, 12289),
+         (768, 128, 1536), (520, 64, 40000), (33, 72, 1), (16385, 64, 383), (1000, 136, 385)]
+
+
+def cdiv(a, b):
+    return -(-a // b)
+
+
+def rup(a, b):
+    return cdiv(a, b) * b
+
+
+class Extents:
+    """Largest byte (exclusive end) formed in each buffer, against the buffer's size."""
+
+    def __init__(self):
+        self.ends = {}
+
+    def touch(self, buf, end):
+        self.ends[buf] = max(self.ends.get(buf, 0), end)
+
+    def check(self, sizes, where):
+        for buf, end in self.ends.items():
+            assert end <= sizes[buf], f"{where}: {buf} reaches byte {end} of {sizes[buf]}"
+
+
+def walk(n, d, v, nv, ld_h=None, ld_w=None):
+    """Extents of one lce_forward + lce_backward of an [n, d] x [v, d] problem with nv valid rows."""
+    ld_h = ld_h or d
+    ld_w = ld_w or d
+    info = B.lce_plan_info(B.problem(n, d, v, ld_h=ld_h, ld_w=ld_w))
+    npad, rows_g, vc, nslab = info["npad"], info["rows_g"], info["vc"], info["nslab"]
+    e = Extents()
+    # caller tensors: the last row holds only d elements of its stride
+    sizes = {"H": 2 * ((n - 1) * ld_h + d) if n else 0, "W": 2 * ((v - 1) * ld_w + d),
+             "dH": 2 * n * d, "dW": 2 * v * d, "lse": 4 * n, "targets": 4 * n,
+             "idx": 4 * npad, "pos": 4 * npad, "hv": 2 * npad * d,
+             "pm": 4 * info["part_rows"] * npad, "ps": 4 * info["part_rows"] * npad, "terms": 4 * npad,
+             "G": 2 * rows_g * vc, "dh32": 4 * rows_g * d, "dh32b": 4 * rows_g * d if info["dh_kz"] > 1 else 0}
+    twelve = d % 64 == 0
+    tm_rows = 384 if twelve else 256          # vocabulary (A) rows of a forward / G tile
+
+    # compaction: idx[0..nv), pos[0..n), the targets
+    if nv:
+        e.touch("idx", 4 * nv)
+    e.touch("pos", 4 * n)
+    e.touch("targets", 4 * n)
+
+    def w_rows(v0, rows):
+        # rows [v0, v0 + rows) of W, full K (the rows past V of a last tile are masked)
+        last = min(v0 + rows, v) - 1
+        e.touch("W", 2 * (last * ld_w + d))
+
+    # forward statistics
+    if nv:
+        if twelve and info["fwd_gathers"]:
+            e.touch("hv", 2 * rup(nv, 64) * d)                      # gather, zero rows to a multiple of 64
+            for n0 in range(0, nv, 256):
+                e.touch("hv", 2 * (n0 + 256) * d)                   # B: 256 dense rows of Hv
+            for v0 in range(0, v, 384):
+                w_rows(v0, 384)
+            vt3 = cdiv(v, 384)
+            if info["fwd_one_launch"]:
+                e.touch("pm", 4 * ((vt3 - 1) * npad + nv))
+            else:
+                gw = vc // 384
+                e.touch("pm", 4 * (2 * gw * npad + nv))             # running pair after the two row sets
+        else:
+            e.touch("H", 2 * ((n - 1) * ld_h + d))                  # rows gathered through idx (< n)
+            for v0 in range(0, v, 256):
+                w_rows(v0, 256)
+            e.touch("pm", 4 * ((2 * min(cdiv(v, 256), 32) - 1) * npad + nv))
+        e.touch("ps", e.ends["pm"])
+        e.touch("terms", 4 * nv)
+        e.touch("lse", 4 * n)
+
+    # backward
+    if nv:
+        e.touch("hv", 2 * rup(nv, 64) * d)
+    dh_kz = info["dh_kz"]
+    for s in range(nslab):
+        v0 = s * vc
+        vs = min(vc, v - v0)
+        if not nv:
+            continue
+        # G tiles: W rows v0 + [vt0, vt0 + tm_rows) (masked past V), Hv / gathered H rows, G written whole
+        for vt0 in range(0, vs, tm_rows):
+            w_rows(v0 + vt0, tm_rows)
+            for n0 in range(0, nv, 256):
+                if twelve:
+                    e.touch("hv", 2 * (n0 + 256) * d)
+                e.touch("G", 2 * ((n0 + 255) * vc + vt0 + tm_rows))
+        # dH: 384-row tiles of G rows, K over [k0, k0 + kzn), W slab rows v0 + k (< v0 + vs), columns < d
+        kt = rup(vs, 64)
+        kh = rup(cdiv(kt, dh_kz), 64)
+        for z in range(dh_kz):
+            k0 = z * kh
+            kzn = min(vs - k0, kh)
+            for m0 in range(0, nv, 384):
+                acc = "dh32" if z == 0 else "dh32b"
+                e.touch(acc, 4 * (m0 + 384) * d)                   # read-modify-write of the tile's rows
+                if kzn > 0:
+                    e.touch("G", 2 * ((m0 + 383) * vc + k0 + kzn))
+                    w_rows(v0 + k0, kzn)
+        # dW: G and Hv read K-major over round_up(Nv, 64) token rows; dW rows of the slab only
+        kpad = rup(nv, 64)
+        for m0 in range(0, vs, 384):
+            e.touch("G", 2 * ((kpad - 1) * vc + m0 + 384))
+            e.touch("dW", 2 * (v0 + min(vs, m0 + 384)) * d)
+        e.touch("hv", 2 * ((kpad - 1) * d + d))
+    e.touch("dH", 2 * n * d)
+    return e, sizes, info
+
+
+CASES = [(n, d, v, nv) for (n, d, v) in HEADS + EDGES
+         for nv in sorted({0, 1, max(n // 2, 1), max(n - 1, 0), n}) if nv <= n]
+
+
+@pytest.mark.parametrize("n,d,v,nv", CASES)
+def test_no_access_leaves_its_buffer(n, d, v, nv):
+    e, sizes, _ = walk(n, d, v, nv)
+    e.check(sizes, f"n={n} d={d} v={v} nv={nv}")
+
+
+@pytest.mark.parametrize("n,d,v", [(300, 64, 1000), (1000, 136, 385), (16384, 4096, 128256)])
+def test_no_access_leaves_its_buffer_with_row_strides(n, d, v):
+    for nv in (1, n):
+        e, sizes, _ = walk(n, d, v, nv, ld_h=d + 64, ld_w=d + 8)
+        e.check(sizes, f"strided n={n} d={d} v={v} nv={nv}")
+
+
+@pytest.mark.parametrize("n,d,v", HEADS + EDGES)
+def test_workspace_regions_are_disjoint_and_inside_the_workspace(n, d, v):
+    info = B.lce_plan_info(B.problem(n, d, v))
+    npad, rows_g, vc = info["npad"], info["rows_g"], info["vc"]
+    prefix = [("idx", info["o_idx"], 4 * npad), ("pos", info["o_pos"], 4 * npad), ("nv", info["o_nv"], 4),
+              ("hv", info["o_hv"], 2 * npad * d)]
+    fwd = prefix + [("pm", info["o_pm"], 4 * info["part_rows"] * npad), ("ps", info["o_ps"], 4 * info["part_rows"] * npad),
+                    ("terms", info["o_terms"], 4 * npad)]
+    bwd = prefix + [("G", info["o_g"], 2 * rows_g * vc), ("dh32", info["o_dh32"], 4 * rows_g * d)]
+    if info["dh_kz"] > 1:
+        bwd.append(("dh32b", info["o_dh32b"], 4 * rows_g * d))
+    assert rows_g % 384 == 0 and rows_g >= npad and npad % 256 == 0 and npad >= n
+    assert vc % 768 == 0
+    for regions, total in ((fwd, info["fwd_bytes"]), (bwd, info["bwd_bytes"])):
+        regions = sorted(regions, key=lambda r: r[1])
+        for (a, oa, sa), (b, ob, sb) in zip(regions, regions[1:]):
+            assert oa + sa <= ob, f"{a} overlaps {b}"
+        for name, o, size in regions:
+            assert o % 256 == 0, name
+        assert regions[-1][1] + regions[-1][2] <= total
+
+
+@pytest.mark.parametrize("n,d,v", HEADS + EDGES)
+def test_in_tile_offsets_fit_a_buffer_resource(n, d, v):
+    # buffer resources hold at most 2^31 - 1 bytes; every tile's offsets from its resource base
+    # (a W tile, a G tile row block, a dH accumulator tile, a 64-row K slice) stay below that
+    info = B.lce_plan_info(B.problem(n, d, v))
+    vc = info["vc"]
+    lim = 2 ** 31 - 1
+    assert 384 * d * 2 <= lim                      # W / Hv tile
+    assert 256 * vc * 2 <= lim                     # G rows of one token tile
+    assert 384 * d * 4 <= lim                      # dH accumulator tile
+    assert 64 * max(d, vc) * 2 <= lim              # one K-major slice
+
+
+def test_the_walk_flags_regions_sized_to_npad_rows():
+    # with G and the dH accumulators sized to Npad rows (not the 384-row tile grid), the dH tiles of
+    # the last token rows of the 8B head with every token valid reach past them
+    e, sizes, info = walk(16384, 4096, 128256, 16384)
+    assert info["rows_g"] > info["npad"]
+    for buf, row_bytes in (("G", 2 * info["vc"]), ("dh32", 4 * 4096)):
+        short = dict(sizes)
+        short[buf] = info["npad"] * row_bytes
+        with pytest.raises(AssertionError, match=buf):
+            e.check(short, "npad rows")
