@@ -187,6 +187,25 @@ lce_status_t lce_backward(const lce_problem_t* p,
                           void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * lce_forward for callers that cannot allocate device memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid allocation): the same computation and outputs as
+ * lce_forward, bit for bit, with the workspace taken from a fixed device array inside the library
+ * instead of from the caller. The array holds LCE_NOALLOC_SCRATCH_BYTES (256 MiB) on every GPU
+ * the library runs on, from the first call on that GPU until the process ends; problems whose
+ * forward workspace (lce_workspace_size's fwd_bytes) is larger are rejected with
+ * LCE_ERR_WORKSPACE before anything is launched. The call itself allocates nothing. All calls on
+ * one GPU share its array: calls that may overlap on one GPU (on different streams, or from
+ * several threads onto different streams) race and must be ordered by the caller; calls on one
+ * stream are ordered by it. `stream` must belong to the current device (else LCE_ERR_ARG). The
+ * backward of a problem forwarded this way is lce_backward with a workspace of its own.
+ */
+#define LCE_NOALLOC_SCRATCH_BYTES (256u * 1024u * 1024u)
+lce_status_t lce_forward_noalloc(const lce_problem_t* p,
+                                 const void* H, const void* W, const void* targets,
+                                 float* loss, float* lse, int32_t* n_valid, int32_t* dev_status,
+                                 void* stream);
+
+/*
  * Two-phase optimizer step (the standard path that in-backward fusion replaces, paper Sec.
  * 4.1): one AdamW step on the bf16 parameter W [V, D] (row stride ld_w, 0 means d) with the
  * bf16 gradient dW [V, D] (dense, as lce_backward writes it; NULL means a zero gradient).

@@ -38,7 +38,8 @@ EXPORTED = ("lce_workspace_size", "lce_forward", "lce_backward", "lce_status_str
             "lce_timing_enable", "lce_timing_kernel_count", "lce_timing_kernel_name",
             "lce_timing_read", "lce_adamw_step", "lce_backward_adamw", "lce_forward_shard",
             "lce_combine_shards", "lce_backward_shard", "lce_kd_workspace_size", "lce_kd_forward",
-            "lce_kd_backward", "lce_kd_workspace_size_fused", "lce_kd_forward_backward", "lce_plan_info")
+            "lce_kd_backward", "lce_kd_workspace_size_fused", "lce_kd_forward_backward", "lce_plan_info",
+            "lce_forward_noalloc")
 
 
 class LceError(RuntimeError):
@@ -130,6 +131,7 @@ def load() -> ctypes.CDLL:
         lib.lce_kd_workspace_size_fused.argtypes = [KP, ctypes.POINTER(sz)]
         lib.lce_kd_forward_backward.argtypes = [KP, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
         lib.lce_plan_info.argtypes = [P, ctypes.POINTER(LcePlanInfo)]
+        lib.lce_forward_noalloc.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, vp]
         lib.lce_status_string.argtypes = [ctypes.c_int]
         lib.lce_status_string.restype = ctypes.c_char_p
         lib.lce_timing_enable.argtypes = [ctypes.c_int]
@@ -142,7 +144,7 @@ def load() -> ctypes.CDLL:
                      "lce_timing_read", "lce_timing_kernel_count", "lce_adamw_step", "lce_backward_adamw",
                      "lce_forward_shard", "lce_combine_shards", "lce_backward_shard", "lce_kd_workspace_size",
                      "lce_kd_forward", "lce_kd_backward", "lce_kd_workspace_size_fused", "lce_kd_forward_backward",
-                     "lce_plan_info"):
+                     "lce_plan_info", "lce_forward_noalloc"):
             getattr(lib, name).restype = ctypes.c_int
         _lib = lib
         return lib
@@ -169,6 +171,15 @@ def lce_plan_info(p: LceProblem) -> dict:
     out = LcePlanInfo()
     _check(load().lce_plan_info(ctypes.byref(p), ctypes.byref(out)), "lce_plan_info")
     return {k: getattr(out, k) for k, _ in LcePlanInfo._fields_}
+
+
+LCE_NOALLOC_SCRATCH_BYTES = 256 * 1024 * 1024
+
+
+def lce_forward_noalloc(p: LceProblem, H: int, W: int, targets: int, loss: int, lse: int, n_valid: int,
+                        dev_status: int, stream: int) -> None:
+    _check(load().lce_forward_noalloc(ctypes.byref(p), H, W, targets, loss, lse, n_valid, dev_status or None,
+                                      stream or None), "lce_forward_noalloc")
 
 
 def lce_forward(p: LceProblem, H: int, W: int, targets: int, loss: int, lse: int, n_valid: int,

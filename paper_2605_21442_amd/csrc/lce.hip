@@ -43,6 +43,11 @@
 
 #include "lce.h"
 
+// Workspace of lce_forward_noalloc: device memory of the code object itself, one copy per GPU,
+// held until the process ends. In host code `scratch` is only a stand-in for the symbol; its
+// device address comes from hipGetSymbolAddress (see noalloc_scratch).
+static __device__ __align__(256) char scratch[LCE_NOALLOC_SCRATCH_BYTES];
+
 namespace {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
@@ -2302,6 +2307,33 @@ lce_status_t lce_plan_info(const lce_problem_t* p, lce_plan_info_t* out) {
   return LCE_OK;
 }
 
+// The device address of `scratch` on the current device, taken once per device (with that
+// device current) and kept: every call on a GPU then shares that GPU's copy.
+struct ScratchAddrs {
+  std::mutex mu;
+  static constexpr int kMaxDevices = 64;
+  void* ptr[kMaxDevices] = {};
+};
+ScratchAddrs g_scratch;
+
+lce_status_t noalloc_scratch(void* stream, void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= ScratchAddrs::kMaxDevices) return LCE_ERR_HIP;
+  if (stream) {
+    hipDevice_t sdev = -1;
+    if (hipStreamGetDevice((hipStream_t)stream, &sdev) != hipSuccess) return LCE_ERR_HIP;
+    if (sdev != dev) return LCE_ERR_ARG;   // the stream must belong to the current device
+  }
+  std::lock_guard<std::mutex> lk(g_scratch.mu);
+  if (!g_scratch.ptr[dev]) {
+    void* a = nullptr;
+    if (hipGetSymbolAddress(&a, HIP_SYMBOL(scratch)) != hipSuccess || !a) return LCE_ERR_HIP;
+    g_scratch.ptr[dev] = a;
+  }
+  *out = g_scratch.ptr[dev];
+  return LCE_OK;
+}
+
 lce_status_t lce_workspace_size(const lce_problem_t* p, size_t* fwd_bytes, size_t* bwd_bytes) {
   Plan pl;
   lce_status_t st = make_plan(p, &pl);
@@ -2316,6 +2348,20 @@ lce_status_t lce_forward(const lce_problem_t* p, const void* H, const void* W, c
                          void* workspace, size_t workspace_bytes, void* stream) {
   return forward_impl(p, nullptr, H, W, targets, loss, lse, nullptr, n_valid, dev_status, workspace,
                       workspace_bytes, stream);
+}
+
+lce_status_t lce_forward_noalloc(const lce_problem_t* p, const void* H, const void* W, const void* targets,
+                                 float* loss, float* lse, int32_t* n_valid, int32_t* dev_status, void* stream) {
+  Plan pl;
+  lce_status_t st = make_plan(p, &pl);
+  if (st != LCE_OK) return st;
+  if (pl.fwd_bytes > (size_t)LCE_NOALLOC_SCRATCH_BYTES) return LCE_ERR_WORKSPACE;
+  void* ws = nullptr;
+  st = noalloc_scratch(stream, &ws);
+  if (st != LCE_OK) return st;
+  // nothing of the previous call's contents is read: every region is written before it is used
+  return forward_impl(p, nullptr, H, W, targets, loss, lse, nullptr, n_valid, dev_status, ws,
+                      (size_t)LCE_NOALLOC_SCRATCH_BYTES, stream);
 }
 
 lce_status_t lce_forward_shard(const lce_problem_t* p, const lce_shard_t* shard, const void* H, const void* W,

@@ -280,3 +280,16 @@ def test_overlapping_rows_are_copied_before_the_call():
     assert _rows_usable((4, 64), (64, 1), 0)             # dense
     assert _rows_usable((4, 64), (160, 1), 64)           # strided view of wider rows
     assert _rows_usable((1, 64), (0, 1), 0)              # one row: its stride is never used
+
+
+def test_noalloc_forward_rejects_problems_beyond_its_array_before_any_launch():
+    # the Qwen2.5-7B head's forward workspace is larger than the library's fixed array: rejected
+    # before any HIP call, so this runs without a GPU
+    p = B.problem(32768, 3584, 152064)
+    assert B.lce_workspace_size(p)[0] > B.LCE_NOALLOC_SCRATCH_BYTES
+    with pytest.raises(B.LceError) as e:
+        B.lce_forward_noalloc(p, _fake(), _fake(), _fake(), _fake(), _fake(), _fake(), 0, 0)
+    assert e.value.code == B.LCE_ERR_WORKSPACE
+    with pytest.raises(B.LceError) as e:
+        B.lce_forward_noalloc(B.problem(4, 60, 10), _fake(), _fake(), _fake(), _fake(), _fake(), _fake(), 0, 0)
+    assert e.value.code == B.LCE_ERR_UNSUPPORTED
