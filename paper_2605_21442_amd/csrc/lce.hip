@@ -1136,14 +1136,29 @@ __global__ __launch_bounds__(Geo<WM>::NT, WM) void k_bwd_g(const uint16_t* __res
                                                        const int* __restrict__ n_norm, int reduction, int d, int tm_count,
                                                        uint16_t* __restrict__ G, int vc, int ldt,
                                                        float scale2, float inv_t, float* __restrict__ P,
-                                                       float* __restrict__ qpart, int64_t qrow) {
+                                                       float* __restrict__ qpart, int64_t qrow, int gsub) {
   // 12 waves (WM = 3, 384 ids per tile) serve the one-hot LCE gradient when D % 64 == 0; the
   // distillation modes and other widths keep 8 waves and the LDS-staged epilogue below
   static_assert(WM == 2 || kMode == G_ONEHOT || kMode == P_WRITE, "");
   constexpr int TM = Geo<WM>::TM;
   __shared__ __attribute__((aligned(16))) char smem[Geo<WM>::LDS];
   const int nv = *nv_ptr;
-  const int tm = blockIdx.x % tm_count, tn = blockIdx.x / tm_count;
+  // tiles in groups of gsub consecutive id tiles by all token tiles, ids fastest: the group's W
+  // rows stay in the MALL while the token tiles pass (gsub = tm_count: one group, the whole slab)
+  int tm, tn;
+  {
+    const int nt = (int)gridDim.x / tm_count, b = (int)blockIdx.x;
+    const int full = tm_count / gsub, g = b / (gsub * nt);
+    if (g < full) {
+      const int r = b - g * gsub * nt;
+      tm = g * gsub + r % gsub;
+      tn = r / gsub;
+    } else {
+      const int r = b - full * gsub * nt, wl = tm_count - full * gsub;
+      tm = full * gsub + r % wl;
+      tn = r / wl;
+    }
+  }
   const int n0 = tn * TILE;
   if (n0 >= nv) return;
   const int vt0 = tm * TM;                   // slab-relative
@@ -1352,16 +1367,15 @@ __global__ __launch_bounds__(Geo<WM>::NT, WM) void k_bwd_g(const uint16_t* __res
 // row offset per element, so that the accumulators are nearly the only registers it holds.
 enum DwMode { DW_STORE = 0, DW_ACCUMULATE = 1, DW_ADAMW = 2 };
 
+// One dW tile (block blk of the dW grid, smem the workgroup's LDS).
 template <int kMode, int WM>
-__global__ __launch_bounds__(Geo<WM>::NT, WM) void k_bwd_dw(const uint16_t* __restrict__ G, int vc, int ldt, int vs,
-                                                           const uint16_t* __restrict__ Hv, int d,
-                                                           const int* __restrict__ nv_ptr, int tm_count,
-                                                           uint16_t* __restrict__ dW, int64_t v0,
-                                                           AdamWState st, AdamWConst oc) {
+__device__ __forceinline__ void dw_tile(char* smem, int blk, const uint16_t* __restrict__ G, int vc, int ldt, int vs,
+                                        const uint16_t* __restrict__ Hv, int d, const int* __restrict__ nv_ptr,
+                                        int tm_count, uint16_t* __restrict__ dW, int64_t v0, const AdamWState& st,
+                                        const AdamWConst& oc) {
   constexpr int TM = Geo<WM>::TM;
-  __shared__ __attribute__((aligned(16))) char smem[Geo<WM>::LDS];
   int tm, tn;
-  if (!band_tile(blockIdx.x, tm_count, (d + TILE - 1) / TILE, tm, tn)) return;
+  if (!band_tile(blk, tm_count, (d + TILE - 1) / TILE, tm, tn)) return;
   const int m0 = tm * TM, d0 = tn * TILE;
   const int nv = *nv_ptr;
   const int kpad = ((nv + KPAD - 1) / KPAD) * KPAD;
@@ -1456,25 +1470,33 @@ __global__ __launch_bounds__(Geo<WM>::NT, WM) void k_bwd_dw(const uint16_t* __re
   }
 }
 
+template <int kMode, int WM>
+__global__ __launch_bounds__(Geo<WM>::NT, WM) void k_bwd_dw(const uint16_t* __restrict__ G, int vc, int ldt, int vs,
+                                                           const uint16_t* __restrict__ Hv, int d,
+                                                           const int* __restrict__ nv_ptr, int tm_count,
+                                                           uint16_t* __restrict__ dW, int64_t v0,
+                                                           AdamWState st, AdamWConst oc) {
+  __shared__ __attribute__((aligned(16))) char smem[Geo<WM>::LDS];
+  dw_tile<kMode, WM>(smem, (int)blockIdx.x, G, vc, ldt, vs, Hv, d, nv_ptr, tm_count, dW, v0, st, oc);
+}
+
 // K6: dH32[m][dd] (+)= sum_k G[m][k] Ws[k][dd] over the slab's k < vs; rows m < Nv. Ws = W + v0 ldw
 // is the slab's first row, read K-major (transposing LDS reads); ws_rows = V - v0 rows follow.
 // kz = 2 splits K in two halves for launches with fewer output tiles than CUs: blocks of the
 // second half (the upper half of the grid) accumulate into a second buffer dH32b, which the
 // finalise adds in a fixed order.
+// One dH tile (block blk of a dH grid of `grid` blocks, smem the workgroup's LDS).
 template <int WM>
-__global__ __launch_bounds__(Geo<WM>::NT, WM) void k_bwd_dh(const uint16_t* __restrict__ G, int vc, int vs,
-                                                        const uint16_t* __restrict__ Ws, int64_t ldw,
-                                                        int64_t ws_rows, int d,
-                                                        const int* __restrict__ nv_ptr,
-                                                        float* __restrict__ dH32, int accumulate, int kz,
-                                                        float* __restrict__ dH32b) {
+__device__ __forceinline__ void dh_tile(char* smem, int blk, int grid, const uint16_t* __restrict__ G, int vc, int vs,
+                                        const uint16_t* __restrict__ Ws, int64_t ldw, int64_t ws_rows, int d,
+                                        const int* __restrict__ nv_ptr, float* __restrict__ dH32, int accumulate,
+                                        int kz, float* __restrict__ dH32b) {
   constexpr int TM = Geo<WM>::TM;
-  __shared__ __attribute__((aligned(16))) char smem[Geo<WM>::LDS];
   const int nv = *nv_ptr;
-  const int g1 = (int)gridDim.x / kz;
-  const int z = (int)blockIdx.x / g1;
+  const int g1 = grid / kz;
+  const int z = blk / g1;
   int tm, tn;
-  if (!band_tile((int)blockIdx.x - z * g1, (nv + TM - 1) / TM, (d + TILE - 1) / TILE, tm, tn)) return;
+  if (!band_tile(blk - z * g1, (nv + TM - 1) / TM, (d + TILE - 1) / TILE, tm, tn)) return;
   const int m0 = tm * TM, d0 = tn * TILE;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, wr = wave >> 2, wc = wave & 3;
   // K = the slab's vs ids; the last slice of a slab whose width is not a multiple of 64 is masked
@@ -1532,6 +1554,18 @@ __global__ __launch_bounds__(Geo<WM>::NT, WM) void k_bwd_dh(const uint16_t* __re
       }
     }
   }
+}
+
+template <int WM>
+__global__ __launch_bounds__(Geo<WM>::NT, WM) void k_bwd_dh(const uint16_t* __restrict__ G, int vc, int vs,
+                                                        const uint16_t* __restrict__ Ws, int64_t ldw,
+                                                        int64_t ws_rows, int d,
+                                                        const int* __restrict__ nv_ptr,
+                                                        float* __restrict__ dH32, int accumulate, int kz,
+                                                        float* __restrict__ dH32b) {
+  __shared__ __attribute__((aligned(16))) char smem[Geo<WM>::LDS];
+  dh_tile<WM>(smem, (int)blockIdx.x, (int)gridDim.x, G, vc, vs, Ws, ldw, ws_rows, d, nv_ptr, dH32, accumulate, kz,
+              dH32b);
 }
 
 // K7: dH[row] = bf16(dH32[pos[row]]) for valid rows, +0.0 for the others. 8 elements per thread.
@@ -1646,7 +1680,8 @@ enum KernelId { K_COMPACT = 0, K_FWD_STATS, K_COMBINE, K_LOSS, K_GATHER_H, K_BWD
                 K_BWD_DW, K_BWD_DH, K_DH_FINAL, K_ADAMW, K_SHARD_COMBINE, K_KD_P, K_KD_Q, K_KD_TERMS, K_MISC,
                 K_COUNT };
 const char* const kKernelNames[K_COUNT] = {"compact", "fwd_stats", "combine", "loss", "gather_h",
-                                           "bwd_g", "bwd_dw", "bwd_dh", "dh_finalize", "adamw", "shard_combine", "kd_teacher_p", "kd_q", "kd_terms", "misc"};
+                                           "bwd_g", "bwd_dw", "bwd_dh", "dh_finalize", "adamw", "shard_combine",
+                                           "kd_teacher_p", "kd_q", "kd_terms", "misc"};
 
 struct Timing {
   std::mutex mu;
@@ -1682,6 +1717,16 @@ inline bool fwd_gathers(const Plan& pl) {
 }
 
 inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+
+// Width, in tiles of tile_rows W rows, of the vocabulary groups the forward and G launches take
+// in turn (each group by all token tiles): `tiles` split into equal groups whose W rows fit
+// kGroupBytes, so that a group stays in the 256 MB MALL while the token tiles pass.
+constexpr int64_t kGroupBytes = (int64_t)160 << 20;
+inline int group_tiles(int64_t tiles, int64_t tile_rows, int64_t d) {
+  const int64_t bytes = tiles * tile_rows * d * 2;
+  const int64_t groups = std::max<int64_t>(1, (bytes + kGroupBytes - 1) / kGroupBytes);
+  return (int)std::max<int64_t>(1, (tiles + groups - 1) / groups);
+}
 
 lce_status_t make_plan(const lce_problem_t* p, Plan* pl) {
   if (!p) return LCE_ERR_NULL;
@@ -1845,8 +1890,11 @@ PartRows launch_fwd_stats(Launcher& L, const Plan& layout, const uint16_t* W, in
   const int gw = (int)(layout.vc / Geo<3>::TM);
   const int ntl = layout.vt_count3;
   if (fwd_one_launch(layout)) {
+    // one launch: the groups only order the tiles (one slab wide, or narrower where a slab's W
+    // rows would not stay in the MALL)
+    const int go = group_tiles(gw, Geo<3>::TM, d);
     L(K_FWD_STATS, k_fwd_tile, dim3((unsigned)(ntl * nt_max)), dim3(Geo<3>::NT), W, ldw, v, (const uint16_t*)hv,
-      (int64_t)d, nv, d, 0, ntl, gw, nt_max, pm, ps, (const float*)nullptr, (const float*)nullptr, 0,
+      (int64_t)d, nv, d, 0, ntl, go, nt_max, pm, ps, (const float*)nullptr, (const float*)nullptr, 0,
       (float*)nullptr, (float*)nullptr, 0, npad, scale2);
     return PartRows{pm, ps, ntl, nullptr, nullptr};
   }
@@ -2013,45 +2061,46 @@ lce_status_t backward_impl(const lce_problem_t* p, const ShardInfo* shard, const
         L(K_KD_P, k_bwd_g<P_WRITE, 3>, dim3((unsigned)(tmg * pl.nt_max)), dim3(Geo<3>::NT), kd->wt, kd->ldwt, v0, vs,
           (const uint16_t*)hvt, (int64_t)kd->dt, pl.n, targets, p->target_bytes, (int64_t)0, (const int*)idx,
           (const int*)nv, kd->lse_t, grad_loss, (const int*)n_valid, p->reduction, kd->dt, tmg, (uint16_t*)nullptr, vc,
-          npad, kd->scale2, kd->inv_t, P, (float*)nullptr, (int64_t)0);
+          npad, kd->scale2, kd->inv_t, P, (float*)nullptr, (int64_t)0, group_tiles(tmg, Geo<3>::TM, kd->dt));
       } else {
         L(K_KD_P, k_bwd_g<P_WRITE, 2>, dim3((unsigned)(tm * pl.nt_max)), dim3(NTHREADS), kd->wt, kd->ldwt, v0, vs,
           kd->ht, kd->ldht, pl.n, targets, p->target_bytes, (int64_t)0, (const int*)idx, (const int*)nv, kd->lse_t,
           grad_loss, (const int*)n_valid, p->reduction, kd->dt, tm, (uint16_t*)nullptr, vc, npad,
-          kd->scale2, kd->inv_t, P, (float*)nullptr, (int64_t)0);
+          kd->scale2, kd->inv_t, P, (float*)nullptr, (int64_t)0, tm);
       }
       if (kd->qpart)
         L(K_BWD_G, k_bwd_g<G_SOFT_Q, 2>, dim3((unsigned)(tm * pl.nt_max)), dim3(NTHREADS), w, pl.ldw, v0, vs, h,
           pl.ldh, pl.n, targets, p->target_bytes, (int64_t)0, (const int*)idx, (const int*)nv, lse, grad_loss,
           (const int*)n_valid, p->reduction, d, tm, g, vc, npad, kd->scale2, kd->inv_t, P, kd->qpart,
-          (int64_t)(2 * (v0 / TILE)));
+          (int64_t)(2 * (v0 / TILE)), tm);
       else
         L(K_BWD_G, k_bwd_g<G_SOFT, 2>, dim3((unsigned)(tm * pl.nt_max)), dim3(NTHREADS), w, pl.ldw, v0, vs, h,
           pl.ldh, pl.n, targets, p->target_bytes, (int64_t)0, (const int*)idx, (const int*)nv, lse, grad_loss,
           (const int*)n_valid, p->reduction, d, tm, g, vc, npad, kd->scale2, kd->inv_t, P, (float*)nullptr,
-          (int64_t)0);
+          (int64_t)0, tm);
     } else {
       if (d % KSLICE == 0) {
         const int tmg = (vs + Geo<kGWM>::TM - 1) / Geo<kGWM>::TM;
         L(K_BWD_G, k_bwd_g<G_ONEHOT, kGWM>, dim3((unsigned)(tmg * pl.nt_max)), dim3(Geo<kGWM>::NT), w, pl.ldw, v0, vs,
           (const uint16_t*)hv, (int64_t)d, pl.n, targets, p->target_bytes, si.v_begin, (const int*)idx, (const int*)nv,
           lse, grad_loss, (const int*)n_valid, p->reduction, d, tmg, g, vc, npad, kLog2e, 1.f, (float*)nullptr,
-          (float*)nullptr, (int64_t)0);
+          (float*)nullptr, (int64_t)0, group_tiles(tmg, Geo<3>::TM, d));
       } else {
         L(K_BWD_G, k_bwd_g<G_ONEHOT, 2>, dim3((unsigned)(tm * pl.nt_max)), dim3(NTHREADS), w, pl.ldw, v0, vs, h,
           pl.ldh, pl.n, targets, p->target_bytes, si.v_begin, (const int*)idx, (const int*)nv, lse, grad_loss,
           (const int*)n_valid, p->reduction, d, tm, g, vc, npad, kLog2e, 1.f, (float*)nullptr, (float*)nullptr,
-          (int64_t)0);
+          (int64_t)0, tm);
       }
     }
+    const unsigned bdh = (unsigned)(pl.dh_kz * 8 * ((dh_tiles + 7) / 8) * dt);
+    const int tmw = (vs + Geo<kDwWM>::TM - 1) / Geo<kDwWM>::TM;
+    const unsigned bdw = (unsigned)(8 * ((tmw + 7) / 8) * dt);
     // dH reads the slab's W rows before the dW launch, whose AdamW epilogue (in-backward step)
     // may update them; later slabs read only their own rows
-    L(K_BWD_DH, k_bwd_dh<kDhWM>, dim3((unsigned)(pl.dh_kz * 8 * ((dh_tiles + 7) / 8) * dt)), dim3(Geo<kDhWM>::NT),
-      (const uint16_t*)g, vc, vs, w + v0 * pl.ldw, pl.ldw, pl.v - v0, d, (const int*)nv, dh32, (int)(s > 0), pl.dh_kz,
-      dh32b);
-    const int tmw = (vs + Geo<kDwWM>::TM - 1) / Geo<kDwWM>::TM;
-    L(K_BWD_DW, dw_kernel, dim3((unsigned)(8 * ((tmw + 7) / 8) * dt)), dim3(Geo<kDwWM>::NT), (const uint16_t*)g, vc,
-      npad, vs, (const uint16_t*)hv, d, (const int*)nv, tmw, dW, v0, as, c);
+    L(K_BWD_DH, k_bwd_dh<kDhWM>, dim3(bdh), dim3(Geo<kDhWM>::NT), (const uint16_t*)g, vc, vs, w + v0 * pl.ldw, pl.ldw,
+      pl.v - v0, d, (const int*)nv, dh32, (int)(s > 0), pl.dh_kz, dh32b);
+    L(K_BWD_DW, dw_kernel, dim3(bdw), dim3(Geo<kDwWM>::NT), (const uint16_t*)g, vc, npad, vs, (const uint16_t*)hv, d,
+      (const int*)nv, tmw, dW, v0, as, c);
   }
   const int64_t nthr = pl.n * pl.d / 8;
   L(K_DH_FINAL, k_dh_finalize, dim3((unsigned)((nthr + 255) / 256)), dim3(256), (const float*)dh32,
@@ -2243,17 +2292,17 @@ lce_status_t kd_forward_impl(const lce_kd_problem_t* p, const void* Hs, const vo
       L(K_KD_P, k_bwd_g<P_WRITE, 3>, dim3((unsigned)(tmg * pl.nt_max)), dim3(Geo<3>::NT), wt, tp.ldw, v0, vs,
         (const uint16_t*)hvt, tp.d, pl.n, targets, p->target_bytes, (int64_t)0, (const int*)idx, (const int*)nv,
         (const float*)lse_t, (const float*)nullptr, (const int*)nullptr, p->reduction, (int)tp.d, tmg,
-        (uint16_t*)nullptr, vc, npad, k.scale2, k.inv_t, P, (float*)nullptr, (int64_t)0);
+        (uint16_t*)nullptr, vc, npad, k.scale2, k.inv_t, P, (float*)nullptr, (int64_t)0, group_tiles(tmg, Geo<3>::TM, tp.d));
     } else {
       L(K_KD_P, k_bwd_g<P_WRITE, 2>, dim3((unsigned)(tm * pl.nt_max)), dim3(NTHREADS), wt, tp.ldw, v0, vs, ht, tp.ldh,
         pl.n, targets, p->target_bytes, (int64_t)0, (const int*)idx, (const int*)nv, (const float*)lse_t,
         (const float*)nullptr, (const int*)nullptr, p->reduction, (int)tp.d, tm, (uint16_t*)nullptr, vc,
-        npad, k.scale2, k.inv_t, P, (float*)nullptr, (int64_t)0);
+        npad, k.scale2, k.inv_t, P, (float*)nullptr, (int64_t)0, tm);
     }
     L(K_KD_Q, k_bwd_g<Q_SOFT, 2>, dim3((unsigned)(tm * pl.nt_max)), dim3(NTHREADS), wsm, pl.ldw, v0, vs, hs, pl.ldh,
       pl.n, targets, p->target_bytes, (int64_t)0, (const int*)idx, (const int*)nv, (const float*)lse_s,
       (const float*)nullptr, (const int*)nullptr, p->reduction, (int)pl.d, tm, (uint16_t*)nullptr, vc,
-      npad, k.scale2, k.inv_t, P, qpart, (int64_t)(2 * (v0 / TILE)));
+      npad, k.scale2, k.inv_t, P, qpart, (int64_t)(2 * (v0 / TILE)), tm);
   }
   L(K_KD_TERMS, k_kd_terms, dim3((unsigned)((pl.n + 255) / 256)), dim3(256), (const float*)qpart,
     2 * pl.vt_count, (int64_t)npad, (const int*)pos, pl.n, (const float*)lse_s, terms, none ? loss : (float*)nullptr);
