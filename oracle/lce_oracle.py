@@ -141,6 +141,44 @@ def backward(h, w, targets, ignore_index=-100, reduction="mean", grad=1.0, block
     return {"dH": dh, "dW": dw}
 
 
+def backward_by_vocab_chunks(h_bits, w_bits, targets, lse, on_dw_chunk, ignore_index=-100,
+                             reduction="mean", grad=1.0, chunk=16384, block=4096, progress=None):
+    """The backward above (dH = G W, dW = G^T H, G the scaled softmax-minus-onehot of the valid
+    rows) for sizes whose whole dW does not fit beside the inputs in host memory: with each valid
+    row's lse given (the forward's), the columns of G for a chunk of vocabulary ids need only that
+    chunk's logits, exp(s[n, v] - lse_n) - [v == t_n]. The ids are taken chunk by chunk and the
+    valid rows block by block within a chunk; dH accumulates over the chunks and each chunk's
+    finished rows of dW go to ``on_dw_chunk(v0, dw_rows)`` (ids v0 ..). Host memory stays
+    O(Nv D + chunk D + block chunk). Returns (valid row ids, dH of those rows) in float64;
+    ``progress(done, total)`` is called after each chunk."""
+    v = w_bits.shape[0]
+    ok, _ = valid_rows(targets, v, ignore_index)
+    rows = np.nonzero(ok)[0]
+    c = scale_c(int(rows.size), reduction, grad)
+    t = np.asarray(targets, dtype=np.int64)
+    hv = bf16_to_f64(h_bits[rows])                             # [Nv, D]
+    dh = np.zeros_like(hv)
+    lse_v = np.asarray(lse, dtype=np.float64)[rows]
+    t_v = t[rows]
+    c_v = c[rows] if reduction == "none" else c
+    for v0 in range(0, v, chunk):
+        v1 = min(v0 + chunk, v)
+        wc = bf16_to_f64(w_bits[v0:v1])                        # [k, D]
+        dwc = np.zeros_like(wc)
+        for s0 in range(0, rows.size, block):
+            s1 = min(s0 + block, rows.size)
+            g = np.exp(hv[s0:s1] @ wc.T - lse_v[s0:s1, None])  # softmax columns v0 .. v1 of these rows
+            hit = np.nonzero((t_v[s0:s1] >= v0) & (t_v[s0:s1] < v1))[0]
+            g[hit, t_v[s0:s1][hit] - v0] -= 1.0
+            g *= c_v[s0:s1, None] if reduction == "none" else c_v
+            dh[s0:s1] += g @ wc
+            dwc += g.T @ hv[s0:s1]
+        on_dw_chunk(v0, dwc)
+        if progress is not None:
+            progress(v1, v)
+    return rows, dh
+
+
 def lce(h_bits, w_bits, targets, ignore_index=-100, reduction="mean", grad=1.0):
     """Whole objective from bf16 bit patterns: loss, lse, Nv, status, dH, dW (all float64)."""
     h = bf16_to_f64(h_bits)

@@ -85,6 +85,12 @@ WORKLOADS = {
                        mask_frac=0.30, mask_kind="prefix", case_id=4),
     "llama70b": Workload("llama70b", n=16384, d=8192, v=128256, batch=2, seq=8192,
                          sigma_w=0.015, mask_frac=0.20, case_id=5),
+    # A check case, not a benchmark workload: the 8B head's tokens, targets, mask and weight draws
+    # (same case id) with the weights scaled up (sigma_w = 0.125), so that each row's softmax is
+    # peaked and the softmax part of G carries more than half of dH and dW (at 0.02 the logits are
+    # nearly flat and the one-hot part dominates both); same shapes, so the same launch plan.
+    "llama8b_spread": Workload("llama8b_spread", n=16384, d=4096, v=128256, batch=8, seq=2048,
+                               sigma_w=0.125, mask_frac=0.25, case_id=3),
 }
 
 
@@ -97,15 +103,21 @@ def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
     x = np.ascontiguousarray(x, dtype=np.float32)
     u = x.view(np.uint32)
     out = np.empty(u.shape, dtype=np.uint16)
-    # process in slabs to bound the temporaries for billion-element weights
+    # process in slabs to bound the temporaries for billion-element weights; 32-bit arithmetic
+    # wraps only for NaN patterns, which are replaced (quiet NaN with the payload's top bits)
     flat_u, flat_o = u.reshape(-1), out.reshape(-1)
     step = 1 << 24
     for s in range(0, flat_u.size, step):
-        b = flat_u[s:s + step].astype(np.uint64)
-        r = (b + 0x7FFF + ((b >> 16) & 1)) >> 16
+        b = flat_u[s:s + step]
+        r = b >> 16
+        r &= 1
+        r += b
+        r += 0x7FFF
+        r >>= 16
         nan = (b & 0x7FFFFFFF) > 0x7F800000
-        r = np.where(nan, (b >> 16) | 0x40, r)
-        flat_o[s:s + step] = r.astype(np.uint16)
+        if nan.any():
+            r[nan] = (b[nan] >> 16) | 0x40
+        flat_o[s:s + step] = r
     return out
 
 
@@ -164,12 +176,22 @@ class Inputs:
     ignore_index: int = IGNORE_INDEX
 
 
+def weight_normals(w: Workload, seed: int = 0) -> np.ndarray:
+    """The standard normal draws [V, D] (float32) behind workload ``w``'s weight: W is their bf16
+    rounding after scaling by sigma_w, so workloads that share a case id share these draws."""
+    return _rng(seed, w.case_id, _S_W).standard_normal((w.v, w.d), dtype=np.float32)
+
+
+def weight_bits(z: np.ndarray, sigma: float) -> np.ndarray:
+    """bf16 bit patterns of the weight ``sigma * z`` (z from weight_normals)."""
+    return f32_to_bf16_bits(z * np.float32(sigma))
+
+
 def generate(w: Workload, seed: int = 0, *, draw_w: bool = True,
              ignore_index: int = IGNORE_INDEX) -> Inputs:
     """Draw the inputs of workload ``w``; ``draw_w=False`` leaves W empty (for callers that only need H and targets)."""
     h = draw_normal_bf16(_rng(seed, w.case_id, _S_H), (w.n, w.d), 1.0)
-    wb = (draw_normal_bf16(_rng(seed, w.case_id, _S_W), (w.v, w.d), w.sigma_w)
-          if draw_w else np.empty((0, w.d), np.uint16))
+    wb = weight_bits(weight_normals(w, seed), w.sigma_w) if draw_w else np.empty((0, w.d), np.uint16)
     t = draw_targets(_rng(seed, w.case_id, _S_T), w.n, w.v, w.targets, w.zipf_s)
     t = apply_mask(_rng(seed, w.case_id, _S_MASK), t, w, ignore_index)
     return Inputs(w, seed, h, wb, t, ignore_index)

@@ -1,11 +1,15 @@
 """HIP path vs the CPU oracle at the full workload sizes, in the launch configuration the
-benchmark times (same library calls, same shapes).
+benchmark times (same library calls, same shapes: the forward keeps its workspace and the backward
+reuses what the forward left in it).
 
 The oracle's forward (loss and every row's lse) for seed 0 is stored under tests/golden/ by
-``tests/golden/make_golden.py`` (oracle only); sampled rows of dH and dW are computed here by the
-oracle one by one: dH rows need only their own logits, dW rows need the stored lse of every valid
-row. Whole-output properties (ignored dH rows are exactly zero, dW columns sum to ~0, everything
-finite) are checked on the full GPU outputs.
+``tests/golden/make_golden.py`` (oracle only). Every head is checked on every row's lse and on
+every element of dH and dW: the oracle's backward runs by vocabulary chunks from the stored lse
+(``backward_by_vocab_chunks``), each chunk of dW compared with the same rows of the GPU's dW as it
+is finished, so that neither a float64 dW nor a float64 copy of the GPU's is held whole. The
+case with spread logits (the 8B head with sigma_w = 0.125) makes the softmax part of G carry more
+than half of both gradients in the 8B launch plan. Whole-output properties (ignored dH rows are
+exactly zero, dW columns sum to ~0, everything finite) are checked on the GPU outputs.
 """
 import os
 
@@ -19,16 +23,27 @@ from tests.golden import make_golden as MG
 
 pytestmark = pytest.mark.gpu
 
-NAMES = ["llama1b", "llama8b", "qwen7b", "llama70b"]
+NAMES = ["llama1b", "llama8b", "qwen7b", "llama70b", "llama8b_spread"]
+
+
+_CAPSYS = []
 
 
 def _say(msg):
-    print(msg, flush=True)
+    # progress of the long oracle passes and the measured errors: past pytest's output capture
+    # where the test has the capsys fixture, else captured like any print
+    if _CAPSYS:
+        with _CAPSYS[0].disabled():
+            print(msg, flush=True)
+    else:
+        print(msg, flush=True)
 
 
 @pytest.mark.parametrize("name", NAMES)
-def test_full_size_against_oracle(name):
+def test_full_size_against_oracle(name, capsys):
     import torch
+    from paper_2605_21442_amd import autograd as A
+    _CAPSYS[:] = [capsys]
     path = MG.path_for(name, 0)
     if not os.path.exists(path):
         pytest.skip(f"{path} missing: run tests/golden/make_golden.py")
@@ -38,18 +53,22 @@ def test_full_size_against_oracle(name):
     inp = WL.generate(wl, 0)
     assert str(gold["fingerprint"]) == MG.fingerprint(inp), "golden file is stale"
     h, w, t = U.to_device(inp)
-    _say(f"[{name}] running lce_forward + lce_backward")
-    gpu = U.run_gpu(h, w, t, backward=True)
-    dh_t, dw_t = gpu.pop("dH_t"), gpu.pop("dW_t")
+    _say(f"[{name}] lce_forward + lce_backward (reusing the forward's workspace)")
+    loss, lse, nv, status, ws = A.forward(h, w, t, keep_workspace=True)
+    g = torch.ones(1, dtype=torch.float32, device=h.device)
+    dh_t, dw_t = A.backward(h, w, t, lse, nv, g, workspace=ws)
+    del ws, w
+    torch.cuda.synchronize()
 
     # forward: exact count, loss, every lse
-    assert gpu["n_valid"] == int(gold["n_valid"]) == wl.n_valid()
-    assert gpu["status"] == 0
-    assert abs(gpu["loss"] - float(gold["loss"])) <= U.LOSS_ABS_TOL, (gpu["loss"], float(gold["loss"]))
+    assert int(nv.item()) == int(gold["n_valid"]) == wl.n_valid()
+    assert int(status.item()) == 0
+    assert abs(float(loss.item()) - float(gold["loss"])) <= U.LOSS_ABS_TOL, (float(loss.item()), float(gold["loss"]))
     valid = inp.targets != inp.ignore_index
-    lse_err = np.max(np.abs(gpu["lse"][valid] - gold["lse"][valid]))
+    lse_np = lse.cpu().numpy().astype(np.float64)
+    lse_err = np.max(np.abs(lse_np[valid] - gold["lse"][valid]))
     assert lse_err <= U.LSE_ABS_TOL, lse_err
-    assert np.all(gpu["lse"][~valid] == 0.0)
+    assert np.all(lse_np[~valid] == 0.0)
 
     # whole-output properties on the GPU
     ign = torch.from_numpy(~valid).to(h.device)
@@ -59,28 +78,41 @@ def test_full_size_against_oracle(name):
     budget = 4 * 2.0 ** -8 * dw_t.float().abs().sum(0)
     assert bool((col.abs() <= budget).all().item())
 
-    # sampled dH rows (valid and ignored)
-    rng = np.random.default_rng(7)
+    # every element of dW (chunk by chunk) and of dH against the oracle's float64 backward
+    nvalid = int(gold["n_valid"])
+    c = 1.0 / nvalid
+    t64 = inp.targets.astype(np.int64)
     vrows = np.nonzero(valid)[0]
-    irows = np.nonzero(~valid)[0]
-    rows = np.concatenate([rng.choice(vrows, 6, replace=False), vrows[[0, -1]], irows[:2]])
-    _say(f"[{name}] oracle dH rows {rows.tolist()}")
-    ref_dh = O.dh_of_rows(inp.h_bits, inp.w_bits, inp.targets, rows, int(gold["n_valid"]))
-    got_dh = dh_t[torch.from_numpy(rows).to(h.device)].float().cpu().numpy().astype(np.float64)
-    e = U.rel_fro(got_dh, ref_dh)
-    assert e <= U.GRAD_REL_TOL, ("dH", e)
-    assert np.all(got_dh[-2:] == 0.0)
+    acc = dict(dw_err=0.0, dw_ref=0.0, dw_soft=0.0)
 
-    # sampled dW rows: most frequent ids, tile and slab edges, the last id, random ids
-    v = wl.v
-    ids = [0, 1, 2, 255, 256, 4095, 4096, 8191, 8192, v - 1] + rng.integers(3, v, 4).tolist()
-    ids = np.array(sorted(set(i for i in ids if i < v)))
-    _say(f"[{name}] oracle dW rows {ids.tolist()}")
-    ref_dw = O.dw_of_rows(inp.h_bits, inp.w_bits, inp.targets, ids, gold["lse"])
-    got_dw = dw_t[torch.from_numpy(ids).to(h.device)].float().cpu().numpy().astype(np.float64)
-    e = U.rel_fro(got_dw, ref_dw)
-    assert e <= U.GRAD_REL_TOL, ("dW", e)
-    _say(f"[{name}] ok: loss {gpu['loss']:.6f} (oracle {float(gold['loss']):.6f}), lse err {lse_err:.2e}")
+    def on_chunk(v0, ref):
+        got = dw_t[v0:v0 + ref.shape[0]].double().cpu().numpy()
+        acc["dw_err"] += float(np.sum((got - ref) ** 2))
+        acc["dw_ref"] += float(np.sum(ref ** 2))
+        # softmax part of the chunk: the reference plus the one-hot part c * (rows whose target is here)
+        onehot = np.zeros_like(ref)
+        sel = vrows[(t64[vrows] >= v0) & (t64[vrows] < v0 + ref.shape[0])]
+        np.add.at(onehot, t64[sel] - v0, O.bf16_to_f64(inp.h_bits[sel]))
+        acc["dw_soft"] += float(np.sum((ref + c * onehot) ** 2))
+
+    def progress(done, total):
+        _say(f"[{name}]   oracle vocabulary ids {done}/{total}")
+
+    _say(f"[{name}] oracle backward over {nvalid} valid rows by vocabulary chunks")
+    rows, ref_dh = O.backward_by_vocab_chunks(inp.h_bits, inp.w_bits, inp.targets, gold["lse"], on_chunk,
+                                              progress=progress)
+    got_dh = dh_t[torch.from_numpy(rows).to(h.device)].double().cpu().numpy()
+    e_dh = U.rel_fro(got_dh, ref_dh)
+    e_dw = np.sqrt(acc["dw_err"] / acc["dw_ref"])
+    share_dw = np.sqrt(acc["dw_soft"] / acc["dw_ref"])
+    # softmax part of dH: the reference plus the one-hot part c * W[t_n]
+    share_dh = np.linalg.norm(ref_dh + c * O.bf16_to_f64(inp.w_bits[t64[rows]])) / np.linalg.norm(ref_dh)
+    _say(f"[{name}] every element: dH rel Frobenius {e_dh:.2e}, dW rel Frobenius {e_dw:.2e}; "
+         f"softmax share of dH {share_dh:.3f}, of dW {share_dw:.3f}; loss {float(loss.item()):.6f} "
+         f"(oracle {float(gold['loss']):.6f}), lse err {lse_err:.2e}")
+    assert e_dh <= U.GRAD_REL_TOL and e_dw <= U.GRAD_REL_TOL, (e_dh, e_dw)
+    if name == "llama8b_spread":
+        assert share_dh >= 0.5 and share_dw >= 0.5, (share_dh, share_dw)
 
 
 def test_full_size_fused_adamw_llama8b():
@@ -287,37 +319,3 @@ def test_full_size_allocates_nothing_beyond_the_workspace():
     for x in (h, w, dh, dw, ws):
         assert x.numel() * x.element_size() < logits_bf16 // 2
     assert int(nv.item()) == wl.n_valid() and int(status.item()) == 0
-
-
-@pytest.mark.parametrize("name", ["llama1b", "llama8b"])
-def test_full_size_every_element_of_the_gradients(name):
-    """1B and 8B heads: every element of dH and dW against the oracle's full float64 backward
-    (about 10 s and 50 s of host BLAS); the Qwen and 70B heads are checked on sampled rows above."""
-    path = MG.path_for(name, 0)
-    if not os.path.exists(path):
-        pytest.skip(f"{path} missing: run tests/golden/make_golden.py")
-    gold = np.load(path, allow_pickle=False)
-    wl = WL.WORKLOADS[name]
-    inp = WL.generate(wl, 0)
-    assert str(gold["fingerprint"]) == MG.fingerprint(inp), "golden file is stale"
-    h, w, t = U.to_device(inp)
-    _say(f"[{name}] running lce_forward + lce_backward")
-    gpu = U.run_gpu(h, w, t, backward=True)
-    del gpu["dH_t"], gpu["dW_t"], h, w, t
-    assert gpu["n_valid"] == int(gold["n_valid"])
-    _say(f"[{name}] oracle backward over {gpu['n_valid']} valid rows")
-    ticks = [0]
-
-    def progress(done, total):
-        if done * 10 // total > ticks[0] or done == total:
-            ticks[0] = done * 10 // total
-            _say(f"[{name}]   oracle rows {done}/{total}")
-
-    ref = O.backward(O.bf16_to_f64(inp.h_bits), O.bf16_to_f64(inp.w_bits), inp.targets, inp.ignore_index,
-                     "mean", 1.0, progress=progress)
-    e_dh = U.rel_fro(gpu["dH"], ref["dH"])
-    e_dw = U.rel_fro(gpu["dW"], ref["dW"])
-    valid = inp.targets != inp.ignore_index
-    assert np.all(gpu["dH"][~valid] == 0.0)
-    _say(f"[{name}] every element: dH rel Frobenius {e_dh:.2e}, dW rel Frobenius {e_dw:.2e}")
-    assert e_dh <= U.GRAD_REL_TOL and e_dw <= U.GRAD_REL_TOL, (e_dh, e_dw)

@@ -356,3 +356,41 @@ def test_shard_partials_combine_to_the_full_objective(reduction, cuts):
           for a, b in zip(cuts[:-1], cuts[1:])]
     np.testing.assert_allclose(sum(b["dH_part"] for b in bw), full["dH"], rtol=1e-11, atol=1e-14)
     np.testing.assert_allclose(np.concatenate([b["dW"] for b in bw]), full["dW"], rtol=1e-11, atol=1e-14)
+
+
+# ---- the backward by vocabulary chunks (full-size checks) -------------------------------------
+
+@pytest.mark.parametrize("reduction", ["mean", "sum", "none"])
+@pytest.mark.parametrize("chunk,block", [(7, 5), (53, 64), (20, 1)])
+def test_backward_by_vocab_chunks_matches_torch_autograd(reduction, chunk, block):
+    inp = WL.custom(37, 24, 53, seed=41, mask_frac=0.25, sigma_w=0.5)
+    h, w = O.bf16_to_f64(inp.h_bits), O.bf16_to_f64(inp.w_bits)
+    t = inp.targets.astype(np.int64)
+    g = np.linspace(0.5, 1.5, 37) if reduction == "none" else 0.75
+    H = torch.tensor(h, requires_grad=True)
+    W = torch.tensor(w, requires_grad=True)
+    loss = torch.nn.functional.cross_entropy(H @ W.T, torch.tensor(t), ignore_index=-100, reduction=reduction)
+    (loss * torch.tensor(g)).sum().backward()
+    lse = O.forward(h, w, t, -100, reduction)["lse"]
+    got = {}
+    rows, dh = O.backward_by_vocab_chunks(inp.h_bits, inp.w_bits, inp.targets, lse,
+                                          lambda v0, dw: got.__setitem__(v0, dw), reduction=reduction,
+                                          grad=g, chunk=chunk, block=block)
+    dw = np.concatenate([got[k] for k in sorted(got)])
+    assert sorted(got) == list(range(0, 53, chunk))
+    full_dh = np.zeros_like(h)
+    full_dh[rows] = dh
+    np.testing.assert_allclose(full_dh, H.grad.numpy(), rtol=1e-11, atol=1e-14)
+    np.testing.assert_allclose(dw, W.grad.numpy(), rtol=1e-11, atol=1e-14)
+    assert np.array_equal(rows, np.nonzero(inp.targets != -100)[0])
+
+
+def test_backward_by_vocab_chunks_matches_the_whole_oracle():
+    inp = WL.custom(300, 64, 1000, seed=42, mask_frac=0.3, sigma_w=0.2, targets="zipf")
+    full = O.lce(inp.h_bits, inp.w_bits, inp.targets)
+    parts = []
+    rows, dh = O.backward_by_vocab_chunks(inp.h_bits, inp.w_bits, inp.targets, full["lse"],
+                                          lambda v0, dw: parts.append((v0, dw)), chunk=384, block=100)
+    np.testing.assert_allclose(dh, full["dH"][rows], rtol=1e-12, atol=1e-17)
+    np.testing.assert_allclose(np.concatenate([p for _, p in parts]), full["dW"], rtol=1e-11, atol=1e-17)
+    assert np.all(full["dH"][np.setdiff1d(np.arange(300), rows)] == 0.0)

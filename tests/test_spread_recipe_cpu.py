@@ -1,0 +1,93 @@
+"""The full-size case whose logits are spread (the 8B head with sigma_w = 0.125): on a sample of its
+valid rows, the oracle's gradients get more than half of their norm from the softmax part of G, so
+a softmax taken from the wrong vocabulary slab moves dW (not only dH) beyond the 1e-2 tolerance;
+with the benchmark recipe (sigma_w = 0.02) the same mistake stays inside the tolerance in dW. The
+mistake is planted in the oracle's G, on the CPU.
+
+dW restricted to the sample is G_s^T H_s ([V, D]); its Frobenius norms come from the sample's Gram
+matrices, ||G_s^T H_s||^2 = sum((G_s G_s^T) * (H_s H_s^T)), so it is never formed.
+"""
+import numpy as np
+import pytest
+
+from oracle import lce_oracle as O
+from paper_2605_21442_amd import workloads as WL
+
+SLAB = 18432          # the 8B head's backward slab width (lce_plan_info vc)
+
+
+_CACHE = {}
+
+
+def _inputs():
+    # the two recipes share H, targets, mask and the weight's normal draws (same case id): draw once
+    if not _CACHE:
+        base = WL.WORKLOADS["llama8b"]
+        inp = WL.generate(base, 0, draw_w=False)
+        z = WL.weight_normals(base, 0)
+        _CACHE["inp"] = inp
+        for name in ("llama8b", "llama8b_spread"):
+            _CACHE[name] = WL.weight_bits(z, WL.WORKLOADS[name].sigma_w)
+        del z
+    return _CACHE["inp"], _CACHE
+
+
+def _shares_and_mutation(name, rows=64, chunk=16384):
+    inp, cache = _inputs()
+    w_bits = cache[name]
+    valid = np.nonzero(inp.targets != inp.ignore_index)[0][:rows]
+    h = O.bf16_to_f64(inp.h_bits[valid])
+    t = inp.targets[valid].astype(np.int64)
+    v = w_bits.shape[0]
+    s = np.concatenate([h @ O.bf16_to_f64(w_bits[v0:v0 + chunk]).T for v0 in range(0, v, chunk)], axis=1)
+    m = s.max(1, keepdims=True)
+    p = np.exp(s - m)
+    p /= p.sum(1, keepdims=True)
+    y = np.zeros_like(p)
+    y[np.arange(len(t)), t] = 1.0
+    g = p - y                                   # the scale c cancels in every ratio below
+    g_bad = np.roll(p, SLAB, axis=1) - y        # the softmax of the slab one slab away
+    # [g; p; g_bad] @ W by vocabulary chunks: dH of the sample, its softmax part, the mutant's dH
+    stack = np.concatenate([g, p, g_bad])
+    prod = sum(stack[:, v0:v0 + chunk] @ O.bf16_to_f64(w_bits[v0:v0 + chunk]) for v0 in range(0, v, chunk))
+    dh, dh_soft, dh_bad = np.split(prod, 3)
+    share_dh = np.linalg.norm(dh_soft) / np.linalg.norm(dh)
+    err_dh = np.linalg.norm(dh_bad - dh) / np.linalg.norm(dh)
+    n_dw = _fro_dw(g, g, h)
+    share_dw = np.sqrt(_fro_dw(p, p, h) / n_dw)
+    err_dw = np.sqrt(_fro_dw(g_bad - g, g_bad - g, h) / n_dw)
+    return share_dh, share_dw, err_dh, err_dw
+
+
+def _fro_dw(a, b, h):
+    # <a^T h, b^T h>_F for [rows, V] matrices a, b and the sample's rows h
+    return float(np.sum((a @ b.T) * (h @ h.T)))
+
+
+def test_the_shared_draws_are_the_workloads_own():
+    # the weights built here from the shared draws are those generate() draws for each workload
+    from tests.golden import make_golden as MG
+    import os
+    inp, cache = _inputs()
+    for name in ("llama8b", "llama8b_spread"):
+        path = MG.path_for(name, 0)
+        if not os.path.exists(path):
+            pytest.skip(f"{path} missing")
+        full = WL.Inputs(WL.WORKLOADS[name], 0, inp.h_bits, cache[name], inp.targets)
+        assert str(np.load(path, allow_pickle=False)["fingerprint"]) == MG.fingerprint(full)
+
+
+@pytest.mark.parametrize("name", ["llama8b_spread"])
+def test_spread_recipe_puts_most_of_the_gradient_in_the_softmax_part(name):
+    share_dh, share_dw, err_dh, err_dw = _shares_and_mutation(name)
+    print(f"{name}: softmax share of dH {share_dh:.3f}, of dW {share_dw:.3f}; "
+          f"wrong-slab softmax moves dH by {err_dh:.3f}, dW by {err_dw:.3f}")
+    assert share_dh >= 0.5 and share_dw >= 0.5
+    assert err_dh > 1e-2 and err_dw > 1e-2        # the planted mistake fails the tolerance in both
+
+
+def test_benchmark_recipe_hides_the_same_mistake_in_dw():
+    share_dh, share_dw, err_dh, err_dw = _shares_and_mutation("llama8b")
+    print(f"llama8b: softmax share of dH {share_dh:.3f}, of dW {share_dw:.3f}; "
+          f"wrong-slab softmax moves dH by {err_dh:.4f}, dW by {err_dw:.4f}")
+    assert share_dw < 0.05 and err_dw < 1e-2      # dW cannot see it at this recipe
