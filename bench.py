@@ -138,12 +138,10 @@ def _kernel_breakdown(B, step, steps):
     return kernels, steps
 
 
-def _traffic(kernel):
-    """HBM bytes per launch of `kernel` from the committed counter summary, or None when that
-    summary was taken on a different kernel source."""
-    import hashlib
-    path = os.path.join(ROOT, "profiles", "traffic_llama8b.txt")
-    src = os.path.join(ROOT, "paper_2605_21442_amd", "csrc", "lce.hip")
+def _traffic(kernel, workload):
+    """HBM bytes per launch of `kernel` from the committed counter summary of `workload`, or None
+    when there is none or it was taken on a different kernel source."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.txt")
     if not os.path.exists(path):
         return None
     kv = {}
@@ -151,7 +149,7 @@ def _traffic(kernel):
         if ":" in line and not line.startswith("#"):
             k, v = line.split(":", 1)
             kv[k.strip()] = v.strip()
-    if kv.get("lce.hip sha256") != hashlib.sha256(open(src, "rb").read()).hexdigest():
+    if kv.get("lce.hip sha256") != _source_hash():
         return None
     key = f"{kernel} bytes per launch"
     return float(kv[key]) if key in kv else None
@@ -346,7 +344,7 @@ def main():
         "workspace_bytes": int(max(fwd_bytes, bwd_bytes)),
         "logits_bytes_avoided_fp32": int(n) * int(v) * 4,
         "roofline": {"bound": "mfma", "kernel": dom, "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
-                     "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS, "traffic": _traffic(dom) if (wl.name, args.variant) == ("llama8b", "lce") else None,
+                     "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS, "traffic": _traffic(dom, wl.name) if args.variant == "lce" else None,
                      "flops_per_launch": flops_launch, "avg_launch_ms": kernels[dom]["avg_ms"]},
         "kernels_ms_per_step": {k: r["total_ms"] / kpass for k, r in kernels.items()},
         "kernel_timing": f"second pass of {kpass} steps after the timed region, HIP events around each launch",

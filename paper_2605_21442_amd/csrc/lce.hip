@@ -121,6 +121,16 @@ __device__ __forceinline__ void store16_padded(void* p, i32x4_t v) {
   asm volatile("global_store_dwordx4 %0, %1, off\n\ts_nop 7" : : "v"(p), "v"(v) : "memory");
 }
 
+// The same for a 16-byte store through a buffer resource (descriptor words rw, per-lane voffset,
+// uniform soffset).
+__device__ __forceinline__ void buffer_store16_padded(i32x4_t v, const i32x4_t& rw, uint32_t voffset,
+                                                      uint32_t soffset) {
+  asm volatile("buffer_store_dwordx4 %0, %1, %2, %3 offen\n\ts_nop 7"
+               :
+               : "v"(v), "v"(voffset), "s"(rw), "s"(soffset)
+               : "memory");
+}
+
 __device__ __forceinline__ float bf16_to_f32(uint32_t bits16) { return __uint_as_float(bits16 << 16); }
 
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
@@ -1211,42 +1221,48 @@ __global__ __launch_bounds__(Geo<WM>::NT, WM) void k_bwd_g(const uint16_t* __res
     // group, the others the odd one), stored as 16 bytes. Rows of tokens >= Nv and ids >= the
     // slab width get zeros, so the whole 256 x 384 tile is written (the slab width vc is a
     // multiple of 384).
-    const __amdgpu_buffer_rsrc_t rg = make_rsrc(G + (int64_t)n0 * vc, (uint64_t)TILE * vc * 2);
+    const i32x4_t rg = make_rsrc_words(G + (int64_t)n0 * vc, (uint64_t)TILE * vc * 2);
     const uint32_t voff = (uint32_t)(((wc * 64 + (lane & 31)) * vc + vt0 + wr * 128 + (lane >> 5) * 8) * 2);
+    // A tile whose tokens are all valid and whose ids all lie in the slab needs no test per
+    // element; on the other tiles the values out of range are replaced by zeros (a select, not a
+    // branch per element: the exponential of a row past Nv may be anything, even NaN).
+    auto store_tile = [&](auto kFull) {
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const bool tok_ok = tok[j] < nv;
+      for (int j = 0; j < 2; ++j) {
+        const bool tok_ok = tok[j] < nv;
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int p = 0; p < 2; ++p) {
-          u32x2_t pk[2];
+          for (int p = 0; p < 2; ++p) {
+            u32x2_t pk[2];
 #pragma unroll
-          for (int h = 0; h < 2; ++h) {
-            const int q = 2 * p + h;
-            float gq[4];
+            for (int h = 0; h < 2; ++h) {
+              const int q = 2 * p + h;
+              float gq[4];
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              const int vr = vb + i * 32 + q * 8 + e;
-              float g = 0.f;
-              if (tok_ok && vr < vleft) {
-                g = cj[j] * __builtin_amdgcn_exp2f(fmaf(acc[i][j][q * 4 + e], scale2, -l2[j]));
-                if (vr == tgt[j]) g -= cj[j];
+              for (int e = 0; e < 4; ++e) {
+                const int vr = vb + i * 32 + q * 8 + e;
+                float g = cj[j] * __builtin_amdgcn_exp2f(fmaf(acc[i][j][q * 4 + e], scale2, -l2[j]));
+                g = vr == tgt[j] ? g - cj[j] : g;
+                if constexpr (!decltype(kFull)::value) g = (tok_ok && vr < vleft) ? g : 0.f;
+                gq[e] = g;
               }
-              gq[e] = g;
+              pk[h].x = pack_bf16x2(gq[0], gq[1]);
+              pk[h].y = pack_bf16x2(gq[2], gq[3]);
             }
-            pk[h].x = pack_bf16x2(gq[0], gq[1]);
-            pk[h].y = pack_bf16x2(gq[2], gq[3]);
+            // lane L < 32: (its group 2p ids 0-3, lane L + 32's ids 4-7); lane L + 32: (lane L's
+            // group 2p + 1 ids 0-3, its own ids 4-7)
+            const auto sx = __builtin_amdgcn_permlane32_swap(pk[0].x, pk[1].x, false, false);
+            const auto sy = __builtin_amdgcn_permlane32_swap(pk[0].y, pk[1].y, false, false);
+            const i32x4_t v16 = {(int)sx[0], (int)sy[0], (int)sx[1], (int)sy[1]};
+            const uint32_t so = (uint32_t)((j * 32 * vc + i * 32 + p * 16) * 2);
+            // (the compiled code may rewrite v16's registers right after the store: padded)
+            buffer_store16_padded(v16, rg, voff, so);
           }
-          // lane L < 32: (its group 2p ids 0-3, lane L + 32's ids 4-7); lane L + 32: (lane L's
-          // group 2p + 1 ids 0-3, its own ids 4-7)
-          const auto sx = __builtin_amdgcn_permlane32_swap(pk[0].x, pk[1].x, false, false);
-          const auto sy = __builtin_amdgcn_permlane32_swap(pk[0].y, pk[1].y, false, false);
-          const i32x4_t v16 = {(int)sx[0], (int)sy[0], (int)sx[1], (int)sy[1]};
-          const uint32_t so = (uint32_t)((j * 32 * vc + i * 32 + p * 16) * 2);
-          __builtin_amdgcn_raw_buffer_store_b128(v16, rg, (int)voff, (int)so, 0);
-        }
-    }
+      }
+    };
+    if (n0 + TILE <= nv && vleft >= TM) store_tile(std::true_type{});
+    else store_tile(std::false_type{});
     return;
   } else if constexpr (kMode == P_WRITE || kMode == Q_SOFT) {
     // P[v][token] rows of this tile: lanes of a half-wave hold 32 consecutive tokens of one row
@@ -1400,26 +1416,34 @@ __device__ __forceinline__ void dw_tile(char* smem, int blk, const uint16_t* __r
   if constexpr (kMode != DW_ADAMW) {
     const __amdgpu_buffer_rsrc_t rw = make_rsrc(dW + r0 * d, (uint64_t)rows * d * 2);
     const uint32_t voff = (uint32_t)((lrow * d + dc) * 2);
+    // tiles with all their rows in the vocabulary and all columns inside D test nothing per element
+    auto store_tile = [&](auto kFull) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        if (!col_ok[j]) continue;
-        float old[16];
-        if constexpr (kMode == DW_ACCUMULATE) {
+        for (int j = 0; j < 2; ++j) {
+          if (!decltype(kFull)::value && !col_ok[j]) continue;
+          float old[16];
+          if constexpr (kMode == DW_ACCUMULATE) {
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+              const uint32_t so = (uint32_t)((erow(i, r) * d + j * 32) * 2);
+              old[r] = (decltype(kFull)::value || row_ok(i, r))
+                           ? bf16_to_f32(__builtin_amdgcn_raw_buffer_load_b16(rw, (int)voff, (int)so, 0))
+                           : 0.f;
+            }
+          }
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
             const uint32_t so = (uint32_t)((erow(i, r) * d + j * 32) * 2);
-            old[r] = row_ok(i, r) ? bf16_to_f32(__builtin_amdgcn_raw_buffer_load_b16(rw, (int)voff, (int)so, 0)) : 0.f;
+            const float x = kMode == DW_ACCUMULATE ? old[r] + acc[i][j][r] : acc[i][j][r];
+            if (decltype(kFull)::value || row_ok(i, r))
+              __builtin_amdgcn_raw_buffer_store_b16(to_bf16(x), rw, (int)voff, (int)so, 0);
           }
         }
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const uint32_t so = (uint32_t)((erow(i, r) * d + j * 32) * 2);
-          const float x = kMode == DW_ACCUMULATE ? old[r] + acc[i][j][r] : acc[i][j][r];
-          if (row_ok(i, r)) __builtin_amdgcn_raw_buffer_store_b16(to_bf16(x), rw, (int)voff, (int)so, 0);
-        }
-      }
+    };
+    if (!partial && d0 + TILE <= d) store_tile(std::true_type{});
+    else store_tile(std::false_type{});
   } else {
     // moments (and master) fp32 with row stride d, W bf16 with row stride ldw
     const __amdgpu_buffer_rsrc_t rm = make_rsrc(st.m + r0 * d, (uint64_t)rows * d * 4);
@@ -1531,28 +1555,40 @@ __device__ __forceinline__ void dh_tile(char* smem, int blk, int grid, const uin
   const int dc = d0 + wc * 64 + (lane & 31);
   const uint32_t voff = (uint32_t)(((wr * 128 + (lane >> 5) * 4) * d + dc) * 4);
   const bool col_ok[2] = {dc < d, dc + 32 < d};
+  // (a column past D would be the next row's: never touched; tiles of whole 256-column blocks
+  // test nothing per element, and the first slab's tiles read nothing)
+  auto rmw = [&](auto kFull, auto kAcc) {
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    float old[2][16];
+    for (int i = 0; i < 4; ++i) {
+      float old[2][16];
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+      for (int j = 0; j < 2; ++j)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const uint32_t so = (uint32_t)(((i * 32 + (r >> 2) * 8 + (r & 3)) * d + j * 32) * 4);
-        old[j][r] = (accumulate && col_ok[j])
-                        ? __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rd, (int)voff, (int)so, 0))
-                        : 0.f;
-      }
+        for (int r = 0; r < 16; ++r) {
+          const uint32_t so = (uint32_t)(((i * 32 + (r >> 2) * 8 + (r & 3)) * d + j * 32) * 4);
+          old[j][r] = (decltype(kAcc)::value && (decltype(kFull)::value || col_ok[j]))
+                          ? __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rd, (int)voff, (int)so, 0))
+                          : 0.f;
+        }
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      if (!col_ok[j]) continue;
+      for (int j = 0; j < 2; ++j) {
+        if (!decltype(kFull)::value && !col_ok[j]) continue;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const uint32_t so = (uint32_t)(((i * 32 + (r >> 2) * 8 + (r & 3)) * d + j * 32) * 4);
-        __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, old[j][r] + acc[i][j][r]), rd, (int)voff,
-                                              (int)so, 0);
+        for (int r = 0; r < 16; ++r) {
+          const uint32_t so = (uint32_t)(((i * 32 + (r >> 2) * 8 + (r & 3)) * d + j * 32) * 4);
+          __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, old[j][r] + acc[i][j][r]), rd,
+                                                (int)voff, (int)so, 0);
+        }
       }
     }
+  };
+  const bool full = d0 + TILE <= d;
+  if (accumulate) {
+    if (full) rmw(std::true_type{}, std::true_type{});
+    else rmw(std::false_type{}, std::true_type{});
+  } else {
+    if (full) rmw(std::true_type{}, std::false_type{});
+    else rmw(std::false_type{}, std::false_type{});
   }
 }
 
