@@ -132,14 +132,15 @@ lce_status_t lce_workspace_size(const lce_problem_t* p, size_t* fwd_bytes, size_
  * and inverse map pos ([npad] int32 each), the count Nv, and the gathered valid rows of H
  * ([npad][d] bf16). The forward then holds its vocabulary partial pairs (two [part_rows][npad]
  * fp32 arrays) and per-row terms ([npad] fp32); the backward holds G ([rows_g][vc] bf16, one
- * vocabulary slab of vc ids, nslab slabs) and the fp32 dH accumulator ([rows_g][d]), plus a
- * second one when the dH launches split K in two halves (dh_kz = 2; else o_dh32b = 0).
+ * vocabulary slab of vc ids, nslab slabs) and the fp32 dH accumulators: dh_kz of them, [rows_g][d]
+ * each, one after the other from o_dh32, when the dH launches split K into dh_kz parts (launches
+ * with fewer output tiles than compute units; o_dh32b is the second one's offset, or 0).
  */
 typedef struct lce_plan_info {
   int64_t npad;             /* N rounded up to 256 */
   int64_t rows_g;           /* npad rounded up to 384: rows of G and of the dH accumulators */
   int64_t vc, nslab;        /* backward slab width (ids) and slab count */
-  int64_t dh_kz;            /* 1, or 2 when the dH launches split K in two halves */
+  int64_t dh_kz;            /* K parts of the dH launches: 1, or up to 8 for launches with few tiles */
   int64_t part_rows;        /* partial rows of the forward statistics */
   int64_t fwd_gathers;      /* 1 if the forward leaves the gathered rows of H in the prefix */
   int64_t fwd_one_launch;   /* 1 if the forward statistics run as one launch */

@@ -1506,9 +1506,9 @@ __global__ __launch_bounds__(Geo<WM>::NT, WM) void k_bwd_dw(const uint16_t* __re
 
 // K6: dH32[m][dd] (+)= sum_k G[m][k] Ws[k][dd] over the slab's k < vs; rows m < Nv. Ws = W + v0 ldw
 // is the slab's first row, read K-major (transposing LDS reads); ws_rows = V - v0 rows follow.
-// kz = 2 splits K in two halves for launches with fewer output tiles than CUs: blocks of the
-// second half (the upper half of the grid) accumulate into a second buffer dH32b, which the
-// finalise adds in a fixed order.
+// kz > 1 splits K in kz parts for launches with fewer output tiles than CUs: the blocks of part z
+// (the z-th kz-th of the grid) accumulate into accumulator z, at dH32 + z (dH32b - dH32) (the
+// parts follow each other), and the finalise adds the kz accumulators in a fixed order.
 // One dH tile (block blk of a dH grid of `grid` blocks, smem the workgroup's LDS).
 template <int WM>
 __device__ __forceinline__ void dh_tile(char* smem, int blk, int grid, const uint16_t* __restrict__ G, int vc, int vs,
@@ -1545,7 +1545,7 @@ __device__ __forceinline__ void dh_tile(char* smem, int blk, int grid, const uin
 #pragma unroll
       for (int j = 0; j < 2; ++j) acc[i][j] = (f32x16_t){};
   }
-  if (z) dH32 = dH32b;
+  if (z) dH32 += (int64_t)z * (dH32b - dH32);
   // Read-modify-write of the fp32 accumulator through a buffer resource over this tile's valid
   // rows (rows past Nv read 0 and drop their stores): one 32-bit per-lane offset and a
   // wave-uniform row offset per element, so that only the accumulators occupy registers; one
@@ -1605,11 +1605,11 @@ __global__ __launch_bounds__(Geo<WM>::NT, WM) void k_bwd_dh(const uint16_t* __re
 }
 
 // K7: dH[row] = bf16(dH32[pos[row]]) for valid rows, +0.0 for the others. 8 elements per thread.
-__global__ __launch_bounds__(256) void k_dh_finalize(const float* __restrict__ dH32,
-                                                     const float* __restrict__ dH32b, const int* __restrict__ pos,
-                                                     int64_t n, int d, uint16_t* __restrict__ dH,
-                                                     float* __restrict__ dHf, int has_slabs) {
-  // dH32b (may be null): the second K half of split dH launches, added after dH32
+__global__ __launch_bounds__(256) void k_dh_finalize(const float* __restrict__ dH32, int64_t part, int kz,
+                                                     const int* __restrict__ pos, int64_t n, int d,
+                                                     uint16_t* __restrict__ dH, float* __restrict__ dHf,
+                                                     int has_slabs) {
+  // kz accumulators (the K parts of split dH launches), `part` elements apart, added in order
   const int64_t e = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 8;
   if (e >= n * d) return;
   const int64_t row = e / d;
@@ -1619,9 +1619,10 @@ __global__ __launch_bounds__(256) void k_dh_finalize(const float* __restrict__ d
   if (p >= 0 && has_slabs) {
     a = *reinterpret_cast<const float4*>(dH32 + (int64_t)p * d + col);
     b = *reinterpret_cast<const float4*>(dH32 + (int64_t)p * d + col + 4);
-    if (dH32b) {
-      const float4 a2 = *reinterpret_cast<const float4*>(dH32b + (int64_t)p * d + col);
-      const float4 b2 = *reinterpret_cast<const float4*>(dH32b + (int64_t)p * d + col + 4);
+    for (int z = 1; z < kz; ++z) {
+      const float* q = dH32 + z * part + (int64_t)p * d + col;
+      const float4 a2 = *reinterpret_cast<const float4*>(q);
+      const float4 b2 = *reinterpret_cast<const float4*>(q + 4);
       a = make_float4(a.x + a2.x, a.y + a2.y, a.z + a2.z, a.w + a2.w);
       b = make_float4(b.x + b2.x, b.y + b2.y, b.z + b2.z, b.w + b2.w);
     }
@@ -1736,8 +1737,8 @@ struct Plan {
   int64_t rows_g;                            // rows of G and dH32: Npad rounded up to a 384-row tile
   // workspace offsets; idx, pos, Nv and the gathered rows Hv form a prefix both passes share
   size_t o_idx, o_pos, o_nv, o_hv, o_pm, o_ps, o_terms, fwd_bytes;
-  size_t o_g, o_dh32, o_dh32b, bwd_bytes;    // o_dh32b: second K half of split dH (or 0)
-  int dh_kz;                                 // K halves of the dH launches (1 or 2)
+  size_t o_g, o_dh32, o_dh32b, bwd_bytes;    // o_dh32b: accumulator of the second K part (or 0)
+  int dh_kz;                                 // K parts of the dH launches (1 to 8)
   int part_rows;                             // partial rows of the forward statistics
 };
 
@@ -1822,12 +1823,13 @@ lce_status_t make_plan(const lce_problem_t* p, Plan* pl) {
   // the last token rows reach past Npad), so that no access leaves its region
   pl->rows_g = round_up(pl->npad, 384);
   pl->o_g = take(cur, 2 * (size_t)pl->rows_g * vc);
-  pl->o_dh32 = take(cur, 4 * (size_t)pl->rows_g * p->d);
-  // dH launches with fewer 384 x 256 output tiles than the 256 CUs split K in two halves, the
-  // second accumulated in a buffer of its own
+  // dH launches with fewer 384 x 256 output tiles than the 256 CUs split K into kz parts (enough
+  // to give every CU a block, at most 8), each accumulated in an accumulator of its own
   const int64_t dh_tiles = (pl->npad + 383) / 384 * ((p->d + TILE - 1) / TILE);
-  pl->dh_kz = dh_tiles < 256 ? 2 : 1;
-  pl->o_dh32b = pl->dh_kz > 1 ? take(cur, 4 * (size_t)pl->rows_g * p->d) : 0;
+  pl->dh_kz = (int)std::min<int64_t>(8, (256 + dh_tiles - 1) / dh_tiles);
+  const size_t part = 4 * (size_t)pl->rows_g * p->d;     // a multiple of 256 bytes
+  pl->o_dh32 = take(cur, part * pl->dh_kz);
+  pl->o_dh32b = pl->dh_kz > 1 ? pl->o_dh32 + part : 0;
   pl->bwd_bytes = cur;
   return LCE_OK;
 }
@@ -2060,7 +2062,7 @@ lce_status_t backward_impl(const lce_problem_t* p, const ShardInfo* shard, const
   uint16_t* hv = (uint16_t*)(ws + pl.o_hv);
   uint16_t* g = (uint16_t*)(ws + pl.o_g);
   float* dh32 = (float*)(ws + pl.o_dh32);
-  float* dh32b = pl.dh_kz > 1 ? (float*)(ws + pl.o_dh32b) : nullptr;
+  float* dh32b = pl.dh_kz > 1 ? (float*)(ws + pl.o_dh32b) : nullptr;   // accumulator of K part 1 (parts follow)
   const uint16_t* h = (const uint16_t*)H;
   const uint16_t* w = (const uint16_t*)W;
   const int d = (int)pl.d, npad = (int)pl.npad, vc = (int)pl.vc;
@@ -2140,7 +2142,7 @@ lce_status_t backward_impl(const lce_problem_t* p, const ShardInfo* shard, const
   }
   const int64_t nthr = pl.n * pl.d / 8;
   L(K_DH_FINAL, k_dh_finalize, dim3((unsigned)((nthr + 255) / 256)), dim3(256), (const float*)dh32,
-    (const float*)dh32b, (const int*)pos, pl.n, d, (uint16_t*)dH, dHf, 1);
+    (int64_t)pl.rows_g * d, pl.dh_kz, (const int*)pos, pl.n, d, (uint16_t*)dH, dHf, 1);
   return L.st;
 }
 

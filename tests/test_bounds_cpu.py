@@ -10,7 +10,7 @@ kernels' index expressions:
   the last vocabulary tile past V are loaded through the out-of-range offset (zeros, no address),
   so the W rows addressed are those below V;
 * K-major operands send the lanes whose columns lie past D (the hidden width) to the same offset;
-* dH runs K over the slab's vs ids (a ragged last slice masks the rest), in one or two halves;
+* dH runs K over the slab's vs ids (a ragged last slice masks the rest), split into 1 to 8 parts;
 * G and the dH accumulators hold rows_g rows, the 384-row tiles of the last token rows included;
 * the dW / AdamW epilogues touch only the rows of the slab that exist.
 
@@ -60,7 +60,7 @@ def walk(n, d, v, nv, ld_h=None, ld_w=None):
              "dH": 2 * n * d, "dW": 2 * v * d, "lse": 4 * n, "targets": 4 * n,
              "idx": 4 * npad, "pos": 4 * npad, "hv": 2 * npad * d,
              "pm": 4 * info["part_rows"] * npad, "ps": 4 * info["part_rows"] * npad, "terms": 4 * npad,
-             "G": 2 * rows_g * vc, "dh32": 4 * rows_g * d, "dh32b": 4 * rows_g * d if info["dh_kz"] > 1 else 0}
+             "G": 2 * rows_g * vc, "dh32": 4 * rows_g * d * info["dh_kz"]}
     twelve = d % 64 == 0
     tm_rows = 384 if twelve else 256          # vocabulary (A) rows of a forward / G tile
 
@@ -121,8 +121,8 @@ def walk(n, d, v, nv, ld_h=None, ld_w=None):
             k0 = z * kh
             kzn = min(vs - k0, kh)
             for m0 in range(0, nv, 384):
-                acc = "dh32" if z == 0 else "dh32b"
-                e.touch(acc, 4 * (m0 + 384) * d)                   # read-modify-write of the tile's rows
+                # read-modify-write of the tile's rows in accumulator z (the parts follow each other)
+                e.touch("dh32", 4 * (z * rows_g + m0 + 384) * d)
                 if kzn > 0:
                     e.touch("G", 2 * ((m0 + 383) * vc + k0 + kzn))
                     w_rows(v0 + k0, kzn)
@@ -161,9 +161,9 @@ def test_workspace_regions_are_disjoint_and_inside_the_workspace(n, d, v):
               ("hv", info["o_hv"], 2 * npad * d)]
     fwd = prefix + [("pm", info["o_pm"], 4 * info["part_rows"] * npad), ("ps", info["o_ps"], 4 * info["part_rows"] * npad),
                     ("terms", info["o_terms"], 4 * npad)]
-    bwd = prefix + [("G", info["o_g"], 2 * rows_g * vc), ("dh32", info["o_dh32"], 4 * rows_g * d)]
-    if info["dh_kz"] > 1:
-        bwd.append(("dh32b", info["o_dh32b"], 4 * rows_g * d))
+    bwd = prefix + [("G", info["o_g"], 2 * rows_g * vc), ("dh32", info["o_dh32"], 4 * rows_g * d * info["dh_kz"])]
+    assert 1 <= info["dh_kz"] <= 8
+    assert info["o_dh32b"] == (info["o_dh32"] + 4 * rows_g * d if info["dh_kz"] > 1 else 0)
     assert rows_g % 384 == 0 and rows_g >= npad and npad % 256 == 0 and npad >= n
     assert vc % 768 == 0
     for regions, total in ((fwd, info["fwd_bytes"]), (bwd, info["bwd_bytes"])):
@@ -193,7 +193,7 @@ def test_the_walk_flags_regions_sized_to_npad_rows():
     # the last token rows of the 8B head with every token valid reach past them
     e, sizes, info = walk(16384, 4096, 128256, 16384)
     assert info["rows_g"] > info["npad"]
-    for buf, row_bytes in (("G", 2 * info["vc"]), ("dh32", 4 * 4096)):
+    for buf, row_bytes in (("G", 2 * info["vc"]), ("dh32", 4 * 4096 * info["dh_kz"])):
         short = dict(sizes)
         short[buf] = info["npad"] * row_bytes
         with pytest.raises(AssertionError, match=buf):
