@@ -30,6 +30,12 @@ its MFMA work per step is 6 Nv V Dt + 10 Nv V Ds (teacher statistics and two
 probability passes; student statistics, Q pass, G recompute, dW and dH).
 ``kd_fused`` runs the same step as one lce_kd_forward_backward call: 4 Nv V Dt
 + 8 Nv V Ds (one teacher probability pass, one student pass for G and Q).
+
+Two diagnostics put the contractions' rate in context; neither is the benchmark:
+``--data zeros`` runs the same launches on all-zero H and W (the workload's targets and mask),
+so that the operands toggle no bits and the chip's power limit holds its clock near the maximum;
+``--gemm-reference`` times torch.matmul (the vendor BLAS) on the forward's logits product,
+[Nv, D] x [D, V] in bf16, with the workload's data, and prints its own JSON line instead.
 """
 from __future__ import annotations
 
@@ -114,6 +120,33 @@ def _copy_calibration(gib=1.0, reps=3):
     print(json.dumps({"copy_bytes_per_launch": n, "launches": reps}), flush=True)
 
 
+def _gemm_reference(args, wl, h, w, inp):
+    """torch.matmul of the valid rows of H by W^T ([Nv, D] x [D, V] -> [Nv, V] bf16): the forward's
+    logits product as one plain library GEMM, timed with HIP events over `steps` launches. It
+    materialises the logits, which the LCE path never does; it is a yardstick, not a step."""
+    import torch
+    valid = torch.from_numpy(np.flatnonzero(inp.targets != inp.ignore_index)).to(h.device)
+    hv = h.index_select(0, valid).contiguous()
+    out = torch.empty((hv.shape[0], w.shape[0]), dtype=torch.bfloat16, device=h.device)
+    for _ in range(args.warmup):
+        torch.matmul(hv, w.t(), out=out)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(args.steps):
+        torch.matmul(hv, w.t(), out=out)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    tflops = 2.0 * hv.shape[0] * wl.d * wl.v / (ms * 1e-3) / 1e12
+    print(json.dumps({"metric": "bf16 GEMM rate of torch.matmul on the forward logits product (context)",
+                      "value": tflops, "unit": "TFLOP/s", "frac": tflops / PEAK_BF16_TFLOPS, "ms": ms,
+                      "steps": args.steps, "warmup": args.warmup,
+                      "shape": {"m": int(hv.shape[0]), "n": wl.v, "k": wl.d},
+                      "data": "synthetic" if args.data == "random" else "synthetic, all-zero H and W",
+                      "config": {"workload": wl.name}}), flush=True)
+
+
 def _source_hash():
     import hashlib
     src = os.path.join(ROOT, "paper_2605_21442_amd", "csrc", "lce.hip")
@@ -166,6 +199,10 @@ def main():
     ap.add_argument("--variant", default="lce",
                     choices=("lce", "adamw_fused", "adamw_two_phase", "vocab_shard", "kd", "kd_fused"))
     ap.add_argument("--shards", type=int, default=8, help="vocabulary shards (vocab_shard variant)")
+    ap.add_argument("--data", default="random", choices=("random", "zeros"),
+                    help="zeros: all-zero H and W, a power diagnostic (not the benchmark)")
+    ap.add_argument("--gemm-reference", action="store_true",
+                    help="time only torch.matmul on the forward logits product, for context")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a 1 GiB device copy (for scaling HBM byte counters)")
     args = ap.parse_args()
@@ -197,7 +234,13 @@ def main():
     v_rows = (wl.v + args.shards - 1) // args.shards if sharded else wl.v
     w = torch.from_numpy(inp.w_bits[:v_rows].view(np.int16)).view(torch.bfloat16).to(dev)
     t = torch.from_numpy(inp.targets).to(dev)
+    if args.data == "zeros":
+        h.zero_()
+        w.zero_()
     n, d, v = wl.n, wl.d, wl.v
+    if args.gemm_reference:
+        _gemm_reference(args, wl, h, w, inp)
+        return
     v_total = v
     if sharded:
         v = v_rows
@@ -329,7 +372,7 @@ def main():
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16",
-        "data": "synthetic",
+        "data": "synthetic" if args.data == "random" else "synthetic, all-zero H and W (power diagnostic)",
         "config": {"workload": wl.name, "n_tokens": n, "hidden": d, "vocab": v, "n_valid": nvalid,
                    "global_batch": wl.batch, "seq_len": wl.seq_len, "parallelism": "none",
                    "reduction": "mean", "ignore_index": inp.ignore_index, "variant": args.variant,
@@ -350,7 +393,7 @@ def main():
         "kernel_timing": f"second pass of {kpass} steps after the timed region, HIP events around each launch",
         "lce_hip_sha256": _source_hash(),
     }
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and args.data == "random":
         print("[bench] timing the CPU oracle on a token sample ...", file=sys.stderr, flush=True)
         out["cpu_baseline"] = _cpu_baseline(inp)
         out["host"] = _host_info()
