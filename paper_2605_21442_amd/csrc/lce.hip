@@ -133,9 +133,11 @@ __device__ __forceinline__ void buffer_store16_padded(i32x4_t v, const i32x4_t& 
 
 __device__ __forceinline__ float bf16_to_f32(uint32_t bits16) { return __uint_as_float(bits16 << 16); }
 
+// two floats rounded to nearest-even bf16 in one packed conversion (lo in the low half)
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  __bf16 a = (__bf16)lo, b = (__bf16)hi;
-  return (uint32_t)__builtin_bit_cast(uint16_t, a) | ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
+  typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+  typedef float f32x2_t __attribute__((ext_vector_type(2)));
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){lo, hi}, bf16x2_t));
 }
 
 __device__ __forceinline__ uint16_t to_bf16(float x) { return __builtin_bit_cast(uint16_t, (__bf16)x); }
@@ -1230,6 +1232,10 @@ __global__ __launch_bounds__(Geo<WM>::NT, WM) void k_bwd_g(const uint16_t* __res
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
         const bool tok_ok = tok[j] < nv;
+        // the lane's element (i, q, e) is the target's when dt == 32 i + 8 q + e: one compare
+        // with a constant per element, and the one-hot term folded into the scaling fma
+        const int dt = tgt[j] - vb;
+        const float nc = -cj[j];
 #pragma unroll
         for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -1241,10 +1247,10 @@ __global__ __launch_bounds__(Geo<WM>::NT, WM) void k_bwd_g(const uint16_t* __res
               float gq[4];
 #pragma unroll
               for (int e = 0; e < 4; ++e) {
-                const int vr = vb + i * 32 + q * 8 + e;
-                float g = cj[j] * __builtin_amdgcn_exp2f(fmaf(acc[i][j][q * 4 + e], scale2, -l2[j]));
-                g = vr == tgt[j] ? g - cj[j] : g;
-                if constexpr (!decltype(kFull)::value) g = (tok_ok && vr < vleft) ? g : 0.f;
+                const int k = i * 32 + q * 8 + e;
+                const float ex = __builtin_amdgcn_exp2f(fmaf(acc[i][j][q * 4 + e], scale2, -l2[j]));
+                float g = fmaf(cj[j], ex, dt == k ? nc : 0.f);
+                if constexpr (!decltype(kFull)::value) g = (tok_ok && vb + k < vleft) ? g : 0.f;
                 gq[e] = g;
               }
               pk[h].x = pack_bf16x2(gq[0], gq[1]);
@@ -1677,7 +1683,7 @@ __global__ __launch_bounds__(256) void k_adamw(int64_t v, int d, const uint16_t*
     }
 #pragma unroll
     for (int e = 0; e < 4; ++e)
-      wout[e] = (uint32_t)to_bf16(p[2 * e]) | ((uint32_t)to_bf16(p[2 * e + 1]) << 16);
+      wout[e] = pack_bf16x2(p[2 * e], p[2 * e + 1]);
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       *reinterpret_cast<float4*>(st.m + o + 4 * h) = make_float4(mo[4 * h], mo[4 * h + 1], mo[4 * h + 2], mo[4 * h + 3]);
