@@ -5,6 +5,11 @@ handle) to the library and turns a non-zero status into ``LceError``. Nothing
 is computed in Python. The library is loaded on first use from this package's
 directory; if it was not built, loading raises instead of falling back to
 anything else.
+
+The pointers and streams come from PyTorch, whose wheel carries its own HIP runtime. torch is
+imported before the library is loaded, so that the library's HIP runtime dependency resolves to
+that same, already loaded runtime: loaded first, the library would bring the system's runtime
+into the process beside torch's, and its launches would then find no device.
 """
 from __future__ import annotations
 
@@ -111,6 +116,7 @@ def load() -> ctypes.CDLL:
         if not os.path.exists(LIB_PATH):
             raise RuntimeError(f"{LIB_PATH} is not built; run `python -c 'import __graft_entry__ as g; "
                                f"g.build()'` from the repository root")
+        import torch  # noqa: F401  (its HIP runtime first: see the module docstring)
         lib = ctypes.CDLL(LIB_PATH)
         P = ctypes.POINTER(LceProblem)
         vp, sz = ctypes.c_void_p, ctypes.c_size_t

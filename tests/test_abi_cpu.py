@@ -293,3 +293,20 @@ def test_noalloc_forward_rejects_problems_beyond_its_array_before_any_launch():
     with pytest.raises(B.LceError) as e:
         B.lce_forward_noalloc(B.problem(4, 60, 10), _fake(), _fake(), _fake(), _fake(), _fake(), _fake(), 0, 0)
     assert e.value.code == B.LCE_ERR_UNSUPPORTED
+
+
+def test_loading_the_library_first_keeps_one_hip_runtime_in_the_process():
+    # torch carries its own HIP runtime; the library must bind to it even when it is loaded before
+    # torch is imported (two runtimes in one process leave the library's launches without a device)
+    import subprocess
+    import sys
+    code = ("import sys; sys.path.insert(0, %r)\n"
+            "from paper_2605_21442_amd import binding as B\n"
+            "B.load()\n"
+            "import torch\n"
+            "maps = open('/proc/self/maps').read()\n"
+            "print(sorted({l.split()[-1] for l in maps.splitlines() if 'libamdhip64' in l}))\n") % ROOT
+    r = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, timeout=300)
+    assert r.returncode == 0, r.stderr[-2000:]
+    libs = eval(r.stdout.strip().splitlines()[-1])
+    assert len(libs) == 1, libs
