@@ -1113,6 +1113,48 @@ __device__ __forceinline__ bool band_tile(int blk, int tm_live, int tn_count, in
   return true;
 }
 
+// dH launches whose K the host did not split. With T = tm_live x dt live output tiles (tm_live =
+// ceil(Nv / 384) row tiles of 384 tokens, dt column tiles of 256), XCD x takes the tiles [c0(x),
+// c0(x + 1)) of a balanced cut, c0(x) = floor(x T / 8), in an order that keeps consecutive tiles on
+// few operand tiles: bands of 4 row tiles, each walked column by column. An XCD runs its ~32
+// resident workgroups in rounds; the n_tail tiles of its last, partial round are split along K
+// into dh_tail_parts(n_tail) parts, so that they fill that round instead of leaving most of its
+// CUs idle. Part 0 of a tile accumulates into the tile's rows of the accumulator (row stride D);
+// part z >= 1 of tail tile t into slot dh_slot0(x) + (z - 1) * n_tail + t, a 384 x 256 fp32 block
+// (row stride 256) in the accumulator's rows at or past tm_live * 384, which hold no valid token.
+// When those rows cannot hold every slot, no tile is split. The finalise adds the parts in order.
+constexpr int kDhBand = 4;                       // row tiles per band
+constexpr int64_t kDhSlot = 384 * 256;           // floats per slot
+__device__ __forceinline__ int dh_c0(int x, int t) { return (int)(((int64_t)x * t) >> 3); }
+__device__ __forceinline__ int dh_tail_parts(int n_tail) {
+  return n_tail > 0 && n_tail <= 16 ? (32 / n_tail < 8 ? 32 / n_tail : 8) : 1;
+}
+// slots taken by the XCDs before x (the slots are numbered XCD by XCD, each XCD's in part-major
+// order); dh_slot0(8, t) is the total
+__device__ __forceinline__ int dh_slot0(int x, int t) {
+  int n = 0;
+  for (int y = 0; y < x; ++y) {
+    const int nt = (dh_c0(y + 1, t) - dh_c0(y, t)) & 31;
+    n += (dh_tail_parts(nt) - 1) * nt;
+  }
+  return n;
+}
+__device__ __forceinline__ bool dh_tail_fits(int t, int tm_live, int d, int acc_rows) {
+  return (int64_t)dh_slot0(8, t) * kDhSlot <= (int64_t)(acc_rows - tm_live * 384) * d;
+}
+__device__ __forceinline__ void dh_band_tile(int l, int tm_live, int dt, int& tm, int& tn) {
+  const int band = l / (kDhBand * dt), r0 = band * kDhBand;
+  const int rows = tm_live - r0 < kDhBand ? tm_live - r0 : kDhBand;
+  const int k = l - band * kDhBand * dt;
+  tm = r0 + k % rows;
+  tn = k / rows;
+}
+__device__ __forceinline__ int dh_band_index(int tm, int tn, int tm_live, int dt) {
+  const int band = tm / kDhBand, r0 = band * kDhBand;
+  const int rows = tm_live - r0 < kDhBand ? tm_live - r0 : kDhBand;
+  return band * kDhBand * dt + tn * rows + (tm - r0);
+}
+
 // scale c = g / n_norm (mean) or g (sum), 0 when the count is 0; for NONE the caller reads
 // the per-token gradient instead
 __device__ __forceinline__ float grad_scale(const float* grad, const int* n_norm, int reduction) {
@@ -1520,20 +1562,61 @@ template <int WM>
 __device__ __forceinline__ void dh_tile(char* smem, int blk, int grid, const uint16_t* __restrict__ G, int vc, int vs,
                                         const uint16_t* __restrict__ Ws, int64_t ldw, int64_t ws_rows, int d,
                                         const int* __restrict__ nv_ptr, float* __restrict__ dH32, int accumulate,
-                                        int kz, float* __restrict__ dH32b) {
+                                        int kz, float* __restrict__ dH32b, int acc_rows) {
+  static_assert(Geo<WM>::TM == 384, "the tail slots and the finalise assume 384-row tiles");
   constexpr int TM = Geo<WM>::TM;
   const int nv = *nv_ptr;
-  const int g1 = grid / kz;
-  const int z = blk / g1;
-  int tm, tn;
-  if (!band_tile(blk - z * g1, (nv + TM - 1) / TM, (d + TILE - 1) / TILE, tm, tn)) return;
+  const int dt = (d + TILE - 1) / TILE, tm_live = (nv + TM - 1) / TM;
+  // this block's tile, K part z of kzl, and the fp32 block it accumulates into (tile origin,
+  // row stride, column of the tile's first column)
+  int tm, tn, z, kzl;
+  float* acc_tile;
+  int ldacc, cb;
+  if (kz > 1) {
+    // the host split every tile's K into kz parts (launches with fewer tiles than CUs)
+    const int g1 = grid / kz;
+    z = blk / g1;
+    kzl = kz;
+    if (!band_tile(blk - z * g1, tm_live, dt, tm, tn)) return;
+    acc_tile = (z ? dH32 + (int64_t)z * (dH32b - dH32) : dH32) + (int64_t)tm * TM * d;
+    ldacc = d;
+    cb = tn * TILE;
+  } else {
+    const int t = tm_live * dt, x = blk & 7, k = blk >> 3;
+    const int c0 = dh_c0(x, t), n = dh_c0(x + 1, t) - c0, nmain = n & ~31, nt = n - nmain;
+    const int kzt = dh_tail_fits(t, tm_live, d, acc_rows) ? dh_tail_parts(nt) : 1;
+    int l, slot = 0;
+    if (k < nmain) {
+      l = c0 + k;
+      z = 0;
+      kzl = 1;
+    } else {
+      const int j = k - nmain;
+      if (j >= kzt * nt) return;
+      const int ti = j % nt;
+      z = j / nt;
+      kzl = kzt;
+      l = c0 + nmain + ti;
+      slot = dh_slot0(x, t) + (z - 1) * nt + ti;
+    }
+    dh_band_tile(l, tm_live, dt, tm, tn);
+    if (z == 0) {
+      acc_tile = dH32 + (int64_t)tm * TM * d;
+      ldacc = d;
+      cb = tn * TILE;
+    } else {
+      acc_tile = dH32 + (int64_t)tm_live * TM * d + (int64_t)slot * kDhSlot;
+      ldacc = TILE;
+      cb = 0;
+    }
+  }
   const int m0 = tm * TM, d0 = tn * TILE;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, wr = wave >> 2, wc = wave & 3;
   // K = the slab's vs ids; the last slice of a slab whose width is not a multiple of 64 is masked
   // (lanes past K load zeros), so no W row past the vocabulary is addressed. Half z covers
   // [k0, k0 + kzn), the first half a whole number of 64-wide slices.
   const int kt = (vs + KSLICE - 1) / KSLICE * KSLICE;
-  const int kh = ((kt + kz - 1) / kz + KSLICE - 1) / KSLICE * KSLICE;
+  const int kh = ((kt + kzl - 1) / kzl + KSLICE - 1) / KSLICE * KSLICE;
   const int k0 = z * kh;
   const int kzn = vs - k0 < kh ? vs - k0 : kh;
   f32x16_t acc[4][2];
@@ -1551,15 +1634,14 @@ __device__ __forceinline__ void dh_tile(char* smem, int blk, int grid, const uin
 #pragma unroll
       for (int j = 0; j < 2; ++j) acc[i][j] = (f32x16_t){};
   }
-  if (z) dH32 += (int64_t)z * (dH32b - dH32);
-  // Read-modify-write of the fp32 accumulator through a buffer resource over this tile's valid
-  // rows (rows past Nv read 0 and drop their stores): one 32-bit per-lane offset and a
+  // Read-modify-write of the fp32 accumulator block through a buffer resource over this tile's
+  // valid rows (rows past Nv read 0 and drop their stores): one 32-bit per-lane offset and a
   // wave-uniform row offset per element, so that only the accumulators occupy registers; one
   // 32-row block (32 values per lane) at a time, its loads in flight together.
   const int rows = nv - m0 < TM ? nv - m0 : TM;
-  const __amdgpu_buffer_rsrc_t rd = make_rsrc(dH32 + (int64_t)m0 * d, (uint64_t)rows * d * 4);
-  const int dc = d0 + wc * 64 + (lane & 31);
-  const uint32_t voff = (uint32_t)(((wr * 128 + (lane >> 5) * 4) * d + dc) * 4);
+  const __amdgpu_buffer_rsrc_t rd = make_rsrc(acc_tile, (uint64_t)rows * ldacc * 4);
+  const int dc = d0 + wc * 64 + (lane & 31);      // column of dH (validity)
+  const uint32_t voff = (uint32_t)(((wr * 128 + (lane >> 5) * 4) * ldacc + cb + wc * 64 + (lane & 31)) * 4);
   const bool col_ok[2] = {dc < d, dc + 32 < d};
   // (a column past D would be the next row's: never touched; tiles of whole 256-column blocks
   // test nothing per element, and the first slab's tiles read nothing)
@@ -1571,7 +1653,7 @@ __device__ __forceinline__ void dh_tile(char* smem, int blk, int grid, const uin
       for (int j = 0; j < 2; ++j)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const uint32_t so = (uint32_t)(((i * 32 + (r >> 2) * 8 + (r & 3)) * d + j * 32) * 4);
+          const uint32_t so = (uint32_t)(((i * 32 + (r >> 2) * 8 + (r & 3)) * ldacc + j * 32) * 4);
           old[j][r] = (decltype(kAcc)::value && (decltype(kFull)::value || col_ok[j]))
                           ? __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rd, (int)voff, (int)so, 0))
                           : 0.f;
@@ -1581,7 +1663,7 @@ __device__ __forceinline__ void dh_tile(char* smem, int blk, int grid, const uin
         if (!decltype(kFull)::value && !col_ok[j]) continue;
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const uint32_t so = (uint32_t)(((i * 32 + (r >> 2) * 8 + (r & 3)) * d + j * 32) * 4);
+          const uint32_t so = (uint32_t)(((i * 32 + (r >> 2) * 8 + (r & 3)) * ldacc + j * 32) * 4);
           __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, old[j][r] + acc[i][j][r]), rd,
                                                 (int)voff, (int)so, 0);
         }
@@ -1604,33 +1686,50 @@ __global__ __launch_bounds__(Geo<WM>::NT, WM) void k_bwd_dh(const uint16_t* __re
                                                         int64_t ws_rows, int d,
                                                         const int* __restrict__ nv_ptr,
                                                         float* __restrict__ dH32, int accumulate, int kz,
-                                                        float* __restrict__ dH32b) {
+                                                        float* __restrict__ dH32b, int acc_rows) {
   __shared__ __attribute__((aligned(16))) char smem[Geo<WM>::LDS];
   dh_tile<WM>(smem, (int)blockIdx.x, (int)gridDim.x, G, vc, vs, Ws, ldw, ws_rows, d, nv_ptr, dH32, accumulate, kz,
-              dH32b);
+              dH32b, acc_rows);
 }
 
 // K7: dH[row] = bf16(dH32[pos[row]]) for valid rows, +0.0 for the others. 8 elements per thread.
 __global__ __launch_bounds__(256) void k_dh_finalize(const float* __restrict__ dH32, int64_t part, int kz,
                                                      const int* __restrict__ pos, int64_t n, int d,
                                                      uint16_t* __restrict__ dH, float* __restrict__ dHf,
-                                                     int has_slabs) {
-  // kz accumulators (the K parts of split dH launches), `part` elements apart, added in order
+                                                     int has_slabs, const int* __restrict__ nv_ptr, int acc_rows) {
+  // kz accumulators (the K parts of split dH launches), `part` elements apart, added in order;
+  // with kz = 1, the slots of the tail tiles' K parts z = 1, 2, ... after part 0 (dh_tile)
   const int64_t e = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 8;
   if (e >= n * d) return;
   const int64_t row = e / d;
   const int col = (int)(e - row * d);
   const int p = pos[row];
   float4 a = make_float4(0.f, 0.f, 0.f, 0.f), b = a;
+  auto add = [&](const float* q) {
+    const float4 a2 = *reinterpret_cast<const float4*>(q);
+    const float4 b2 = *reinterpret_cast<const float4*>(q + 4);
+    a = make_float4(a.x + a2.x, a.y + a2.y, a.z + a2.z, a.w + a2.w);
+    b = make_float4(b.x + b2.x, b.y + b2.y, b.z + b2.z, b.w + b2.w);
+  };
   if (p >= 0 && has_slabs) {
     a = *reinterpret_cast<const float4*>(dH32 + (int64_t)p * d + col);
     b = *reinterpret_cast<const float4*>(dH32 + (int64_t)p * d + col + 4);
-    for (int z = 1; z < kz; ++z) {
-      const float* q = dH32 + z * part + (int64_t)p * d + col;
-      const float4 a2 = *reinterpret_cast<const float4*>(q);
-      const float4 b2 = *reinterpret_cast<const float4*>(q + 4);
-      a = make_float4(a.x + a2.x, a.y + a2.y, a.z + a2.z, a.w + a2.w);
-      b = make_float4(b.x + b2.x, b.y + b2.y, b.z + b2.z, b.w + b2.w);
+    for (int z = 1; z < kz; ++z) add(dH32 + z * part + (int64_t)p * d + col);
+    if (kz == 1) {
+      const int nv = *nv_ptr;
+      const int tm_live = (nv + 383) / 384, dt = (d + TILE - 1) / TILE, t = tm_live * dt;
+      if (dh_tail_fits(t, tm_live, d, acc_rows)) {
+        const int tm = p / 384, tn = col / TILE;
+        const int l = dh_band_index(tm, tn, tm_live, dt);
+        int x = 0;
+        while (x < 7 && dh_c0(x + 1, t) <= l) ++x;
+        const int c0 = dh_c0(x, t), nmain = (dh_c0(x + 1, t) - c0) & ~31, nt = dh_c0(x + 1, t) - c0 - nmain;
+        if (l - c0 >= nmain) {
+          const int kzt = dh_tail_parts(nt), s0 = dh_slot0(x, t) + (l - c0 - nmain);
+          const float* q = dH32 + (int64_t)tm_live * 384 * d + (int64_t)(p - tm * 384) * TILE + (col - tn * TILE);
+          for (int z = 1; z < kzt; ++z) add(q + (int64_t)(s0 + (z - 1) * nt) * kDhSlot);
+        }
+      }
     }
   }
   if (dHf) {   // fp32 rows (a vocabulary shard's term of dH, to be summed over shards)
@@ -1883,6 +1982,9 @@ struct Launcher {
       }
     }
     if (slot >= 0 && hipEventRecord(g_timing.ev[2 * slot], s) != hipSuccess) { st = LCE_ERR_HIP; return; }
+    // the thread's last-error slot may hold an earlier call's status (for instance hipErrorNotReady
+    // from another library's event query): clear it, so that only this launch's status is read
+    (void)hipGetLastError();
     hipLaunchKernelGGL(kern, grid, block, 0, s, static_cast<KArgs>(args)...);
     if (hipGetLastError() != hipSuccess) { st = LCE_ERR_HIP; return; }
     if (slot >= 0 && hipEventRecord(g_timing.ev[2 * slot + 1], s) != hipSuccess) st = LCE_ERR_HIP;
@@ -2136,19 +2238,22 @@ lce_status_t backward_impl(const lce_problem_t* p, const ShardInfo* shard, const
           (int64_t)0, tm);
       }
     }
-    const unsigned bdh = (unsigned)(pl.dh_kz * 8 * ((dh_tiles + 7) / 8) * dt);
+    // split launches: kz copies of the banded grid; otherwise 8 XCDs x 32 CUs x (whole rounds of the
+    // largest per-XCD share + one round for the split tail)
+    const unsigned bdh = pl.dh_kz > 1 ? (unsigned)(pl.dh_kz * 8 * ((dh_tiles + 7) / 8) * dt)
+                                      : (unsigned)(256 * (((int64_t)dh_tiles * dt + 7) / 8 / 32 + 1));
     const int tmw = (vs + Geo<kDwWM>::TM - 1) / Geo<kDwWM>::TM;
     const unsigned bdw = (unsigned)(8 * ((tmw + 7) / 8) * dt);
     // dH reads the slab's W rows before the dW launch, whose AdamW epilogue (in-backward step)
     // may update them; later slabs read only their own rows
     L(K_BWD_DH, k_bwd_dh<kDhWM>, dim3(bdh), dim3(Geo<kDhWM>::NT), (const uint16_t*)g, vc, vs, w + v0 * pl.ldw, pl.ldw,
-      pl.v - v0, d, (const int*)nv, dh32, (int)(s > 0), pl.dh_kz, dh32b);
+      pl.v - v0, d, (const int*)nv, dh32, (int)(s > 0), pl.dh_kz, dh32b, (int)pl.rows_g);
     L(K_BWD_DW, dw_kernel, dim3(bdw), dim3(Geo<kDwWM>::NT), (const uint16_t*)g, vc, npad, vs, (const uint16_t*)hv, d,
       (const int*)nv, tmw, dW, v0, as, c);
   }
   const int64_t nthr = pl.n * pl.d / 8;
   L(K_DH_FINAL, k_dh_finalize, dim3((unsigned)((nthr + 255) / 256)), dim3(256), (const float*)dh32,
-    (int64_t)pl.rows_g * d, pl.dh_kz, (const int*)pos, pl.n, d, (uint16_t*)dH, dHf, 1);
+    (int64_t)pl.rows_g * d, pl.dh_kz, (const int*)pos, pl.n, d, (uint16_t*)dH, dHf, 1, (const int*)nv, (int)pl.rows_g);
   return L.st;
 }
 

@@ -48,6 +48,38 @@ class Extents:
             assert end <= sizes[buf], f"{where}: {buf} reaches byte {end} of {sizes[buf]}"
 
 
+def dh_tail_parts(nv, d, acc_rows):
+    """The K parts z >= 1 of the tail tiles of a dH launch the host did not split, as the kernel
+    assigns them: (xcd, first row of the tile, z, parts of the tile, slot)."""
+    tm_live, dtc = cdiv(nv, 384), cdiv(d, 256)
+    t = tm_live * dtc
+
+    def c0(x):
+        return (x * t) >> 3
+
+    def parts(nt):
+        return min(8, 32 // nt) if 0 < nt <= 16 else 1
+
+    tails = [(c0(x + 1) - c0(x)) & 31 for x in range(8)]
+    if sum((parts(nt) - 1) * nt for nt in tails) * 384 * 256 > (acc_rows - tm_live * 384) * d:
+        return []
+    out, slot0 = [], 0
+    for x in range(8):
+        n = c0(x + 1) - c0(x)
+        nmain, nt = n & ~31, n & 31
+        kz = parts(nt)
+        for z in range(1, kz):
+            for ti in range(nt):
+                l = c0(x) + nmain + ti
+                band, = divmod(l, 4 * dtc)[:1]
+                r0 = band * 4
+                rows = min(4, tm_live - r0)
+                tm = r0 + (l - band * 4 * dtc) % rows
+                out.append((x, tm * 384, z, kz, slot0 + (z - 1) * nt + ti))
+        slot0 += (kz - 1) * nt
+    return out
+
+
 def walk(n, d, v, nv, ld_h=None, ld_w=None):
     """Extents of one lce_forward + lce_backward of an [n, d] x [v, d] problem with nv valid rows."""
     ld_h = ld_h or d
@@ -116,16 +148,29 @@ def walk(n, d, v, nv, ld_h=None, ld_w=None):
                 e.touch("G", 2 * ((n0 + 255) * vc + vt0 + tm_rows))
         # dH: 384-row tiles of G rows, K over [k0, k0 + kzn), W slab rows v0 + k (< v0 + vs), columns < d
         kt = rup(vs, 64)
-        kh = rup(cdiv(kt, dh_kz), 64)
-        for z in range(dh_kz):
+
+        def dh_part(m0, z, kz, acc_end):
+            kh = rup(cdiv(kt, kz), 64)
             k0 = z * kh
             kzn = min(vs - k0, kh)
+            e.touch("dh32", acc_end)            # read-modify-write of the part's accumulator block
+            if kzn > 0:
+                e.touch("G", 2 * ((m0 + 383) * vc + k0 + kzn))
+                w_rows(v0 + k0, kzn)
+
+        if dh_kz > 1:
+            for z in range(dh_kz):
+                for m0 in range(0, nv, 384):
+                    # the tile's rows in accumulator z (the parts follow each other)
+                    dh_part(m0, z, dh_kz, 4 * (z * rows_g + m0 + 384) * d)
+        else:
+            # device-side split of each XCD's last partial round (dh_tile): part 0 in the tile's rows,
+            # parts z >= 1 in 384 x 256 slots after row tm_live * 384
+            tm_live, dtc = cdiv(nv, 384), cdiv(d, 256)
             for m0 in range(0, nv, 384):
-                # read-modify-write of the tile's rows in accumulator z (the parts follow each other)
-                e.touch("dh32", 4 * (z * rows_g + m0 + 384) * d)
-                if kzn > 0:
-                    e.touch("G", 2 * ((m0 + 383) * vc + k0 + kzn))
-                    w_rows(v0 + k0, kzn)
+                dh_part(m0, 0, 1, 4 * (m0 + 384) * d)
+            for x, m0, z, kz, slot in dh_tail_parts(nv, d, rows_g):
+                dh_part(m0, z, kz, 4 * (tm_live * 384 * d + (slot + 1) * 384 * 256))
         # dW: G and Hv read K-major over round_up(Nv, 64) token rows; dW rows of the slab only
         kpad = rup(nv, 64)
         for m0 in range(0, vs, 384):
@@ -198,3 +243,38 @@ def test_the_walk_flags_regions_sized_to_npad_rows():
         short[buf] = info["npad"] * row_bytes
         with pytest.raises(AssertionError, match=buf):
             e.check(short, "npad rows")
+
+
+@pytest.mark.parametrize("n,d,v,nv", [(12288, 2048, 1000, 300), (12288, 2048, 1000, 1400), (12288, 2048, 1000, 3686),
+                                      (12288, 2048, 1000, 4423), (8192, 4096, 1000, 6209),
+                                      (32768, 3584, 152064, 22936), (16384, 8192, 128256, 13107)])
+def test_split_dh_tails_stay_inside_the_accumulator(n, d, v, nv):
+    # the shapes whose dH tails the kernel splits on the device (and one whose tails do not fit)
+    e, sizes, info = walk(n, d, v, nv)
+    e.check(sizes, f"n={n} d={d} v={v} nv={nv}")
+    parts = dh_tail_parts(nv, d, info["rows_g"])
+    slots = sorted(p[4] for p in parts)
+    assert slots == list(range(len(slots)))            # numbered densely, each once
+    tm_live = cdiv(nv, 384)
+    assert len(slots) * 384 * 256 <= (info["rows_g"] - tm_live * 384) * d
+
+
+@pytest.mark.parametrize("nv,d", [(300, 2048), (3686, 2048), (22936, 3584), (13107, 8192), (12288, 4096), (1, 64)])
+def test_split_dh_blocks_cover_every_tile_and_k_part_once(nv, d):
+    # the blocks of a launch the host did not split, as dh_tile maps them: every live tile once,
+    # with parts 0 .. kz - 1 of one kz
+    tm_live, dtc = cdiv(nv, 384), cdiv(d, 256)
+    t = tm_live * dtc
+    rows_g = rup(rup(max(nv, 1), 256), 384) + 384 * 64
+    tails = {(p[1] // 384, p[2]): p[3] for p in dh_tail_parts(nv, d, rows_g)}
+    seen = {}
+    for x in range(8):
+        c0, c1 = (x * t) >> 3, ((x + 1) * t) >> 3
+        for l in range(c0, c1):
+            band = l // (4 * dtc)
+            rows = min(4, tm_live - band * 4)
+            k = l - band * 4 * dtc
+            seen.setdefault((band * 4 + k % rows, k // rows), set()).add(0)
+    assert sorted(seen) == sorted((tm, tn) for tm in range(tm_live) for tn in range(dtc))
+    for (tm, z), kz in tails.items():
+        assert 1 <= z < kz <= 8
