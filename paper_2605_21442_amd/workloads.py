@@ -98,26 +98,40 @@ def _rng(seed: int, case: int, stream: int) -> np.random.Generator:
     return np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, case, stream])))
 
 
-def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
-    """Round float32 values to bfloat16 (nearest, ties to even); returns uint16 bit patterns."""
+_SLAB = 1 << 22
+
+
+def f32_to_bf16_bits(x: np.ndarray, scale: Optional[float] = None) -> np.ndarray:
+    """Round float32 values (times ``scale`` in float32, if given) to bfloat16 (nearest, ties to
+    even); returns uint16 bit patterns."""
     x = np.ascontiguousarray(x, dtype=np.float32)
-    u = x.view(np.uint32)
-    out = np.empty(u.shape, dtype=np.uint16)
-    # process in slabs to bound the temporaries for billion-element weights; 32-bit arithmetic
-    # wraps only for NaN patterns, which are replaced (quiet NaN with the payload's top bits)
-    flat_u, flat_o = u.reshape(-1), out.reshape(-1)
-    step = 1 << 24
-    for s in range(0, flat_u.size, step):
-        b = flat_u[s:s + step]
-        r = b >> 16
-        r &= 1
-        r += b
-        r += 0x7FFF
-        r >>= 16
-        nan = (b & 0x7FFFFFFF) > 0x7F800000
+    out = np.empty(x.shape, dtype=np.uint16)
+    # in slabs through temporaries allocated once (fresh large allocations cost a page fault per
+    # page, which dominates for billion-element weights); 32-bit arithmetic wraps only for NaN
+    # patterns, which are replaced (quiet NaN with the payload's top bits)
+    flat_x, flat_o = x.reshape(-1), out.reshape(-1)
+    m = min(_SLAB, flat_x.size)
+    f = np.empty(m, dtype=np.float32)
+    r = np.empty(m, dtype=np.uint32)
+    t = np.empty(m, dtype=np.uint32)
+    for s in range(0, flat_x.size, _SLAB):
+        k = min(_SLAB, flat_x.size - s)
+        fb, rb, tb = f[:k], r[:k], t[:k]
+        if scale is None:
+            fb[...] = flat_x[s:s + k]
+        else:
+            np.multiply(flat_x[s:s + k], np.float32(scale), out=fb)
+        b = fb.view(np.uint32)
+        np.right_shift(b, 16, out=rb)
+        np.bitwise_and(rb, 1, out=rb)
+        np.add(rb, b, out=rb)
+        np.add(rb, 0x7FFF, out=rb)
+        np.right_shift(rb, 16, out=rb)
+        np.bitwise_and(b, 0x7FFFFFFF, out=tb)
+        nan = tb > 0x7F800000
         if nan.any():
-            r[nan] = (b[nan] >> 16) | 0x40
-        flat_o[s:s + step] = r
+            rb[nan] = (b[nan] >> 16) | 0x40
+        flat_o[s:s + k] = rb
     return out
 
 
@@ -128,9 +142,7 @@ def bf16_bits_to_f32(bits: np.ndarray) -> np.ndarray:
 
 def draw_normal_bf16(rng: np.random.Generator, shape, sigma: float) -> np.ndarray:
     x = rng.standard_normal(shape, dtype=np.float32)
-    if sigma != 1.0:
-        x *= np.float32(sigma)
-    return f32_to_bf16_bits(x)
+    return f32_to_bf16_bits(x, None if sigma == 1.0 else sigma)
 
 
 def draw_targets(rng: np.random.Generator, n: int, v: int, kind: str, zipf_s: float) -> np.ndarray:
@@ -183,8 +195,8 @@ def weight_normals(w: Workload, seed: int = 0) -> np.ndarray:
 
 
 def weight_bits(z: np.ndarray, sigma: float) -> np.ndarray:
-    """bf16 bit patterns of the weight ``sigma * z`` (z from weight_normals)."""
-    return f32_to_bf16_bits(z * np.float32(sigma))
+    """bf16 bit patterns of the weight ``sigma * z`` (z from weight_normals; the product in float32)."""
+    return f32_to_bf16_bits(z, sigma)
 
 
 def generate(w: Workload, seed: int = 0, *, draw_w: bool = True,

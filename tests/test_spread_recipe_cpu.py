@@ -32,7 +32,7 @@ def _inputs():
     return _CACHE["inp"], _CACHE
 
 
-def _shares_and_mutation(name, rows=64, chunk=16384):
+def _shares_and_mutation(name, rows=64, chunk=512):
     inp, cache = _inputs()
     w_bits = cache[name]
     valid = np.nonzero(inp.targets != inp.ignore_index)[0][:rows]
