@@ -1870,7 +1870,7 @@ inline int group_tiles(int64_t tiles, int64_t tile_rows, int64_t d) {
   return (int)std::max<int64_t>(1, (tiles + groups - 1) / groups);
 }
 
-lce_status_t make_plan(const lce_problem_t* p, Plan* pl) {
+lce_status_t make_plan(const lce_problem_t* p, Plan* pl, bool wide_slabs = true) {
   if (!p) return LCE_ERR_NULL;
   if ((p->flags & ~(LCE_FLAG_ACCUMULATE_DW | LCE_FLAG_REUSE_FORWARD)) != 0) return LCE_ERR_ARG;
   if (p->n < 0 || p->d < 1 || p->v < 1) return LCE_ERR_SHAPE;
@@ -1893,9 +1893,13 @@ lce_status_t make_plan(const lce_problem_t* p, Plan* pl) {
   pl->nparts = pl->vt_count < MAX_PARTS ? pl->vt_count : MAX_PARTS;
   pl->vt_count3 = (int)((p->v + 383) / 384);
   // backward vocabulary slab: about 4 D columns (at least 8192) keeps G at O(N D) while halving
-  // the dH accumulator passes of a 2 D slab; a multiple of 16 tiles of 384 ids, so that the dW
-  // launch of a 4096-wide head is whole rounds of workgroups on 256 CUs
+  // the dH accumulator passes of a 2 D slab. Narrower heads take up to 24576 ids while the slab's
+  // W rows fit kGroupBytes (they stay in the MALL while G's token tiles pass), which cuts their
+  // fp32 accumulator passes further (the distillation calls keep the narrow slab: their teacher
+  // probabilities take 4 bytes per slab id and token). A multiple of 16 tiles of 384 ids, so that
+  // the dW launch of a 4096-wide head is whole rounds of workgroups on 256 CUs.
   int64_t vc = 4 * p->d;
+  if (wide_slabs) vc = std::max<int64_t>(vc, std::min<int64_t>(24576, kGroupBytes / (2 * p->d) / 6144 * 6144));
   if (vc < 8192) vc = 8192;
   vc = round_up(vc, 16 * 384);
   // a multiple of 768 in any case: both 256- and 384-wide G tiles end inside a G row
@@ -2273,9 +2277,9 @@ lce_status_t make_kd_plan(const lce_kd_problem_t* p, KdPlan* k) {
   if (p->flags & LCE_FLAG_REUSE_FORWARD) return LCE_ERR_ARG;   // the KD calls lay out their own workspace
   k->ps = lce_problem_t{p->n, p->ds, p->v, p->ld_hs, p->ld_ws, p->ignore_index, p->reduction, p->target_bytes, p->flags};
   k->pt = lce_problem_t{p->n, p->dt, p->v, p->ld_ht, p->ld_wt, p->ignore_index, p->reduction, p->target_bytes, 0};
-  lce_status_t st = make_plan(&k->ps, &k->s);
+  lce_status_t st = make_plan(&k->ps, &k->s, false);
   if (st != LCE_OK) return st;
-  st = make_plan(&k->pt, &k->t);
+  st = make_plan(&k->pt, &k->t, false);
   if (st != LCE_OK) return st;
   k->scale2 = (float)(1.4426950408889634 / (double)p->temperature);
   k->inv_t = (float)(1.0 / (double)p->temperature);
