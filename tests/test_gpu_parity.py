@@ -49,18 +49,18 @@ def test_tile_exact_shapes(n, d, v):
     _case(WL.custom(n, d, v, seed=n + d, mask_frac=0.0, sigma_w=0.3))
 
 
-@pytest.mark.parametrize("n,d,v", [(300, 64, 12300), (200, 128, 12289)])
+@pytest.mark.parametrize("n,d,v", [(300, 64, 24588), (200, 128, 24577)])
 def test_last_slab_shorter_than_one_k_slice(n, d, v):
-    # 12288-id slabs at these widths: the last slab holds 12 ids (1 id), less than one 64-wide K
-    # slice, so in the split dH launches (fewer output tiles than CUs) the second K half is empty
-    # and only writes zeros into its accumulator
+    # 24576-id slabs at these widths: the last slab holds 12 ids (1 id), less than one 64-wide K
+    # slice, so in the split dH launches (fewer output tiles than CUs: eight K parts) every part
+    # past the first is empty and only writes zeros into its accumulator
     _case(WL.custom(n, d, v, seed=n + v, mask_frac=0.2, sigma_w=0.3))
 
 
-@pytest.mark.parametrize("n,d,v", [(300, 64, 20000), (270, 128, 30000), (520, 64, 40000)])
+@pytest.mark.parametrize("n,d,v", [(300, 64, 40000), (270, 128, 60000), (520, 64, 90000)])
 def test_forward_vocabulary_groups(n, d, v):
     # with D % 64 == 0 the forward runs one launch per group of 384-id tiles as wide as a backward
-    # slab (12288 ids at these widths): 2, 3 and 4 groups, a ragged last group, both partial row
+    # slab (24576 ids at these widths): 2, 3 and 4 groups, a ragged last group, both partial row
     # sets and the running pair
     _case(WL.custom(n, d, v, seed=n + d, mask_frac=0.2, sigma_w=0.3))
 
@@ -214,7 +214,7 @@ def test_random_shapes_sweep(case):
     rng = np.random.default_rng(1000 + case)
     n = int(rng.integers(1, 900))
     d = int(rng.integers(1, 80)) * 8
-    v = int(rng.choice([int(rng.integers(1, 600)), int(rng.integers(8000, 17000))]))
+    v = int(rng.choice([int(rng.integers(1, 600)), int(rng.integers(8000, 34000))]))
     reduction = ["mean", "sum", "none"][case % 3]
     grad = (rng.standard_normal(n).astype(np.float32) if reduction == "none" else float(rng.uniform(0.2, 2.0)))
     inp = WL.custom(n, d, v, seed=case, mask_frac=float(rng.uniform(0, 0.5)), sigma_w=0.3)
