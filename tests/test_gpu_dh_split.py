@@ -70,3 +70,18 @@ def test_a_stale_hip_error_of_another_call_does_not_fail_the_launches():
     assert hip.hipSetDevice(ctypes.c_int(1 << 20)) != 0          # invalid device: an error, no effect
     gpu = U.run_gpu(h, w, t, inp.ignore_index, "mean", 1.0)
     U.assert_parity(gpu, O.lce(inp.h_bits, inp.w_bits, inp.targets, inp.ignore_index, "mean", 1.0))
+
+
+def test_vocabulary_shards_with_split_tails_reproduce_the_oracle():
+    # the shard backward returns fp32 dH terms through the same finalise, here with tail parts
+    from tests.test_gpu_shard import _run_shards
+    n, d, nv = 12288, 2048, 1400
+    info = B.lce_plan_info(B.problem(n, d, 500))
+    assert info["dh_kz"] == 1 and dh_tail_parts(nv, d, info["rows_g"])
+    inp, valid = _inputs(n, d, nv, seed=5)
+    gpu = _run_shards(inp, [0, 500, V])
+    ref = O.lce(inp.h_bits, inp.w_bits, inp.targets, inp.ignore_index, "mean", 1.0)
+    U.assert_parity(gpu, ref)
+    for m0 in range(0, nv, 384):
+        blk, rb = gpu["dH"][valid][m0:m0 + 384], ref["dH"][valid][m0:m0 + 384]
+        assert np.linalg.norm(blk - rb) / np.linalg.norm(rb) <= U.GRAD_REL_TOL, m0
