@@ -118,8 +118,9 @@ typedef struct lce_adamw {
 
 /*
  * Workspace sizes, in bytes, for lce_forward (*fwd_bytes) and lce_backward
- * (*bwd_bytes). They grow as O(N*D + N*V_slab) with V_slab = max(8192, 4*D)
- * rounded up to a multiple of 6144 (at most V rounded up to 768): never O(N*V).
+ * (*bwd_bytes). They grow as O(N*D + N*V_slab) with V_slab = max(8192, 4*D, Vw)
+ * rounded up to a multiple of 6144 (at most V rounded up to 768), Vw = min(24576,
+ * 160 MiB / (2*D) rounded down to 6144): never O(N*V).
  * The backward's size does not depend on V; the forward's vocabulary partials
  * take at most 2*D bytes per token. Either output pointer may be NULL.
  */
@@ -134,7 +135,9 @@ lce_status_t lce_workspace_size(const lce_problem_t* p, size_t* fwd_bytes, size_
  * fp32 arrays) and per-row terms ([npad] fp32); the backward holds G ([rows_g][vc] bf16, one
  * vocabulary slab of vc ids, nslab slabs) and the fp32 dH accumulators: dh_kz of them, [rows_g][d]
  * each, one after the other from o_dh32, when the dH launches split K into dh_kz parts (launches
- * with fewer output tiles than compute units; o_dh32b is the second one's offset, or 0).
+ * with fewer output tiles than compute units; o_dh32b is the second one's offset, or 0). With
+ * dh_kz = 1 the launches split the K range of the tiles of each XCD's last partial round on the
+ * device, and keep those parts in the accumulator's rows past the valid ones.
  */
 typedef struct lce_plan_info {
   int64_t npad;             /* N rounded up to 256 */
