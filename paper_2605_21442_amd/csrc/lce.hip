@@ -2143,7 +2143,8 @@ lce_status_t backward_impl(const lce_problem_t* p, const ShardInfo* shard, const
                            void* dH, float* dHf, uint16_t* dW, const AdamWState* adamw, const AdamWConst* oc,
                            void* workspace, size_t workspace_bytes, void* stream, const KdArgs* kd = nullptr) {
   Plan pl;
-  lce_status_t st = make_plan(p, &pl);
+  // the distillation calls keep the narrow slab of their own plan (make_kd_plan)
+  lce_status_t st = make_plan(p, &pl, kd == nullptr);
   if (st != LCE_OK) return st;
   const ShardInfo si = shard ? *shard : ShardInfo{pl.v, 0};
   void* dH_any = dHf ? (void*)dHf : dH;

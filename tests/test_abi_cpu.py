@@ -310,3 +310,4 @@ def test_loading_the_library_first_keeps_one_hip_runtime_in_the_process():
     assert r.returncode == 0, r.stderr[-2000:]
     libs = eval(r.stdout.strip().splitlines()[-1])
     assert len(libs) == 1, libs
+

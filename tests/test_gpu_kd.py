@@ -59,7 +59,8 @@ def _check(gpu, ref):
 
 
 @pytest.mark.parametrize("n,ds,dt,v", [(300, 264, 136, 1000), (600, 128, 256, 9000), (1, 8, 16, 5),
-                                       (257, 64, 72, 300), (513, 96, 520, 4097), (300, 64, 128, 9000)])
+                                       (257, 64, 72, 300), (513, 96, 520, 4097), (300, 64, 128, 9000),
+                                       (300, 64, 128, 20000)])       # two slabs of the narrow KD width
 @pytest.mark.parametrize("temperature", [1.0, 2.0])
 def test_kd_matches_oracle(n, ds, dt, v, temperature):
     print(f"kd n={n} ds={ds} dt={dt} v={v} T={temperature}", flush=True)
@@ -126,7 +127,7 @@ def test_kd_autograd_function():
 
 @pytest.mark.parametrize("n,ds,dt,v,reduction", [(600, 128, 256, 9000, "mean"), (300, 264, 136, 1000, "none"),
                                                  (1, 8, 16, 5, "sum"), (40, 16, 32, 300, "mean"),
-                                                 (300, 64, 128, 9000, "mean")])
+                                                 (300, 64, 128, 9000, "mean"), (300, 64, 128, 20000, "mean")])
 def test_fused_forward_backward_is_bitwise_the_two_calls(n, ds, dt, v, reduction):
     import torch
     from paper_2605_21442_amd import autograd as AG
