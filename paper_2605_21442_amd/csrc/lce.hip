@@ -1973,6 +1973,12 @@ unsigned adamw_grid(int64_t v, int64_t d) {
 struct Launcher {
   hipStream_t s;
   lce_status_t st = LCE_OK;
+  // the kernel's arguments, converted to its parameter types, passed by address
+  template <typename... KArgs>
+  hipError_t launch(void (*kern)(KArgs...), dim3 grid, dim3 block, KArgs... a) {
+    void* ptrs[sizeof...(KArgs) + 1] = {static_cast<void*>(&a)..., nullptr};
+    return hipLaunchKernel(reinterpret_cast<const void*>(kern), grid, block, ptrs, 0, s);
+  }
   template <typename... KArgs, typename... Args>
   void operator()(int kind, void (*kern)(KArgs...), dim3 grid, dim3 block, Args... args) {
     if (st != LCE_OK) return;
@@ -1986,11 +1992,12 @@ struct Launcher {
       }
     }
     if (slot >= 0 && hipEventRecord(g_timing.ev[2 * slot], s) != hipSuccess) { st = LCE_ERR_HIP; return; }
-    // the thread's last-error slot may hold an earlier call's status (for instance hipErrorNotReady
-    // from another library's event query): clear it, so that only this launch's status is read
-    (void)hipGetLastError();
-    hipLaunchKernelGGL(kern, grid, block, 0, s, static_cast<KArgs>(args)...);
-    if (hipGetLastError() != hipSuccess) { st = LCE_ERR_HIP; return; }
+    // the launch's own status, without reading (and clearing) the thread's last-error slot, which
+    // may hold an earlier, unrelated call's error
+    if (launch(kern, grid, block, static_cast<KArgs>(args)...) != hipSuccess) {
+      st = LCE_ERR_HIP;
+      return;
+    }
     if (slot >= 0 && hipEventRecord(g_timing.ev[2 * slot + 1], s) != hipSuccess) st = LCE_ERR_HIP;
   }
 };

@@ -55,20 +55,43 @@ def test_dh_with_split_tails_matches_the_oracle_blockwise(n, d, nv, parts):
     assert np.all(gpu["dH"][inp.targets == inp.ignore_index] == 0.0)
 
 
-def test_a_stale_hip_error_of_another_call_does_not_fail_the_launches():
-    # a failed runtime call earlier on the thread leaves its status in HIP's last-error slot; the
-    # library's launches must report only their own status
+def test_a_stale_hip_error_of_another_call_neither_fails_the_launches_nor_is_consumed():
+    # a failed runtime call earlier on the thread leaves its status in HIP's last-error slot: the
+    # library's launches report only their own status and leave that slot to its owner
     import ctypes
+    import torch
     inp = WL.custom(300, 264, 1000, seed=1, sigma_w=0.3)
     h, w, t = U.to_device(inp)
-    B.load()
+    n, d, v = 300, 264, 1000
+    p = B.problem(n, d, v, ignore_index=inp.ignore_index, reduction="mean", target_bytes=4)
+    fb, bb = B.lce_workspace_size(p)
+    dev = h.device
+    ws = torch.empty(max(fb, bb), dtype=torch.uint8, device=dev)
+    loss = torch.empty((), dtype=torch.float32, device=dev)
+    lse = torch.empty(n, dtype=torch.float32, device=dev)
+    nv = torch.empty(1, dtype=torch.int32, device=dev)
+    st = torch.empty(1, dtype=torch.int32, device=dev)
+    grad = torch.ones(1, dtype=torch.float32, device=dev)
+    dh = torch.empty((n, d), dtype=torch.bfloat16, device=dev)
+    dw = torch.empty((v, d), dtype=torch.bfloat16, device=dev)
+    s = torch.cuda.current_stream(dev).cuda_stream
+    torch.cuda.synchronize()
     # the HIP runtime already in the process (torch's, which the library also uses)
     maps = open("/proc/self/maps").read()
     path = sorted({l.split()[-1] for l in maps.splitlines() if "libamdhip64" in l})
     assert len(path) == 1, path
     hip = ctypes.CDLL(path[0])
-    assert hip.hipSetDevice(ctypes.c_int(1 << 20)) != 0          # invalid device: an error, no effect
-    gpu = U.run_gpu(h, w, t, inp.ignore_index, "mean", 1.0)
+    bad = hip.hipSetDevice(ctypes.c_int(1 << 20))           # invalid device: an error, no effect
+    assert bad != 0
+    B.lce_forward(p, h.data_ptr(), w.data_ptr(), t.data_ptr(), loss.data_ptr(), lse.data_ptr(), nv.data_ptr(),
+                  st.data_ptr(), ws.data_ptr(), fb, s)
+    B.lce_backward(p, h.data_ptr(), w.data_ptr(), t.data_ptr(), lse.data_ptr(), nv.data_ptr(), grad.data_ptr(),
+                   dh.data_ptr(), dw.data_ptr(), ws.data_ptr(), bb, s)
+    assert hip.hipGetLastError() == bad                       # still there for its owner (and now cleared)
+    torch.cuda.synchronize()
+    gpu = {"loss": float(loss.item()), "lse": lse.cpu().numpy().astype(np.float64), "n_valid": int(nv.item()),
+           "status": int(st.item()), "dH": dh.float().cpu().numpy().astype(np.float64),
+           "dW": dw.float().cpu().numpy().astype(np.float64)}
     U.assert_parity(gpu, O.lce(inp.h_bits, inp.w_bits, inp.targets, inp.ignore_index, "mean", 1.0))
 
 
