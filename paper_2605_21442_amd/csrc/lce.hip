@@ -12,9 +12,10 @@
 //             S^T = W Hv^T, each reduced to a (max, sum-exp) partial per token) ->
 //             combine (merge partials, target logit, per-row loss) -> loss (fixed-order
 //             reduction)
-//   backward: compact -> gather Hv -> per vocabulary slab: G tile (recompute S^T,
-//             G = c (softmax - onehot)), dH32 (+)= G W_slab, dW slab = G^T Hv ->
-//             finalise dH
+//   backward: compact -> gather Hv (both skipped when the forward's are reused) -> per
+//             vocabulary slab: G tile (recompute S^T, G = c (softmax - onehot)),
+//             dH32 (+)= G W_slab (K split into parts where a launch would leave CUs idle),
+//             dW slab = G^T Hv -> finalise dH (parts added in order)
 // Built on the same kernels: the backward with an AdamW step on each finished dW block
 // (paper Sec. 4.1), a vocabulary-shard (loss-parallel) forward / combine / backward, and a
 // fused linear knowledge-distillation loss whose G kernel takes the teacher's probabilities
