@@ -524,6 +524,8 @@ def bench_kd(args, fused=False):
                      "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
                      "flops_per_launch": per_launch, "avg_launch_ms": kernels[dom]["avg_ms"]},
         "kernels_ms_per_step": {kk: r["total_ms"] / kpass for kk, r in kernels.items()},
+        "kernel_timing": f"second pass of {kpass} steps after the timed region, HIP events around each launch",
+        "lce_hip_sha256": _source_hash(),
         "cpu_baseline": None if args.no_cpu_baseline else _kd_cpu_baseline(inp, T),
     }
     if not args.no_cpu_baseline:
