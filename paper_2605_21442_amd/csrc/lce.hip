@@ -1439,8 +1439,13 @@ __device__ __forceinline__ void dw_tile(char* smem, int blk, const uint16_t* __r
                                         int tm_count, uint16_t* __restrict__ dW, int64_t v0, const AdamWState& st,
                                         const AdamWConst& oc) {
   constexpr int TM = Geo<WM>::TM;
+  // the slab's T = tm_count x dt tiles in the balanced cut of the dH launches: XCD x takes
+  // [c0(x), c0(x + 1)), walked in bands of 4 row tiles, column by column
+  const int dt = (d + TILE - 1) / TILE, t = tm_count * dt, x = blk & 7, k = blk >> 3;
+  const int c0 = dh_c0(x, t);
+  if (k >= dh_c0(x + 1, t) - c0) return;
   int tm, tn;
-  if (!band_tile(blk, tm_count, (d + TILE - 1) / TILE, tm, tn)) return;
+  dh_band_tile(c0 + k, tm_count, dt, tm, tn);
   const int m0 = tm * TM, d0 = tn * TILE;
   const int nv = *nv_ptr;
   const int kpad = ((nv + KPAD - 1) / KPAD) * KPAD;
@@ -1840,6 +1845,7 @@ struct Plan {
   int64_t n, d, v, ldh, ldw, npad;
   int nt_max, vt_count, nparts, vt_count3;   // vt_count3: 384-id tiles
   int64_t vc, nslab;
+  int64_t gw;                                // 384-id tiles of the forward's vocabulary groups
   int64_t rows_g;                            // rows of G and dH32: Npad rounded up to a 384-row tile
   // workspace offsets; idx, pos, Nv and the gathered rows Hv form a prefix both passes share
   size_t o_idx, o_pos, o_nv, o_hv, o_pm, o_ps, o_terms, fwd_bytes;
@@ -1871,6 +1877,38 @@ inline int group_tiles(int64_t tiles, int64_t tile_rows, int64_t d) {
   return (int)std::max<int64_t>(1, (tiles + groups - 1) / groups);
 }
 
+// Workgroup rounds of the dW launches over the whole vocabulary with slabs of r 384-id row tiles:
+// a slab's ceil(vs / 384) x ceil(D / 256) tiles are cut evenly over the 8 XCDs of 32 CUs each.
+int64_t dw_rounds(int64_t v, int64_t d, int64_t r) {
+  const int64_t dt = (d + 255) / 256, vt = (v + 383) / 384;
+  int64_t total = 0;
+  for (int64_t t0 = 0; t0 < vt; t0 += r) {
+    const int64_t tiles = std::min(r, vt - t0) * dt;
+    total += ((tiles + 7) / 8 + 31) / 32;
+  }
+  return total;
+}
+
+// The slab width, among multiples of 768 ids from max(8192, 4 D) up to what the MALL rule allows
+// (the slab's W rows within kGroupBytes, at most 24576 ids), that gives the dW launches the fewest
+// workgroup rounds; vc (the rule's own width) unless another needs strictly fewer, and of those
+// the widest. A head whose column tiles do not divide 256 (3584 wide: 14) leaves most of a last
+// round idle in every slab at the rule's width.
+int64_t whole_round_slab(int64_t v, int64_t d, int64_t vc) {
+  const int64_t lo = std::max<int64_t>(8192, 4 * d);
+  const int64_t hi = std::min(round_up(v, 768), std::max<int64_t>(vc, std::min<int64_t>(24576, kGroupBytes / (2 * d))));
+  const int64_t c0 = dw_rounds(v, d, vc / 384);
+  int64_t best = vc / 384, cost = c0;
+  for (int64_t r = (lo + 767) / 768 * 2; r * 384 <= hi; r += 2) {
+    const int64_t c = dw_rounds(v, d, r);
+    if (c < cost || (c == cost && c < c0)) {   // r grows: of equal counts the widest
+      best = r;
+      cost = c;
+    }
+  }
+  return best * 384;
+}
+
 lce_status_t make_plan(const lce_problem_t* p, Plan* pl, bool wide_slabs = true) {
   if (!p) return LCE_ERR_NULL;
   if ((p->flags & ~(LCE_FLAG_ACCUMULATE_DW | LCE_FLAG_REUSE_FORWARD)) != 0) return LCE_ERR_ARG;
@@ -1898,7 +1936,8 @@ lce_status_t make_plan(const lce_problem_t* p, Plan* pl, bool wide_slabs = true)
   // W rows fit kGroupBytes (they stay in the MALL while G's token tiles pass), which cuts their
   // fp32 accumulator passes further (the distillation calls keep the narrow slab: their teacher
   // probabilities take 4 bytes per slab id and token). A multiple of 16 tiles of 384 ids, so that
-  // the dW launch of a 4096-wide head is whole rounds of workgroups on 256 CUs.
+  // the dW launch of a 4096-wide head is whole rounds of workgroups on 256 CUs; for other widths
+  // whole_round_slab picks the width whose dW launches leave the fewest idle CUs.
   int64_t vc = 4 * p->d;
   if (wide_slabs) vc = std::max<int64_t>(vc, std::min<int64_t>(24576, kGroupBytes / (2 * p->d) / 6144 * 6144));
   if (vc < 8192) vc = 8192;
@@ -1906,6 +1945,10 @@ lce_status_t make_plan(const lce_problem_t* p, Plan* pl, bool wide_slabs = true)
   // a multiple of 768 in any case: both 256- and 384-wide G tiles end inside a G row
   const int64_t vround = round_up(p->v, 768);
   if (vc > vround) vc = vround;
+  // the forward's groups keep the rule's width (they only order its tiles; a wider group's W rows
+  // leave the MALL)
+  pl->gw = vc / 384;
+  if (wide_slabs && vc < vround) vc = whole_round_slab(p->v, p->d, vc);
   pl->vc = vc;
   pl->nslab = (p->v + vc - 1) / vc;
   if ((uint64_t)TILE * pl->npad * 2 > 0x7FFFFFFFull || (uint64_t)TILE * vc * 2 > 0x7FFFFFFFull) return LCE_ERR_SHAPE;
@@ -2048,9 +2091,9 @@ PartRows launch_fwd_stats(Launcher& L, const Plan& layout, const uint16_t* W, in
   const int gw = (int)(layout.vc / Geo<3>::TM);
   const int ntl = layout.vt_count3;
   if (fwd_one_launch(layout)) {
-    // one launch: the groups only order the tiles (one slab wide, or narrower where a slab's W
-    // rows would not stay in the MALL)
-    const int go = group_tiles(gw, Geo<3>::TM, d);
+    // one launch: the groups only order the tiles (as wide as the slab rule's width, or narrower
+    // where its W rows would not stay in the MALL)
+    const int go = group_tiles(layout.gw, Geo<3>::TM, d);
     L(K_FWD_STATS, k_fwd_tile, dim3((unsigned)(ntl * nt_max)), dim3(Geo<3>::NT), W, ldw, v, (const uint16_t*)hv,
       (int64_t)d, nv, d, 0, ntl, go, nt_max, pm, ps, (const float*)nullptr, (const float*)nullptr, 0,
       (float*)nullptr, (float*)nullptr, 0, npad, scale2);
@@ -2256,7 +2299,7 @@ lce_status_t backward_impl(const lce_problem_t* p, const ShardInfo* shard, const
     const unsigned bdh = pl.dh_kz > 1 ? (unsigned)(pl.dh_kz * 8 * ((dh_tiles + 7) / 8) * dt)
                                       : (unsigned)(256 * (((int64_t)dh_tiles * dt + 7) / 8 / 32 + 1));
     const int tmw = (vs + Geo<kDwWM>::TM - 1) / Geo<kDwWM>::TM;
-    const unsigned bdw = (unsigned)(8 * ((tmw + 7) / 8) * dt);
+    const unsigned bdw = (unsigned)(8 * (((int64_t)tmw * dt + 7) / 8));
     // dH reads the slab's W rows before the dW launch, whose AdamW epilogue (in-backward step)
     // may update them; later slabs read only their own rows
     L(K_BWD_DH, k_bwd_dh<kDhWM>, dim3(bdh), dim3(Geo<kDhWM>::NT), (const uint16_t*)g, vc, vs, w + v0 * pl.ldw, pl.ldw,

@@ -278,3 +278,56 @@ def test_split_dh_blocks_cover_every_tile_and_k_part_once(nv, d):
     assert sorted(seen) == sorted((tm, tn) for tm in range(tm_live) for tn in range(dtc))
     for (tm, z), kz in tails.items():
         assert 1 <= z < kz <= 8
+
+
+def dw_block_tile(blk, tm_count, d):
+    """The dW tile of block blk as dw_tile maps it (None: the block has no tile): the slab's
+    tm_count x ceil(D / 256) tiles cut evenly over the 8 XCDs, bands of 4 row tiles walked column
+    by column."""
+    dtc = cdiv(d, 256)
+    t = tm_count * dtc
+    x, k = blk & 7, blk >> 3
+    c0, c1 = (x * t) >> 3, ((x + 1) * t) >> 3
+    if k >= c1 - c0:
+        return None
+    l = c0 + k
+    band = l // (4 * dtc)
+    rows = min(4, tm_count - band * 4)
+    kk = l - band * 4 * dtc
+    return band * 4 + kk % rows, kk // rows
+
+
+@pytest.mark.parametrize("tm_count,d", [(48, 4096), (54, 3584), (18, 3584), (64, 2048), (14, 2048), (96, 8192),
+                                        (12, 512), (1, 8), (3, 264), (5, 72)])
+def test_dw_blocks_cover_every_tile_once_in_balanced_xcd_shares(tm_count, d):
+    dtc = cdiv(d, 256)
+    t = tm_count * dtc
+    grid = 8 * cdiv(t, 8)                      # the host's dW grid
+    tiles = [dw_block_tile(b, tm_count, d) for b in range(grid)]
+    live = [tt for tt in tiles if tt is not None]
+    assert sorted(live) == sorted((tm, tn) for tm in range(tm_count) for tn in range(dtc))
+    per_xcd = [sum(tiles[b] is not None for b in range(x, grid, 8)) for x in range(8)]
+    assert max(per_xcd) - min(per_xcd) <= 1
+
+
+def dw_rounds(v, d, r):
+    # workgroup rounds of the dW launches with slabs of r row tiles (8 XCDs x 32 CUs)
+    dtc, vt = cdiv(d, 256), cdiv(v, 384)
+    return sum(cdiv(cdiv(min(r, vt - t0) * dtc, 8), 32) for t0 in range(0, vt, r))
+
+
+@pytest.mark.parametrize("d,v", [(512, 4096), (2048, 128256), (4096, 128256), (3584, 152064), (8192, 128256),
+                                 (2560, 151936), (1536, 151936), (5120, 152064), (3584, 1000)])
+def test_the_slab_width_gives_the_dw_launches_the_fewest_rounds_in_its_range(d, v):
+    info = B.lce_plan_info(B.problem(4096, d, v))
+    vc = info["vc"]
+    assert vc % 768 == 0 and info["nslab"] == cdiv(v, vc)
+    lo = max(8192, 4 * d)
+    hi = min(rup(v, 768), max(vc, min(24576, (160 << 20) // (2 * d))))
+    if vc >= rup(v, 768):
+        return                                  # one slab holds the whole vocabulary
+    best = min(dw_rounds(v, d, r) for r in range(cdiv(lo, 768) * 2, hi // 384 + 1, 2))
+    assert dw_rounds(v, d, vc // 384) <= best
+    assert lo <= vc <= hi
+    if (d, v) == (3584, 152064):                # the 3584-wide head: whole rounds, as few as the tiles allow
+        assert dw_rounds(v, d, vc // 384) == cdiv(cdiv(v, 384) * cdiv(d, 256), 256) == 22
