@@ -737,6 +737,31 @@ __device__ __forceinline__ void merge_pair(float& m, float& s, float m2, float s
   m = mn;
 }
 
+// XCD-aware order of the tiles of a forward or G launch: `tiles` vocabulary tiles by nt token tiles,
+// workgroups dealt round-robin to the 8 XCDs (block b runs on XCD b mod 8). The first a = tiles & ~7
+// vocabulary tiles go in groups of gw tiles (a and gw multiples of 8; a last group may be narrower)
+// by all token tiles, vocabulary tiles fastest: XCD x then takes the tiles = x (mod 8) of each
+// group, and a round of its ~32 workgroups shares a few W tiles and a few H tiles, while the group's
+// W rows stay in the MALL as the token tiles pass. The last tiles - a (< 8) vocabulary tiles are
+// dealt by token tile instead: XCD x takes the token tiles = x (mod 8), each with all of them.
+// (Dealt the first way, a group whose width is not a multiple of 8 would give every XCD most of the
+// group's W tiles.) False for blocks past the last tile.
+__device__ __forceinline__ bool xcd_tile(int b, int tiles, int gw, int nt, int& tm, int& tn) {
+  const int a = tiles & ~7, ba = a * nt;
+  if (b < ba) {
+    const int full = a / gw, g = b / (gw * nt);
+    const int wl = g < full ? gw : a - full * gw, r = b - g * gw * nt;
+    tm = g * gw + r % wl;
+    tn = r / wl;
+    return true;
+  }
+  const int rem = tiles - a, r = b - ba, k = r >> 3;
+  if (rem == 0) return false;
+  tm = a + k % rem;
+  tn = (r & 7) + 8 * (k / rem);
+  return tn < nt;
+}
+
 __global__ __launch_bounds__(Geo<3>::NT, 3) void k_fwd_tile(const uint16_t* __restrict__ W, int64_t ldw, int v,
                                                             const uint16_t* __restrict__ Hv, int64_t ldh,
                                                             const int* __restrict__ nv_ptr, int d, int tm0,
@@ -748,19 +773,8 @@ __global__ __launch_bounds__(Geo<3>::NT, 3) void k_fwd_tile(const uint16_t* __re
                                                             int run_init, int npad, float scale2) {
   constexpr int WM = 3, TM = Geo<WM>::TM;
   __shared__ __attribute__((aligned(16))) char smem[Geo<WM>::LDS];
-  const int b = blockIdx.x;
-  const int full = vt_launch / gw;
-  const int g = b / (gw * nt_max);
   int tl, tn;   // launch-relative vocabulary tile, token tile
-  if (g < full) {
-    const int r = b - g * gw * nt_max;
-    tl = g * gw + r % gw;
-    tn = r / gw;
-  } else {
-    const int r = b - full * gw * nt_max, wl = vt_launch - full * gw;
-    tl = full * gw + r % wl;
-    tn = r / wl;
-  }
+  if (!xcd_tile((int)blockIdx.x, vt_launch, gw, nt_max, tl, tn)) return;
   const int tm = tm0 + tl;
   const int nv = *nv_ptr;
   const int n0 = tn * TILE;
@@ -1198,22 +1212,10 @@ __global__ __launch_bounds__(Geo<WM>::NT, WM) void k_bwd_g(const uint16_t* __res
   constexpr int TM = Geo<WM>::TM;
   __shared__ __attribute__((aligned(16))) char smem[Geo<WM>::LDS];
   const int nv = *nv_ptr;
-  // tiles in groups of gsub consecutive id tiles by all token tiles, ids fastest: the group's W
-  // rows stay in the MALL while the token tiles pass (gsub = tm_count: one group, the whole slab)
+  // tiles in the XCD-aware order of xcd_tile, in groups of gsub id tiles (ldt = Npad: ldt / 256
+  // token tiles)
   int tm, tn;
-  {
-    const int nt = (int)gridDim.x / tm_count, b = (int)blockIdx.x;
-    const int full = tm_count / gsub, g = b / (gsub * nt);
-    if (g < full) {
-      const int r = b - g * gsub * nt;
-      tm = g * gsub + r % gsub;
-      tn = r / gsub;
-    } else {
-      const int r = b - full * gsub * nt, wl = tm_count - full * gsub;
-      tm = full * gsub + r % wl;
-      tn = r / wl;
-    }
-  }
+  if (!xcd_tile((int)blockIdx.x, tm_count, gsub, ldt / TILE, tm, tn)) return;
   const int n0 = tn * TILE;
   if (n0 >= nv) return;
   const int vt0 = tm * TM;                   // slab-relative
@@ -1877,6 +1879,18 @@ inline int group_tiles(int64_t tiles, int64_t tile_rows, int64_t d) {
   return (int)std::max<int64_t>(1, (tiles + groups - 1) / groups);
 }
 
+// Grid and group width of a launch in the order of xcd_tile: `tiles` vocabulary tiles by nt token
+// tiles, in groups at most `width` tiles wide (rounded down to a multiple of 8).
+struct TileOrder {
+  unsigned grid;
+  int gw;
+};
+inline TileOrder tile_order(int64_t tiles, int64_t nt, int64_t width) {
+  const int64_t a = tiles & ~(int64_t)7, rem = tiles - a;
+  return TileOrder{(unsigned)(a * nt + (rem ? 8 * rem * ((nt + 7) / 8) : 0)),
+                   (int)std::max<int64_t>(8, std::min(width, a) & ~(int64_t)7)};
+}
+
 // Workgroup rounds of the dW launches over the whole vocabulary with slabs of r 384-id row tiles:
 // a slab's ceil(vs / 384) x ceil(D / 256) tiles are cut evenly over the 8 XCDs of 32 CUs each.
 int64_t dw_rounds(int64_t v, int64_t d, int64_t r) {
@@ -2093,9 +2107,9 @@ PartRows launch_fwd_stats(Launcher& L, const Plan& layout, const uint16_t* W, in
   if (fwd_one_launch(layout)) {
     // one launch: the groups only order the tiles (as wide as the slab rule's width, or narrower
     // where its W rows would not stay in the MALL)
-    const int go = group_tiles(layout.gw, Geo<3>::TM, d);
-    L(K_FWD_STATS, k_fwd_tile, dim3((unsigned)(ntl * nt_max)), dim3(Geo<3>::NT), W, ldw, v, (const uint16_t*)hv,
-      (int64_t)d, nv, d, 0, ntl, go, nt_max, pm, ps, (const float*)nullptr, (const float*)nullptr, 0,
+    const TileOrder to = tile_order(ntl, nt_max, group_tiles(layout.gw, Geo<3>::TM, d));
+    L(K_FWD_STATS, k_fwd_tile, dim3(to.grid), dim3(Geo<3>::NT), W, ldw, v, (const uint16_t*)hv,
+      (int64_t)d, nv, d, 0, ntl, to.gw, nt_max, pm, ps, (const float*)nullptr, (const float*)nullptr, 0,
       (float*)nullptr, (float*)nullptr, 0, npad, scale2);
     return PartRows{pm, ps, ntl, nullptr, nullptr};
   }
@@ -2108,8 +2122,9 @@ PartRows launch_fwd_stats(Launcher& L, const Plan& layout, const uint16_t* W, in
   for (int g = 0; g < ng; ++g) {
     const int tm0 = g * gw, wl = std::min(gw, ntl - tm0);
     const int64_t cur = (g & 1) * rs, prev = ((g + 1) & 1) * rs;
-    L(K_FWD_STATS, k_fwd_tile, dim3((unsigned)(wl * nt_max)), dim3(Geo<3>::NT), W, ldw, v, (const uint16_t*)hv,
-      (int64_t)d, nv, d, tm0, wl, gw, nt_max, pm + cur, ps + cur,
+    const TileOrder to = tile_order(wl, nt_max, wl);
+    L(K_FWD_STATS, k_fwd_tile, dim3(to.grid), dim3(Geo<3>::NT), W, ldw, v, (const uint16_t*)hv,
+      (int64_t)d, nv, d, tm0, wl, to.gw, nt_max, pm + cur, ps + cur,
       g > 0 ? (const float*)(pm + prev) : (const float*)nullptr, (const float*)(ps + prev), gw, run_m, run_s,
       g == 1 ? 1 : 0, npad, scale2);
   }
@@ -2260,38 +2275,43 @@ lce_status_t backward_impl(const lce_problem_t* p, const ShardInfo* shard, const
       float* P = (float*)(ws + pl.bwd_bytes);
       if (hvt) {
         const int tmg = (vs + Geo<3>::TM - 1) / Geo<3>::TM;
-        L(K_KD_P, k_bwd_g<P_WRITE, 3>, dim3((unsigned)(tmg * pl.nt_max)), dim3(Geo<3>::NT), kd->wt, kd->ldwt, v0, vs,
+        const TileOrder to = tile_order(tmg, pl.nt_max, group_tiles(tmg, Geo<3>::TM, kd->dt));
+        L(K_KD_P, k_bwd_g<P_WRITE, 3>, dim3(to.grid), dim3(Geo<3>::NT), kd->wt, kd->ldwt, v0, vs,
           (const uint16_t*)hvt, (int64_t)kd->dt, pl.n, targets, p->target_bytes, (int64_t)0, (const int*)idx,
           (const int*)nv, kd->lse_t, grad_loss, (const int*)n_valid, p->reduction, kd->dt, tmg, (uint16_t*)nullptr, vc,
-          npad, kd->scale2, kd->inv_t, P, (float*)nullptr, (int64_t)0, group_tiles(tmg, Geo<3>::TM, kd->dt));
+          npad, kd->scale2, kd->inv_t, P, (float*)nullptr, (int64_t)0, to.gw);
       } else {
-        L(K_KD_P, k_bwd_g<P_WRITE, 2>, dim3((unsigned)(tm * pl.nt_max)), dim3(NTHREADS), kd->wt, kd->ldwt, v0, vs,
+        const TileOrder to = tile_order(tm, pl.nt_max, tm);
+        L(K_KD_P, k_bwd_g<P_WRITE, 2>, dim3(to.grid), dim3(NTHREADS), kd->wt, kd->ldwt, v0, vs,
           kd->ht, kd->ldht, pl.n, targets, p->target_bytes, (int64_t)0, (const int*)idx, (const int*)nv, kd->lse_t,
           grad_loss, (const int*)n_valid, p->reduction, kd->dt, tm, (uint16_t*)nullptr, vc, npad,
-          kd->scale2, kd->inv_t, P, (float*)nullptr, (int64_t)0, tm);
+          kd->scale2, kd->inv_t, P, (float*)nullptr, (int64_t)0, to.gw);
       }
+      const TileOrder to = tile_order(tm, pl.nt_max, tm);
       if (kd->qpart)
-        L(K_BWD_G, k_bwd_g<G_SOFT_Q, 2>, dim3((unsigned)(tm * pl.nt_max)), dim3(NTHREADS), w, pl.ldw, v0, vs, h,
+        L(K_BWD_G, k_bwd_g<G_SOFT_Q, 2>, dim3(to.grid), dim3(NTHREADS), w, pl.ldw, v0, vs, h,
           pl.ldh, pl.n, targets, p->target_bytes, (int64_t)0, (const int*)idx, (const int*)nv, lse, grad_loss,
           (const int*)n_valid, p->reduction, d, tm, g, vc, npad, kd->scale2, kd->inv_t, P, kd->qpart,
-          (int64_t)(2 * (v0 / TILE)), tm);
+          (int64_t)(2 * (v0 / TILE)), to.gw);
       else
-        L(K_BWD_G, k_bwd_g<G_SOFT, 2>, dim3((unsigned)(tm * pl.nt_max)), dim3(NTHREADS), w, pl.ldw, v0, vs, h,
+        L(K_BWD_G, k_bwd_g<G_SOFT, 2>, dim3(to.grid), dim3(NTHREADS), w, pl.ldw, v0, vs, h,
           pl.ldh, pl.n, targets, p->target_bytes, (int64_t)0, (const int*)idx, (const int*)nv, lse, grad_loss,
           (const int*)n_valid, p->reduction, d, tm, g, vc, npad, kd->scale2, kd->inv_t, P, (float*)nullptr,
-          (int64_t)0, tm);
+          (int64_t)0, to.gw);
     } else {
       if (d % KSLICE == 0) {
         const int tmg = (vs + Geo<kGWM>::TM - 1) / Geo<kGWM>::TM;
-        L(K_BWD_G, k_bwd_g<G_ONEHOT, kGWM>, dim3((unsigned)(tmg * pl.nt_max)), dim3(Geo<kGWM>::NT), w, pl.ldw, v0, vs,
+        const TileOrder to = tile_order(tmg, pl.nt_max, group_tiles(tmg, Geo<3>::TM, d));
+        L(K_BWD_G, k_bwd_g<G_ONEHOT, kGWM>, dim3(to.grid), dim3(Geo<kGWM>::NT), w, pl.ldw, v0, vs,
           (const uint16_t*)hv, (int64_t)d, pl.n, targets, p->target_bytes, si.v_begin, (const int*)idx, (const int*)nv,
           lse, grad_loss, (const int*)n_valid, p->reduction, d, tmg, g, vc, npad, kLog2e, 1.f, (float*)nullptr,
-          (float*)nullptr, (int64_t)0, group_tiles(tmg, Geo<3>::TM, d));
+          (float*)nullptr, (int64_t)0, to.gw);
       } else {
-        L(K_BWD_G, k_bwd_g<G_ONEHOT, 2>, dim3((unsigned)(tm * pl.nt_max)), dim3(NTHREADS), w, pl.ldw, v0, vs, h,
+        const TileOrder to = tile_order(tm, pl.nt_max, tm);
+        L(K_BWD_G, k_bwd_g<G_ONEHOT, 2>, dim3(to.grid), dim3(NTHREADS), w, pl.ldw, v0, vs, h,
           pl.ldh, pl.n, targets, p->target_bytes, si.v_begin, (const int*)idx, (const int*)nv, lse, grad_loss,
           (const int*)n_valid, p->reduction, d, tm, g, vc, npad, kLog2e, 1.f, (float*)nullptr, (float*)nullptr,
-          (int64_t)0, tm);
+          (int64_t)0, to.gw);
       }
     }
     // split launches: kz copies of the banded grid; otherwise 8 XCDs x 32 CUs x (whole rounds of the
@@ -2494,20 +2514,23 @@ lce_status_t kd_forward_impl(const lce_kd_problem_t* p, const void* Hs, const vo
     const int tm = (vs + TILE - 1) / TILE;
     if (hvt) {
       const int tmg = (vs + Geo<3>::TM - 1) / Geo<3>::TM;
-      L(K_KD_P, k_bwd_g<P_WRITE, 3>, dim3((unsigned)(tmg * pl.nt_max)), dim3(Geo<3>::NT), wt, tp.ldw, v0, vs,
+      const TileOrder to = tile_order(tmg, pl.nt_max, group_tiles(tmg, Geo<3>::TM, tp.d));
+      L(K_KD_P, k_bwd_g<P_WRITE, 3>, dim3(to.grid), dim3(Geo<3>::NT), wt, tp.ldw, v0, vs,
         (const uint16_t*)hvt, tp.d, pl.n, targets, p->target_bytes, (int64_t)0, (const int*)idx, (const int*)nv,
         (const float*)lse_t, (const float*)nullptr, (const int*)nullptr, p->reduction, (int)tp.d, tmg,
-        (uint16_t*)nullptr, vc, npad, k.scale2, k.inv_t, P, (float*)nullptr, (int64_t)0, group_tiles(tmg, Geo<3>::TM, tp.d));
+        (uint16_t*)nullptr, vc, npad, k.scale2, k.inv_t, P, (float*)nullptr, (int64_t)0, to.gw);
     } else {
-      L(K_KD_P, k_bwd_g<P_WRITE, 2>, dim3((unsigned)(tm * pl.nt_max)), dim3(NTHREADS), wt, tp.ldw, v0, vs, ht, tp.ldh,
+      const TileOrder to = tile_order(tm, pl.nt_max, tm);
+      L(K_KD_P, k_bwd_g<P_WRITE, 2>, dim3(to.grid), dim3(NTHREADS), wt, tp.ldw, v0, vs, ht, tp.ldh,
         pl.n, targets, p->target_bytes, (int64_t)0, (const int*)idx, (const int*)nv, (const float*)lse_t,
         (const float*)nullptr, (const int*)nullptr, p->reduction, (int)tp.d, tm, (uint16_t*)nullptr, vc,
-        npad, k.scale2, k.inv_t, P, (float*)nullptr, (int64_t)0, tm);
+        npad, k.scale2, k.inv_t, P, (float*)nullptr, (int64_t)0, to.gw);
     }
-    L(K_KD_Q, k_bwd_g<Q_SOFT, 2>, dim3((unsigned)(tm * pl.nt_max)), dim3(NTHREADS), wsm, pl.ldw, v0, vs, hs, pl.ldh,
+    const TileOrder to = tile_order(tm, pl.nt_max, tm);
+    L(K_KD_Q, k_bwd_g<Q_SOFT, 2>, dim3(to.grid), dim3(NTHREADS), wsm, pl.ldw, v0, vs, hs, pl.ldh,
       pl.n, targets, p->target_bytes, (int64_t)0, (const int*)idx, (const int*)nv, (const float*)lse_s,
       (const float*)nullptr, (const int*)nullptr, p->reduction, (int)pl.d, tm, (uint16_t*)nullptr, vc,
-      npad, k.scale2, k.inv_t, P, qpart, (int64_t)(2 * (v0 / TILE)), tm);
+      npad, k.scale2, k.inv_t, P, qpart, (int64_t)(2 * (v0 / TILE)), to.gw);
   }
   L(K_KD_TERMS, k_kd_terms, dim3((unsigned)((pl.n + 255) / 256)), dim3(256), (const float*)qpart,
     2 * pl.vt_count, (int64_t)npad, (const int*)pos, pl.n, (const float*)lse_s, terms, none ? loss : (float*)nullptr);

@@ -331,3 +331,46 @@ def test_the_slab_width_gives_the_dw_launches_the_fewest_rounds_in_its_range(d, 
     assert lo <= vc <= hi
     if (d, v) == (3584, 152064):                # the 3584-wide head: whole rounds, as few as the tiles allow
         assert dw_rounds(v, d, vc // 384) == cdiv(cdiv(v, 384) * cdiv(d, 256), 256) == 22
+
+
+def xcd_tile(b, tiles, gw, nt):
+    """The (vocabulary tile, token tile) of block b of a forward or G launch, as xcd_tile maps it."""
+    a = tiles & ~7
+    ba = a * nt
+    if b < ba:
+        full, g = a // gw, b // (gw * nt)
+        wl = gw if g < full else a - full * gw
+        r = b - g * gw * nt
+        return g * gw + r % wl, r // wl
+    rem, r = tiles - a, b - ba
+    if rem == 0:
+        return None
+    k = r >> 3
+    tn = (r & 7) + 8 * (k // rem)
+    return (a + k % rem, tn) if tn < nt else None
+
+
+def tile_order(tiles, nt, width):
+    a = tiles & ~7
+    rem = tiles - a
+    return a * nt + (8 * rem * cdiv(nt, 8) if rem else 0), max(8, min(width, a) & ~7)
+
+
+@pytest.mark.parametrize("tiles,nt,width", [(334, 48, 48), (54, 90, 54), (46, 48, 46), (96, 52, 24), (64, 24, 64),
+                                            (12, 1, 12), (11, 2, 11), (3, 5, 3), (72, 64, 72), (17, 9, 17), (1, 1, 1),
+                                            (8, 7, 8), (40, 33, 16)])
+def test_forward_and_g_blocks_cover_every_tile_once_and_keep_w_tiles_on_one_xcd(tiles, nt, width):
+    grid, gw = tile_order(tiles, nt, width)
+    assert gw % 8 == 0
+    got = [xcd_tile(b, tiles, gw, nt) for b in range(grid)]
+    live = [t for t in got if t is not None]
+    assert sorted(live) == [(tm, tn) for tm in range(tiles) for tn in range(nt)]
+    a = tiles & ~7
+    for b, t in enumerate(got):
+        if t is None:
+            continue
+        tm, tn = t
+        if tm < a:
+            assert tm % 8 == b % 8          # each XCD keeps its own W tiles of the aligned part
+        else:
+            assert tn % 8 == b % 8          # and its own token tiles of the last few vocabulary tiles
