@@ -120,7 +120,9 @@ typedef struct lce_adamw {
  * Workspace sizes, in bytes, for lce_forward (*fwd_bytes) and lce_backward
  * (*bwd_bytes). They grow as O(N*D + N*V_slab) with V_slab = max(8192, 4*D, Vw)
  * rounded up to a multiple of 6144 (at most V rounded up to 768), Vw = min(24576,
- * 160 MiB / (2*D) rounded down to 6144): never O(N*V).
+ * 160 MiB / (2*D) rounded down to 6144), or, where it gives the dW launches fewer
+ * workgroup rounds, another multiple of 768 between max(8192, 4*D) and
+ * min(24576, 160 MiB / (2*D)) (lce_plan_info reports the width): never O(N*V).
  * The backward's size does not depend on V; the forward's vocabulary partials
  * take at most 2*D bytes per token. Either output pointer may be NULL.
  */
