@@ -811,17 +811,27 @@ __global__ __launch_bounds__(Geo<3>::NT, 3) void k_fwd_tile(const uint16_t* __re
 
   // rows (vocabulary ids) of this lane: v0 + wr*128 + 32 bi + 8 (r/4) + 4 (lane/32) + r%4
   const int vb = wr * 128 + (lane >> 5) * 4;
-  const bool ragged = vleft < TM;
+  // the rows past V of the last vocabulary tile drop out of the max and the sum; every other tile
+  // takes a path with no per-element test (a runtime test would be kept, as masks, on every tile)
+  auto mask_rows = [&](auto kRagged) {
+    if constexpr (decltype(kRagged)::value) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            if (vb + i * 32 + (r >> 2) * 8 + (r & 3) >= vleft) acc[i][j][r] = -INFINITY;
+    }
+  };
+  if (vleft < TM) mask_rows(std::true_type{});
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
     float mx = -INFINITY;
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        if (ragged && (vb + i * 32 + (r >> 2) * 8 + (r & 3)) >= vleft) acc[i][j][r] = -INFINITY;
-        mx = fmaxf(mx, acc[i][j][r]);
-      }
+      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, acc[i][j][r]);
     const float nm = mx * scale2;
     float st = 0.f;
     if (nm != -INFINITY) {
