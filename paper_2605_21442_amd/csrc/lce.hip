@@ -29,6 +29,12 @@
 // the forward and G kernels; G in dH) or K-major (G and Hv in dW, the W slab in dH: the
 // MFMA fragments then come from transposing LDS reads), so G is written once, token-major,
 // and W is never copied.
+//
+// Launch shapes follow the 8 XCDs, each with its own L2 (workgroups are dealt to them round-
+// robin): the forward and G tiles go in vocabulary groups a multiple of 8 tiles wide, so that each
+// XCD keeps its own W tiles while the token tiles pass (xcd_tile); the dH and dW tiles are cut into
+// balanced per-XCD shares walked in bands of 4 row tiles; and the backward slab width is chosen so
+// that the dW launches fill whole rounds of the 256 CUs (whole_round_slab).
 
 #include <hip/hip_runtime.h>
 
