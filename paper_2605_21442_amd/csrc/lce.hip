@@ -1376,51 +1376,58 @@ __global__ __launch_bounds__(Geo<WM>::NT, WM) void k_bwd_g(const uint16_t* __res
   // hold the same half of 32 consecutive token rows, then write 32 distinct 8-byte bank slots.
   char* T = smem;
   float qs[2] = {0.f, 0.f};
+  // a tile whose tokens are all valid and whose ids all lie in the slab tests nothing per element
+  // (a runtime test would be kept, as masks and branches, on every tile)
+  auto fill = [&](auto kFull) {
+    constexpr bool kF = decltype(kFull)::value;
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    const bool tok_ok = tok[j] < nv;
-    const int nl = wc * 64 + j * 32 + (lane & 31);
+    for (int j = 0; j < 2; ++j) {
+      const bool tok_ok = kF || tok[j] < nv;
+      const int nl = wc * 64 + j * 32 + (lane & 31);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      float pt[16];
-      if constexpr (kMode == G_SOFT || kMode == G_SOFT_Q) {
-        // the block's 16 teacher probabilities are loaded together, then used
+      for (int i = 0; i < 4; ++i) {
+        float pt[16];
+        if constexpr (kMode == G_SOFT || kMode == G_SOFT_Q) {
+          // the block's 16 teacher probabilities are loaded together, then used
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int vr = vb + i * 32 + (r >> 2) * 8 + (r & 3);
-          pt[r] = (tok_ok && vr < vleft) ? P[(int64_t)(vt0 + vr) * ldt + tok[j]] : 0.f;
-        }
-      }
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        float gq[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int r = q * 4 + e;
-          const int vr = vb + i * 32 + q * 8 + e;
-          float g = 0.f;
-          if (tok_ok && vr < vleft) {
-            const float e2 = __builtin_amdgcn_exp2f(fmaf(acc[i][j][r], scale2, -l2[j]));
-            if constexpr (kMode == G_SOFT || kMode == G_SOFT_Q) {
-              g = cj[j] * inv_t * (e2 - pt[r]);
-              if constexpr (kMode == G_SOFT_Q) qs[j] = fmaf(pt[r], acc[i][j][r] * inv_t, qs[j]);
-            } else {
-              g = cj[j] * e2;
-              if (vr == tgt[j]) g -= cj[j];
-            }
+          for (int r = 0; r < 16; ++r) {
+            const int vr = vb + i * 32 + (r >> 2) * 8 + (r & 3);
+            pt[r] = (kF || (tok_ok && vr < vleft)) ? P[(int64_t)(vt0 + vr) * ldt + tok[j]] : 0.f;
           }
-          gq[e] = g;
         }
-        const int vl = vb + i * 32 + q * 8;
-        u32x2_t pk;
-        pk.x = pack_bf16x2(gq[0], gq[1]);
-        pk.y = pack_bf16x2(gq[2], gq[3]);
-        const uint32_t a = (uint32_t)(nl * 512 + ((((vl >> 3) ^ (nl & 31))) << 4) +
-                                      ((((vl >> 2) & 1) ^ ((nl >> 4) & 1)) << 3));
-        *reinterpret_cast<u32x2_t*>(T + a) = pk;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          float gq[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int r = q * 4 + e;
+            const int vr = vb + i * 32 + q * 8 + e;
+            float g = 0.f;
+            if (kF || (tok_ok && vr < vleft)) {
+              const float e2 = __builtin_amdgcn_exp2f(fmaf(acc[i][j][r], scale2, -l2[j]));
+              if constexpr (kMode == G_SOFT || kMode == G_SOFT_Q) {
+                g = cj[j] * inv_t * (e2 - pt[r]);
+                if constexpr (kMode == G_SOFT_Q) qs[j] = fmaf(pt[r], acc[i][j][r] * inv_t, qs[j]);
+              } else {
+                g = cj[j] * e2;
+                if (vr == tgt[j]) g -= cj[j];
+              }
+            }
+            gq[e] = g;
+          }
+          const int vl = vb + i * 32 + q * 8;
+          u32x2_t pk;
+          pk.x = pack_bf16x2(gq[0], gq[1]);
+          pk.y = pack_bf16x2(gq[2], gq[3]);
+          const uint32_t a = (uint32_t)(nl * 512 + ((((vl >> 3) ^ (nl & 31))) << 4) +
+                                        ((((vl >> 2) & 1) ^ ((nl >> 4) & 1)) << 3));
+          *reinterpret_cast<u32x2_t*>(T + a) = pk;
+        }
       }
     }
-  }
+  };
+  if (n0 + TILE <= nv && vleft >= TM) fill(std::true_type{});
+  else fill(std::false_type{});
   if constexpr (kMode == G_SOFT_Q) {
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
