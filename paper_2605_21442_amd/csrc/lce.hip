@@ -1532,44 +1532,50 @@ __device__ __forceinline__ void dw_tile(char* smem, int blk, const uint16_t* __r
     const bool has_master = st.master != nullptr;
     const uint32_t vo4 = (uint32_t)((lrow * d + dc) * 4);
     const uint32_t voW = (uint32_t)((lrow * st.ldw + dc) * 2);
+    // as for the stores above: full tiles test nothing per element
+    auto update_tile = [&](auto kFull) {
+      constexpr bool kF = decltype(kFull)::value;
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        if (!col_ok[j]) continue;
-        // four consecutive rows at a time: all their loads first, then the updates and stores
+        for (int j = 0; j < 2; ++j) {
+          if (!kF && !col_ok[j]) continue;
+          // four consecutive rows at a time: all their loads first, then the updates and stores
 #pragma unroll
-        for (int rq = 0; rq < 4; ++rq) {
-          float p[4], mo[4], vo[4];
+          for (int rq = 0; rq < 4; ++rq) {
+            float p[4], mo[4], vo[4];
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const int row = erow(i, rq * 4 + e);
-            const uint32_t s4 = (uint32_t)((row * d + j * 32) * 4);
-            const uint32_t sW = (uint32_t)((row * st.ldw + j * 32) * 2);
-            mo[e] = vo[e] = p[e] = 0.f;
-            if (row_ok(i, rq * 4 + e)) {
-              mo[e] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rm, (int)vo4, (int)s4, 0));
-              vo[e] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rv, (int)vo4, (int)s4, 0));
-              p[e] = has_master ? __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rp, (int)vo4, (int)s4, 0))
-                                : bf16_to_f32(__builtin_amdgcn_raw_buffer_load_b16(rW, (int)voW, (int)sW, 0));
+            for (int e = 0; e < 4; ++e) {
+              const int row = erow(i, rq * 4 + e);
+              const uint32_t s4 = (uint32_t)((row * d + j * 32) * 4);
+              const uint32_t sW = (uint32_t)((row * st.ldw + j * 32) * 2);
+              mo[e] = vo[e] = p[e] = 0.f;
+              if (kF || row_ok(i, rq * 4 + e)) {
+                mo[e] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rm, (int)vo4, (int)s4, 0));
+                vo[e] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rv, (int)vo4, (int)s4, 0));
+                p[e] = has_master ? __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rp, (int)vo4, (int)s4, 0))
+                                  : bf16_to_f32(__builtin_amdgcn_raw_buffer_load_b16(rW, (int)voW, (int)sW, 0));
+              }
+            }
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const int row = erow(i, rq * 4 + e);
+              const uint32_t s4 = (uint32_t)((row * d + j * 32) * 4);
+              const uint32_t sW = (uint32_t)((row * st.ldw + j * 32) * 2);
+              if (!kF && !row_ok(i, rq * 4 + e)) continue;
+              const float g = bf16_to_f32(to_bf16(acc[i][j][rq * 4 + e]));
+              adamw_update(p[e], mo[e], vo[e], g, oc);
+              __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, mo[e]), rm, (int)vo4, (int)s4, 0);
+              __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, vo[e]), rv, (int)vo4, (int)s4, 0);
+              if (has_master)
+                __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, p[e]), rp, (int)vo4, (int)s4, 0);
+              __builtin_amdgcn_raw_buffer_store_b16(to_bf16(p[e]), rW, (int)voW, (int)sW, 0);
             }
           }
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const int row = erow(i, rq * 4 + e);
-            const uint32_t s4 = (uint32_t)((row * d + j * 32) * 4);
-            const uint32_t sW = (uint32_t)((row * st.ldw + j * 32) * 2);
-            if (!row_ok(i, rq * 4 + e)) continue;
-            const float g = bf16_to_f32(to_bf16(acc[i][j][rq * 4 + e]));
-            adamw_update(p[e], mo[e], vo[e], g, oc);
-            __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, mo[e]), rm, (int)vo4, (int)s4, 0);
-            __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, vo[e]), rv, (int)vo4, (int)s4, 0);
-            if (has_master)
-              __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, p[e]), rp, (int)vo4, (int)s4, 0);
-            __builtin_amdgcn_raw_buffer_store_b16(to_bf16(p[e]), rW, (int)voW, (int)sW, 0);
-          }
         }
-      }
+    };
+    if (!partial && d0 + TILE <= d) update_tile(std::true_type{});
+    else update_tile(std::false_type{});
   }
 }
 
