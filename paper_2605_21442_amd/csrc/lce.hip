@@ -1128,12 +1128,13 @@ __global__ __launch_bounds__(256) void k_gather_rows(const uint16_t* __restrict_
   }
 }
 
-// Tile scheduling for the backward contractions. Workgroups are dispatched round-robin over the
+// Tile scheduling of the dH launches whose K the host splits into parts (launches with fewer
+// tiles than CUs; one copy of this grid per part). Workgroups are dispatched round-robin over the
 // 8 XCDs (block b runs on XCD b % 8), each with its own L2. XCD x owns the band of row tiles
-// [x T / 8, (x + 1) T / 8) (T = live row tiles) and walks it column by column, so the ~32
-// workgroups resident on one XCD share the band's A tiles and a few B tiles in its L2, and each
-// large A operand is fetched by one XCD only. The grid is 8 * ceil(T_max / 8) * tn_count blocks;
-// blocks past the live tiles return false.
+// [x T / 8, (x + 1) T / 8) (T = live row tiles) and walks it column by column, so the workgroups
+// resident on one XCD share the band's A tiles and a few B tiles in its L2, and each A operand is
+// fetched by one XCD only. The grid is 8 * ceil(T_max / 8) * tn_count blocks; blocks past the live
+// tiles return false.
 __device__ __forceinline__ bool band_tile(int blk, int tm_live, int tn_count, int& tm, int& tn) {
   const int x = blk & 7, k = blk >> 3;
   const int r0 = (x * tm_live) >> 3, r1 = ((x + 1) * tm_live) >> 3;
