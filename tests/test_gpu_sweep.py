@@ -88,6 +88,23 @@ def test_c_abi_strided_sweep(case):
 
 
 @pytest.mark.parametrize("case", range(6))
+def test_many_token_tiles_sweep(case):
+    # more token tiles than the strided sweep (8 to 17 of 256): the forward and G launches deal the
+    # vocabulary tiles past the last multiple of 8 to the XCDs by token tile, and the dW and dH
+    # launches cut their tiles into per-XCD shares of several rounds
+    rng = np.random.default_rng(3000 + case)
+    n = int(rng.integers(1800, 4300))
+    d = int(rng.choice([64, 128, 192, 256]))
+    v = int(rng.integers(5000, 30000))
+    reduction = ["mean", "sum"][case % 2]
+    inp = WL.custom(n, d, v, seed=case, mask_frac=float(rng.uniform(0, 0.4)), sigma_w=0.3, case_id=51)
+    print(f"token-tile sweep {case}: n={n} d={d} v={v} {reduction}", flush=True)
+    h, w, t = U.to_device(inp)
+    gpu = U.run_gpu(h, w, t, inp.ignore_index, reduction, 1.0)
+    U.assert_parity(gpu, O.lce(inp.h_bits, inp.w_bits, inp.targets, inp.ignore_index, reduction, 1.0))
+
+
+@pytest.mark.parametrize("case", range(6))
 def test_kd_random_sweep(case):
     rng = np.random.default_rng(3000 + case)
     n = int(rng.integers(1, 600))
