@@ -191,34 +191,31 @@ __device__ __forceinline__ float wave_sum(float x) {
   for (int m = 32; m >= 1; m >>= 1) x += __shfl_xor(x, m);
   return x;
 }
-__device__ __forceinline__ float wave_max(float x) {
-  for (int m = 32; m >= 1; m >>= 1) x = fmaxf(x, __shfl_xor(x, m));
-  return x;
-}
-
 // ---------------------------------------------------------------------------------------------
-// MFMA main loop: acc[bi][bj] = A[256 x K] * B[256 x K]^T for this workgroup's 256x256 tile.
+// MFMA main loop: acc[bi][bj] = A[128 WM x K] * B[256 x K]^T for this workgroup's (128 WM) x 256
+// tile, WM = 2 (256 x 256, 8 waves, two per SIMD) or WM = 3 (384 x 256, 12 waves, three per SIMD;
+// the waves of a SIMD cover each other's memory stalls with their MFMAs).
 //
-// Eight waves (two per SIMD, so one wave's memory stalls are covered by the other's MFMAs) in a
-// 2 x 4 grid; wave w = 4 wr + wc owns output rows wr*128.. (A rows) and columns wc*64.. (B rows).
-// acc[bi][bj] (bi < 4, bj < 2) is the 32x32 block (bi, bj) of that 128x64 wave tile; lane l,
-// register r of a block holds row 8 (r / 4) + 4 (l / 32) + r % 4, column l % 32. A fragment
-// for v_mfma_f32_32x32x16_bf16 is 8 consecutive K values of one row (lane l: row l % 32, K
-// chunk l / 32 of the 16-wide substep).
+// The waves form a WM x 4 grid; wave w = 4 wr + wc owns output rows wr*128.. (A rows) and
+// columns wc*64.. (B rows). acc[bi][bj] (bi < 4, bj < 2) is the 32x32 block (bi, bj) of that
+// 128x64 wave tile; lane l, register r of a block holds row 8 (r / 4) + 4 (l / 32) + r % 4,
+// column l % 32. A fragment for v_mfma_f32_32x32x16_bf16 is 8 consecutive K values of one row
+// (lane l: row l % 32, K chunk l / 32 of the 16-wide substep).
 //
-// K streams through two LDS buffers of 64-wide slices (A and B 32 KB each: 64 KB per buffer),
+// K streams through two LDS buffers of 64-wide slices (A 32 or 48 KB and B 32 KB per buffer),
 // copied global -> LDS by buffer loads that write LDS directly, one 16-byte chunk per lane and
 // 1 KB per instruction. An operand is stored in one of two ways:
 //
-//  * row-major (K contiguous, e.g. H [N, D], W [V, D]): a slice is 256 rows x 128 bytes; each
+//  * row-major (K contiguous, e.g. H [N, D], W [V, D]): a slice is 256 or 384 rows x 128 bytes; each
 //    load instruction moves 8 rows (one full cache line per row, which the memory pipeline turns
 //    into whole-line requests). Chunk c of row r sits at position c ^ swz(r), swz(r) = (r & 7) ^
 //    ((r >> 3) & 1), so that the 128-bit fragment reads of any 8 or 16 consecutive rows hit
 //    distinct banks;
-//  * K-major (the 256 tile elements contiguous, e.g. G [Nv, Vc] as the A operand of G^T H, or
-//    W [V, D] as the B operand of G W): a slice is 64 K-rows x 512 bytes; each load instruction
-//    moves 2 K-rows (4 whole lines each). Chunk c of K-row k sits at position c ^ kswz(k),
-//    kswz(k) = 4 (k & 3) + 16 ((k >> 3) & 1). Fragments come from pairs of transposing reads
+//  * K-major (the tile's 256 or 384 elements contiguous, e.g. G [Nv, Vc] as the A operand of
+//    G^T H, or W [V, D] as the B operand of G W): a slice is 64 K-rows x 512 or 768 bytes; each
+//    load instruction moves whole lines of consecutive K-rows. For a 256-wide operand chunk c of
+//    K-row k sits at position c ^ kswz(k), kswz(k) = 4 (k & 3) + 16 ((k >> 3) & 1) (the 384-wide
+//    swizzle is kpos below). Fragments come from pairs of transposing reads
 //    (ds_read_b64_tr_b16): in a 16-lane group, lane i reads 4 consecutive elements (8 bytes) of
 //    K-row i / 4 and lane j receives element j of the group's 16 columns from K-rows 0..3; the
 //    second read covers K-rows 4..7. The swizzle spreads the 4 K-rows x 64 bytes that a half-wave
@@ -226,13 +223,13 @@ __device__ __forceinline__ float wave_max(float x) {
 //
 // Each load picks its source chunk so that it lands in the swizzled position.
 //
-// Schedule of slice j (four 16-wide substeps, fragments read one substep ahead): after the
-// third substep's MFMAs are issued, one barrier both publishes slice j+1 (its loads were issued
-// about a slice earlier) and frees slice j's buffer, into which slice j+2 is then loaded while
-// the fourth substep runs and the first fragments of slice j+1 are read. Waves 0..3 issue their
-// loads at the barrier, waves 4..7 one or two substeps later (kLateGroups): on this part a whole
-// workgroup's 64 load instructions at once fill the texture-address queues and stall the
-// issuing waves (measured: 3-9 % per kernel; the better delay depends on the operand stream).
+// Schedule of slice j (four 16-wide substeps; WM = 2 reads fragments one substep ahead, WM = 3
+// just before use): after the third substep's MFMAs are issued, one barrier both publishes slice
+// j+1 (its loads were issued about a slice earlier) and frees slice j's buffer, into which slice
+// j+2 is then loaded while the fourth substep runs. Waves 0..3 issue their loads at the barrier,
+// the others one or two substeps later (kLateGroups): on this part a whole workgroup's load
+// instructions at once fill the texture-address queues and stall the issuing waves (measured:
+// 3-9 % per kernel; the better delay depends on the operand stream).
 //
 // K must be a multiple of 8; a ragged last slice is zero-filled by pointing the lanes past K
 // outside the buffer resource (buffer loads return 0 there).
@@ -1450,8 +1447,8 @@ __global__ __launch_bounds__(Geo<WM>::NT, WM) void k_bwd_g(const uint16_t* __res
 }
 
 // K5: dW[v0 + m][dd] = sum_k G[k][m] Hv[k][dd] over k < round_up(Nv, 64), G [Npad][vc] and the
-// gathered valid rows Hv [Npad][D] both read K-major (transposing LDS reads); tiles of (128 WM) ids x 256 hidden
-// columns. The epilogue either writes the block in bf16 (each element once), adds it to the bf16
+// gathered valid rows Hv [Npad][D] both read K-major (transposing LDS reads); tiles of (128 WM)
+// ids x 256 hidden columns. The epilogue either writes the block in bf16 (each element once), adds it to the bf16
 // values already there, or hands each bf16-rounded element straight to the AdamW update of W (the
 // in-backward step). Its accesses go through buffer resources over the tile's rows below the slab
 // width (rows past it read 0 and drop their stores): a per-lane 32-bit offset and a wave-uniform
