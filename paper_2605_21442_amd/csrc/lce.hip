@@ -723,10 +723,10 @@ __global__ __launch_bounds__(1024) void k_compact(const void* targets, int tbyte
 //    through idx by the main loop; two partial rows (one per wave row) per partition.
 // In both, a tile's S^T = W_tile H^T runs a token's logits down a lane's registers.
 // ---------------------------------------------------------------------------------------------
-// Tiles are taken in groups of gw consecutive vocabulary tiles (one backward slab's width) by all
-// token tiles, ids fastest: the group's W rows stay in the MALL while the token tiles pass, and the
-// workgroups resident on one XCD (consecutive blocks go to the 8 XCDs in turn) share their W and H
-// tiles through its L2 as in the backward's G launches. One launch covers vt_launch tiles from tm0
+// Tiles are taken in the order of xcd_tile (below), in groups of gw vocabulary tiles (the slab
+// rule's width, within the MALL cap, a multiple of 8) by all token tiles, ids fastest: the group's
+// W rows stay in the MALL while the token tiles pass, and the workgroups resident on one XCD share
+// their W and H tiles through its L2 as in the backward's G launches. One launch covers vt_launch tiles from tm0
 // on and writes one partial row per tile (row tm - tm0). When the rows of all tiles would take
 // more than 2 D bytes per token (one bf16 row of H), the host launches one group at a time
 // instead: group g writes to one of two row sets (by the parity of g), and in launch g >= 1 the
