@@ -1,6 +1,7 @@
 """Seeded random sweeps through the C ABI and the KD / vocabulary-shard entry points.
 
-The LCE sweep draws shapes across tile and slab boundaries and, per case, row strides on both H
+The LCE sweeps draw shapes across tile and slab boundaries (one of them 40 shapes of any width, up
+to 5000 tokens and 40000 ids) and, in the strided one, per case row strides on both H
 and W whose padding columns hold NaN (a kernel that read them would poison the results), int32 or
 int64 targets, an ignore_index that may lie inside [0, V), and a few out-of-range targets (the
 device status bit and the ignored-row treatment are checked against the oracle). The KD and
@@ -85,6 +86,29 @@ def test_c_abi_strided_sweep(case):
                 grad.astype(np.float64) if reduction == "none" else float(grad[0]))
     U.assert_parity(gpu, ref)
     assert ref["status"] == (1 if np.any((t != ignore) & ((t < 0) | (t >= v))) else 0)
+
+
+@pytest.mark.parametrize("case", range(40))
+def test_random_shape_sweep(case):
+    # any hidden width that is a multiple of 8 (both tile forms), token counts from 1 to 5000,
+    # vocabularies from 1 to 40000 ids, all three reductions, 0-60 % masked, three weight scales
+    rng = np.random.default_rng([4000, case])
+    while True:
+        n = int(rng.integers(1, 5000))
+        d = int(rng.integers(1, 129)) * 8
+        v = int(rng.integers(1, 40000))
+        if n * v * d <= 3e9:                      # the oracle finishes in well under a second
+            break
+    reduction = ["mean", "sum", "none"][case % 3]
+    inp = WL.custom(n, d, v, seed=case, mask_frac=float(rng.uniform(0, 0.6)),
+                    sigma_w=float(rng.choice([0.02, 0.3, 1.0])), case_id=52)
+    grad = rng.standard_normal(n).astype(np.float32) if reduction == "none" else 1.0
+    print(f"random sweep {case}: n={n} d={d} v={v} {reduction}", flush=True)
+    h, w, t = U.to_device(inp)
+    gpu = U.run_gpu(h, w, t, inp.ignore_index, reduction, grad)
+    ref = O.lce(inp.h_bits, inp.w_bits, inp.targets, inp.ignore_index, reduction,
+                grad.astype(np.float64) if reduction == "none" else 1.0)
+    U.assert_parity(gpu, ref)
 
 
 @pytest.mark.parametrize("case", range(6))
